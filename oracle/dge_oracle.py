@@ -1,0 +1,266 @@
+"""Float64 CPU oracle for the Draft-Guided Eviction (DGE) eviction step.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the package smoke check and the
+benchmark's CPU-baseline leg may import this module.  It shares no code with the
+GPU library (no kernels, helpers, tables or constants) and never imports it.
+
+Every function is the plain definition of one step, written from the paper
+(arxiv 2609.33334, "Draft-Guided Eviction"), in float64, with no blocking or
+fusion.  Notation, per layer, KV head h and sequence b:
+
+* G = H_q / H_kv query heads share KV head h (native GQA layout, app:complexity);
+* L prompt rows, w window rows, k draft rows, N = L + k cached rows;
+* the protected tail is the last n_tail = w + k cached rows (window + draft tail,
+  Alg. 1 step C and app:dg implementation notes);
+* C = N - n_tail candidate rows, B' = min(B - w, C) selected rows.
+
+Readings of points the paper leaves open (each also listed with its evidence in
+the design notes): softmax runs causally over every cached key j <= p, tail
+included; the score is the SUM over scoring rows (app:diagnostics "score sum"),
+which ranks identically to Alg. 1's 1/k mean; the GQA group MEAN is taken before
+max-pooling; pooling only spans the candidates, out-of-range counting as -inf;
+top-B ties go to the lower position; selected indices are returned ascending.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# scoring-row modes (Alg. 1 step B): window+draft (default), draft only (DGE), window only (DGE-W)
+ROWS_WINDOW_DRAFT, ROWS_DRAFT, ROWS_WINDOW = 0, 1, 2
+
+
+def as_f64(x) -> np.ndarray:
+    """Exact up-cast of stored float32 values (bf16 inputs arrive already widened)."""
+    return np.asarray(x, dtype=np.float64)
+
+
+def scoring_rows(N: int, w: int, k: int, mode: int):
+    """First position p0 and count of the scoring rows for one sequence.
+
+    Alg. 1 step B (DGE): the k draft rows, positions [N-k, N).
+    Alg. 1 step B alternative (DGE-W, SnapKV's window): the last w prompt rows,
+    positions [L-w, L) with L = N - k.  Default here: window and draft rows together.
+    """
+    if mode == ROWS_WINDOW_DRAFT:
+        return N - w - k, w + k
+    if mode == ROWS_DRAFT:
+        return N - k, k
+    if mode == ROWS_WINDOW:
+        return N - k - w, w
+    raise ValueError(mode)
+
+
+def causal_probs(qrows: np.ndarray, keys: np.ndarray, positions: np.ndarray) -> np.ndarray:
+    """softmax_j(q_r . k_j / sqrt(d)) over keys j <= position of row r, 0 beyond.
+
+    Alg. 1 step B (the softmax of q K^T / sqrt(d)); fp32 softmax in the paper
+    (app:diagnostics), float64 here.  qrows [R][d], keys [N][d] -> [R][N].
+    """
+    d = keys.shape[1]
+    x = (qrows @ keys.T) / math.sqrt(d)
+    j = np.arange(keys.shape[0])[None, :]
+    valid = j <= positions[:, None]
+    x = np.where(valid, x, -np.inf)
+    m = x.max(axis=1, keepdims=True)
+    e = np.where(valid, np.exp(x - m), 0.0)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def window_scores(q, k, kv_offsets, n_q_heads: int, n_kv_heads: int, w: int, k_draft: int,
+                  mode: int = ROWS_WINDOW_DRAFT) -> np.ndarray:
+    """Per-KV-head attention mass each cached key receives from the scoring rows.
+
+    raw[h][j] = (1/G) * sum_{g in group h} sum_{r} softmax_j(q_{g,r} K^T / sqrt(d)),
+    i.e. the score sum over past keys of app:diagnostics, from the rows Alg. 1 step B
+    names, averaged over the query heads of the GQA group (app:complexity,
+    gqa_score_agg).  q [H_q][batch*n_rows][d] holds the mode's rows in ascending
+    position; k [H_kv][T][d] -> raw [H_kv][T].
+    """
+    q = as_f64(q)
+    k = as_f64(k)
+    G = n_q_heads // n_kv_heads
+    offs = [int(o) for o in kv_offsets]
+    T = offs[-1]
+    raw = np.zeros((n_kv_heads, T), np.float64)
+    for b in range(len(offs) - 1):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        p0, nr = scoring_rows(N, w, k_draft, mode)
+        pos = p0 + np.arange(nr)
+        r0 = b * nr  # q holds exactly this mode's n_rows rows per sequence
+        for h in range(n_kv_heads):
+            acc = np.zeros(N, np.float64)
+            for g in range(G):
+                P = causal_probs(q[h * G + g, r0:r0 + nr], k[h, s0:s0 + N], pos)
+                acc += P.sum(axis=0)
+            raw[h, s0:s0 + N] = acc / G
+    return raw
+
+
+def maxpool(raw_row: np.ndarray, C: int, kappa: int) -> np.ndarray:
+    """SnapKV 1-D max-pool (kernel kappa, stride 1, same length) over candidates [0, C).
+
+    pooled[j] = max{raw[i] : |i - j| <= kappa // 2, 0 <= i < C} (app:diagnostics,
+    Sec. 6 compression settings: kernel 7).  Keys outside the candidate range do
+    not take part.
+    """
+    r = kappa // 2
+    x = np.asarray(raw_row[:C], np.float64)
+    out = np.empty(C, np.float64)
+    for j in range(C):
+        out[j] = x[max(0, j - r):min(C, j + r + 1)].max()
+    return out
+
+
+def select_topb(pooled: np.ndarray, n_select: int) -> np.ndarray:
+    """Indices of the n_select largest pooled scores, ties to the lower index, ascending.
+
+    Alg. 1 step B: I <- R_E(s, B - w) with per-head top-B; app:dg implementation
+    notes: indices are sorted to keep temporal order.  Keeps everything when
+    n_select >= C.
+    """
+    C = pooled.shape[0]
+    n = min(int(n_select), C)
+    order = np.lexsort((np.arange(C), -np.asarray(pooled, np.float64)))
+    return np.sort(order[:n]).astype(np.int64)
+
+
+def compact(k_rows: np.ndarray, v_rows: np.ndarray, idx: np.ndarray, C: int):
+    """[retained past, ascending] || [window + draft tail] (app:dg implementation notes)."""
+    N = k_rows.shape[0]
+    keep = np.concatenate([np.asarray(idx, np.int64), np.arange(C, N)])
+    return k_rows[keep].copy(), v_rows[keep].copy()
+
+
+def evict_layer(q, k, v, kv_offsets, n_q_heads, n_kv_heads, w, k_draft, budget, kappa,
+                mode=ROWS_WINDOW_DRAFT, n_tail=None):
+    """Whole eviction step for one layer: score -> pool -> top-(B-w) -> compact.
+
+    Returns raw [H_kv][T], and per (b, h): pooled, idx, compacted K and V.
+    """
+    raw = window_scores(q, k, kv_offsets, n_q_heads, n_kv_heads, w, k_draft, mode)
+    n_tail = w + k_draft if n_tail is None else n_tail
+    offs = [int(o) for o in kv_offsets]
+    out = {}
+    for b in range(len(offs) - 1):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        C = N - n_tail
+        for h in range(n_kv_heads):
+            pooled = maxpool(raw[h, s0:s0 + N], C, kappa)
+            idx = select_topb(pooled, budget - w)
+            ko, vo = compact(np.asarray(k)[h, s0:s0 + N], np.asarray(v)[h, s0:s0 + N], idx, C)
+            out[(b, h)] = dict(pooled=pooled, idx=idx, k=ko, v=vo)
+    return raw, out
+
+
+# ---------------------------------------------------------------------------------------
+# Alternative retention rules
+# ---------------------------------------------------------------------------------------
+def h2o_row_lse(q_all, k, kv_offsets, n_q_heads: int, n_kv_heads: int, block: int = 1024):
+    """log sum_{j <= p} exp(q_p . k_j / sqrt(d)) for every cached row p and query head."""
+    q_all = as_f64(q_all)
+    k = as_f64(k)
+    G = n_q_heads // n_kv_heads
+    offs = [int(o) for o in kv_offsets]
+    lse = np.zeros((n_q_heads, offs[-1]), np.float64)
+    d = k.shape[2]
+    for b in range(len(offs) - 1):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        for hq in range(n_q_heads):
+            K = k[hq // G, s0:s0 + N]
+            for p0 in range(0, N, block):
+                p1 = min(N, p0 + block)
+                x = (q_all[hq, s0 + p0:s0 + p1] @ K[:p1].T) / math.sqrt(d)
+                valid = np.arange(p1)[None, :] <= np.arange(p0, p1)[:, None]
+                x = np.where(valid, x, -np.inf)
+                m = x.max(axis=1)
+                lse[hq, s0 + p0:s0 + p1] = m + np.log(np.where(valid, np.exp(x - m[:, None]), 0).sum(axis=1))
+    return lse
+
+
+def h2o_colsum(q_all, k, kv_offsets, n_q_heads: int, n_kv_heads: int, block: int = 1024):
+    """H2O accumulated attention, kept running through the draft rows.
+
+    colsum[h][j] = (1/G) * sum_g sum_{p = j}^{N-1} softmax_j(q_{g,p} K^T / sqrt(d)):
+    the causal attention every cached row (all prefill rows plus the k draft rows)
+    pays to key j (tab:complexity footnote a), meaned over the GQA group.
+    """
+    q_all = as_f64(q_all)
+    k = as_f64(k)
+    G = n_q_heads // n_kv_heads
+    offs = [int(o) for o in kv_offsets]
+    col = np.zeros((n_kv_heads, offs[-1]), np.float64)
+    for b in range(len(offs) - 1):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        for h in range(n_kv_heads):
+            K = k[h, s0:s0 + N]
+            acc = np.zeros(N, np.float64)
+            for g in range(G):
+                qh = q_all[h * G + g, s0:s0 + N]
+                for p0 in range(0, N, block):
+                    p1 = min(N, p0 + block)
+                    P = causal_probs(qh[p0:p1], K[:p1], np.arange(p0, p1))
+                    acc[:p1] += P.sum(axis=0)
+            col[h, s0:s0 + N] = acc / G
+    return col
+
+
+def h2o_select(colsum_row: np.ndarray, budget: int, n_recent: int) -> np.ndarray:
+    """H2O retention: heavy hitters = top-(B - n_recent) accumulated scores among the
+    non-recent rows, plus the n_recent most recent rows (kept as the tail)."""
+    N = colsum_row.shape[0]
+    C = N - n_recent
+    return select_topb(colsum_row[:C], budget - n_recent)
+
+
+def streaming_select(N: int, n_sink: int, n_recent: int) -> np.ndarray:
+    """StreamingLLM: keep the first n_sink rows (attention sinks) and the last n_recent
+    rows; no scores (Sec. 6 baselines; app:analysis: four sinks and a recency window).
+    Returns the kept sink indices; the recent rows are the protected tail."""
+    C = max(N - n_recent, 0)
+    return np.arange(min(n_sink, C), dtype=np.int64)
+
+
+def pyramid_budgets(B: int, w: int, n_layers: int, beta: int = 20) -> np.ndarray:
+    """PyramidKV per-layer total budgets B_l (app:analysis, discrete schedule).
+
+    c = B - w past tokens; the ramp starts at max = 2c - floor(c/beta) on layer 0 and
+    falls by steps = floor((max - min) / (n_layers - 1)) per layer, min = floor(c/beta)
+    (the paper states max and steps; this min reproduces its five worked examples).
+    B_l = c_l + w.
+    """
+    c = B - w
+    mx = 2 * c - c // beta
+    mn = c // beta
+    steps = (mx - mn) // (n_layers - 1) if n_layers > 1 else 0
+    return np.array([mx - l * steps + w for l in range(n_layers)], np.int64)
+
+
+# ---------------------------------------------------------------------------------------
+# Identities used to check compaction (Eq. 1 / eq:evict-mass, eq:match)
+# ---------------------------------------------------------------------------------------
+def attention_output(qrow: np.ndarray, keys: np.ndarray, vals: np.ndarray) -> np.ndarray:
+    """o = sum_j softmax_j(q . k_j / sqrt(d)) v_j over the given keys."""
+    d = keys.shape[1]
+    x = keys @ as_f64(qrow) / math.sqrt(d)
+    a = np.exp(x - x.max())
+    a /= a.sum()
+    return a @ vals
+
+
+def evicted_mass(qrow: np.ndarray, keys: np.ndarray, evicted: np.ndarray) -> float:
+    """m(E) = sum_{j in E} softmax_j(q . k_j / sqrt(d)) (eq:evict-mass, eq:match rho_q)."""
+    d = keys.shape[1]
+    x = keys @ as_f64(qrow) / math.sqrt(d)
+    a = np.exp(x - x.max())
+    a /= a.sum()
+    return float(a[evicted].sum())
+
+
+def log_partition(qrow: np.ndarray, keys: np.ndarray) -> float:
+    """log Z(q) = log sum_j exp(q . k_j / sqrt(d)) (eq:match)."""
+    d = keys.shape[1]
+    x = keys @ as_f64(qrow) / math.sqrt(d)
+    m = x.max()
+    return float(m + np.log(np.exp(x - m).sum()))

@@ -1,0 +1,292 @@
+"""Pins of the float64 oracle against facts that do not come from the oracle itself.
+
+Each test names what fixes the expected value: a worked example the paper prints,
+a closed form, an invariant, a library routine that computes the same definition
+independently (torch SDPA, max_pool1d, topk, logsumexp), or brute force.
+CPU only.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import dge_inputs as di
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand(shape, seed, scale=1.0):
+    return np.random.default_rng(seed).standard_normal(shape) * scale
+
+
+# ----------------------------------------------------------------------------------
+# PyramidKV: the paper's five worked examples (app:analysis)
+# ----------------------------------------------------------------------------------
+def test_pyramid_worked_examples():
+    cases = json.load(open(os.path.join(GOLDEN, "pyramidkv_worked_examples.json")))["cases"]
+    for c in cases:
+        Bl = oracle.pyramid_budgets(c["B"], c["w"], c["n_layers"])
+        past = Bl - c["w"]
+        assert len(past) == c["n_layers"]
+        steps = set((past[:-1] - past[1:]).tolist())
+        assert steps == {c["steps"]}, (c, past)
+        if "last_layers_past" in c:
+            tail = c["last_layers_past"]
+            assert past[-len(tail):].tolist() == tail, (c, past)
+        if "every_layer_past" in c:
+            assert (past == c["every_layer_past"]).all()
+
+
+# ----------------------------------------------------------------------------------
+# Scoring: closed forms, invariants and an independent library implementation
+# ----------------------------------------------------------------------------------
+def test_score_hand_example_scale_and_mask():
+    # d = 4, sqrt(d) = 2.  One draft row at position 1 sees keys 0 and 1:
+    # logits 0 and (2 * ln 3) / 2 = ln 3  ->  softmax (1/4, 3/4).  A dropped 1/sqrt(d)
+    # gives (1/10, 9/10); a flipped sign gives (3/4, 1/4).
+    q = np.zeros((1, 1, 4)); q[0, 0, 0] = 2.0
+    k = np.zeros((1, 2, 4)); k[0, 1, 0] = math.log(3.0)
+    raw = oracle.window_scores(q, k, [0, 2], 1, 1, w=0, k_draft=1, mode=oracle.ROWS_DRAFT)
+    assert np.allclose(raw[0], [0.25, 0.75], rtol=0, atol=1e-15)
+    # A window row at position 0 (the last prompt row, L = 1) sees key 0 only.
+    raw = oracle.window_scores(q, k, [0, 2], 1, 1, w=1, k_draft=1, mode=oracle.ROWS_WINDOW)
+    assert raw[0].tolist() == [1.0, 0.0]
+
+
+@pytest.mark.parametrize("mode", [oracle.ROWS_WINDOW_DRAFT, oracle.ROWS_DRAFT, oracle.ROWS_WINDOW])
+def test_score_mass_equals_rows(mode):
+    # every softmax row sums to 1, so each head's total mass is the number of scoring rows
+    Hq, Hkv, d, w, kd = 8, 2, 16, 5, 3
+    offs = [0, 40, 97]
+    nr = oracle.scoring_rows(10, w, kd, mode)[1]
+    q = _rand((Hq, 2 * nr, d), 1, 2.0)
+    k = _rand((Hkv, offs[-1], d), 2, 2.0)
+    raw = oracle.window_scores(q, k, offs, Hq, Hkv, w, kd, mode)
+    for b in range(2):
+        tot = raw[:, offs[b]:offs[b + 1]].sum(axis=1)
+        assert np.allclose(tot, nr, rtol=1e-12, atol=0)
+
+
+def test_score_uniform_closed_form():
+    # identical keys: a row at position p spreads 1/(p+1) over keys 0..p, so
+    # raw[j] = sum_{p = max(j, p0)}^{N-1} 1/(p+1)  (the group mean of equal heads)
+    Hq, Hkv, d, w, kd, N = 4, 1, 8, 6, 2, 30
+    q = _rand((Hq, w + kd, d), 3)
+    k = np.tile(_rand((1, 1, d), 4), (Hkv, N, 1))
+    raw = oracle.window_scores(q, k, [0, N], Hq, Hkv, w, kd)
+    p0 = N - w - kd
+    want = [sum(1.0 / (p + 1) for p in range(max(j, p0), N)) for j in range(N)]
+    assert np.allclose(raw[0], want, rtol=1e-13, atol=0)
+
+
+def _sdpa_probs(qrows, keys, positions):
+    # torch's SDPA with V = identity returns the attention probabilities themselves,
+    # with its own default scale 1/sqrt(d) and the boolean mask j <= p.
+    Q = torch.tensor(qrows)[None, None]
+    K = torch.tensor(keys)[None, None]
+    V = torch.eye(keys.shape[0], dtype=torch.float64)[None, None]
+    mask = torch.arange(keys.shape[0])[None, :] <= torch.tensor(positions)[:, None]
+    return torch.nn.functional.scaled_dot_product_attention(Q, K, V, attn_mask=mask)[0, 0].numpy()
+
+
+@pytest.mark.parametrize("mode", [oracle.ROWS_WINDOW_DRAFT, oracle.ROWS_DRAFT, oracle.ROWS_WINDOW])
+def test_score_matches_torch_sdpa(mode):
+    Hq, Hkv, d, w, kd = 6, 3, 32, 7, 2
+    offs = [0, 23, 64]
+    G = Hq // Hkv
+    nr = oracle.scoring_rows(10, w, kd, mode)[1]
+    q = _rand((Hq, 2 * nr, d), 5, 1.5)
+    k = _rand((Hkv, offs[-1], d), 6, 1.5)
+    raw = oracle.window_scores(q, k, offs, Hq, Hkv, w, kd, mode)
+    for b in range(2):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        p0, _ = oracle.scoring_rows(N, w, kd, mode)
+        pos = np.arange(p0, p0 + nr)
+        for h in range(Hkv):
+            cols = [_sdpa_probs(q[h * G + g, b * nr:(b + 1) * nr], k[h, s0:s0 + N], pos).sum(0)
+                    for g in range(G)]
+            assert np.allclose(raw[h, s0:s0 + N], np.mean(cols, axis=0), rtol=1e-12, atol=1e-15)
+
+
+def test_dgew_timing_invariance():
+    # DGE-W keeps the window scorer and only moves the eviction step: the window rows'
+    # scores of the prompt keys do not change when k draft rows are appended to the cache
+    Hq, Hkv, d, w, L, kd = 4, 2, 16, 8, 50, 3
+    q = _rand((Hq, w, d), 7)
+    k_prompt = _rand((Hkv, L, d), 8)
+    k_full = np.concatenate([k_prompt, _rand((Hkv, kd, d), 9)], axis=1)
+    a = oracle.window_scores(q, k_prompt, [0, L], Hq, Hkv, w, 0, oracle.ROWS_WINDOW)
+    b = oracle.window_scores(q, k_full, [0, L + kd], Hq, Hkv, w, kd, oracle.ROWS_WINDOW)
+    assert np.array_equal(a, b[:, :L])
+    assert (b[:, L:] == 0).all()
+
+
+# ----------------------------------------------------------------------------------
+# Pooling and selection
+# ----------------------------------------------------------------------------------
+@pytest.mark.parametrize("kappa", [1, 3, 5, 7])
+def test_maxpool_matches_torch(kappa):
+    x = np.random.default_rng(10 + kappa).random(57)
+    C = 50
+    want = torch.nn.functional.max_pool1d(torch.tensor(x[:C])[None, None], kappa, 1, kappa // 2)[0, 0]
+    assert np.array_equal(oracle.maxpool(x, C, kappa), want.numpy())
+
+
+def test_select_matches_torch_topk_tie_free():
+    rng = np.random.default_rng(11)
+    for C, n in [(100, 10), (257, 64), (64, 64), (30, 100)]:
+        s = rng.random(C)
+        idx = oracle.select_topb(s, n)
+        want = torch.topk(torch.tensor(s), min(n, C)).indices.numpy()
+        assert set(idx.tolist()) == set(want.tolist())
+        assert (np.diff(idx) > 0).all()
+
+
+def test_select_bruteforce_with_ties():
+    # max-sum subsets of size n, lexicographically smallest ascending tuple on ties
+    rng = np.random.default_rng(12)
+    for trial in range(40):
+        C = int(rng.integers(1, 11))
+        n = int(rng.integers(1, C + 1))
+        s = rng.integers(0, 4, size=C).astype(np.float64)   # exact sums, many ties
+        best = None
+        for sub in itertools.combinations(range(C), n):
+            key = (-sum(s[list(sub)]), sub)
+            if best is None or key < best:
+                best = key
+        assert oracle.select_topb(s, n).tolist() == list(best[1]), (s, n)
+
+
+def test_keep_all_when_budget_exceeds_candidates():
+    # B >= L keeps every token; compaction is then the identity
+    Hq, Hkv, d, w, kd, L = 4, 2, 8, 4, 2, 20
+    N = L + kd
+    q = _rand((Hq, w + kd, d), 13)
+    k = _rand((Hkv, N, d), 14)
+    v = _rand((Hkv, N, d), 15)
+    raw, out = oracle.evict_layer(q, k, v, [0, N], Hq, Hkv, w, kd, budget=L + 5, kappa=3)
+    for h in range(Hkv):
+        assert out[(0, h)]["idx"].tolist() == list(range(N - w - kd))
+        assert np.array_equal(out[(0, h)]["k"], k[h]) and np.array_equal(out[(0, h)]["v"], v[h])
+
+
+def test_streaming_closed_form_c5():
+    wl = di.WORKLOADS["c5"]
+    N = wl.cached_lens[0]
+    idx = oracle.streaming_select(N, wl.slm_sinks, wl.slm_recent)
+    kept = np.concatenate([idx, np.arange(N - wl.slm_recent, N)])
+    want = np.concatenate([np.arange(4), np.arange(N - 1020, N)])
+    assert np.array_equal(kept, want)
+    assert oracle.streaming_select(10, 4, 8).tolist() == [0, 1]     # sinks clipped to C
+    assert oracle.streaming_select(5, 4, 8).tolist() == []
+
+
+# ----------------------------------------------------------------------------------
+# Compaction: exact identities of Eq. 1 / eq:evict-mass and eq:match
+# ----------------------------------------------------------------------------------
+def test_compaction_attention_identities():
+    Hq, Hkv, d, w, kd, L = 4, 1, 16, 4, 2, 60
+    N = L + kd
+    q = _rand((Hq, w + kd, d), 16, 1.5)
+    k = _rand((Hkv, N, d), 17, 1.5)
+    v = _rand((Hkv, N, d), 18)
+    raw, out = oracle.evict_layer(q, k, v, [0, N], Hq, Hkv, w, kd, budget=20, kappa=3)
+    o = out[(0, 0)]
+    C = N - w - kd
+    kept = np.concatenate([o["idx"], np.arange(C, N)])
+    E = np.setdiff1d(np.arange(N), kept)
+    assert len(E) == N - (20 - w) - w - kd
+    for t in range(3):
+        qt = _rand((d,), 100 + t, 1.5)
+        full = oracle.attention_output(qt, k[0], v[0])
+        comp = oracle.attention_output(qt, o["k"], o["v"])      # renormalized over R
+        m = oracle.evicted_mass(qt, k[0], E)
+        a = np.exp(k[0] @ qt / math.sqrt(d)); a /= a.sum()
+        mu_E = (a[E] @ v[0][E]) / m
+        assert np.allclose(full, (1 - m) * comp + m * mu_E, rtol=1e-12, atol=1e-13)
+        dlogz = oracle.log_partition(qt, k[0]) - oracle.log_partition(qt, o["k"])
+        assert abs(dlogz - (-math.log(1 - m))) < 1e-12
+
+
+# ----------------------------------------------------------------------------------
+# H2O accumulated attention
+# ----------------------------------------------------------------------------------
+def test_h2o_uniform_is_harmonic():
+    # identical keys: colsum[j] = sum_{p=j}^{N-1} 1/(p+1) = H_N - H_j
+    Hq, Hkv, d, N = 4, 2, 8, 37
+    q = _rand((Hq, N, d), 19)
+    k = np.tile(_rand((1, 1, d), 20), (Hkv, N, 1))
+    col = oracle.h2o_colsum(q, k, [0, N], Hq, Hkv, block=8)
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, N + 1))])
+    assert np.allclose(col, (H[N] - H[:N])[None, :], rtol=1e-13, atol=0)
+    assert np.allclose(col.sum(axis=1), N, rtol=1e-13)
+
+
+def test_h2o_matches_causal_sdpa():
+    Hq, Hkv, d = 4, 2, 16
+    offs = [0, 33, 70]
+    G = Hq // Hkv
+    q = _rand((Hq, offs[-1], d), 21, 1.5)
+    k = _rand((Hkv, offs[-1], d), 22, 1.5)
+    col = oracle.h2o_colsum(q, k, offs, Hq, Hkv, block=16)
+    lse = oracle.h2o_row_lse(q, k, offs, Hq, Hkv, block=16)
+    for b in range(2):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        for h in range(Hkv):
+            acc = np.zeros(N)
+            for g in range(G):
+                Q = torch.tensor(q[h * G + g, s0:s0 + N])[None, None]
+                K = torch.tensor(k[h, s0:s0 + N])[None, None]
+                P = torch.nn.functional.scaled_dot_product_attention(
+                    Q, K, torch.eye(N, dtype=torch.float64)[None, None], is_causal=True)[0, 0]
+                acc += P.sum(0).numpy()
+                x = (Q[0, 0] @ K[0, 0].T) / math.sqrt(d)
+                x = x.masked_fill(torch.ones(N, N, dtype=torch.bool).triu(1), float("-inf"))
+                assert np.allclose(lse[h * G + g, s0:s0 + N], torch.logsumexp(x, 1).numpy(), rtol=1e-13)
+            assert np.allclose(col[h, s0:s0 + N], acc / G, rtol=1e-12, atol=1e-15)
+
+
+def test_h2o_select_splits_heavy_and_recent():
+    s = np.array([5, 1, 4, 4, 0, 9, 9, 9], np.float64)
+    # budget 5 = 3 heavy among the first 5 + 3 recent (positions 5..7)
+    assert oracle.h2o_select(s, 6, 3).tolist() == [0, 2, 3]
+
+
+# ----------------------------------------------------------------------------------
+# Input storage (the shared generator's bf16 rounding vs torch's own conversion)
+# ----------------------------------------------------------------------------------
+def test_bf16_rounding_matches_torch():
+    x = np.random.default_rng(23).standard_normal(10000).astype(np.float32) * 7
+    x[:4] = [0.0, -0.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8]   # ties to even both ways
+    bits = di.f32_to_bf16_bits(x)
+    want = torch.tensor(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(bits, want)
+    assert np.array_equal(di.bf16_bits_to_f32(bits), torch.tensor(x).to(torch.bfloat16).float().numpy())
+
+
+def test_byte_accounting_pins_bf16_storage():
+    # app:complexity: 3.79 GiB (KV repeated to 32 heads) vs 0.95 GiB (8 KV heads) at L = 7762;
+    # intro: ~16 GiB for an 8B model at 128K; app:dg: ~60 MB of prompt queries per layer
+    def kv_bytes(layers, H, L, d=128, elt=2):
+        return layers * 2 * H * L * d * elt
+    assert round(kv_bytes(32, 32, 7762) / 2 ** 30, 2) == 3.79
+    assert round(kv_bytes(32, 8, 7762) / 2 ** 30, 2) == 0.95
+    assert round(kv_bytes(32, 8, 128 * 1024) / 2 ** 30) == 16
+    assert round(32 * 7762 * 128 * 2 / 2 ** 20, 1) == 60.6
+
+
+def test_c1_planted_keys_survive():
+    # the eight x4-scaled keys per KV head attract attention and survive eviction
+    wl = di.WORKLOADS["c1"]
+    x = di.make_layer(wl)
+    raw, out = oracle.evict_layer(x.q, x.k, x.v, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                  wl.window, wl.k_draft, wl.budget, wl.pool)
+    for h in range(wl.n_kv_heads):
+        kept = set(out[(0, h)]["idx"].tolist())
+        hits = sum(int(r) in kept for r in x.planted[(0, h)])
+        assert hits >= 6, (h, hits)
