@@ -1,0 +1,237 @@
+"""Benchmark of the DGE eviction step on one MI355X.
+
+One step = one pass of the whole hot path over one layer's synthetic input:
+dge_score -> dge_select_topb (max-pool + top-(B-w)) -> dge_compact.  Default
+workload: one Llama-3-8B-shaped layer (32 query / 8 KV heads, d 128, batch 1,
+L 4096, window 32 + k 2 draft rows, B 512, pool 7, bf16).
+
+Inputs are resident in HBM before timing.  They are rotated over ``--sets``
+distinct device copies (default 48, ~0.8 GB in total) so that no step finds its
+K/V in the 256 MB Infinity Cache from an earlier step.  Steps are captured in
+HIP graphs (8 steps per graph) so the timed region measures the GPU, not Python
+launch overhead; the graphs are checked against the eager result first.
+
+Prints ONE JSON line (metric, value, roofline of the dominant kernel, CPU
+oracle baseline).  Progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+GRAPH_STEPS = 8
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=4000)
+    p.add_argument("--warmup", type=int, default=64)
+    p.add_argument("--workload", default="c2")
+    p.add_argument("--sets", type=int, default=48)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(every step is independent per KV head and sequence, see the sharding notes "
+              "in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import dge_inputs as di
+    import paper_2609_33334_amd as dge
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = "cuda:0"
+    wl = di.WORKLOADS[args.workload]
+    if wl.h2o or wl.n_layers != 1:
+        print("bench.py: the timed step covers one layer (workload c1 or c2)", file=sys.stderr)
+        sys.exit(2)
+    log(f"[bench] workload {wl.name}: generating inputs")
+    x = di.make_layer(wl)
+    is_bf16 = wl.dtype == "bf16"
+    elt = 2 if is_bf16 else 4
+
+    def dev_t(bits):
+        t = torch.from_numpy(np.ascontiguousarray(bits))
+        if is_bf16:
+            t = t.view(torch.int16).view(torch.bfloat16)
+        return t.to(dev)
+
+    geom = dge.Geometry(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.window, wl.k_draft,
+                        wl.cached_lens, dtype=dge.DGE_BF16 if is_bf16 else dge.DGE_F32, device=dev)
+    q0, k0, v0 = dev_t(x.q_bits), dev_t(x.k_bits), dev_t(x.v_bits)
+    S = max(1, args.sets)
+    sets = []
+    n_tail = wl.window + wl.k_draft
+    n_sel = wl.budget - wl.window
+    ws_score = torch.empty(dge.workspace_size(geom, dge.OP_SCORE), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(dge.workspace_size(geom, dge.OP_SELECT), dtype=torch.uint8, device=dev)
+    for i in range(S):
+        out = dict(raw=torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=dev),
+                   idx=torch.empty(geom.batch, geom.n_kv_heads, n_sel, dtype=torch.int32, device=dev),
+                   n_kept=torch.zeros(max(geom.batch, 4), dtype=torch.int32, device=dev),
+                   k=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
+                                 dtype=k0.dtype, device=dev),
+                   v=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
+                                 dtype=k0.dtype, device=dev))
+        sets.append((q0.clone(), k0.clone(), v0.clone(), out))
+    torch.cuda.synchronize()
+
+    def step(i):
+        q, k, v, out = sets[i % S]
+        dge.evict_layer(geom, q, k, v, wl.budget, wl.pool, ws_score=ws_score, ws_select=ws_sel,
+                        out=out)
+
+    def score_only(i):
+        q, k, v, out = sets[i % S]
+        dge.score(geom, dge.ROWS_WINDOW_DRAFT, q, k, raw=out["raw"], ws=ws_score)
+
+    # eager warmup and reference result
+    for i in range(max(args.warmup, S)):
+        step(i)
+    torch.cuda.synchronize()
+    ref = {kk: vv.clone() for kk, vv in sets[0][3].items()}
+
+    # HIP graphs of GRAPH_STEPS consecutive steps, covering every buffer set
+    stream = torch.cuda.Stream()
+    graphs, sgraphs = [], []
+    n_graphs = max(1, S // GRAPH_STEPS)
+    with torch.cuda.stream(stream):
+        for gi in range(n_graphs):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                for j in range(GRAPH_STEPS):
+                    step(gi * GRAPH_STEPS + j)
+            graphs.append(g)
+            sg = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(sg, stream=stream):
+                for j in range(GRAPH_STEPS):
+                    score_only(gi * GRAPH_STEPS + j)
+            sgraphs.append(sg)
+    torch.cuda.synchronize()
+    # graph replays must reproduce the eager result (set 0 is step 0 of graph 0)
+    for kk in ref:
+        sets[0][3][kk].zero_()
+    torch.cuda.synchronize()
+    graphs[0].replay()
+    torch.cuda.synchronize()
+    for kk in ref:
+        assert torch.equal(sets[0][3][kk], ref[kk]), f"graph replay differs from eager ({kk})"
+
+    K = args.steps
+    n_rep = (K + GRAPH_STEPS - 1) // GRAPH_STEPS
+    K = n_rep * GRAPH_STEPS
+    for r in range(min(n_rep, 2 * n_graphs)):
+        graphs[r % n_graphs].replay()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {K} steps ({n_rep} graph replays of {GRAPH_STEPS} steps, {S} buffer sets)")
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for r in range(n_rep):
+        graphs[r % n_graphs].replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    ms_per_step = gpu_ms / K
+    # dominant kernel (dge_score) timed the same way, on the same stream
+    es0 = torch.cuda.Event(enable_timing=True)
+    es1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    es0.record()
+    for r in range(n_rep):
+        sgraphs[r % n_graphs].replay()
+    es1.record()
+    torch.cuda.synchronize()
+    score_us = es0.elapsed_time(es1) * 1e3 / K
+    log(f"[bench] {ms_per_step * 1e3:.2f} us/step (event), wall {wall * 1e6 / K:.2f} us/step; "
+        f"dge_score {score_us:.2f} us/call")
+
+    L = sum(wl.prompt_lens)
+    units = L * wl.n_kv_heads                      # prefix tokens x KV heads per step
+    value = units / (ms_per_step * 1e-3)
+    # algorithmic bytes of dge_score: K once + the scoring queries
+    n_rows = wl.window + wl.k_draft
+    score_bytes = (wl.n_kv_heads * geom.total_rows * wl.head_dim * elt
+                   + wl.n_q_heads * wl.batch * n_rows * wl.head_dim * elt)
+    achieved = score_bytes / (score_us * 1e-6) / 1e9
+    roofline = {"kernel": "dge_score (stats + reduce + colsum launches)", "bound": "hbm",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "bytes_per_launch": int(score_bytes), "us_per_launch": round(score_us, 3)}
+    # whole step against its own algorithmic bytes (score + compaction + indices)
+    step_bytes = score_bytes + 4 * wl.n_kv_heads * wl.batch * (n_sel + n_tail) * wl.head_dim * elt \
+        + 4 * wl.n_kv_heads * wl.batch * n_sel
+    step_frac = step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, x, args.cpu_seconds)
+    line = {
+        "metric": "prefix tokens x KV heads scored+compacted per second (DGE eviction step)",
+        "value": round(value, 1), "unit": "token*kvhead/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if is_bf16 else "f32",
+        "data": "synthetic (seeded Gaussian Q/K/V with planted spans; no model weights)",
+        "config": {"workload": wl.name + ": one Llama-3-8B-shaped layer, 32q/8kv heads, d=128, "
+                   "batch 1, L=4096, window 32 + k=2 draft rows, B=512, max-pool 7",
+                   "global_batch": wl.batch, "seq_len": L, "parallelism": "single GPU",
+                   "step": "dge_score -> dge_select_topb -> dge_compact",
+                   "step_hbm_frac": round(step_frac, 4), "buffer_sets": S},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(wl, x, seconds):
+    """The float64 oracle, untuned, on this host's cores: repeats of the same layer."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    L = sum(wl.prompt_lens)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.evict_layer(x.q, x.k, x.v, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                           wl.k_draft, wl.budget, wl.pool)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    rate = reps * L * wl.n_kv_heads / el
+    log(f"[bench] cpu oracle: {reps} layers in {el:.1f}s -> {rate:.3g} token*kvhead/s")
+    return {"value": round(rate, 1), "unit": "token*kvhead/s", "cores": cores, "kind": "oracle",
+            "sample": f"{reps} repeats of the full {wl.name} layer (score, pool, select, compact) "
+                      f"in float64 numpy, {el:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -212,7 +212,8 @@ def make_layer(wl: Workload, layer: int = 0, with_v: bool = True) -> LayerInputs
                 # non-overlapping 16-token spans at random candidate starts: one span
                 # inside each of n_spans distinct 32-row slots, at a random offset
                 n_slots = C // 32
-                slots = np.sort(prng.choice(n_slots, size=n_spans, replace=False))
+                n_spans = min(n_spans, n_slots)
+                slots = np.sort(prng.choice(max(n_slots, 1), size=n_spans, replace=False))
                 starts = slots * 32 + prng.integers(0, 17, size=n_spans)
                 rows = (starts[:, None] + np.arange(16)[None, :]).reshape(-1)
                 k[h, s0 + rows] += np.float32(wl.plant_scale * math.sqrt(d)) * u.astype(np.float32)

@@ -1,0 +1,189 @@
+/*
+ * dge.h - C ABI of the Draft-Guided Eviction (DGE) eviction step on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The paper (arxiv 2609.33334) defers KV-cache eviction until k answer tokens
+ * have been drafted on the full cache, then, once per layer (Alg. 1, steps B-C):
+ *   1. scores every cached key by the softmax attention the scoring queries pay
+ *      to it (window and/or draft queries; fp32 softmax, score summed over the
+ *      queries, meaned over each GQA group, 1-D max-pooled: app:diagnostics,
+ *      app:complexity);
+ *   2. keeps the top (B - w) past keys per KV head (R_E of Alg. 1);
+ *   3. rewrites the cache as [retained past, ascending] || [window + draft tail]
+ *      (app:dg, implementation notes).
+ * Alternative retention rules the paper composes with DGE: H2O accumulated
+ * attention (tab:complexity, footnote a), StreamingLLM sinks + recency (Sec. 6)
+ * and PyramidKV layer budgets (app:analysis).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensor pointers are DEVICE pointers unless the name ends in _host.  The
+ *   caller owns all memory; the library never allocates device memory.
+ * - Calls are asynchronous on the given HIP stream.  All arguments are validated
+ *   on the host BEFORE anything is launched: a call that returns an error has
+ *   launched nothing and written nothing.  A failed launch returns DGE_ERR_HIP.
+ * - Outputs must not alias inputs.  Device pointers must be 16-byte aligned.
+ * - Results are deterministic: no floating-point atomics; reruns are bit-identical.
+ * - Layouts are packed and head-major.  For a batch of sequences, sequence b owns
+ *   cached rows [kv_offsets[b], kv_offsets[b+1]) of every KV head: N_b rows, of
+ *   which the first L_b = N_b - k are prompt rows and the last k draft rows.
+ *     K, V      : [H_kv][kv_head_stride] elements; row r of head h starts at
+ *                 h*kv_head_stride + r*head_dim; head_dim elements contiguous.
+ *     scores    : [H_kv][T] float32, T = kv_offsets[batch] (total cached rows).
+ *   Element type of Q, K, V: bfloat16 (DGE_BF16) or float32 (DGE_F32).
+ * - Thread safety: no global mutable state; concurrent calls on different
+ *   streams with disjoint outputs and workspaces are safe.
+ */
+#ifndef DGE_H_
+#define DGE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DGE_ABI_VERSION 1
+
+typedef enum {
+  DGE_OK = 0,
+  DGE_ERR_INVALID = 1,      /* argument violates the documented contract */
+  DGE_ERR_UNSUPPORTED = 2,  /* valid request this build does not implement (e.g. head_dim) */
+  DGE_ERR_WORKSPACE = 3,    /* workspace pointer NULL or smaller than dge_workspace_size */
+  DGE_ERR_HIP = 4           /* a HIP launch or runtime call failed */
+} dge_status_t;
+
+typedef enum { DGE_BF16 = 0, DGE_F32 = 1 } dge_dtype_t;
+
+/* Which cached rows score the keys (Alg. 1, step B).  For a sequence with
+ * N = L + k cached rows:
+ *   WINDOW_DRAFT : the last w prompt rows and the k draft rows, positions [N-w-k, N)
+ *   DRAFT        : the k draft rows only (DGE's own scorer),     positions [N-k, N)
+ *   WINDOW       : the last w prompt rows only (DGE-W / SnapKV),  positions [L-w, L)
+ * A row at position p attends keys j <= p (causal). */
+typedef enum {
+  DGE_ROWS_WINDOW_DRAFT = 0,
+  DGE_ROWS_DRAFT = 1,
+  DGE_ROWS_WINDOW = 2
+} dge_rows_t;
+
+typedef enum { DGE_OP_SCORE = 0, DGE_OP_SELECT = 1, DGE_OP_H2O = 2 } dge_op_t;
+
+/* Geometry of one layer's cache and the eviction parameters it is read with. */
+typedef struct {
+  int32_t batch;        /* sequences, >= 1 */
+  int32_t n_q_heads;    /* H_q, a multiple of n_kv_heads (G = H_q / H_kv <= 64) */
+  int32_t n_kv_heads;   /* H_kv >= 1 */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t window;       /* w >= 0 observation-window rows (last prompt rows) */
+  int32_t k_draft;      /* k >= 0 draft rows cached after the prompt */
+  const int64_t *kv_offsets;       /* device [batch+1], kv_offsets[0] == 0, non-decreasing */
+  const int64_t *kv_offsets_host;  /* host copy with the same values (validation, launch sizing) */
+  int64_t kv_head_stride;          /* elements between KV heads of K and V, >= T*head_dim */
+  int32_t dtype;                   /* dge_dtype_t of Q, K and V */
+} dge_geom_t;
+
+/* DGE_ABI_VERSION of the built library. */
+int dge_abi_version(void);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char *dge_status_string(int status);
+
+/* Bytes of device workspace the given operation needs for this geometry.
+ * DGE_OP_SCORE: per-row softmax partials of dge_score (sized for w + k scoring rows).
+ * DGE_OP_SELECT: radix keys of dge_select_topb.
+ * DGE_OP_H2O: per-row log-sum-exp of dge_h2o_colsum when the caller supplies none.
+ * Writes *bytes (host pointer).  Errors: DGE_ERR_INVALID for a bad geometry. */
+dge_status_t dge_workspace_size(const dge_geom_t *geom, int32_t op, size_t *bytes);
+
+/* Step 1 of the eviction (Alg. 1 step B; app:diagnostics; app:complexity):
+ *   raw[h][j] = (1/G) sum_{g in group h} sum_{scoring rows r} softmax_j(q_{g,r} . k_j / sqrt(d))
+ * for every cached row j of every sequence (tail rows included), softmax in fp32
+ * over keys j <= p_r, scores accumulated in fp32.  Each sequence's scores sum to
+ * the number of scoring rows.
+ *   q   : [H_q][batch * n_rows][d], the rows of `rows` for each sequence in ascending
+ *         position, n_rows = w+k, k or w (see dge_rows_t); query head hq belongs to KV
+ *         head hq / G.
+ *   k   : keys, layout above.
+ *   raw : [H_kv][T] float32 output.
+ *   ws  : workspace of at least dge_workspace_size(geom, DGE_OP_SCORE) bytes.
+ * Errors: DGE_ERR_INVALID if a sequence has fewer than w + k rows or n_rows == 0;
+ * DGE_ERR_UNSUPPORTED for head_dim outside {64, 128}. */
+dge_status_t dge_score(const dge_geom_t *geom, int32_t rows, const void *q, const void *k,
+                       float *raw, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Steps 1b-2 (SnapKV max-pool, then R_E = per-head top-B; Alg. 1; app:dg notes).
+ * For every (sequence b, KV head h), with C_b = N_b - n_tail candidate rows:
+ *   pooled[j] = max{ scores[h][off_b + i] : |i - j| <= pool_kernel/2, 0 <= i < C_b }
+ *   idx[b][h][0 .. n_kept[b]) = the n_kept[b] = min(n_select, C_b) candidates with the
+ *   largest pooled score, ties to the lower position, in ascending order; entries
+ *   [n_kept[b], n_select) are set to -1.
+ *   scores      : [H_kv][T] float32, non-negative (dge_score or dge_h2o_colsum output).
+ *   pool_kernel : odd >= 1 (1 = no pooling).
+ *   n_tail      : protected rows at the end of each sequence (w + k for DGE; the recent
+ *                 window for H2O); 0 <= n_tail <= N_b.
+ *   n_select    : B - w for DGE (B - n_recent for H2O), >= 0.
+ *   idx         : [batch][H_kv][n_select] int32 output (row index within the sequence);
+ *                 may be NULL when n_select == 0.
+ *   n_kept      : [batch] int32 output.
+ *   ws          : at least dge_workspace_size(geom, DGE_OP_SELECT) bytes.
+ * Selection is exact on the float32 scores (radix select on their bit patterns).
+ * Errors: DGE_ERR_INVALID for an even or < 1 pool_kernel, n_select < 0, or
+ * n_tail outside [0, N_b]. */
+dge_status_t dge_select_topb(const dge_geom_t *geom, const float *scores, int32_t pool_kernel,
+                             int32_t n_tail, int32_t n_select, int32_t *idx, int32_t *n_kept,
+                             void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* StreamingLLM retention (Sec. 6; app:analysis: four sinks and a recency window):
+ * idx[b][h][0 .. n_kept[b]) = 0, 1, ..., n_kept[b]-1 with n_kept[b] = min(n_sink, N_b - n_recent);
+ * remaining entries up to n_sink are -1.  The n_recent rows are the tail passed to
+ * dge_compact.  No scores are read.
+ *   idx    : [batch][H_kv][n_sink] int32 output;  n_kept : [batch] int32 output.
+ * Errors: DGE_ERR_INVALID if n_sink < 0 or n_recent outside [0, N_b]. */
+dge_status_t dge_select_streaming(const dge_geom_t *geom, int32_t n_sink, int32_t n_recent,
+                                  int32_t *idx, int32_t *n_kept, hipStream_t stream);
+
+/* Step 3 (Alg. 1 step C; app:dg notes: [retained past] || [window + draft tail]).
+ * For every (b, h), with C_b = N_b - n_tail and n_out = n_select + n_tail:
+ *   out[b][h][r] = K[h][off_b + idx[b][h][r]]        for r < n_kept[b]
+ *   out[b][h][r] = K[h][off_b + C_b + r - n_kept[b]] for n_kept[b] <= r < n_kept[b] + n_tail
+ *   out[b][h][r] = 0                                for the remaining rows up to n_out
+ * and the same for V.  Bit-exact copies of the stored elements.
+ *   idx, n_kept : dge_select_topb / dge_select_streaming output (n_kept[b] <= min(n_select, C_b),
+ *                 idx entries in [0, C_b)).
+ *   k_out, v_out: [batch][H_kv][n_out][d] outputs, same element type as K/V.
+ * Errors: DGE_ERR_INVALID for n_select < 0 or n_tail outside [0, N_b]. */
+dge_status_t dge_compact(const dge_geom_t *geom, const int32_t *idx, const int32_t *n_kept,
+                         int32_t n_select, int32_t n_tail, const void *k, const void *v,
+                         void *k_out, void *v_out, hipStream_t stream);
+
+/* H2O accumulated attention, kept running through the draft rows
+ * (tab:complexity, footnote a; app:dg notes on H2O's prompt-query buffer):
+ *   colsum[h][j] = (1/G) sum_{g in group h} sum_{p = j}^{N_b - 1} softmax_j(q_{g,p} . k_j / sqrt(d))
+ * over every cached row p of the sequence (all prompt rows and the k draft rows).
+ *   q_all  : [H_q][T][d] queries of every cached row (same element type as K).
+ *   lse    : NULL, or [H_q][T] float32 natural-log partition log sum_{j<=p} exp(q_p . k_j / sqrt(d))
+ *            supplied by the caller (e.g. from its attention forward); when NULL the
+ *            library computes it first into the workspace.
+ *   colsum : [H_kv][T] float32 output; each sequence's colsum sums to N_b.
+ *   ws     : dge_workspace_size(geom, DGE_OP_H2O) bytes when lse == NULL (else may be NULL).
+ * Only bfloat16 inputs are supported (DGE_ERR_UNSUPPORTED otherwise). */
+dge_status_t dge_h2o_colsum(const dge_geom_t *geom, const void *q_all, const void *k,
+                            const float *lse, float *colsum, void *ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* PyramidKV per-layer budgets (app:analysis), host only:
+ *   c = B - w;  max = 2c - floor(c/beta);  min = floor(c/beta);
+ *   steps = floor((max - min) / (n_layers - 1));  out_host[l] = max - l*steps + w.
+ * Errors: DGE_ERR_INVALID for B < w, n_layers < 1, beta < 1 or a NULL output. */
+dge_status_t dge_pyramid_budgets(int32_t B, int32_t w, int32_t n_layers, int32_t beta,
+                                 int32_t *out_host);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DGE_H_ */

@@ -1,0 +1,203 @@
+"""MI355X (gfx950) eviction step of Draft-Guided Eviction (arxiv 2609.33334).
+
+Thin Python binding over the C ABI of ``libdge.so`` (include/dge.h).  Functions
+here only marshal arguments: they take torch tensors that already live on the
+GPU, pass their device pointers and the current HIP stream to the library, and
+allocate outputs/workspaces with torch when the caller does not pass them.
+Every step of the path runs in the library's HIP kernels.
+
+Names follow the C ABI: ``score`` (dge_score), ``select_topb``,
+``select_streaming``, ``compact``, ``h2o_colsum``, ``pyramid_budgets``,
+``workspace_size``; ``evict_layer`` chains score -> select_topb -> compact.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+from . import _lib
+from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  # noqa: F401
+                   ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
+
+__all__ = ["Geometry", "score", "select_topb", "select_streaming", "compact", "h2o_colsum",
+           "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
+           "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def n_scoring_rows(window: int, k_draft: int, rows: int) -> int:
+    return {ROWS_WINDOW_DRAFT: window + k_draft, ROWS_DRAFT: k_draft, ROWS_WINDOW: window}[rows]
+
+
+@dataclass
+class Geometry:
+    """One layer's cache geometry (dge_geom_t) with the offsets kept alive.
+
+    ``kv_lens`` are the cached rows N_b = L_b + k of each sequence.  K and V are
+    [H_kv][sum N_b][head_dim] (``kv_head_stride`` elements between heads).
+    """
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    window: int
+    k_draft: int
+    kv_lens: Sequence[int]
+    dtype: int = DGE_BF16
+    kv_head_stride: Optional[int] = None
+    device: str = "cuda"
+
+    def __post_init__(self):
+        torch = _torch()
+        self.offsets_host = np.concatenate([[0], np.cumsum(np.asarray(self.kv_lens, np.int64))]).astype(np.int64)
+        self.offsets_dev = torch.tensor(self.offsets_host, dtype=torch.int64, device=self.device)
+        if self.kv_head_stride is None:
+            self.kv_head_stride = int(self.offsets_host[-1]) * self.head_dim
+        self._c = Geom(len(self.kv_lens), self.n_q_heads, self.n_kv_heads, self.head_dim,
+                       self.window, self.k_draft, self.offsets_dev.data_ptr(),
+                       self.offsets_host.ctypes.data, int(self.kv_head_stride), int(self.dtype))
+
+    @property
+    def batch(self) -> int:
+        return len(self.kv_lens)
+
+    @property
+    def total_rows(self) -> int:
+        return int(self.offsets_host[-1])
+
+    @property
+    def c(self) -> Geom:
+        return self._c
+
+    @property
+    def elt_dtype(self):
+        torch = _torch()
+        return torch.bfloat16 if self.dtype == DGE_BF16 else torch.float32
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def workspace_size(geom: Geometry, op: int) -> int:
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().dge_workspace_size(ctypes.byref(geom.c), op, ctypes.byref(n)),
+               "dge_workspace_size")
+    return int(n.value)
+
+
+def _workspace(geom: Geometry, op: int, ws):
+    torch = _torch()
+    if ws is None:
+        ws = torch.empty(workspace_size(geom, op), dtype=torch.uint8, device=geom.device)
+    return ws
+
+
+def score(geom: Geometry, rows: int, q, k, raw=None, ws=None, stream=None):
+    """dge_score: raw[h][j] for every cached key.  Returns raw [H_kv][T] float32."""
+    torch = _torch()
+    if raw is None:
+        raw = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=geom.device)
+    ws = _workspace(geom, OP_SCORE, ws)
+    _lib.check(_lib.lib().dge_score(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k), _ptr(raw),
+                                    _ptr(ws), ws.numel(), _stream(stream)), "dge_score")
+    return raw
+
+
+def select_topb(geom: Geometry, scores, pool_kernel: int, n_tail: int, n_select: int,
+                idx=None, n_kept=None, ws=None, stream=None):
+    """dge_select_topb: per-head top-n_select after max-pooling.  Returns (idx, n_kept)."""
+    torch = _torch()
+    if idx is None:
+        idx = torch.empty(geom.batch, geom.n_kv_heads, max(n_select, 0), dtype=torch.int32,
+                          device=geom.device)
+    if n_kept is None:
+        n_kept = torch.empty(max(geom.batch, 4), dtype=torch.int32, device=geom.device)
+    ws = _workspace(geom, OP_SELECT, ws)
+    _lib.check(_lib.lib().dge_select_topb(ctypes.byref(geom.c), _ptr(scores), pool_kernel, n_tail,
+                                          n_select, _ptr(idx), _ptr(n_kept), _ptr(ws), ws.numel(),
+                                          _stream(stream)), "dge_select_topb")
+    return idx, n_kept[:geom.batch]
+
+
+def select_streaming(geom: Geometry, n_sink: int, n_recent: int, idx=None, n_kept=None,
+                     stream=None):
+    """dge_select_streaming: StreamingLLM sinks.  Returns (idx, n_kept)."""
+    torch = _torch()
+    if idx is None:
+        idx = torch.empty(geom.batch, geom.n_kv_heads, max(n_sink, 1), dtype=torch.int32,
+                          device=geom.device)
+    if n_kept is None:
+        n_kept = torch.empty(max(geom.batch, 4), dtype=torch.int32, device=geom.device)
+    _lib.check(_lib.lib().dge_select_streaming(ctypes.byref(geom.c), n_sink, n_recent, _ptr(idx),
+                                               _ptr(n_kept), _stream(stream)),
+               "dge_select_streaming")
+    return idx[..., :n_sink], n_kept[:geom.batch]
+
+
+def compact(geom: Geometry, idx, n_kept, n_select: int, n_tail: int, k, v, k_out=None,
+            v_out=None, stream=None):
+    """dge_compact: [retained past] || [tail] per (b, h).  Returns (k_out, v_out)
+    shaped [batch][H_kv][n_select + n_tail][head_dim]."""
+    torch = _torch()
+    shape = (geom.batch, geom.n_kv_heads, n_select + n_tail, geom.head_dim)
+    if k_out is None:
+        k_out = torch.empty(shape, dtype=k.dtype, device=geom.device)
+    if v_out is None:
+        v_out = torch.empty(shape, dtype=v.dtype, device=geom.device)
+    _lib.check(_lib.lib().dge_compact(ctypes.byref(geom.c), _ptr(idx), _ptr(n_kept), n_select,
+                                      n_tail, _ptr(k), _ptr(v), _ptr(k_out), _ptr(v_out),
+                                      _stream(stream)), "dge_compact")
+    return k_out, v_out
+
+
+def h2o_colsum(geom: Geometry, q_all, k, lse=None, colsum=None, ws=None, stream=None):
+    """dge_h2o_colsum: H2O accumulated attention.  Returns colsum [H_kv][T] float32."""
+    torch = _torch()
+    if colsum is None:
+        colsum = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32,
+                             device=geom.device)
+    if lse is None:
+        ws = _workspace(geom, OP_H2O, ws)
+    nbytes = 0 if ws is None else ws.numel()
+    _lib.check(_lib.lib().dge_h2o_colsum(ctypes.byref(geom.c), _ptr(q_all), _ptr(k), _ptr(lse),
+                                         _ptr(colsum), _ptr(ws), nbytes, _stream(stream)),
+               "dge_h2o_colsum")
+    return colsum
+
+
+def pyramid_budgets(B: int, w: int, n_layers: int, beta: int = 20) -> list:
+    """dge_pyramid_budgets (host): PyramidKV per-layer total budgets B_l."""
+    out = (ctypes.c_int32 * max(n_layers, 1))()
+    _lib.check(_lib.lib().dge_pyramid_budgets(B, w, n_layers, beta, out), "dge_pyramid_budgets")
+    return list(out)[:n_layers]
+
+
+def evict_layer(geom: Geometry, q, k, v, budget: int, pool_kernel: int, rows: int = ROWS_WINDOW_DRAFT,
+                stream=None, ws_score=None, ws_select=None, out=None):
+    """score -> select_topb (B - w, tail w + k) -> compact for one layer.
+
+    Returns dict(raw, idx, n_kept, k, v).  ``out`` may hold preallocated tensors
+    under the same keys.
+    """
+    out = out or {}
+    n_tail = geom.window + geom.k_draft
+    n_select = budget - geom.window
+    raw = score(geom, rows, q, k, raw=out.get("raw"), ws=ws_score, stream=stream)
+    idx, n_kept = select_topb(geom, raw, pool_kernel, n_tail, n_select, idx=out.get("idx"),
+                              n_kept=out.get("n_kept"), ws=ws_select, stream=stream)
+    k_out, v_out = compact(geom, idx, n_kept, n_select, n_tail, k, v, k_out=out.get("k"),
+                           v_out=out.get("v"), stream=stream)
+    return dict(raw=raw, idx=idx, n_kept=n_kept, k=k_out, v=v_out)

@@ -1,0 +1,174 @@
+// C ABI of the eviction-step library: argument validation on the host, then
+// asynchronous launches on the caller's stream.  Nothing is launched when a
+// check fails.  See include/dge.h for the contract of every entry point.
+#include <cstddef>
+#include <cstdint>
+
+#include "dge.h"
+#include "dge_internal.hpp"
+
+using dge::ScorePlan;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+dge_status_t check_geom(const dge_geom_t* g) {
+  if (g == nullptr) return DGE_ERR_INVALID;
+  if (g->batch < 1 || g->n_kv_heads < 1 || g->n_q_heads < 1) return DGE_ERR_INVALID;
+  if (g->n_q_heads % g->n_kv_heads != 0) return DGE_ERR_INVALID;
+  if (g->n_q_heads / g->n_kv_heads > 64) return DGE_ERR_UNSUPPORTED;
+  if (g->window < 0 || g->k_draft < 0) return DGE_ERR_INVALID;
+  if (g->dtype != DGE_BF16 && g->dtype != DGE_F32) return DGE_ERR_INVALID;
+  if (g->head_dim != 64 && g->head_dim != 128) return DGE_ERR_UNSUPPORTED;
+  if (g->kv_offsets == nullptr || g->kv_offsets_host == nullptr) return DGE_ERR_INVALID;
+  if ((reinterpret_cast<uintptr_t>(g->kv_offsets) & 7u) != 0) return DGE_ERR_INVALID;
+  const int64_t* o = g->kv_offsets_host;
+  if (o[0] != 0) return DGE_ERR_INVALID;
+  for (int b = 0; b < g->batch; ++b) {
+    if (o[b + 1] < o[b]) return DGE_ERR_INVALID;
+    if (o[b + 1] - o[b] > (int64_t)INT32_MAX / 2) return DGE_ERR_UNSUPPORTED;
+  }
+  if (g->kv_head_stride < o[g->batch] * (int64_t)g->head_dim) return DGE_ERR_INVALID;
+  if ((g->kv_head_stride * (g->dtype == DGE_BF16 ? 2 : 4)) % 16 != 0) return DGE_ERR_INVALID;
+  return DGE_OK;
+}
+
+int64_t seq_rows(const dge_geom_t* g, int b) {
+  return g->kv_offsets_host[b + 1] - g->kv_offsets_host[b];
+}
+
+dge_status_t check_tail(const dge_geom_t* g, int32_t n_tail) {
+  if (n_tail < 0) return DGE_ERR_INVALID;
+  for (int b = 0; b < g->batch; ++b)
+    if (seq_rows(g, b) < n_tail) return DGE_ERR_INVALID;
+  return DGE_OK;
+}
+
+dge_status_t hip_status(hipError_t e) { return e == hipSuccess ? DGE_OK : DGE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int dge_abi_version(void) { return DGE_ABI_VERSION; }
+
+const char* dge_status_string(int status) {
+  switch (status) {
+    case DGE_OK: return "DGE_OK";
+    case DGE_ERR_INVALID: return "DGE_ERR_INVALID: argument violates the contract";
+    case DGE_ERR_UNSUPPORTED: return "DGE_ERR_UNSUPPORTED: valid request not implemented by this build";
+    case DGE_ERR_WORKSPACE: return "DGE_ERR_WORKSPACE: workspace missing or too small";
+    case DGE_ERR_HIP: return "DGE_ERR_HIP: HIP launch or runtime failure";
+    default: return "unknown dge status";
+  }
+}
+
+dge_status_t dge_workspace_size(const dge_geom_t* geom, int32_t op, size_t* bytes) {
+  if (bytes == nullptr) return DGE_ERR_INVALID;
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  switch (op) {
+    case DGE_OP_SCORE: {
+      // the largest scoring-row set (window + draft) bounds every mode
+      const ScorePlan p = dge::plan_score(*geom, DGE_ROWS_WINDOW_DRAFT);
+      size_t best = dge::score_workspace_bytes(*geom, p);
+      for (int m = 1; m <= 2; ++m) {
+        const size_t s = dge::score_workspace_bytes(*geom, dge::plan_score(*geom, m));
+        best = s > best ? s : best;
+      }
+      *bytes = best;
+      return DGE_OK;
+    }
+    case DGE_OP_SELECT: *bytes = dge::select_workspace_bytes(*geom); return DGE_OK;
+    case DGE_OP_H2O: *bytes = dge::h2o_workspace_bytes(*geom); return DGE_OK;
+    default: return DGE_ERR_INVALID;
+  }
+}
+
+dge_status_t dge_score(const dge_geom_t* geom, int32_t rows, const void* q, const void* k,
+                       float* raw, void* ws, size_t ws_bytes, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (rows < DGE_ROWS_WINDOW_DRAFT || rows > DGE_ROWS_WINDOW) return DGE_ERR_INVALID;
+  if (!q || !k || !raw || !aligned16(q) || !aligned16(k) || !aligned16(raw)) return DGE_ERR_INVALID;
+  for (int b = 0; b < geom->batch; ++b)
+    if (seq_rows(geom, b) < (int64_t)geom->window + geom->k_draft || seq_rows(geom, b) < 1)
+      return DGE_ERR_INVALID;
+  const ScorePlan p = dge::plan_score(*geom, rows);
+  if (p.n_rows <= 0) return DGE_ERR_INVALID;
+  if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::score_workspace_bytes(*geom, p))
+    return DGE_ERR_WORKSPACE;
+  return hip_status(dge::launch_score(*geom, p, q, k, raw, ws, stream));
+}
+
+dge_status_t dge_select_topb(const dge_geom_t* geom, const float* scores, int32_t pool_kernel,
+                             int32_t n_tail, int32_t n_select, int32_t* idx, int32_t* n_kept,
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (pool_kernel < 1 || (pool_kernel & 1) == 0) return DGE_ERR_INVALID;
+  if (n_select < 0) return DGE_ERR_INVALID;
+  if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
+  if (!scores || !n_kept || (n_select > 0 && !idx) || !aligned16(scores) || !aligned16(idx) ||
+      !aligned16(n_kept))
+    return DGE_ERR_INVALID;
+  if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::select_workspace_bytes(*geom))
+    return DGE_ERR_WORKSPACE;
+  return hip_status(
+      dge::launch_select_topb(*geom, scores, pool_kernel, n_tail, n_select, idx, n_kept, ws, stream));
+}
+
+dge_status_t dge_select_streaming(const dge_geom_t* geom, int32_t n_sink, int32_t n_recent,
+                                  int32_t* idx, int32_t* n_kept, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (n_sink < 0) return DGE_ERR_INVALID;
+  if ((st = check_tail(geom, n_recent)) != DGE_OK) return st;
+  if (!n_kept || !aligned16(n_kept) || (n_sink > 0 && (!idx || !aligned16(idx))))
+    return DGE_ERR_INVALID;
+  return hip_status(dge::launch_select_streaming(*geom, n_sink, n_recent, idx, n_kept, stream));
+}
+
+dge_status_t dge_compact(const dge_geom_t* geom, const int32_t* idx, const int32_t* n_kept,
+                         int32_t n_select, int32_t n_tail, const void* k, const void* v,
+                         void* k_out, void* v_out, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (n_select < 0) return DGE_ERR_INVALID;
+  if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
+  if (!n_kept || !k || !v || !k_out || !v_out || (n_select > 0 && !idx)) return DGE_ERR_INVALID;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out) ||
+      !aligned16(n_kept) || (idx && !aligned16(idx)))
+    return DGE_ERR_INVALID;
+  return hip_status(
+      dge::launch_compact(*geom, idx, n_kept, n_select, n_tail, k, v, k_out, v_out, stream));
+}
+
+dge_status_t dge_h2o_colsum(const dge_geom_t* geom, const void* q_all, const void* k,
+                            const float* lse, float* colsum, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (geom->dtype != DGE_BF16 || geom->head_dim != 128) return DGE_ERR_UNSUPPORTED;
+  if (!q_all || !k || !colsum || !aligned16(q_all) || !aligned16(k) || !aligned16(colsum) ||
+      (lse && !aligned16(lse)))
+    return DGE_ERR_INVALID;
+  if (lse == nullptr &&
+      (ws == nullptr || !aligned16(ws) || ws_bytes < dge::h2o_workspace_bytes(*geom)))
+    return DGE_ERR_WORKSPACE;
+  return hip_status(dge::launch_h2o(*geom, q_all, k, lse, colsum, ws, stream));
+}
+
+dge_status_t dge_pyramid_budgets(int32_t B, int32_t w, int32_t n_layers, int32_t beta,
+                                 int32_t* out_host) {
+  if (out_host == nullptr || n_layers < 1 || beta < 1 || w < 0 || B < w) return DGE_ERR_INVALID;
+  const int64_t c = (int64_t)B - w;
+  const int64_t top = 2 * c - c / beta;
+  const int64_t bottom = c / beta;
+  const int64_t steps = n_layers > 1 ? (top - bottom) / (n_layers - 1) : 0;
+  for (int l = 0; l < n_layers; ++l) out_host[l] = (int32_t)(top - l * steps + w);
+  return DGE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Device-side helpers shared by the gfx950 kernels of the eviction step.
+//
+// Matrix-core fragments.  Every QK^T product here runs on the 16x16 MFMA tiles of
+// CDNA4 with 64-lane wavefronts:
+//   bf16: v_mfma_f32_16x16x32_bf16  (A 16x32, B 32x16, one 16-byte chunk per lane)
+//   f32 : v_mfma_f32_16x16x4_f32    (four issues consume one 16-byte chunk per lane)
+// Lane l supplies row (l % 16) of A and column (l % 16) of B; lane group g = l / 16
+// supplies a contiguous run of the reduction dimension.  Because the same run is
+// loaded for A (query rows) and B (key rows), the pairing of reduction indices
+// inside the instruction never matters.  The accumulator tile is read as
+//   D[4*g + t][l % 16], t = 0..3,
+// i.e. a lane holds 4 query rows of one key column.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dge {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kWave = 64;
+
+// Storage tags: bf16 elements are moved as raw 16-bit patterns.
+struct bf16_t { uint16_t bits; };
+
+template <typename T> struct Elem;
+template <> struct Elem<bf16_t> { static constexpr int kBytes = 2; };
+template <> struct Elem<float> { static constexpr int kBytes = 4; };
+
+// Number of 16-byte chunk steps a wave needs to cover one row of D elements
+// (each step covers 64 bytes of the row: 16 bytes from each lane group).
+template <typename T, int D>
+struct RowChunks {
+  static constexpr int kElemsPerLane = 16 / Elem<T>::kBytes;   // per lane per step
+  static constexpr int kElemsPerStep = 4 * kElemsPerLane;       // per wave per step
+  static constexpr int kSteps = D / kElemsPerStep;
+};
+
+__device__ __forceinline__ uint4 load16(const void* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+
+__device__ __forceinline__ f32x4_t mma_step(bf16_t, uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4_t mma_step(float, uint4 a, uint4 b, f32x4_t c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  return c;
+}
+
+// Element offset, within a row, of the 16 bytes lane group g loads at chunk step s.
+template <typename T, int D>
+__device__ __forceinline__ int chunk_elem(int s, int g) {
+  return s * RowChunks<T, D>::kElemsPerStep + g * RowChunks<T, D>::kElemsPerLane;
+}
+
+// Online softmax statistics in the log2 domain: value m (running max) and
+// s = sum 2^(x - m).  One exp2 per element: the larger of (x, m) becomes the max.
+__device__ __forceinline__ void online_push(float x, float& m, float& s) {
+  const float dlt = x - m;              // m == -inf on the first push gives +inf
+  const float e = exp2f(-fabsf(dlt));
+  const bool up = dlt > 0.0f;
+  s = up ? fmaf(s, e, 1.0f) : s + e;
+  m = up ? x : m;
+}
+
+__device__ __forceinline__ void online_merge(float& m, float& s, float m2, float s2) {
+  const float mx = fmaxf(m, m2);
+  if (mx == -INFINITY) { m = mx; s = 0.0f; return; }
+  s = s * exp2f(m - mx) + s2 * exp2f(m2 - mx);
+  m = mx;
+}
+
+template <int kMask>
+__device__ __forceinline__ float shfl_xor_f(float v) {
+  return __shfl_xor(v, kMask, kWave);
+}
+
+}  // namespace dge

@@ -1,0 +1,48 @@
+// Host-side launch interface between the C ABI (api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dge.h"
+
+namespace dge {
+
+// How dge_score splits one layer over the GPU.  Derived from the geometry alone so
+// that dge_workspace_size and dge_score always agree.
+struct ScorePlan {
+  int n_rows;          // scoring rows per sequence
+  int p0_from_end;     // first scoring position = N_b - p0_from_end
+  int M;               // G * n_rows query rows per KV head and sequence
+  int M_pad;           // M rounded up to 16
+  int mt;              // 16-row tiles held in registers at once
+  int groups;          // row groups of mt tiles covering M_pad
+  int tiles_per_wave;  // 16-key tiles each wavefront scores
+  int chunk_keys;      // keys per workgroup (4 wavefronts)
+  int n_chunks;        // workgroups per (sequence, KV head)
+};
+
+int64_t total_rows(const dge_geom_t& g);
+int64_t max_seq_rows(const dge_geom_t& g);
+ScorePlan plan_score(const dge_geom_t& g, int rows_mode);
+size_t score_workspace_bytes(const dge_geom_t& g, const ScorePlan& p);
+
+hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, const void* k,
+                        float* raw, void* ws, hipStream_t stream);
+
+size_t select_workspace_bytes(const dge_geom_t& g);
+hipError_t launch_select_topb(const dge_geom_t& g, const float* scores, int pool_kernel,
+                              int n_tail, int n_select, int32_t* idx, int32_t* n_kept, void* ws,
+                              hipStream_t stream);
+hipError_t launch_select_streaming(const dge_geom_t& g, int n_sink, int n_recent, int32_t* idx,
+                                   int32_t* n_kept, hipStream_t stream);
+
+hipError_t launch_compact(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,
+                          int n_select, int n_tail, const void* k, const void* v, void* k_out,
+                          void* v_out, hipStream_t stream);
+
+size_t h2o_workspace_bytes(const dge_geom_t& g);
+hipError_t launch_h2o(const dge_geom_t& g, const void* q_all, const void* k, const float* lse,
+                      float* colsum, void* ws, hipStream_t stream);
+
+}  // namespace dge

@@ -1,0 +1,299 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Tolerances (written here, derived in the design notes):
+* scores: |gpu - oracle| <= 1e-3 * |oracle| + 1e-20 elementwise (bf16 inputs, fp32
+  products/softmax/accumulation; the absolute floor only covers entries that
+  underflow fp32);
+* selection in isolation (identical fp32 scores on both sides): bit-exact indices;
+* selection end to end: every candidate whose oracle pooled score exceeds the oracle's
+  B'-th value t by more than 1e-3 relative is kept, every one below t by more than
+  1e-3 is dropped, and the counts agree;
+* compaction: byte-exact given the GPU's own indices.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import dge_inputs as di
+import oracle
+import paper_2609_33334_amd as dge
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+RTOL, ATOL = 1e-3, 1e-20
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(bits, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(bits))
+    if dtype == "bf16":
+        t = t.view(torch.int16).view(torch.bfloat16)
+    return t.to(DEV)
+
+
+def geom_of(wl, **kw):
+    dt = dge.DGE_BF16 if wl.dtype == "bf16" else dge.DGE_F32
+    return dge.Geometry(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.window, wl.k_draft,
+                        wl.cached_lens, dtype=dt, device=DEV, **kw)
+
+
+def mode_rows(x, wl, mode):
+    """The scoring rows of a mode, packed per sequence (taken from the w+k block)."""
+    nr = wl.window + wl.k_draft
+    sl = {oracle.ROWS_WINDOW_DRAFT: slice(0, nr), oracle.ROWS_DRAFT: slice(wl.window, nr),
+          oracle.ROWS_WINDOW: slice(0, wl.window)}[mode]
+    def pick(a):
+        a = a.reshape(a.shape[0], wl.batch, nr, a.shape[-1])[:, :, sl]
+        return np.ascontiguousarray(a.reshape(a.shape[0], -1, a.shape[-1]))
+    return pick(x.q), pick(x.q_bits)
+
+
+def check_scores(got, want, what):
+    got = np.asarray(got, np.float64)
+    err = np.abs(got - want)
+    bad = err > RTOL * np.abs(want) + ATOL
+    worst = float((err / (np.abs(want) + ATOL)).max())
+    _log(f"  {what}: max rel err {worst:.2e}")
+    assert not bad.any(), f"{what}: {int(bad.sum())} scores out of tolerance (worst rel {worst:.3g})"
+
+
+def run_score(wl, x, mode=oracle.ROWS_WINDOW_DRAFT):
+    g = geom_of(wl)
+    q, qb = mode_rows(x, wl, mode)
+    raw = dge.score(g, mode, to_dev(qb, wl.dtype), to_dev(x.k_bits, wl.dtype))
+    torch.cuda.synchronize()
+    want = oracle.window_scores(q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                wl.k_draft, mode)
+    return raw.cpu().numpy(), want
+
+
+SCORE_CASES = {
+    "c1": di.WORKLOADS["c1"],
+    "c2_700": di.small_variant("c2", [700]),
+    "c2_ragged": di.small_variant("c2", [300, 517, 1029, 70]),
+    "f32_d128": di.small_variant("c2", [333], dtype="f32", plant="none"),
+    "bf16_d64": di.small_variant("c1", [400, 129], dtype="bf16"),
+    "big_M": di.small_variant("c2", [260], n_q_heads=64, window=64, k_draft=8, plant="none"),
+    "w0": di.small_variant("c2", [96], window=0, k_draft=3, plant="none"),
+}
+
+
+@pytest.mark.parametrize("case", list(SCORE_CASES))
+def test_score_parity(case):
+    wl = SCORE_CASES[case]
+    _log(f"score parity {case} lens={wl.prompt_lens}")
+    x = di.make_layer(wl)
+    got, want = run_score(wl, x)
+    check_scores(got, want, case)
+    # each sequence's scores sum to its number of scoring rows
+    for b in range(wl.batch):
+        s0, s1 = wl.kv_offsets[b], wl.kv_offsets[b + 1]
+        assert np.allclose(got[:, s0:s1].sum(1), wl.n_rows, rtol=1e-4)
+
+
+@pytest.mark.parametrize("mode", [oracle.ROWS_DRAFT, oracle.ROWS_WINDOW])
+def test_score_modes(mode):
+    wl = di.small_variant("c2", [450, 1100])
+    _log(f"score mode {mode}")
+    x = di.make_layer(wl)
+    got, want = run_score(wl, x, mode)
+    check_scores(got, want, f"mode{mode}")
+
+
+def test_score_full_c2():
+    wl = di.WORKLOADS["c2"]
+    _log("score parity c2 full")
+    x = di.make_layer(wl)
+    got, want = run_score(wl, x)
+    check_scores(got, want, "c2")
+
+
+def test_score_c3_layer():
+    wl = di.WORKLOADS["c3"]
+    _log("score parity c3 layer 5 (L=16384)")
+    x = di.make_layer(wl, layer=5, with_v=False)
+    got, want = run_score(wl, x)
+    check_scores(got, want, "c3/l5")
+
+
+def test_score_deterministic():
+    wl = di.small_variant("c2", [2000, 900])
+    x = di.make_layer(wl, with_v=False)
+    g = geom_of(wl)
+    q, k = to_dev(x.q_bits, wl.dtype), to_dev(x.k_bits, wl.dtype)
+    a = dge.score(g, 0, q, k).clone()
+    b = dge.score(g, 0, q, k)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+# ------------------------------------------------------------------------------------------
+# Selection
+# ------------------------------------------------------------------------------------------
+SELECT_CASES = [
+    # (lens, kind, pool, n_tail, n_select)
+    ((4098,), "continuous", 7, 34, 480),
+    ((4098,), "plateau", 7, 34, 480),
+    ((700, 1500, 33, 4000), "ints", 5, 10, 200),
+    ((700, 1500, 33, 4000), "plateau", 1, 10, 64),
+    ((1000,), "continuous", 3, 34, 5000),       # budget covers every candidate
+    ((1000,), "continuous", 7, 34, 0),          # budget equal to the window
+    ((50, 34), "continuous", 7, 34, 10),        # a sequence with no candidates
+    ((32770,), "plateau", 7, 34, 2016),         # largest per-sequence length of the c4 mix
+    ((9000,), "ints", 1, 512, 512),             # H2O-like split
+]
+
+
+@pytest.mark.parametrize("case", range(len(SELECT_CASES)))
+def test_select_isolated_bit_exact(case):
+    lens, kind, pool, n_tail, n_select = SELECT_CASES[case]
+    _log(f"select {lens} {kind} pool={pool} tail={n_tail} sel={n_select}")
+    H = 4
+    T = sum(lens)
+    scores = di.random_scores((H, T), seed=case, kind=kind)
+    g = dge.Geometry(8, H, 128, 0, 0, lens, device=DEV)
+    idx, nk = dge.select_topb(g, torch.from_numpy(scores).to(DEV), pool, n_tail, n_select)
+    torch.cuda.synchronize()
+    idx, nk = idx.cpu().numpy(), nk.cpu().numpy()
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    for b, N in enumerate(lens):
+        C = N - n_tail
+        assert nk[b] == min(n_select, C)
+        for h in range(H):
+            pooled = oracle.maxpool(scores[h, offs[b]:offs[b + 1]], C, pool)
+            want = oracle.select_topb(pooled, n_select)
+            got = idx[b, h]
+            assert np.array_equal(got[:len(want)], want), (b, h)
+            assert (got[len(want):] == -1).all()
+
+
+def test_select_end_to_end_c2():
+    wl = di.WORKLOADS["c2"]
+    _log("select end-to-end c2")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    out = dge.evict_layer(g, to_dev(x.q_bits, "bf16"), to_dev(x.k_bits, "bf16"),
+                          to_dev(x.v_bits, "bf16"), wl.budget, wl.pool)
+    torch.cuda.synchronize()
+    raw_ref, ref = oracle.evict_layer(x.q, x.k, x.v, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                      wl.window, wl.k_draft, wl.budget, wl.pool)
+    idx = out["idx"].cpu().numpy()
+    nsel = wl.budget - wl.window
+    for h in range(wl.n_kv_heads):
+        pooled = ref[(0, h)]["pooled"]
+        t = np.sort(pooled)[::-1][nsel - 1]
+        got = set(idx[0, h].tolist())
+        assert len(got) == nsel
+        must = set(np.nonzero(pooled > t * (1 + 1e-3))[0].tolist())
+        never = set(np.nonzero(pooled < t * (1 - 1e-3))[0].tolist())
+        assert must <= got and not (never & got), h
+        # planted spans are found
+        hits = np.isin(x.planted[(0, h)], idx[0, h]).mean()
+        assert hits > 0.5, hits
+
+
+def test_compact_bit_exact():
+    wl = di.small_variant("c2", [600, 1200, 40])
+    _log("compact bit-exact")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    k, v = to_dev(x.k_bits, "bf16"), to_dev(x.v_bits, "bf16")
+    out = dge.evict_layer(g, to_dev(x.q_bits, "bf16"), k, v, wl.budget, wl.pool)
+    torch.cuda.synchronize()
+    idx, nk = out["idx"].cpu().numpy(), out["n_kept"].cpu().numpy()
+    ko = out["k"].cpu().view(torch.int16).numpy()
+    vo = out["v"].cpu().view(torch.int16).numpy()
+    kb, vb = x.k_bits.view(np.int16), x.v_bits.view(np.int16)
+    n_tail = wl.window + wl.k_draft
+    n_out = wl.budget - wl.window + n_tail
+    assert ko.shape == (wl.batch, wl.n_kv_heads, n_out, wl.head_dim)
+    for b in range(wl.batch):
+        s0, N = wl.kv_offsets[b], wl.cached_lens[b]
+        C = N - n_tail
+        assert nk[b] == min(wl.budget - wl.window, C)
+        for h in range(wl.n_kv_heads):
+            rows = np.concatenate([idx[b, h, :nk[b]], np.arange(C, N)]) + s0
+            m = len(rows)
+            assert np.array_equal(ko[b, h, :m], kb[h, rows]) and np.array_equal(vo[b, h, :m], vb[h, rows])
+            assert (ko[b, h, m:] == 0).all() and (vo[b, h, m:] == 0).all()
+
+
+def test_compact_keep_all_is_identity():
+    wl = di.small_variant("c1", [60], budget=1000)
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    k, v = to_dev(x.k_bits, "f32"), to_dev(x.v_bits, "f32")
+    out = dge.evict_layer(g, to_dev(x.q_bits, "f32"), k, v, wl.budget, wl.pool)
+    torch.cuda.synchronize()
+    N = wl.cached_lens[0]
+    assert torch.equal(out["k"][0, :, :N].cpu(), k.cpu()) and torch.equal(out["v"][0, :, :N].cpu(), v.cpu())
+    assert out["idx"][0, :, :N - 10].cpu().numpy().tolist() == [list(range(N - 10))] * wl.n_kv_heads
+
+
+def test_streaming_closed_form():
+    wl = di.WORKLOADS["c5"]
+    _log("streaming c5 + ragged")
+    for lens in [wl.cached_lens, (1022, 1030, 3000, 1020)]:   # C_b = 2, 10, 1980, 0
+        g = dge.Geometry(32, 8, 128, 0, 2, lens, device=DEV)
+        idx, nk = dge.select_streaming(g, wl.slm_sinks, wl.slm_recent)
+        torch.cuda.synchronize()
+        for b, N in enumerate(lens):
+            want = oracle.streaming_select(N, wl.slm_sinks, wl.slm_recent)
+            assert nk[b].item() == len(want)
+            for h in range(8):
+                got = idx[b, h].cpu().numpy()
+                assert got[:len(want)].tolist() == want.tolist() and (got[len(want):] == -1).all()
+
+
+# ------------------------------------------------------------------------------------------
+# H2O accumulated attention
+# ------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("supply_lse", [False, True])
+def test_h2o_parity_small(supply_lse):
+    wl = di.small_variant("c5", [300, 77, 1000])
+    _log(f"h2o small supply_lse={supply_lse}")
+    x = di.make_layer(wl, with_v=False)
+    g = geom_of(wl)
+    lse = None
+    if supply_lse:
+        lse_ref = oracle.h2o_row_lse(x.q_all, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads)
+        lse = torch.from_numpy(lse_ref.astype(np.float32)).to(DEV)
+    col = dge.h2o_colsum(g, to_dev(x.q_all_bits, "bf16"), to_dev(x.k_bits, "bf16"), lse=lse)
+    torch.cuda.synchronize()
+    want = oracle.h2o_colsum(x.q_all, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads)
+    got = col.cpu().numpy()
+    check_scores(got, want, "h2o_small")
+    for b in range(wl.batch):
+        s0, s1 = wl.kv_offsets[b], wl.kv_offsets[b + 1]
+        assert np.allclose(got[:, s0:s1].sum(1), s1 - s0, rtol=1e-4)
+
+
+def test_h2o_c5_two_heads_and_select():
+    wl = di.WORKLOADS["c5"]
+    _log("h2o c5 full size, oracle on KV heads 0 and 5")
+    x = di.make_layer(wl, with_v=False)
+    g = geom_of(wl)
+    col = dge.h2o_colsum(g, to_dev(x.q_all_bits, "bf16"), to_dev(x.k_bits, "bf16"))
+    idx, nk = dge.select_topb(g, col, 1, wl.n_recent, wl.budget - wl.n_recent)
+    torch.cuda.synchronize()
+    got = col.cpu().numpy()
+    N = wl.cached_lens[0]
+    assert np.allclose(got.sum(1), N, rtol=1e-4)
+    G = wl.group
+    for h in (0, 5):
+        qs = x.q_all[h * G:(h + 1) * G]
+        want = oracle.h2o_colsum(qs, x.k[h:h + 1], wl.kv_offsets, G, 1)[0]
+        check_scores(got[h], want, f"h2o c5 head {h}")
+        ref_idx = oracle.h2o_select(want, wl.budget, wl.n_recent)
+        t = np.sort(want[:N - wl.n_recent])[::-1][len(ref_idx) - 1]
+        gi = set(idx[0, h].cpu().numpy().tolist())
+        assert len(gi) == wl.budget - wl.n_recent
+        must = set(np.nonzero(want[:N - wl.n_recent] > t * (1 + 1e-3))[0].tolist())
+        never = set(np.nonzero(want[:N - wl.n_recent] < t * (1 - 1e-3))[0].tolist())
+        assert must <= gi and not (never & gi)
