@@ -137,6 +137,17 @@ dge_status_t dge_select_topb(const dge_geom_t *geom, const float *scores, int32_
                              int32_t n_tail, int32_t n_select, int32_t *idx, int32_t *n_kept,
                              void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Steps 1b-3 in one call: dge_select_topb followed by dge_compact with the same
+ * n_tail and n_select (Alg. 1 steps B-C; app:dg notes).  Writes idx, n_kept, k_out
+ * and v_out exactly as the two separate calls would; the selection is repeated by
+ * several workgroups per KV head so that the row copies spread over the chip.
+ * Arguments, layouts and errors are those of the two calls; ws is the
+ * DGE_OP_SELECT workspace. */
+dge_status_t dge_select_compact(const dge_geom_t *geom, const float *scores, int32_t pool_kernel,
+                                int32_t n_tail, int32_t n_select, int32_t *idx, int32_t *n_kept,
+                                const void *k, const void *v, void *k_out, void *v_out, void *ws,
+                                size_t ws_bytes, hipStream_t stream);
+
 /* StreamingLLM retention (Sec. 6; app:analysis: four sinks and a recency window):
  * idx[b][h][0 .. n_kept[b]) = 0, 1, ..., n_kept[b]-1 with n_kept[b] = min(n_sink, N_b - n_recent);
  * remaining entries up to n_sink are -1.  The n_recent rows are the tail passed to

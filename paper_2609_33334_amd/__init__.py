@@ -22,7 +22,7 @@ from . import _lib
 from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  # noqa: F401
                    ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
 
-__all__ = ["Geometry", "score", "select_topb", "select_streaming", "compact", "h2o_colsum",
+__all__ = ["Geometry", "score", "select_topb", "select_compact", "select_streaming", "compact", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
 
@@ -132,6 +132,29 @@ def select_topb(geom: Geometry, scores, pool_kernel: int, n_tail: int, n_select:
     return idx, n_kept[:geom.batch]
 
 
+def select_compact(geom: Geometry, scores, pool_kernel: int, n_tail: int, n_select: int, k, v,
+                   idx=None, n_kept=None, k_out=None, v_out=None, ws=None, stream=None):
+    """dge_select_compact: select_topb and compact in one call.
+    Returns (idx, n_kept, k_out, v_out)."""
+    torch = _torch()
+    if idx is None:
+        idx = torch.empty(geom.batch, geom.n_kv_heads, max(n_select, 0), dtype=torch.int32,
+                          device=geom.device)
+    if n_kept is None:
+        n_kept = torch.empty(max(geom.batch, 4), dtype=torch.int32, device=geom.device)
+    shape = (geom.batch, geom.n_kv_heads, n_select + n_tail, geom.head_dim)
+    if k_out is None:
+        k_out = torch.empty(shape, dtype=k.dtype, device=geom.device)
+    if v_out is None:
+        v_out = torch.empty(shape, dtype=v.dtype, device=geom.device)
+    ws = _workspace(geom, OP_SELECT, ws)
+    _lib.check(_lib.lib().dge_select_compact(ctypes.byref(geom.c), _ptr(scores), pool_kernel,
+                                             n_tail, n_select, _ptr(idx), _ptr(n_kept), _ptr(k),
+                                             _ptr(v), _ptr(k_out), _ptr(v_out), _ptr(ws),
+                                             ws.numel(), _stream(stream)), "dge_select_compact")
+    return idx, n_kept[:geom.batch], k_out, v_out
+
+
 def select_streaming(geom: Geometry, n_sink: int, n_recent: int, idx=None, n_kept=None,
                      stream=None):
     """dge_select_streaming: StreamingLLM sinks.  Returns (idx, n_kept)."""
@@ -186,18 +209,25 @@ def pyramid_budgets(B: int, w: int, n_layers: int, beta: int = 20) -> list:
 
 
 def evict_layer(geom: Geometry, q, k, v, budget: int, pool_kernel: int, rows: int = ROWS_WINDOW_DRAFT,
-                stream=None, ws_score=None, ws_select=None, out=None):
-    """score -> select_topb (B - w, tail w + k) -> compact for one layer.
+                stream=None, ws_score=None, ws_select=None, out=None, fused: bool = True):
+    """score -> select (B - w, tail w + k) -> compact for one layer.
 
-    Returns dict(raw, idx, n_kept, k, v).  ``out`` may hold preallocated tensors
-    under the same keys.
+    ``fused`` runs selection and compaction as dge_select_compact, otherwise as
+    dge_select_topb then dge_compact.  Returns dict(raw, idx, n_kept, k, v); ``out``
+    may hold preallocated tensors under the same keys.
     """
     out = out or {}
     n_tail = geom.window + geom.k_draft
     n_select = budget - geom.window
     raw = score(geom, rows, q, k, raw=out.get("raw"), ws=ws_score, stream=stream)
-    idx, n_kept = select_topb(geom, raw, pool_kernel, n_tail, n_select, idx=out.get("idx"),
-                              n_kept=out.get("n_kept"), ws=ws_select, stream=stream)
-    k_out, v_out = compact(geom, idx, n_kept, n_select, n_tail, k, v, k_out=out.get("k"),
-                           v_out=out.get("v"), stream=stream)
+    if fused:
+        idx, n_kept, k_out, v_out = select_compact(
+            geom, raw, pool_kernel, n_tail, n_select, k, v, idx=out.get("idx"),
+            n_kept=out.get("n_kept"), k_out=out.get("k"), v_out=out.get("v"), ws=ws_select,
+            stream=stream)
+    else:
+        idx, n_kept = select_topb(geom, raw, pool_kernel, n_tail, n_select, idx=out.get("idx"),
+                                  n_kept=out.get("n_kept"), ws=ws_select, stream=stream)
+        k_out, v_out = compact(geom, idx, n_kept, n_select, n_tail, k, v, k_out=out.get("k"),
+                               v_out=out.get("v"), stream=stream)
     return dict(raw=raw, idx=idx, n_kept=n_kept, k=k_out, v=v_out)

@@ -119,6 +119,27 @@ dge_status_t dge_select_topb(const dge_geom_t* geom, const float* scores, int32_
       dge::launch_select_topb(*geom, scores, pool_kernel, n_tail, n_select, idx, n_kept, ws, stream));
 }
 
+dge_status_t dge_select_compact(const dge_geom_t* geom, const float* scores, int32_t pool_kernel,
+                                int32_t n_tail, int32_t n_select, int32_t* idx, int32_t* n_kept,
+                                const void* k, const void* v, void* k_out, void* v_out, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (pool_kernel < 1 || (pool_kernel & 1) == 0) return DGE_ERR_INVALID;
+  if (n_select < 0) return DGE_ERR_INVALID;
+  if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
+  if (!scores || !n_kept || (n_select > 0 && !idx) || !aligned16(scores) || !aligned16(idx) ||
+      !aligned16(n_kept))
+    return DGE_ERR_INVALID;
+  if (!k || !v || !k_out || !v_out || !aligned16(k) || !aligned16(v) || !aligned16(k_out) ||
+      !aligned16(v_out))
+    return DGE_ERR_INVALID;
+  if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::select_workspace_bytes(*geom))
+    return DGE_ERR_WORKSPACE;
+  return hip_status(dge::launch_select_compact(*geom, scores, pool_kernel, n_tail, n_select, idx,
+                                               n_kept, k, v, k_out, v_out, ws, stream));
+}
+
 dge_status_t dge_select_streaming(const dge_geom_t* geom, int32_t n_sink, int32_t n_recent,
                                   int32_t* idx, int32_t* n_kept, hipStream_t stream) {
   dge_status_t st = check_geom(geom);

@@ -84,4 +84,14 @@ __device__ __forceinline__ float shfl_xor_f(float v) {
   return __shfl_xor(v, kMask, kWave);
 }
 
+// 2^x on the transcendental unit (v_exp_f32); results below 2^-126 may flush to 0,
+// far below anything a softmax score resolves.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Rescale factor 2^(m - mx) for merging a (max, sum) pair into a larger max mx,
+// well defined when both are -inf (empty partial).
+__device__ __forceinline__ float rescale(float m, float mx) {
+  return m == mx ? 1.0f : fast_exp2(m - mx);
+}
+
 }  // namespace dge

@@ -15,9 +15,10 @@ struct ScorePlan {
   int p0_from_end;     // first scoring position = N_b - p0_from_end
   int M;               // G * n_rows query rows per KV head and sequence
   int M_pad;           // M rounded up to 16
-  int mt;              // 16-row tiles held in registers at once
-  int groups;          // row groups of mt tiles covering M_pad
-  int tiles_per_wave;  // 16-key tiles each wavefront scores
+  int n_tiles;         // 16-row tiles (M_pad / 16)
+  int mt;              // row tiles each wavefront holds in registers at once
+  int groups;          // row groups of 4 * mt tiles covering all tiles
+  int tiles_per_wave;  // 64-key iterations per workgroup
   int chunk_keys;      // keys per workgroup (4 wavefronts)
   int n_chunks;        // workgroups per (sequence, KV head)
 };
@@ -34,6 +35,10 @@ size_t select_workspace_bytes(const dge_geom_t& g);
 hipError_t launch_select_topb(const dge_geom_t& g, const float* scores, int pool_kernel,
                               int n_tail, int n_select, int32_t* idx, int32_t* n_kept, void* ws,
                               hipStream_t stream);
+hipError_t launch_select_compact(const dge_geom_t& g, const float* scores, int pool_kernel,
+                                 int n_tail, int n_select, int32_t* idx, int32_t* n_kept,
+                                 const void* k, const void* v, void* k_out, void* v_out, void* ws,
+                                 hipStream_t stream);
 hipError_t launch_select_streaming(const dge_geom_t& g, int n_sink, int n_recent, int32_t* idx,
                                    int32_t* n_kept, hipStream_t stream);
 

@@ -1,29 +1,40 @@
 // Window / draft scoring of every cached key (Alg. 1 step B; app:diagnostics).
 //
 //   raw[h][j] = (1/G) sum_{g in group h} sum_r softmax_j(q_{g,r} . k_j / sqrt(d)),
-//   softmax over keys j <= p_r (causal), fp32 throughout after the bf16/fp32 product.
+//   softmax over keys j <= p_r (causal), fp32 after the bf16/fp32 product.
 //
-// The column sums need every scoring row's global normaliser before any column can
-// be summed, so a layer runs as three launches over the same split of the keys:
-//   1. stats : each workgroup streams its chunk of K, forms the logits of all G*n_rows
-//              query rows on the matrix cores and keeps an online (max, sum) per row;
-//   2. reduce: one small workgroup per (sequence, KV head) merges the chunk partials
-//              into c_r = log2 Z_r (log2 domain, max folded in);
-//   3. colsum: each workgroup streams its chunk again, P = 2^(x - c_r), sums over the
-//              rows of the group and writes raw[] for its keys.
-// The second pass re-reads K; a layer's K slab (8-34 MB at Llama-3-8B geometry)
-// stays in the 256 MB Infinity Cache between the two passes.
+// A column sum needs every scoring row's global normaliser first, so one layer runs
+// as three launches over the same split of the keys into chunks:
+//   1. stats : each workgroup streams its chunk of K and keeps, per query row, the
+//              running (max, sum of 2^(x - max)) of its logits (log2 domain);
+//   2. reduce: one wavefront per (row, sequence, KV head) merges the chunk partials
+//              into c_r = log2 Z_r;
+//   3. colsum: each workgroup streams its chunk again, P = 2^(x - c_r), sums over all
+//              rows of the group and writes raw[] (the K slab of one layer, 8-34 MB at
+//              Llama-3-8B geometry, is still in the 256 MB Infinity Cache).
 //
-// Work split: a workgroup is 4 wavefronts; each wavefront owns 16-key tiles and ALL
-// query rows of the group, so a key tile is loaded exactly once per pass, straight
-// from HBM into matrix-core B fragments (16-byte loads per lane), and the column sum
-// over rows stays inside the wavefront.  Query fragments (the A operand) stay in
-// registers for the whole chunk.
+// Work split inside a workgroup (4 wavefronts, one KV head, one chunk of keys):
+// - The G * n_rows query rows form 16-row tiles; wavefront w owns tiles w, w+4, w+8...
+//   Its query fragments stay in registers for the whole chunk (<= 48 VGPRs at
+//   Llama-3-8B geometry), so several workgroups fit on a compute unit.
+// - Each 64-key tile of K is read from HBM once per workgroup with 16-byte loads, one
+//   coalesced row per 16 threads, and staged in LDS with the 16-byte units of row r
+//   XOR-swizzled by r: the 16 lanes that read one fragment column hit 16 different
+//   bank groups.  The next tile's global loads are in flight while the current tile
+//   is on the matrix cores.
+// - stats uses the transposed product (A = keys, B = query rows): a lane then holds
+//   4 keys of ONE row, so the per-row max/sum is mostly in-lane and needs two
+//   cross-lane steps per row tile at the end of the chunk.
+// - colsum uses A = query rows, B = keys: a lane holds 4 rows of ONE key, the sum
+//   over rows is in-lane, then across the 4 lane groups and the 4 wavefronts.
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
 
 namespace dge {
 namespace {
+
+constexpr int KT = 64;          // keys per workgroup iteration
+constexpr int kThreads = 256;
 
 struct ScoreArgs {
   const void* q;
@@ -36,19 +47,64 @@ struct ScoreArgs {
   int64_t q_head_stride;    // elements between query heads = batch * n_rows * D
   int64_t total_rows;       // T
   int n_kv_heads, G, n_rows, p0_from_end;
-  int M, M_pad, groups, tiles_per_wave, chunk_keys, n_chunks;
+  int M, M_pad, n_tiles, groups, iters, chunk_keys, n_chunks;
   float scale_log2;         // log2(e) / sqrt(d)
   float inv_G;
 };
 
-template <typename T, int D, int MT>
-__device__ __forceinline__ void load_q_frags(const ScoreArgs& a, int h, int b, int grp, int c16,
-                                             int g16, uint4 (&qf)[MT][RowChunks<T, D>::kSteps]) {
+template <typename T, int D>
+struct KTile {
+  static constexpr int kRowBytes = D * Elem<T>::kBytes;
+  static constexpr int kUnits = kRowBytes / 16;                // 16-byte units per row
+  static constexpr int kPerThread = KT * kUnits / kThreads;    // units each thread stages
+  static constexpr int kBytes = KT * kRowBytes;
+};
+
+// Issue the global loads of one 64-key tile (rows past the sequence are clamped to
+// its last row; their logits are masked later).
+template <typename T, int D>
+__device__ __forceinline__ void ktile_load(const char* kb, int j0, int N, int tid,
+                                           uint4 (&st)[KTile<T, D>::kPerThread]) {
+  using KTl = KTile<T, D>;
+#pragma unroll
+  for (int i = 0; i < KTl::kPerThread; ++i) {
+    const int e = tid + kThreads * i;
+    const int r = e / KTl::kUnits, u = e % KTl::kUnits;
+    const int j = min(j0 + r, N - 1);
+    st[i] = load16(kb + (int64_t)j * KTl::kRowBytes + u * 16);
+  }
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void ktile_store(char* lds, int tid,
+                                            const uint4 (&st)[KTile<T, D>::kPerThread]) {
+  using KTl = KTile<T, D>;
+#pragma unroll
+  for (int i = 0; i < KTl::kPerThread; ++i) {
+    const int e = tid + kThreads * i;
+    const int r = e / KTl::kUnits, u = e % KTl::kUnits;
+    *reinterpret_cast<uint4*>(lds + r * KTl::kRowBytes + ((u ^ (r % KTl::kUnits)) * 16)) = st[i];
+  }
+}
+
+// Fragment of key row r (0..63 within the tile) for chunk step s and lane group g16.
+template <typename T, int D>
+__device__ __forceinline__ uint4 ktile_frag(const char* lds, int r, int s, int g16) {
+  using KTl = KTile<T, D>;
+  const int u = s * 4 + g16;
+  return *reinterpret_cast<const uint4*>(lds + r * KTl::kRowBytes + ((u ^ (r % KTl::kUnits)) * 16));
+}
+
+// Query fragments of the row tiles owned by wavefront wv in row group grp.
+template <typename T, int D, int MTW>
+__device__ __forceinline__ void load_q_frags(const ScoreArgs& a, int h, int b, int tile0, int wv,
+                                             int c16, int g16,
+                                             uint4 (&qf)[MTW][RowChunks<T, D>::kSteps]) {
   constexpr int NS = RowChunks<T, D>::kSteps;
   const T* qb = reinterpret_cast<const T*>(a.q);
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = (grp * MT + mt) * 16 + c16;   // A operand: lane supplies row l % 16
+  for (int mt = 0; mt < MTW; ++mt) {
+    const int m = (tile0 + wv + 4 * mt) * 16 + c16;   // lane supplies row l % 16
     if (m < a.M) {
       const int g = m / a.n_rows;
       const int r = m - g * a.n_rows;
@@ -62,178 +118,216 @@ __device__ __forceinline__ void load_q_frags(const ScoreArgs& a, int h, int b, i
   }
 }
 
-template <typename T, int D, int MT>
-__global__ __launch_bounds__(256) void score_stats_kernel(ScoreArgs a) {
+template <typename T, int D, int MTW>
+__global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
+  using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
   const int c0 = chunk * a.chunk_keys;
   if (c0 >= N) return;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g16 = lane >> 4, c16 = lane & 15;
   const int p0 = N - a.p0_from_end;
-  const T* kb = reinterpret_cast<const T*>(a.k) + (int64_t)h * a.kv_head_stride + s0 * D;
-
-  __shared__ float2 red[4][MT * 16];
+  const int c1 = min(N, c0 + a.chunk_keys);
+  const char* kb = reinterpret_cast<const char*>(a.k) +
+                   ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
+  __shared__ __attribute__((aligned(16))) char lds[KTl::kBytes];
 
   for (int grp = 0; grp < a.groups; ++grp) {
-    uint4 qf[MT][NS];
-    load_q_frags<T, D, MT>(a, h, b, grp, c16, g16, qf);
-    float mrow[MT][4], srow[MT][4];
+    const int tile0 = grp * 4 * MTW;
+    uint4 qf[MTW][NS];
+    load_q_frags<T, D, MTW>(a, h, b, tile0, wv, c16, g16, qf);
+    // this lane's row in each owned tile, and that row's position
+    int pos[MTW];
+    bool live[MTW];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MTW; ++mt) {
+      const int m = (tile0 + wv + 4 * mt) * 16 + c16;
+      live[mt] = m < a.M;
+      pos[mt] = p0 + (live[mt] ? m % a.n_rows : 0);
+    }
+    float mrow[MTW], srow[MTW];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) { mrow[mt][i] = -INFINITY; srow[mt][i] = 0.0f; }
+    for (int mt = 0; mt < MTW; ++mt) { mrow[mt] = -INFINITY; srow[mt] = 0.0f; }
 
-    for (int t = 0; t < a.tiles_per_wave; ++t) {
-      const int j0 = c0 + 16 * (wv + 4 * t);
-      if (j0 >= N) break;
-      const int j = j0 + c16;
-      const T* krow = kb + (int64_t)min(j, N - 1) * D;
-      uint4 kf[NS];
+    uint4 st[KTl::kPerThread];
+    ktile_load<T, D>(kb, c0, N, tid, st);
+    for (int j0 = c0; j0 < c1; j0 += KT) {
+      __syncthreads();
+      ktile_store<T, D>(lds, tid, st);
+      __syncthreads();
+      if (j0 + KT < c1) ktile_load<T, D>(kb, j0 + KT, N, tid, st);
+      // no key of this tile is past the sequence or beyond any row's position
+      const bool need_mask = (j0 + KT - 1 > p0);
 #pragma unroll
-      for (int s = 0; s < NS; ++s) kf[s] = load16(krow + chunk_elem<T, D>(s, g16));
-      // keys of this tile that some row cannot see, or that lie past the sequence
-      const bool need_mask = (j0 + 15 > p0);
+      for (int sub = 0; sub < KT / 16; ++sub) {
+        uint4 kf[NS];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
 #pragma unroll
-        for (int s = 0; s < NS; ++s) acc = mma_step(T{}, qf[mt][s], kf[s], acc);
+        for (int mt = 0; mt < MTW; ++mt) {
+          if (tile0 + wv + 4 * mt >= a.n_tiles) continue;   // wave-uniform
+          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float x = acc[i] * a.scale_log2;
-          if (!need_mask) {
-            online_push(x, mrow[mt][i], srow[mt][i]);
-          } else {
-            const int m = (grp * MT + mt) * 16 + 4 * g16 + i;
-            const int pos = p0 + (m < a.M ? m % a.n_rows : 0);
-            if (m < a.M && j < N && j <= pos) online_push(x, mrow[mt][i], srow[mt][i]);
+          for (int s = 0; s < NS; ++s) acc = mma_step(T{}, kf[s], qf[mt][s], acc);
+          // acc[t] = logit of key j0 + sub*16 + 4*g16 + t for this lane's row
+          float x[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            x[t] = acc[t] * a.scale_log2;
+            if (need_mask) {
+              const int j = j0 + sub * 16 + 4 * g16 + t;
+              x[t] = (live[mt] && j < N && j <= pos[mt]) ? x[t] : -INFINITY;
+            }
           }
+          const float mx = fmaxf(fmaxf(mrow[mt], fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
+          const float base = mx == -INFINITY ? 0.0f : mx;
+          srow[mt] = srow[mt] * fast_exp2(mrow[mt] - base) + fast_exp2(x[0] - base) +
+                     fast_exp2(x[1] - base) + fast_exp2(x[2] - base) + fast_exp2(x[3] - base);
+          mrow[mt] = mx;
         }
       }
     }
-    // merge the 16 lanes that hold the same rows (different key columns)
+    // merge the four lane groups that hold the same row
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float m = mrow[mt][i], s = srow[mt][i];
-        online_merge(m, s, shfl_xor_f<1>(m), shfl_xor_f<1>(s));
-        online_merge(m, s, shfl_xor_f<2>(m), shfl_xor_f<2>(s));
-        online_merge(m, s, shfl_xor_f<4>(m), shfl_xor_f<4>(s));
-        online_merge(m, s, shfl_xor_f<8>(m), shfl_xor_f<8>(s));
-        if (c16 == 0) red[wv][mt * 16 + 4 * g16 + i] = make_float2(m, s);
-      }
-    __syncthreads();
-    for (int r = threadIdx.x; r < MT * 16; r += blockDim.x) {
-      const int m = grp * MT * 16 + r;
-      if (m < a.M) {
-        float mm = red[0][r].x, ss = red[0][r].y;
-        for (int w = 1; w < 4; ++w) online_merge(mm, ss, red[w][r].x, red[w][r].y);
-        a.partial[((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad + m] =
-            make_float2(mm, ss);
-      }
+    for (int mt = 0; mt < MTW; ++mt) {
+      if (tile0 + wv + 4 * mt >= a.n_tiles) continue;
+      float m = mrow[mt], s = srow[mt];
+      const float mx = fmaxf(fmaxf(m, shfl_xor_f<16>(m)), fmaxf(shfl_xor_f<32>(m), shfl_xor_f<48>(m)));
+      s *= rescale(m, mx);
+      s += shfl_xor_f<16>(s);
+      s += shfl_xor_f<32>(s);
+      const int row = (tile0 + wv + 4 * mt) * 16 + c16;
+      if (g16 == 0 && row < a.M)
+        a.partial[((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad + row] =
+            make_float2(mx, s);
     }
-    __syncthreads();
   }
 }
 
+// One wavefront per query row: merge that row's chunk partials.
 __global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
-  const int h = blockIdx.x, b = blockIdx.y;
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int h = blockIdx.y, b = blockIdx.z;
+  if (m >= a.M_pad) return;
+  const int64_t base = (int64_t)(b * a.n_kv_heads + h);
+  if (m >= a.M) {   // padding rows: 2^(x - inf) = 0
+    if (lane == 0) a.rowc[base * a.M_pad + m] = INFINITY;
+    return;
+  }
   const int N = (int)(a.offs[b + 1] - a.offs[b]);
   const int nch = (N + a.chunk_keys - 1) / a.chunk_keys;
-  const int64_t base = (int64_t)(b * a.n_kv_heads + h);
-  for (int m = threadIdx.x; m < a.M_pad; m += blockDim.x) {
-    float out = INFINITY;   // padded rows: 2^(x - inf) = 0
-    if (m < a.M) {
-      float mm = -INFINITY, ss = 0.0f;
-      for (int ch = 0; ch < nch; ++ch) {
-        const float2 p = a.partial[(base * a.n_chunks + ch) * a.M_pad + m];
-        online_merge(mm, ss, p.x, p.y);
-      }
-      out = mm + log2f(ss);
-    }
-    a.rowc[base * a.M_pad + m] = out;
+  float mm = -INFINITY, ss = 0.0f;
+  for (int ch = lane; ch < nch; ch += 64) {
+    const float2 p = a.partial[(base * a.n_chunks + ch) * a.M_pad + m];
+    const float mx = fmaxf(mm, p.x);
+    ss = ss * rescale(mm, mx) + p.y * rescale(p.x, mx);
+    mm = mx;
   }
+  float mx = mm;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  ss *= rescale(mm, mx);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) ss += __shfl_xor(ss, o, 64);
+  if (lane == 0) a.rowc[base * a.M_pad + m] = mx + __log2f(ss);
 }
 
-template <typename T, int D, int MT>
-__global__ __launch_bounds__(256) void score_colsum_kernel(ScoreArgs a) {
+template <typename T, int D, int MTW>
+__global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
+  using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
   const int c0 = chunk * a.chunk_keys;
   if (c0 >= N) return;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g16 = lane >> 4, c16 = lane & 15;
   const int p0 = N - a.p0_from_end;
-  const T* kb = reinterpret_cast<const T*>(a.k) + (int64_t)h * a.kv_head_stride + s0 * D;
+  const int c1 = min(N, c0 + a.chunk_keys);
+  const char* kb = reinterpret_cast<const char*>(a.k) +
+                   ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
   const float* rowc = a.rowc + (int64_t)(b * a.n_kv_heads + h) * a.M_pad;
+  float* out = a.raw + (int64_t)h * a.total_rows + s0;
+  __shared__ __attribute__((aligned(16))) char lds[KTl::kBytes];
+  __shared__ float red[4][KT];
 
-  uint4 qf[MT][NS];
-  float cr[MT][4];
-  int loaded = -1;
-  for (int t = 0; t < a.tiles_per_wave; ++t) {
-    const int j0 = c0 + 16 * (wv + 4 * t);
-    if (j0 >= N) break;
-    const int j = j0 + c16;
-    const T* krow = kb + (int64_t)min(j, N - 1) * D;
-    uint4 kf[NS];
+  for (int grp = 0; grp < a.groups; ++grp) {
+    const int tile0 = grp * 4 * MTW;
+    uint4 qf[MTW][NS];
+    load_q_frags<T, D, MTW>(a, h, b, tile0, wv, c16, g16, qf);
+    // normalisers and positions of this lane's 4 rows in each owned tile
+    float cr[MTW][4];
+    int pos[MTW][4];
 #pragma unroll
-    for (int s = 0; s < NS; ++s) kf[s] = load16(krow + chunk_elem<T, D>(s, g16));
-    const bool need_mask = (j0 + 15 > p0);
-    float colp = 0.0f;
-    for (int grp = 0; grp < a.groups; ++grp) {
-      if (grp != loaded) {
-        load_q_frags<T, D, MT>(a, h, b, grp, c16, g16, qf);
+    for (int mt = 0; mt < MTW; ++mt)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int m = (grp * MT + mt) * 16 + 4 * g16 + i;
-            cr[mt][i] = m < a.M ? rowc[m] : INFINITY;   // padding rows contribute 2^-inf = 0
-          }
-        loaded = grp;
+      for (int t = 0; t < 4; ++t) {
+        const int m = (tile0 + wv + 4 * mt) * 16 + 4 * g16 + t;
+        cr[mt][t] = m < a.M ? rowc[m] : INFINITY;
+        pos[mt][t] = p0 + (m < a.M ? m % a.n_rows : 0);
       }
+
+    uint4 st[KTl::kPerThread];
+    ktile_load<T, D>(kb, c0, N, tid, st);
+    for (int j0 = c0; j0 < c1; j0 += KT) {
+      __syncthreads();
+      ktile_store<T, D>(lds, tid, st);
+      __syncthreads();
+      if (j0 + KT < c1) ktile_load<T, D>(kb, j0 + KT, N, tid, st);
+      const bool need_mask = (j0 + KT - 1 > p0);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      for (int sub = 0; sub < KT / 16; ++sub) {
+        uint4 kf[NS];
 #pragma unroll
-        for (int s = 0; s < NS; ++s) acc = mma_step(T{}, qf[mt][s], kf[s], acc);
+        for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
+        const int j = j0 + sub * 16 + c16;
+        float colp = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float p = exp2f(fmaf(acc[i], a.scale_log2, -cr[mt][i]));
-          if (need_mask) {
-            const int m = (grp * MT + mt) * 16 + 4 * g16 + i;
-            const int pos = p0 + (m < a.M ? m % a.n_rows : 0);
-            p = (m < a.M && j < N && j <= pos) ? p : 0.0f;
+        for (int mt = 0; mt < MTW; ++mt) {
+          if (tile0 + wv + 4 * mt >= a.n_tiles) continue;   // wave-uniform
+          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < NS; ++s) acc = mma_step(T{}, qf[mt][s], kf[s], acc);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            float p = fast_exp2(fmaf(acc[t], a.scale_log2, -cr[mt][t]));
+            if (need_mask) p = (j < N && j <= pos[mt][t]) ? p : 0.0f;
+            colp += p;
           }
-          colp += p;
         }
+        colp += shfl_xor_f<16>(colp);
+        colp += shfl_xor_f<32>(colp);
+        if (g16 == 0) red[wv][sub * 16 + c16] = colp;
+      }
+      __syncthreads();
+      if (tid < KT && j0 + tid < c1) {
+        const float v = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
+        if (grp == 0) out[j0 + tid] = v * a.inv_G;
+        else out[j0 + tid] += v * a.inv_G;
       }
     }
-    // rows of a key column are spread over the 4 lane groups
-    colp += shfl_xor_f<16>(colp);
-    colp += shfl_xor_f<32>(colp);
-    if (g16 == 0 && j < N) a.raw[(int64_t)h * a.total_rows + s0 + j] = colp * a.inv_G;
+    __syncthreads();
   }
 }
 
-template <typename T, int D, int MT>
+template <typename T, int D, int MTW>
 hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st) {
   dim3 grid(a.n_chunks, g.n_kv_heads, g.batch);
-  hipLaunchKernelGGL((score_stats_kernel<T, D, MT>), grid, dim3(256), 0, st, a);
-  hipLaunchKernelGGL(score_reduce_kernel, dim3(g.n_kv_heads, g.batch), dim3(256), 0, st, a);
-  hipLaunchKernelGGL((score_colsum_kernel<T, D, MT>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((score_stats_kernel<T, D, MTW>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL(score_reduce_kernel, dim3(a.M_pad / 4, g.n_kv_heads, g.batch), dim3(256), 0,
+                     st, a);
+  hipLaunchKernelGGL((score_colsum_kernel<T, D, MTW>), grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t launch_mt(const ScoreArgs& a, const dge_geom_t& g, int mt, hipStream_t st) {
-  switch (mt) {
+hipError_t launch_mt(const ScoreArgs& a, const dge_geom_t& g, int mtw, hipStream_t st) {
+  switch (mtw) {
     case 1: return launch_typed<T, D, 1>(a, g, st);
     case 2: return launch_typed<T, D, 2>(a, g, st);
     case 3: return launch_typed<T, D, 3>(a, g, st);
@@ -247,10 +341,10 @@ hipError_t launch_mt(const ScoreArgs& a, const dge_geom_t& g, int mt, hipStream_
   }
 }
 
-// Register budget for query fragments: mt * steps <= 36 sixteen-byte chunks per lane.
-int max_mt(const dge_geom_t& g) {
+// Register budget for query fragments: tiles-per-wavefront * steps <= 36 16-byte chunks.
+int max_mtw(const dge_geom_t& g) {
   const int steps = g.head_dim * (g.dtype == DGE_BF16 ? 2 : 4) / 64;
-  int m = 36 / steps;
+  const int m = 36 / steps;
   return m > 9 ? 9 : m;
 }
 
@@ -277,17 +371,19 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
   const int G = g.n_q_heads / g.n_kv_heads;
   p.M = G * p.n_rows;
   p.M_pad = (p.M + 15) / 16 * 16;
-  const int tiles = p.M_pad / 16;
-  const int mtmax = max_mt(g);
-  p.groups = tiles == 0 ? 1 : (tiles + mtmax - 1) / mtmax;
-  p.mt = tiles == 0 ? 1 : (tiles + p.groups - 1) / p.groups;
-  // Aim for ~512 workgroups over the whole layer (two per compute unit).
-  const int64_t cols = (int64_t)g.n_kv_heads * total_rows(g);
-  int64_t per_wg = (cols + 511) / 512;
-  int tpw = (int)((per_wg + 63) / 64);
-  tpw = tpw < 1 ? 1 : (tpw > 64 ? 64 : tpw);
-  p.tiles_per_wave = tpw;
-  p.chunk_keys = 64 * tpw;
+  p.n_tiles = p.M_pad / 16;
+  const int cap = max_mtw(g);
+  const int per_wave = (p.n_tiles + 3) / 4;
+  p.groups = per_wave <= cap ? 1 : (per_wave + cap - 1) / cap;
+  p.mt = (per_wave + p.groups - 1) / p.groups;
+  if (p.mt < 1) p.mt = 1;
+  // Enough workgroups to cover the chip a few times; more keys per workgroup once the
+  // layer is large (amortises the query-fragment loads).
+  const int64_t tiles_total = (int64_t)g.n_kv_heads * ((total_rows(g) + KT - 1) / KT);
+  int iters = (int)(tiles_total / 1024);
+  iters = iters < 1 ? 1 : (iters > 16 ? 16 : iters);
+  p.tiles_per_wave = iters;
+  p.chunk_keys = KT * iters;
   const int64_t nmax = max_seq_rows(g);
   p.n_chunks = (int)((nmax + p.chunk_keys - 1) / p.chunk_keys);
   if (p.n_chunks < 1) p.n_chunks = 1;
@@ -319,8 +415,9 @@ hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, 
   a.p0_from_end = p.p0_from_end;
   a.M = p.M;
   a.M_pad = p.M_pad;
+  a.n_tiles = p.n_tiles;
   a.groups = p.groups;
-  a.tiles_per_wave = p.tiles_per_wave;
+  a.iters = p.tiles_per_wave;
   a.chunk_keys = p.chunk_keys;
   a.n_chunks = p.n_chunks;
   a.scale_log2 = kLog2e / sqrtf((float)g.head_dim);

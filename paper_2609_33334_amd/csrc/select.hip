@@ -26,7 +26,17 @@ struct SelectArgs {
   int64_t total_rows;
   int64_t key_stride;
   int n_kv_heads, pool_half, n_tail, n_select;
+  // fused compaction (k_out == nullptr: selection only)
+  const char* k;
+  const char* v;
+  char* k_out;
+  char* v_out;
+  int64_t head_stride_bytes;
+  int row_bytes, n_out, replicas, rows_per_rep;
 };
+
+constexpr int kMaxRowsPerRep = 1024;
+constexpr int kPoolHalo = 8;   // register path handles pool kernels up to 2*8+1
 
 __global__ __launch_bounds__(kSelThreads) void select_topb_kernel(SelectArgs a) {
   const int h = blockIdx.x, b = blockIdx.y;
@@ -114,13 +124,13 @@ __global__ __launch_bounds__(kSelThreads) void select_topb_kernel(SelectArgs a) 
       cnt_tie[par][wv] = __popcll(mt);
     }
     __syncthreads();
-    int gt_before = 0, tie_before = 0, kept_before = 0, tot_gt = 0, tot_tie = 0;
+    int tie_before = 0, kept_before = 0, tot_gt = 0, tot_tie = 0;
     for (int w = 0; w < kSelWaves; ++w) {
       const int cg = cnt_gt[par][w], ct = cnt_tie[par][w];
       // ties of wave w that are still within the quota
       const int room = need - (tie_base + tot_tie);
       const int kt = room <= 0 ? 0 : (ct < room ? ct : room);
-      if (w < wv) { gt_before += cg; tie_before += ct; kept_before += cg + kt; }
+      if (w < wv) { tie_before += ct; kept_before += cg + kt; }
       tot_gt += cg;
       tot_tie += ct;
     }
@@ -132,6 +142,213 @@ __global__ __launch_bounds__(kSelThreads) void select_topb_kernel(SelectArgs a) 
     const int tie_taken = min(tot_tie, max(0, need - tie_base));
     kept_base += tot_gt + tie_taken;
     tie_base += tot_tie;
+  }
+}
+
+// Fast path for C <= THREADS * KPT.  Thread t owns the KPT consecutive candidates
+// [t*KPT, (t+1)*KPT): their pooled keys stay in registers through the radix passes, and
+// one workgroup-wide exclusive scan of (greater, tied) counts gives every thread the
+// output position of its first kept candidate, so kept indices come out ascending
+// without a sort.  Raw scores are staged in LDS for the max-pool, padded by one word
+// every 16 so that the threads' consecutive segments fall in different banks.
+//
+// With `a.k_out` set, the workgroup also performs the compaction of its slice of
+// output rows (replica `rep` of `a.replicas` per head): every replica repeats the
+// selection (cheap, from L2) and copies rows [rep*rows_per_rep, (rep+1)*rows_per_rep)
+// of [kept rows || tail || zero rows], so the row copies of one head spread over
+// several compute units.
+__host__ __device__ __forceinline__ int stage_pos(int j) { return j + (j >> 4); }
+
+// Workgroup-wide exclusive prefix sum of one int per thread.  Counts here stay
+// below 2^16 per half, so two counters can share one packed word.
+template <int THREADS>
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* sh) {
+  constexpr int WAVES = THREADS / kWave;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t v = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += v;
+  }
+  if (lane == 63) sh[wv] = inc;
+  __syncthreads();
+  uint32_t before = 0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w)
+    if (w < wv) before += sh[w];
+  return before + inc - x;
+}
+
+template <int THREADS, int KPT>
+__global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) {
+  constexpr int WAVES = THREADS / kWave;
+  extern __shared__ __attribute__((aligned(16))) float stage[];
+  const int h = blockIdx.x / a.replicas, rep = blockIdx.x % a.replicas, b = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t s0 = a.offs[b];
+  const int N = (int)(a.offs[b + 1] - s0);
+  const int C = N - a.n_tail;
+  const int nsel = max(0, min(a.n_select, C));
+  const bool writer = rep == 0;
+  int32_t* out = a.idx + ((int64_t)b * a.n_kv_heads + h) * a.n_select;
+  if (writer && h == 0 && tid == 0) a.n_kept[b] = nsel;
+  if (writer)
+    for (int r = nsel + tid; r < a.n_select; r += THREADS) out[r] = -1;
+  // this replica's slice of output rows and the kept index of each
+  const int r0 = rep * a.rows_per_rep;
+  const int r1 = min(a.n_out, r0 + a.rows_per_rep);
+  __shared__ int slice[kMaxRowsPerRep];
+  __shared__ uint32_t scan_sh[WAVES];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t sh_digit, sh_above;
+
+  if (nsel == C) {
+    // every candidate is kept, in order
+    if (writer)
+      for (int r = tid; r < C; r += THREADS) out[r] = r;
+    for (int r = r0 + tid; r < min(r1, nsel); r += THREADS) slice[r - r0] = r;
+  } else if (nsel > 0) {
+    const float* src = a.scores + (int64_t)h * a.total_rows + s0;
+    const int base = tid * KPT;
+    uint32_t key[KPT];
+    if (a.pool_half > 0) {
+      for (int j = tid; j < C; j += THREADS) stage[stage_pos(j)] = src[j];
+      __syncthreads();
+      // the segment and a halo of kPoolHalo on each side, indices clamped into [0, C):
+      // a clamped index repeats a candidate that is inside the window anyway, so the
+      // maximum is unchanged and the loads need no guards
+      float w[KPT + 2 * kPoolHalo];
+#pragma unroll
+      for (int i = 0; i < KPT + 2 * kPoolHalo; ++i)
+        w[i] = stage[stage_pos(min(max(base + i - kPoolHalo, 0), C - 1))];
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        float m = w[i + kPoolHalo];
+#pragma unroll
+        for (int q = 1; q <= kPoolHalo; ++q)
+          if (q <= a.pool_half) m = fmaxf(m, fmaxf(w[i + kPoolHalo - q], w[i + kPoolHalo + q]));
+        key[i] = __float_as_uint(m);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) key[i] = base + i < C ? __float_as_uint(src[base + i]) : 0u;
+    }
+
+    if (tid == 0) { sh_digit = 0; sh_above = 0; }
+    uint32_t prefix = 0, mask = 0;
+    int remaining = nsel;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      if (tid < 256) hist[tid] = 0;
+      __syncthreads();
+      if (shift == 24) {
+        // leading digit: nearly every score shares one or a few values, so same-address
+        // atomics would serialise; count each distinct digit of a wavefront with one
+        // ballot (at most four rounds), then fall back to per-lane atomics
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) {
+          bool pend = base + i < C;
+          const uint32_t dg = key[i] >> 24;
+#pragma unroll
+          for (int round = 0; round < 4; ++round) {
+            const uint64_t pm = __ballot(pend);
+            if (pm == 0) break;
+            const uint32_t lead = __builtin_amdgcn_readlane(dg, __builtin_ctzll(pm));
+            const uint64_t sm = __ballot(pend && dg == lead);
+            if (lane == 0) atomicAdd(&hist[lead], (uint32_t)__popcll(sm));
+            pend = pend && dg != lead;
+          }
+          if (pend) atomicAdd(&hist[dg], 1u);
+        }
+      } else {
+        // later digits are spread out: independent per-lane atomics (no return value)
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) {
+          const bool in = base + i < C && (key[i] & mask) == prefix;
+          if (in) atomicAdd(&hist[(key[i] >> shift) & 255u], 1u);
+        }
+      }
+      __syncthreads();
+      if (wv == 0) {
+        uint32_t c[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c[i] = hist[4 * lane + i];
+        const uint32_t tot = c[0] + c[1] + c[2] + c[3];
+        uint32_t suf = tot;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t v = __shfl_down(suf, o, 64);
+          if (lane + o < 64) suf += v;
+        }
+        uint32_t above = suf - tot;
+#pragma unroll
+        for (int i = 3; i >= 0; --i) {
+          if (above < (uint32_t)remaining && above + c[i] >= (uint32_t)remaining) {
+            sh_digit = 4 * lane + i;
+            sh_above = above;
+          }
+          above += c[i];
+        }
+      }
+      __syncthreads();
+      remaining -= (int)sh_above;
+      prefix |= sh_digit << shift;
+      mask |= 255u << shift;
+      __syncthreads();
+    }
+    const uint32_t thr = prefix;   // the nsel-th largest key
+    const int need = remaining;    // keys equal to thr that are kept
+
+    // (greater, tied) counts of this thread's segment, packed into one scanned word
+    uint32_t packed = 0;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const bool valid = base + i < C;
+      packed += (valid && key[i] > thr) ? 1u : 0u;
+      packed += (valid && key[i] == thr) ? (1u << 16) : 0u;
+    }
+    // C <= 32768, so neither half of the packed prefix overflows 16 bits
+    const uint32_t before = block_excl_scan<THREADS>(packed, scan_sh);
+    const int gt_before = (int)(before & 0xffffu), tie_before = (int)(before >> 16);
+    int pos = gt_before + min(tie_before, need);
+    int trank = tie_before;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const bool valid = base + i < C;
+      bool keep = valid && key[i] > thr;
+      if (valid && key[i] == thr) {
+        keep = trank < need;
+        ++trank;
+      }
+      if (keep && pos < nsel) {
+        if (writer) out[pos] = base + i;
+        if (pos >= r0 && pos < r1) slice[pos - r0] = base + i;
+        ++pos;
+      }
+    }
+  }
+  if (a.k_out == nullptr) return;
+  __syncthreads();
+
+  // compaction of output rows [r0, r1): kept rows, then the tail, then zero rows
+  const int tpr = a.row_bytes / 16;
+  const int rpp = THREADS / tpr;
+  const int part = tid % tpr;
+  const int64_t obase = ((int64_t)b * a.n_kv_heads + h) * a.n_out;
+  for (int r = r0 + tid / tpr; r < r1; r += rpp) {
+    int srow;
+    if (r < nsel) srow = slice[r - r0];
+    else if (r < nsel + a.n_tail) srow = C + (r - nsel);
+    else srow = -1;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (srow >= 0) {
+      const int64_t in = h * a.head_stride_bytes + (s0 + srow) * a.row_bytes + part * 16;
+      kv = load16(a.k + in);
+      vv = load16(a.v + in);
+    }
+    const int64_t o = (obase + r) * a.row_bytes + part * 16;
+    *reinterpret_cast<uint4*>(a.k_out + o) = kv;
+    *reinterpret_cast<uint4*>(a.v_out + o) = vv;
   }
 }
 
@@ -147,15 +364,20 @@ __global__ __launch_bounds__(256) void select_streaming_kernel(int32_t* idx, int
   if (h == 0 && threadIdx.x == 0) n_kept[b] = nk;
 }
 
-}  // namespace
-
-size_t select_workspace_bytes(const dge_geom_t& g) {
-  return (size_t)g.batch * g.n_kv_heads * (size_t)((max_seq_rows(g) + 63) / 64 * 64) * 4 + 256;
+template <int THREADS, int KPT>
+hipError_t launch_seg(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t st) {
+  if (lds > 64 * 1024) {
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&select_topb_seg_kernel<THREADS, KPT>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((select_topb_seg_kernel<THREADS, KPT>), grid, dim3(THREADS), lds, st, a);
+  return hipGetLastError();
 }
 
-hipError_t launch_select_topb(const dge_geom_t& g, const float* scores, int pool_kernel,
-                              int n_tail, int n_select, int32_t* idx, int32_t* n_kept, void* ws,
-                              hipStream_t st) {
+SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, int n_tail,
+                     int n_select, int32_t* idx, int32_t* n_kept, void* ws) {
   SelectArgs a{};
   a.scores = scores;
   a.keys = reinterpret_cast<uint32_t*>(ws);
@@ -168,8 +390,81 @@ hipError_t launch_select_topb(const dge_geom_t& g, const float* scores, int pool
   a.pool_half = pool_kernel / 2;
   a.n_tail = n_tail;
   a.n_select = n_select;
+  a.n_out = n_select + n_tail;
+  a.replicas = 1;
+  a.rows_per_rep = kMaxRowsPerRep;
+  return a;
+}
+
+// Launch the segment kernel when the largest candidate set fits; returns false when
+// the global-memory fallback must be used.
+bool launch_fast(const SelectArgs& a, const dge_geom_t& g, int64_t cmax, hipStream_t st,
+                 hipError_t* err) {
+  if (a.pool_half > kPoolHalo) return false;
+  const dim3 grid(g.n_kv_heads * a.replicas, g.batch);
+  const size_t lds = a.pool_half > 0 ? (size_t)stage_pos((int)(cmax > 0 ? cmax : 1)) * 4 + 64 : 0;
+  if (cmax <= 1024) *err = launch_seg<256, 4>(a, grid, lds, st);
+  else if (cmax <= 2048) *err = launch_seg<256, 8>(a, grid, lds, st);
+  else if (cmax <= 4096) *err = launch_seg<256, 16>(a, grid, lds, st);
+  else if (cmax <= 8192) *err = launch_seg<512, 16>(a, grid, lds, st);
+  else if (cmax <= 16384) *err = launch_seg<1024, 16>(a, grid, lds, st);
+  else if (cmax <= 32768) *err = launch_seg<1024, 32>(a, grid, lds, st);
+  else return false;
+  return true;
+}
+
+}  // namespace
+
+size_t select_workspace_bytes(const dge_geom_t& g) {
+  return (size_t)g.batch * g.n_kv_heads * (size_t)((max_seq_rows(g) + 63) / 64 * 64) * 4 + 256;
+}
+
+hipError_t launch_select_topb(const dge_geom_t& g, const float* scores, int pool_kernel,
+                              int n_tail, int n_select, int32_t* idx, int32_t* n_kept, void* ws,
+                              hipStream_t st) {
+  SelectArgs a = make_args(g, scores, pool_kernel, n_tail, n_select, idx, n_kept, ws);
+  hipError_t err = hipSuccess;
+  if (launch_fast(a, g, max_seq_rows(g) - n_tail, st, &err)) return err;
   hipLaunchKernelGGL(select_topb_kernel, dim3(g.n_kv_heads, g.batch), dim3(kSelThreads), 0, st, a);
   return hipGetLastError();
+}
+
+hipError_t launch_select_compact(const dge_geom_t& g, const float* scores, int pool_kernel,
+                                 int n_tail, int n_select, int32_t* idx, int32_t* n_kept,
+                                 const void* k, const void* v, void* k_out, void* v_out, void* ws,
+                                 hipStream_t st) {
+  SelectArgs a = make_args(g, scores, pool_kernel, n_tail, n_select, idx, n_kept, ws);
+  const int elt = g.dtype == DGE_BF16 ? 2 : 4;
+  a.k = reinterpret_cast<const char*>(k);
+  a.v = reinterpret_cast<const char*>(v);
+  a.k_out = reinterpret_cast<char*>(k_out);
+  a.v_out = reinterpret_cast<char*>(v_out);
+  a.head_stride_bytes = g.kv_head_stride * elt;
+  a.row_bytes = g.head_dim * elt;
+  // Spread each head's row copies over enough replicas to occupy the chip while keeping
+  // the repeated selection bounded: at most 16 replicas of at least 64 rows each.
+  const int units = g.batch * g.n_kv_heads;
+  int reps = 256 / (units > 0 ? units : 1);
+  const int by_rows = (a.n_out + 63) / 64;
+  reps = reps > by_rows ? by_rows : reps;
+  reps = reps > 16 ? 16 : reps;
+  reps = reps < 1 ? 1 : reps;
+  int rpr = (a.n_out + reps - 1) / reps;
+  if (rpr > kMaxRowsPerRep) {
+    rpr = kMaxRowsPerRep;
+    reps = (a.n_out + rpr - 1) / rpr;
+  }
+  a.replicas = reps;
+  a.rows_per_rep = rpr > 0 ? rpr : 1;
+  hipError_t err = hipSuccess;
+  if (launch_fast(a, g, max_seq_rows(g) - n_tail, st, &err)) return err;
+  // candidate sets beyond the register path: select, then the separate row gather
+  a.k_out = nullptr;
+  a.replicas = 1;
+  hipLaunchKernelGGL(select_topb_kernel, dim3(g.n_kv_heads, g.batch), dim3(kSelThreads), 0, st, a);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  return launch_compact(g, idx, n_kept, n_select, n_tail, k, v, k_out, v_out, st);
 }
 
 hipError_t launch_select_streaming(const dge_geom_t& g, int n_sink, int n_recent, int32_t* idx,

@@ -147,6 +147,9 @@ SELECT_CASES = [
     ((50, 34), "continuous", 7, 34, 10),        # a sequence with no candidates
     ((32770,), "plateau", 7, 34, 2016),         # largest per-sequence length of the c4 mix
     ((9000,), "ints", 1, 512, 512),             # H2O-like split
+    ((40000, 300), "plateau", 7, 34, 2016),     # beyond the register path: global fallback
+    ((3000, 700), "continuous", 19, 34, 300),   # pool wider than the register halo
+    ((32768 + 34, 5000), "ints", 17, 34, 2016), # largest register-path candidate set
 ]
 
 
@@ -222,6 +225,33 @@ def test_compact_bit_exact():
             m = len(rows)
             assert np.array_equal(ko[b, h, :m], kb[h, rows]) and np.array_equal(vo[b, h, :m], vb[h, rows])
             assert (ko[b, h, m:] == 0).all() and (vo[b, h, m:] == 0).all()
+
+
+FUSED_CASES = {
+    "c2": (di.WORKLOADS["c2"], None),
+    "ragged": (di.small_variant("c2", [600, 1200, 40, 3000]), None),
+    "c1_f32": (di.WORKLOADS["c1"], None),
+    "keep_all": (di.small_variant("c2", [300, 90]), 1000),
+    "window_only_budget": (di.small_variant("c2", [500]), 32),
+    "fallback_40k": (di.small_variant("c2", [40000], plant="none"), 2048),
+}
+
+
+@pytest.mark.parametrize("case", list(FUSED_CASES))
+def test_select_compact_fused_equals_separate(case):
+    wl, budget = FUSED_CASES[case]
+    budget = wl.budget if budget is None else budget
+    _log(f"fused select+compact {case}")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    q, k, v = to_dev(x.q_bits, wl.dtype), to_dev(x.k_bits, wl.dtype), to_dev(x.v_bits, wl.dtype)
+    a = dge.evict_layer(g, q, k, v, budget, wl.pool, fused=True)
+    b = dge.evict_layer(g, q, k, v, budget, wl.pool, fused=False)
+    torch.cuda.synchronize()
+    for key in ("raw", "idx", "n_kept"):
+        assert torch.equal(a[key], b[key]), key
+    iv = torch.int16 if wl.dtype == "bf16" else torch.int32
+    assert torch.equal(a["k"].view(iv), b["k"].view(iv)) and torch.equal(a["v"].view(iv), b["v"].view(iv))
 
 
 def test_compact_keep_all_is_identity():
