@@ -29,6 +29,13 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+WORKLOAD_TEXT = {
+    "c1": "c1: tiny fp32 layer, 4q/2kv heads, d=64, L=512, window 8 + k=2, B=64, max-pool 5",
+    "c2": "c2: one Llama-3-8B-shaped layer, 32q/8kv heads, d=128, batch 1, L=4096, "
+          "window 32 + k=2 draft rows, B=512, max-pool 7",
+    "c3": "c3: 32 Llama-3-8B-shaped layers, 32q/8kv heads, d=128, batch 1, L=16384, "
+          "window 32 + k=2, PyramidKV-style budgets 2048 -> 256, max-pool 7",
+}
 GRAPH_STEPS = 8
 
 
@@ -44,6 +51,12 @@ def parse():
     p.add_argument("--workload", default="c2")
     p.add_argument("--sets", type=int, default=48)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-cal", action="store_true",
+                   help="only run a plain 256 MiB device-to-device copy 8 times (the reference "
+                        "for scaling FETCH_SIZE / WRITE_SIZE counters to bytes)")
+    p.add_argument("--lse", action="store_true",
+                   help="score with the scoring rows' log-sum-exp supplied (dge_score_lse); the "
+                        "LSE is prepared outside the timed region, as an attention forward would")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     return p.parse_args()
 
@@ -59,13 +72,22 @@ def main():
     import dge_inputs as di
     import paper_2609_33334_amd as dge
 
+    if args.copy_cal:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(8):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": src.numel(), "copies": 8}), flush=True)
+        return
+
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     dev = "cuda:0"
     wl = di.WORKLOADS[args.workload]
-    if wl.h2o or wl.n_layers != 1:
-        print("bench.py: the timed step covers one layer (workload c1 or c2)", file=sys.stderr)
+    if wl.h2o or wl.batch != 1:
+        print("bench.py: workloads c1, c2 and c3 are timed here", file=sys.stderr)
         sys.exit(2)
     log(f"[bench] workload {wl.name}: generating inputs")
     x = di.make_layer(wl)
@@ -81,71 +103,101 @@ def main():
     geom = dge.Geometry(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.window, wl.k_draft,
                         wl.cached_lens, dtype=dge.DGE_BF16 if is_bf16 else dge.DGE_F32, device=dev)
     q0, k0, v0 = dev_t(x.q_bits), dev_t(x.k_bits), dev_t(x.v_bits)
-    S = max(1, args.sets)
-    sets = []
     n_tail = wl.window + wl.k_draft
-    n_sel = wl.budget - wl.window
+    L_layers = wl.n_layers
+    budgets = [wl.budget_of_layer(l) for l in range(L_layers)]
+    # one step = every layer once; single-layer workloads rotate over --sets copies so that
+    # no step finds its inputs in the Infinity Cache, multi-layer ones are large enough
+    S = max(1, args.sets) if L_layers == 1 else 1
     ws_score = torch.empty(dge.workspace_size(geom, dge.OP_SCORE), dtype=torch.uint8, device=dev)
     ws_sel = torch.empty(dge.workspace_size(geom, dge.OP_SELECT), dtype=torch.uint8, device=dev)
+    layers = []   # layers[set][layer] = (q, k, v, out, budget)
     for i in range(S):
-        out = dict(raw=torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=dev),
-                   idx=torch.empty(geom.batch, geom.n_kv_heads, n_sel, dtype=torch.int32, device=dev),
-                   n_kept=torch.zeros(max(geom.batch, 4), dtype=torch.int32, device=dev),
-                   k=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
-                                 dtype=k0.dtype, device=dev),
-                   v=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
-                                 dtype=k0.dtype, device=dev))
-        sets.append((q0.clone(), k0.clone(), v0.clone(), out))
+        row = []
+        for l in range(L_layers):
+            n_sel = budgets[l] - wl.window
+            out = dict(raw=torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=dev),
+                       idx=torch.empty(geom.batch, geom.n_kv_heads, n_sel, dtype=torch.int32, device=dev),
+                       n_kept=torch.zeros(max(geom.batch, 4), dtype=torch.int32, device=dev),
+                       k=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
+                                     dtype=k0.dtype, device=dev),
+                       v=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
+                                     dtype=k0.dtype, device=dev))
+            row.append((q0.clone(), k0.clone(), v0.clone(), out, budgets[l]))
+        layers.append(row)
     torch.cuda.synchronize()
+    row_lse = None
+    if args.lse:
+        # natural-log softmax normaliser of each scoring row over keys j <= p (fp32, torch)
+        nr = wl.window + wl.k_draft
+        N = wl.cached_lens[0]
+        kk = k0.float()
+        qq = q0.float()
+        G = wl.group
+        x = torch.einsum("hrd,hnd->hrn", qq, kk.repeat_interleave(G, dim=0)) / (wl.head_dim ** 0.5)
+        pos = torch.arange(N - nr, N, device=dev)
+        x = x.masked_fill(torch.arange(N, device=dev)[None, None, :] > pos[None, :, None], float("-inf"))
+        row_lse = torch.logsumexp(x, dim=2).contiguous()
+        del x, kk, qq
+
+    def score_call(q, k, out):
+        if row_lse is not None:
+            dge.score_lse(geom, dge.ROWS_WINDOW_DRAFT, q, k, row_lse, raw=out["raw"])
+        else:
+            dge.score(geom, dge.ROWS_WINDOW_DRAFT, q, k, raw=out["raw"], ws=ws_score)
 
     def step(i):
-        q, k, v, out = sets[i % S]
-        dge.evict_layer(geom, q, k, v, wl.budget, wl.pool, ws_score=ws_score, ws_select=ws_sel,
-                        out=out)
+        for (q, k, v, out, B) in layers[i % S]:
+            score_call(q, k, out)
+            dge.select_compact(geom, out["raw"], wl.pool, n_tail, B - wl.window, k, v,
+                               idx=out["idx"], n_kept=out["n_kept"], k_out=out["k"],
+                               v_out=out["v"], ws=ws_sel)
 
     def score_only(i):
-        q, k, v, out = sets[i % S]
-        dge.score(geom, dge.ROWS_WINDOW_DRAFT, q, k, raw=out["raw"], ws=ws_score)
+        for (q, k, v, out, B) in layers[i % S]:
+            score_call(q, k, out)
 
     # eager warmup and reference result
     for i in range(max(args.warmup, S)):
         step(i)
     torch.cuda.synchronize()
-    ref = {kk: vv.clone() for kk, vv in sets[0][3].items()}
+    ref = {kk: vv.clone() for kk, vv in layers[0][0][3].items()}
 
     # HIP graphs of GRAPH_STEPS consecutive steps, covering every buffer set
+    gsteps = GRAPH_STEPS if L_layers == 1 else 1
     stream = torch.cuda.Stream()
     graphs, sgraphs = [], []
-    n_graphs = max(1, S // GRAPH_STEPS)
+    n_graphs = max(1, S // gsteps)
     with torch.cuda.stream(stream):
         for gi in range(n_graphs):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=stream):
-                for j in range(GRAPH_STEPS):
-                    step(gi * GRAPH_STEPS + j)
+                for j in range(gsteps):
+                    step(gi * gsteps + j)
             graphs.append(g)
             sg = torch.cuda.CUDAGraph()
             with torch.cuda.graph(sg, stream=stream):
-                for j in range(GRAPH_STEPS):
-                    score_only(gi * GRAPH_STEPS + j)
+                for j in range(gsteps):
+                    score_only(gi * gsteps + j)
             sgraphs.append(sg)
     torch.cuda.synchronize()
-    # graph replays must reproduce the eager result (set 0 is step 0 of graph 0)
+    # graph replays must reproduce the eager result (layer 0 of set 0 is in graph 0)
     for kk in ref:
-        sets[0][3][kk].zero_()
+        layers[0][0][3][kk].zero_()
     torch.cuda.synchronize()
     graphs[0].replay()
     torch.cuda.synchronize()
     for kk in ref:
-        assert torch.equal(sets[0][3][kk], ref[kk]), f"graph replay differs from eager ({kk})"
+        assert torch.equal(layers[0][0][3][kk], ref[kk]), f"graph replay differs from eager ({kk})"
 
     K = args.steps
-    n_rep = (K + GRAPH_STEPS - 1) // GRAPH_STEPS
-    K = n_rep * GRAPH_STEPS
+    n_rep = (K + gsteps - 1) // gsteps
+    K = n_rep * gsteps
     for r in range(min(n_rep, 2 * n_graphs)):
         graphs[r % n_graphs].replay()
     torch.cuda.synchronize()
-    log(f"[bench] timing {K} steps ({n_rep} graph replays of {GRAPH_STEPS} steps, {S} buffer sets)")
+    log(f"[bench] timing {K} steps ({n_rep} graph replays of {gsteps} steps, {S} buffer sets, "
+        f"{L_layers} layers per step)")
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -167,25 +219,30 @@ def main():
         sgraphs[r % n_graphs].replay()
     es1.record()
     torch.cuda.synchronize()
-    score_us = es0.elapsed_time(es1) * 1e3 / K
+    score_us = es0.elapsed_time(es1) * 1e3 / (K * L_layers)
     log(f"[bench] {ms_per_step * 1e3:.2f} us/step (event), wall {wall * 1e6 / K:.2f} us/step; "
         f"dge_score {score_us:.2f} us/call")
 
     L = sum(wl.prompt_lens)
-    units = L * wl.n_kv_heads                      # prefix tokens x KV heads per step
+    units = L * wl.n_kv_heads * L_layers          # prefix tokens x KV heads per step
     value = units / (ms_per_step * 1e-3)
-    # algorithmic bytes of dge_score: K once + the scoring queries
+    # algorithmic bytes of one dge_score call: K once + the scoring queries
     n_rows = wl.window + wl.k_draft
     score_bytes = (wl.n_kv_heads * geom.total_rows * wl.head_dim * elt
                    + wl.n_q_heads * wl.batch * n_rows * wl.head_dim * elt)
     achieved = score_bytes / (score_us * 1e-6) / 1e9
-    roofline = {"kernel": "dge_score (stats + reduce + colsum launches)", "bound": "hbm",
+    roofline = {"kernel": ("dge_score_lse (colsum launch)" if args.lse else
+                           "dge_score (stats + reduce + colsum launches)"), "bound": "hbm",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(wl.name, args.lse),
                 "bytes_per_launch": int(score_bytes), "us_per_launch": round(score_us, 3)}
     # whole step against its own algorithmic bytes (score + compaction + indices)
-    step_bytes = score_bytes + 4 * wl.n_kv_heads * wl.batch * (n_sel + n_tail) * wl.head_dim * elt \
-        + 4 * wl.n_kv_heads * wl.batch * n_sel
+    step_bytes = 0
+    for B in budgets:
+        n_sel = B - wl.window
+        step_bytes += score_bytes + 4 * wl.n_kv_heads * wl.batch * (n_sel + n_tail) * wl.head_dim * elt \
+            + 4 * wl.n_kv_heads * wl.batch * n_sel
     step_frac = step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS
 
     cpu = None
@@ -197,15 +254,48 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if is_bf16 else "f32",
         "data": "synthetic (seeded Gaussian Q/K/V with planted spans; no model weights)",
-        "config": {"workload": wl.name + ": one Llama-3-8B-shaped layer, 32q/8kv heads, d=128, "
-                   "batch 1, L=4096, window 32 + k=2 draft rows, B=512, max-pool 7",
-                   "global_batch": wl.batch, "seq_len": L, "parallelism": "single GPU",
-                   "step": "dge_score -> dge_select_topb -> dge_compact",
+        "config": {"workload": WORKLOAD_TEXT.get(wl.name, wl.name),
+                   "global_batch": wl.batch, "seq_len": L, "layers": L_layers,
+                   "parallelism": "single GPU",
+                   "step": ("per layer: dge_score_lse (row LSE supplied) -> dge_select_compact"
+                            if args.lse else
+                            "per layer: dge_score -> dge_select_compact (pool, top-(B-w), gather)"),
                    "step_hbm_frac": round(step_frac, 4), "buffer_sets": S},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+SCORE_SOURCES = ("paper_2609_33334_amd/csrc/score.hip", "paper_2609_33334_amd/csrc/dge_device.hpp")
+
+
+def score_source_hash() -> str:
+    """sha256 of the score kernels' code with comments and whitespace removed."""
+    import hashlib
+    import re
+    h = hashlib.sha256()
+    for f in SCORE_SOURCES:
+        with open(os.path.join(ROOT, f)) as fh:
+            code = fh.read()
+        code = re.sub(r"/\*.*?\*/", "", code, flags=re.S)
+        code = re.sub(r"//[^\n]*", "", code)
+        h.update(re.sub(r"\s+", "", code).encode())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, lse: bool):
+    """HBM bytes per dge_score call from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary, or None when there is none or the score kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"score_traffic_{workload}{'_lse' if lse else ''}.json")
+    try:
+        with open(path) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != score_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_call")
 
 
 def cpu_baseline(wl, x, seconds):
@@ -217,11 +307,12 @@ def cpu_baseline(wl, x, seconds):
     except Exception:  # pragma: no cover
         cores = 1
     L = sum(wl.prompt_lens)
+    budget = wl.budget_of_layer(0)
     reps = 0
     t0 = time.perf_counter()
     while True:
         oracle.evict_layer(x.q, x.k, x.v, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
-                           wl.k_draft, wl.budget, wl.pool)
+                           wl.k_draft, budget, wl.pool)
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -229,8 +320,8 @@ def cpu_baseline(wl, x, seconds):
     rate = reps * L * wl.n_kv_heads / el
     log(f"[bench] cpu oracle: {reps} layers in {el:.1f}s -> {rate:.3g} token*kvhead/s")
     return {"value": round(rate, 1), "unit": "token*kvhead/s", "cores": cores, "kind": "oracle",
-            "sample": f"{reps} repeats of the full {wl.name} layer (score, pool, select, compact) "
-                      f"in float64 numpy, {el:.1f} s"}
+            "sample": f"{reps} repeats of one {wl.name} layer (score, pool, select, compact; "
+                      f"budget {budget}) in float64 numpy, {el:.1f} s"}
 
 
 if __name__ == "__main__":

@@ -7,7 +7,7 @@ Both sides read the *stored* values: ``bits`` (uint16 bfloat16 patterns or the
 float32 array itself) and an exact float32 copy of them.
 
 Workload recipes (Llama-3-8B KV geometry: 32 query / 8 KV heads, head dim 128,
-tab:backbones of the paper; lengths cover LongBench's input range, Sec. 6):
+the paper's backbone table (Llama-3-8B); lengths cover LongBench's input range, Sec. 6):
 
 * ``c1`` tiny fp32 case: 4q/2kv heads, d 64, L 512, window 8, k 2, B 64, pool 5,
   eight candidate keys per KV head scaled x4.

@@ -6,14 +6,14 @@
  * have been drafted on the full cache, then, once per layer (Alg. 1, steps B-C):
  *   1. scores every cached key by the softmax attention the scoring queries pay
  *      to it (window and/or draft queries; fp32 softmax, score summed over the
- *      queries, meaned over each GQA group, 1-D max-pooled: app:diagnostics,
- *      app:complexity);
+ *      queries, meaned over each GQA group, 1-D max-pooled: App. "Diagnostic details",
+ *      App. "Complexity and overheads");
  *   2. keeps the top (B - w) past keys per KV head (R_E of Alg. 1);
  *   3. rewrites the cache as [retained past, ascending] || [window + draft tail]
- *      (app:dg, implementation notes).
+ *      (App. "Draft-guided eviction implementation", implementation notes).
  * Alternative retention rules the paper composes with DGE: H2O accumulated
- * attention (tab:complexity, footnote a), StreamingLLM sinks + recency (Sec. 6)
- * and PyramidKV layer budgets (app:analysis).
+ * attention (Table "Complexity and measured overhead", footnote a), StreamingLLM sinks + recency (Sec. 6)
+ * and PyramidKV layer budgets (App. "Additional analysis").
  *
  * Conventions shared by every call
  * --------------------------------
@@ -99,7 +99,7 @@ const char *dge_status_string(int status);
  * Writes *bytes (host pointer).  Errors: DGE_ERR_INVALID for a bad geometry. */
 dge_status_t dge_workspace_size(const dge_geom_t *geom, int32_t op, size_t *bytes);
 
-/* Step 1 of the eviction (Alg. 1 step B; app:diagnostics; app:complexity):
+/* Step 1 of the eviction (Alg. 1 step B; App. "Diagnostic details"; App. "Complexity and overheads"):
  *   raw[h][j] = (1/G) sum_{g in group h} sum_{scoring rows r} softmax_j(q_{g,r} . k_j / sqrt(d))
  * for every cached row j of every sequence (tail rows included), softmax in fp32
  * over keys j <= p_r, scores accumulated in fp32.  Each sequence's scores sum to
@@ -115,7 +115,18 @@ dge_status_t dge_workspace_size(const dge_geom_t *geom, int32_t op, size_t *byte
 dge_status_t dge_score(const dge_geom_t *geom, int32_t rows, const void *q, const void *k,
                        float *raw, void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* Steps 1b-2 (SnapKV max-pool, then R_E = per-head top-B; Alg. 1; app:dg notes).
+/* dge_score with the scoring rows' softmax normalisers supplied by the caller, e.g. the
+ * log-sum-exp an attention forward already produced for the window and draft rows.
+ * Only the column-sum pass runs, so K is read once.
+ *   row_lse : [H_q][batch * n_rows] float32, natural log: log sum_{j <= p_r} exp(q_r . k_j / sqrt(d)),
+ *             rows in the order of q.
+ * Other arguments and the output are those of dge_score; no workspace is needed.
+ * Errors: as dge_score; DGE_ERR_UNSUPPORTED when G * n_rows exceeds what one workgroup
+ * keeps in registers (more than 576 query rows per KV head for bf16, d = 128). */
+dge_status_t dge_score_lse(const dge_geom_t *geom, int32_t rows, const void *q, const void *k,
+                           const float *row_lse, float *raw, hipStream_t stream);
+
+/* Steps 1b-2 (SnapKV max-pool, then R_E = per-head top-B; Alg. 1; App. "Draft-guided eviction implementation").
  * For every (sequence b, KV head h), with C_b = N_b - n_tail candidate rows:
  *   pooled[j] = max{ scores[h][off_b + i] : |i - j| <= pool_kernel/2, 0 <= i < C_b }
  *   idx[b][h][0 .. n_kept[b]) = the n_kept[b] = min(n_select, C_b) candidates with the
@@ -138,7 +149,7 @@ dge_status_t dge_select_topb(const dge_geom_t *geom, const float *scores, int32_
                              void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Steps 1b-3 in one call: dge_select_topb followed by dge_compact with the same
- * n_tail and n_select (Alg. 1 steps B-C; app:dg notes).  Writes idx, n_kept, k_out
+ * n_tail and n_select (Alg. 1 steps B-C; App. "Draft-guided eviction implementation").  Writes idx, n_kept, k_out
  * and v_out exactly as the two separate calls would; the selection is repeated by
  * several workgroups per KV head so that the row copies spread over the chip.
  * Arguments, layouts and errors are those of the two calls; ws is the
@@ -148,7 +159,7 @@ dge_status_t dge_select_compact(const dge_geom_t *geom, const float *scores, int
                                 const void *k, const void *v, void *k_out, void *v_out, void *ws,
                                 size_t ws_bytes, hipStream_t stream);
 
-/* StreamingLLM retention (Sec. 6; app:analysis: four sinks and a recency window):
+/* StreamingLLM retention (Sec. 6; App. "Additional analysis": four sinks and a recency window):
  * idx[b][h][0 .. n_kept[b]) = 0, 1, ..., n_kept[b]-1 with n_kept[b] = min(n_sink, N_b - n_recent);
  * remaining entries up to n_sink are -1.  The n_recent rows are the tail passed to
  * dge_compact.  No scores are read.
@@ -157,7 +168,7 @@ dge_status_t dge_select_compact(const dge_geom_t *geom, const float *scores, int
 dge_status_t dge_select_streaming(const dge_geom_t *geom, int32_t n_sink, int32_t n_recent,
                                   int32_t *idx, int32_t *n_kept, hipStream_t stream);
 
-/* Step 3 (Alg. 1 step C; app:dg notes: [retained past] || [window + draft tail]).
+/* Step 3 (Alg. 1 step C; App. "Draft-guided eviction implementation": [retained past] || [window + draft tail]).
  * For every (b, h), with C_b = N_b - n_tail and n_out = n_select + n_tail:
  *   out[b][h][r] = K[h][off_b + idx[b][h][r]]        for r < n_kept[b]
  *   out[b][h][r] = K[h][off_b + C_b + r - n_kept[b]] for n_kept[b] <= r < n_kept[b] + n_tail
@@ -172,7 +183,7 @@ dge_status_t dge_compact(const dge_geom_t *geom, const int32_t *idx, const int32
                          void *k_out, void *v_out, hipStream_t stream);
 
 /* H2O accumulated attention, kept running through the draft rows
- * (tab:complexity, footnote a; app:dg notes on H2O's prompt-query buffer):
+ * (Table "Complexity and measured overhead", footnote a; App. "Draft-guided eviction implementation" on H2O's prompt-query buffer):
  *   colsum[h][j] = (1/G) sum_{g in group h} sum_{p = j}^{N_b - 1} softmax_j(q_{g,p} . k_j / sqrt(d))
  * over every cached row p of the sequence (all prompt rows and the k draft rows).
  *   q_all  : [H_q][T][d] queries of every cached row (same element type as K).
@@ -186,7 +197,7 @@ dge_status_t dge_h2o_colsum(const dge_geom_t *geom, const void *q_all, const voi
                             const float *lse, float *colsum, void *ws, size_t ws_bytes,
                             hipStream_t stream);
 
-/* PyramidKV per-layer budgets (app:analysis), host only:
+/* PyramidKV per-layer budgets (App. "Additional analysis"), host only:
  *   c = B - w;  max = 2c - floor(c/beta);  min = floor(c/beta);
  *   steps = floor((max - min) / (n_layers - 1));  out_host[l] = max - l*steps + w.
  * Errors: DGE_ERR_INVALID for B < w, n_layers < 1, beta < 1 or a NULL output. */

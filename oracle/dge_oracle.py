@@ -8,15 +8,15 @@ Every function is the plain definition of one step, written from the paper
 (arxiv 2609.33334, "Draft-Guided Eviction"), in float64, with no blocking or
 fusion.  Notation, per layer, KV head h and sequence b:
 
-* G = H_q / H_kv query heads share KV head h (native GQA layout, app:complexity);
+* G = H_q / H_kv query heads share KV head h (native GQA layout, App. "Complexity and overheads");
 * L prompt rows, w window rows, k draft rows, N = L + k cached rows;
 * the protected tail is the last n_tail = w + k cached rows (window + draft tail,
-  Alg. 1 step C and app:dg implementation notes);
+  Alg. 1 step C and App. "Draft-guided eviction implementation", implementation notes);
 * C = N - n_tail candidate rows, B' = min(B - w, C) selected rows.
 
 Readings of points the paper leaves open (each also listed with its evidence in
 the design notes): softmax runs causally over every cached key j <= p, tail
-included; the score is the SUM over scoring rows (app:diagnostics "score sum"),
+included; the score is the SUM over scoring rows (App. "Diagnostic details", "score sum"),
 which ranks identically to Alg. 1's 1/k mean; the GQA group MEAN is taken before
 max-pooling; pooling only spans the candidates, out-of-range counting as -inf;
 top-B ties go to the lower position; selected indices are returned ascending.
@@ -56,7 +56,7 @@ def causal_probs(qrows: np.ndarray, keys: np.ndarray, positions: np.ndarray) -> 
     """softmax_j(q_r . k_j / sqrt(d)) over keys j <= position of row r, 0 beyond.
 
     Alg. 1 step B (the softmax of q K^T / sqrt(d)); fp32 softmax in the paper
-    (app:diagnostics), float64 here.  qrows [R][d], keys [N][d] -> [R][N].
+    (App. "Diagnostic details"), float64 here.  qrows [R][d], keys [N][d] -> [R][N].
     """
     d = keys.shape[1]
     x = (qrows @ keys.T) / math.sqrt(d)
@@ -73,8 +73,8 @@ def window_scores(q, k, kv_offsets, n_q_heads: int, n_kv_heads: int, w: int, k_d
     """Per-KV-head attention mass each cached key receives from the scoring rows.
 
     raw[h][j] = (1/G) * sum_{g in group h} sum_{r} softmax_j(q_{g,r} K^T / sqrt(d)),
-    i.e. the score sum over past keys of app:diagnostics, from the rows Alg. 1 step B
-    names, averaged over the query heads of the GQA group (app:complexity,
+    i.e. the score sum over past keys of App. "Diagnostic details", from the rows Alg. 1 step B
+    names, averaged over the query heads of the GQA group (App. "Complexity and overheads",
     gqa_score_agg).  q [H_q][batch*n_rows][d] holds the mode's rows in ascending
     position; k [H_kv][T][d] -> raw [H_kv][T].
     """
@@ -98,10 +98,31 @@ def window_scores(q, k, kv_offsets, n_q_heads: int, n_kv_heads: int, w: int, k_d
     return raw
 
 
+def scoring_row_lse(q, k, kv_offsets, n_q_heads: int, n_kv_heads: int, w: int, k_draft: int,
+                    mode: int = ROWS_WINDOW_DRAFT) -> np.ndarray:
+    """log sum_{j <= p_r} exp(q_r . k_j / sqrt(d)) of every scoring row (the softmax
+    normaliser of Alg. 1 step B), [H_q][batch * n_rows] in the row order of q."""
+    q = as_f64(q)
+    k = as_f64(k)
+    G = n_q_heads // n_kv_heads
+    offs = [int(o) for o in kv_offsets]
+    d = k.shape[2]
+    out = np.zeros((n_q_heads, q.shape[1]), np.float64)
+    for b in range(len(offs) - 1):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        p0, nr = scoring_rows(N, w, k_draft, mode)
+        for hq in range(n_q_heads):
+            x = (q[hq, b * nr:(b + 1) * nr] @ k[hq // G, s0:s0 + N].T) / math.sqrt(d)
+            x = np.where(np.arange(N)[None, :] <= (p0 + np.arange(nr))[:, None], x, -np.inf)
+            m = x.max(axis=1)
+            out[hq, b * nr:(b + 1) * nr] = m + np.log(np.exp(x - m[:, None]).sum(axis=1))
+    return out
+
+
 def maxpool(raw_row: np.ndarray, C: int, kappa: int) -> np.ndarray:
     """SnapKV 1-D max-pool (kernel kappa, stride 1, same length) over candidates [0, C).
 
-    pooled[j] = max{raw[i] : |i - j| <= kappa // 2, 0 <= i < C} (app:diagnostics,
+    pooled[j] = max{raw[i] : |i - j| <= kappa // 2, 0 <= i < C} (App. "Diagnostic details",
     Sec. 6 compression settings: kernel 7).  Keys outside the candidate range do
     not take part.
     """
@@ -116,8 +137,8 @@ def maxpool(raw_row: np.ndarray, C: int, kappa: int) -> np.ndarray:
 def select_topb(pooled: np.ndarray, n_select: int) -> np.ndarray:
     """Indices of the n_select largest pooled scores, ties to the lower index, ascending.
 
-    Alg. 1 step B: I <- R_E(s, B - w) with per-head top-B; app:dg implementation
-    notes: indices are sorted to keep temporal order.  Keeps everything when
+    Alg. 1 step B: I <- R_E(s, B - w) with per-head top-B; App. "Draft-guided eviction
+    implementation": indices are sorted to keep temporal order.  Keeps everything when
     n_select >= C.
     """
     C = pooled.shape[0]
@@ -127,7 +148,7 @@ def select_topb(pooled: np.ndarray, n_select: int) -> np.ndarray:
 
 
 def compact(k_rows: np.ndarray, v_rows: np.ndarray, idx: np.ndarray, C: int):
-    """[retained past, ascending] || [window + draft tail] (app:dg implementation notes)."""
+    """[retained past, ascending] || [window + draft tail] (App. "Draft-guided eviction implementation", implementation notes)."""
     N = k_rows.shape[0]
     keep = np.concatenate([np.asarray(idx, np.int64), np.arange(C, N)])
     return k_rows[keep].copy(), v_rows[keep].copy()
@@ -184,7 +205,7 @@ def h2o_colsum(q_all, k, kv_offsets, n_q_heads: int, n_kv_heads: int, block: int
 
     colsum[h][j] = (1/G) * sum_g sum_{p = j}^{N-1} softmax_j(q_{g,p} K^T / sqrt(d)):
     the causal attention every cached row (all prefill rows plus the k draft rows)
-    pays to key j (tab:complexity footnote a), meaned over the GQA group.
+    pays to key j (Table "Complexity and measured overhead", footnote a), meaned over the GQA group.
     """
     q_all = as_f64(q_all)
     k = as_f64(k)
@@ -216,14 +237,14 @@ def h2o_select(colsum_row: np.ndarray, budget: int, n_recent: int) -> np.ndarray
 
 def streaming_select(N: int, n_sink: int, n_recent: int) -> np.ndarray:
     """StreamingLLM: keep the first n_sink rows (attention sinks) and the last n_recent
-    rows; no scores (Sec. 6 baselines; app:analysis: four sinks and a recency window).
+    rows; no scores (Sec. 6 baselines; App. "Additional analysis": four sinks and a recency window).
     Returns the kept sink indices; the recent rows are the protected tail."""
     C = max(N - n_recent, 0)
     return np.arange(min(n_sink, C), dtype=np.int64)
 
 
 def pyramid_budgets(B: int, w: int, n_layers: int, beta: int = 20) -> np.ndarray:
-    """PyramidKV per-layer total budgets B_l (app:analysis, discrete schedule).
+    """PyramidKV per-layer total budgets B_l (App. "Additional analysis", discrete schedule).
 
     c = B - w past tokens; the ramp starts at max = 2c - floor(c/beta) on layer 0 and
     falls by steps = floor((max - min) / (n_layers - 1)) per layer, min = floor(c/beta)
@@ -238,7 +259,7 @@ def pyramid_budgets(B: int, w: int, n_layers: int, beta: int = 20) -> np.ndarray
 
 
 # ---------------------------------------------------------------------------------------
-# Identities used to check compaction (Eq. 1 / eq:evict-mass, eq:match)
+# Identities used to check compaction (Eq. 1 / the eviction-mass equation / the attention-matching loss)
 # ---------------------------------------------------------------------------------------
 def attention_output(qrow: np.ndarray, keys: np.ndarray, vals: np.ndarray) -> np.ndarray:
     """o = sum_j softmax_j(q . k_j / sqrt(d)) v_j over the given keys."""
@@ -250,7 +271,7 @@ def attention_output(qrow: np.ndarray, keys: np.ndarray, vals: np.ndarray) -> np
 
 
 def evicted_mass(qrow: np.ndarray, keys: np.ndarray, evicted: np.ndarray) -> float:
-    """m(E) = sum_{j in E} softmax_j(q . k_j / sqrt(d)) (eq:evict-mass, eq:match rho_q)."""
+    """m(E) = sum_{j in E} softmax_j(q . k_j / sqrt(d)) (the eviction-mass equation; rho_q of the attention-matching loss)."""
     d = keys.shape[1]
     x = keys @ as_f64(qrow) / math.sqrt(d)
     a = np.exp(x - x.max())
@@ -259,7 +280,7 @@ def evicted_mass(qrow: np.ndarray, keys: np.ndarray, evicted: np.ndarray) -> flo
 
 
 def log_partition(qrow: np.ndarray, keys: np.ndarray) -> float:
-    """log Z(q) = log sum_j exp(q . k_j / sqrt(d)) (eq:match)."""
+    """log Z(q) = log sum_j exp(q . k_j / sqrt(d)) (attention-matching loss, App. "Attention-matching loss")."""
     d = keys.shape[1]
     x = keys @ as_f64(qrow) / math.sqrt(d)
     m = x.max()

@@ -22,7 +22,7 @@ from . import _lib
 from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  # noqa: F401
                    ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
 
-__all__ = ["Geometry", "score", "select_topb", "select_compact", "select_streaming", "compact", "h2o_colsum",
+__all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact", "select_streaming", "compact", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
 
@@ -113,6 +113,17 @@ def score(geom: Geometry, rows: int, q, k, raw=None, ws=None, stream=None):
     ws = _workspace(geom, OP_SCORE, ws)
     _lib.check(_lib.lib().dge_score(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k), _ptr(raw),
                                     _ptr(ws), ws.numel(), _stream(stream)), "dge_score")
+    return raw
+
+
+def score_lse(geom: Geometry, rows: int, q, k, row_lse, raw=None, stream=None):
+    """dge_score_lse: dge_score with caller-supplied scoring-row log-sum-exp (one pass
+    over K).  row_lse is [H_q][batch * n_rows] float32.  Returns raw [H_kv][T]."""
+    torch = _torch()
+    if raw is None:
+        raw = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=geom.device)
+    _lib.check(_lib.lib().dge_score_lse(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k), _ptr(row_lse),
+                                        _ptr(raw), _stream(stream)), "dge_score_lse")
     return raw
 
 

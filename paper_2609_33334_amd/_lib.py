@@ -18,7 +18,7 @@ OP_SCORE, OP_SELECT, OP_H2O = 0, 1, 2
 ABI_VERSION = 1
 
 # every entry point declared in include/dge.h
-EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_score",
+EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_score", "dge_score_lse",
            "dge_select_topb", "dge_select_compact", "dge_select_streaming", "dge_compact", "dge_h2o_colsum",
            "dge_pyramid_budgets")
 
@@ -66,6 +66,8 @@ def lib() -> ctypes.CDLL:
     L.dge_workspace_size.argtypes = [GP, c_int32, POINTER(c_size_t)]
     L.dge_score.restype = c_int
     L.dge_score.argtypes = [GP, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+    L.dge_score_lse.restype = c_int
+    L.dge_score_lse.argtypes = [GP, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
     L.dge_select_topb.restype = c_int
     L.dge_select_topb.argtypes = [GP, c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                   c_void_p, c_size_t, c_void_p]

@@ -99,7 +99,24 @@ dge_status_t dge_score(const dge_geom_t* geom, int32_t rows, const void* q, cons
   if (p.n_rows <= 0) return DGE_ERR_INVALID;
   if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::score_workspace_bytes(*geom, p))
     return DGE_ERR_WORKSPACE;
-  return hip_status(dge::launch_score(*geom, p, q, k, raw, ws, stream));
+  return hip_status(dge::launch_score(*geom, p, q, k, nullptr, raw, ws, stream));
+}
+
+dge_status_t dge_score_lse(const dge_geom_t* geom, int32_t rows, const void* q, const void* k,
+                           const float* row_lse, float* raw, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (rows < DGE_ROWS_WINDOW_DRAFT || rows > DGE_ROWS_WINDOW) return DGE_ERR_INVALID;
+  if (!q || !k || !raw || !row_lse || !aligned16(q) || !aligned16(k) || !aligned16(raw) ||
+      !aligned16(row_lse))
+    return DGE_ERR_INVALID;
+  for (int b = 0; b < geom->batch; ++b)
+    if (seq_rows(geom, b) < (int64_t)geom->window + geom->k_draft || seq_rows(geom, b) < 1)
+      return DGE_ERR_INVALID;
+  const ScorePlan p = dge::plan_score(*geom, rows);
+  if (p.n_rows <= 0) return DGE_ERR_INVALID;
+  if (p.groups != 1) return DGE_ERR_UNSUPPORTED;
+  return hip_status(dge::launch_score(*geom, p, q, k, row_lse, raw, nullptr, stream));
 }
 
 dge_status_t dge_select_topb(const dge_geom_t* geom, const float* scores, int32_t pool_kernel,

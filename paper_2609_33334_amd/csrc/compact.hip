@@ -1,4 +1,4 @@
-// Cache compaction (Alg. 1 step C; app:dg implementation notes):
+// Cache compaction (Alg. 1 step C; App. "Draft-guided eviction implementation", implementation notes):
 //   out[b][h] = [ K[idx[b][h][0..n_kept)] , K[C_b .. N_b) , zero rows up to n_select + n_tail ]
 // and the same for V.  Rows are copied as raw bytes, so the result is bit-exact for
 // any element type.  Each thread moves one 16-byte piece of one row of K and the
@@ -17,7 +17,7 @@ struct CompactArgs {
   const char* v;
   char* k_out;
   char* v_out;
-  const int64_t* offs;
+  SeqOffsets offs;
   int64_t head_stride_bytes;
   int n_kv_heads, n_select, n_tail, n_out;
 };
@@ -77,7 +77,7 @@ hipError_t launch_compact(const dge_geom_t& g, const int32_t* idx, const int32_t
   a.v = reinterpret_cast<const char*>(v);
   a.k_out = reinterpret_cast<char*>(k_out);
   a.v_out = reinterpret_cast<char*>(v_out);
-  a.offs = g.kv_offsets;
+  a.offs = seq_offsets(g);
   a.head_stride_bytes = g.kv_head_stride * elt;
   a.n_kv_heads = g.n_kv_heads;
   a.n_select = n_select;

@@ -94,4 +94,31 @@ __device__ __forceinline__ float rescale(float m, float mx) {
   return m == mx ? 1.0f : fast_exp2(m - mx);
 }
 
+// XCD-aware work mapping.  The command processor hands workgroups to the 8 XCDs of an
+// MI355X round-robin by linear block id, and each XCD has its own L2.  Grids that use
+// this mapping are 1-D with a multiple of 8 blocks; block L runs on XCD L % 8 and takes
+// unit (L % 8) * per + L / 8, so every XCD owns one contiguous range of units (units
+// that share inputs -- the chunks of one KV head -- then share one L2).  Units at or
+// beyond `total` belong to no work and exit.
+constexpr int kXcds = 8;
+__host__ __device__ __forceinline__ int xcd_per(int total) { return (total + kXcds - 1) / kXcds; }
+__host__ __device__ __forceinline__ int xcd_grid(int total) { return kXcds * xcd_per(total); }
+__device__ __forceinline__ int xcd_unit(int total) {
+  const int L = (int)blockIdx.x;
+  return (L % kXcds) * xcd_per(total) + L / kXcds;
+}
+
+// Sequence offsets as a kernel argument: up to kInlineSeqs sequences travel by value
+// in the argument block (read through the scalar cache, no dependent global load at
+// kernel start); larger batches read the device array.
+constexpr int kInlineSeqs = 16;
+struct SeqOffsets {
+  const int64_t* dev;
+  int64_t inl[kInlineSeqs + 1];
+  int batch;
+  __device__ __forceinline__ int64_t operator[](int i) const {
+    return batch <= kInlineSeqs ? inl[i] : dev[i];
+  }
+};
+
 }  // namespace dge

@@ -23,13 +23,15 @@ struct ScorePlan {
   int n_chunks;        // workgroups per (sequence, KV head)
 };
 
+struct SeqOffsets;
+SeqOffsets seq_offsets(const dge_geom_t& g);
 int64_t total_rows(const dge_geom_t& g);
 int64_t max_seq_rows(const dge_geom_t& g);
 ScorePlan plan_score(const dge_geom_t& g, int rows_mode);
 size_t score_workspace_bytes(const dge_geom_t& g, const ScorePlan& p);
 
 hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, const void* k,
-                        float* raw, void* ws, hipStream_t stream);
+                        const float* row_lse, float* raw, void* ws, hipStream_t stream);
 
 size_t select_workspace_bytes(const dge_geom_t& g);
 hipError_t launch_select_topb(const dge_geom_t& g, const float* scores, int pool_kernel,

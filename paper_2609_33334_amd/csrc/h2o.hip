@@ -1,4 +1,4 @@
-// H2O accumulated attention (tab:complexity footnote a): the causal softmax of every
+// H2O accumulated attention (Table "Complexity and measured overhead", footnote a): the causal softmax of every
 // cached row, summed down each key column and meaned over the GQA group,
 //   colsum[h][j] = (1/G) sum_g sum_{p >= j} exp(q_{g,p} . k_j / sqrt(d) - lse_{g,p}).
 //
@@ -25,7 +25,7 @@ struct H2oArgs {
   const float* lse;     // [H_q][T] natural log
   float* lse_out;       // workspace [H_q][T] (when computing)
   float* colsum;        // [H_kv][T]
-  const int64_t* offs;
+  SeqOffsets offs;
   int64_t kv_head_stride;
   int64_t total_rows;
   int n_q_heads, n_kv_heads, G;
@@ -138,7 +138,7 @@ hipError_t launch_h2o(const dge_geom_t& g, const void* q_all, const void* k, con
   a.q = reinterpret_cast<const bf16_t*>(q_all);
   a.k = reinterpret_cast<const bf16_t*>(k);
   a.colsum = colsum;
-  a.offs = g.kv_offsets;
+  a.offs = seq_offsets(g);
   a.kv_head_stride = g.kv_head_stride;
   a.total_rows = total_rows(g);
   a.n_q_heads = g.n_q_heads;

@@ -1,4 +1,4 @@
-// Window / draft scoring of every cached key (Alg. 1 step B; app:diagnostics).
+// Window / draft scoring of every cached key (Alg. 1 step B; App. "Diagnostic details").
 //
 //   raw[h][j] = (1/G) sum_{g in group h} sum_r softmax_j(q_{g,r} . k_j / sqrt(d)),
 //   softmax over keys j <= p_r (causal), fp32 after the bf16/fp32 product.
@@ -12,6 +12,10 @@
 //   3. colsum: each workgroup streams its chunk again, P = 2^(x - c_r), sums over all
 //              rows of the group and writes raw[] (the K slab of one layer, 8-34 MB at
 //              Llama-3-8B geometry, is still in the 256 MB Infinity Cache).
+//
+// Workgroups are laid out XCD-aware (see xcd_unit): the chunks of one KV head share an
+// XCD, so its query block is fetched into one L2, and the colsum pass finds each chunk
+// in the L2 that streamed it during the stats pass.
 //
 // Work split inside a workgroup (4 wavefronts, one KV head, one chunk of keys):
 // - The G * n_rows query rows form 16-row tiles; wavefront w owns tiles w, w+4, w+8...
@@ -42,11 +46,12 @@ struct ScoreArgs {
   float* raw;
   float2* partial;   // [batch][H_kv][n_chunks][M_pad] (max, sum) per chunk, log2 domain
   float* rowc;       // [batch][H_kv][M_pad]  log2 of each row's softmax normaliser
-  const int64_t* offs;
+  const float* lse_in;      // optional [H_q][batch * n_rows] natural-log row LSE
+  SeqOffsets offs;
   int64_t kv_head_stride;   // elements
   int64_t q_head_stride;    // elements between query heads = batch * n_rows * D
   int64_t total_rows;       // T
-  int n_kv_heads, G, n_rows, p0_from_end;
+  int n_kv_heads, batch, G, n_rows, p0_from_end;
   int M, M_pad, n_tiles, groups, iters, chunk_keys, n_chunks;
   float scale_log2;         // log2(e) / sqrt(d)
   float inv_G;
@@ -122,7 +127,11 @@ template <typename T, int D, int MTW>
 __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int units = a.n_chunks * a.n_kv_heads * a.batch;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int chunk = unit % a.n_chunks, h = (unit / a.n_chunks) % a.n_kv_heads,
+            b = unit / (a.n_chunks * a.n_kv_heads);
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
   const int c0 = chunk * a.chunk_keys;
@@ -152,32 +161,35 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MTW; ++mt) { mrow[mt] = -INFINITY; srow[mt] = 0.0f; }
 
-    uint4 st[KTl::kPerThread];
-    ktile_load<T, D>(kb, c0, N, tid, st);
-    for (int j0 = c0; j0 < c1; j0 += KT) {
-      __syncthreads();
-      ktile_store<T, D>(lds, tid, st);
-      __syncthreads();
-      if (j0 + KT < c1) ktile_load<T, D>(kb, j0 + KT, N, tid, st);
+    // two K tiles in flight per workgroup: tile t+2 loads while tile t is consumed
+    uint4 stA[KTl::kPerThread], stB[KTl::kPerThread];
+    ktile_load<T, D>(kb, c0, N, tid, stA);
+    if (c0 + KT < c1) ktile_load<T, D>(kb, c0 + KT, N, tid, stB);
+    auto consume = [&](int j0) {
       // no key of this tile is past the sequence or beyond any row's position
       const bool need_mask = (j0 + KT - 1 > p0);
-#pragma unroll
+#pragma unroll 2
       for (int sub = 0; sub < KT / 16; ++sub) {
         uint4 kf[NS];
 #pragma unroll
         for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
+        // MTW independent accumulation chains, issued k-step-major
+        f32x4_t acc[MTW];
+#pragma unroll
+        for (int mt = 0; mt < MTW; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+          for (int mt = 0; mt < MTW; ++mt) acc[mt] = mma_step(T{}, kf[s], qf[mt][s], acc[mt]);
+        // acc[mt][t] = logit of key j0 + sub*16 + 4*g16 + t for this lane's row
 #pragma unroll
         for (int mt = 0; mt < MTW; ++mt) {
-          if (tile0 + wv + 4 * mt >= a.n_tiles) continue;   // wave-uniform
-          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s = 0; s < NS; ++s) acc = mma_step(T{}, kf[s], qf[mt][s], acc);
-          // acc[t] = logit of key j0 + sub*16 + 4*g16 + t for this lane's row
           float x[4];
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            x[t] = acc[t] * a.scale_log2;
-            if (need_mask) {
+          for (int t = 0; t < 4; ++t) x[t] = acc[mt][t] * a.scale_log2;
+          if (need_mask) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
               const int j = j0 + sub * 16 + 4 * g16 + t;
               x[t] = (live[mt] && j < N && j <= pos[mt]) ? x[t] : -INFINITY;
             }
@@ -189,11 +201,23 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
           mrow[mt] = mx;
         }
       }
+    };
+    for (int j0 = c0; j0 < c1; j0 += 2 * KT) {
+      __syncthreads();
+      ktile_store<T, D>(lds, tid, stA);
+      __syncthreads();
+      if (j0 + 2 * KT < c1) ktile_load<T, D>(kb, j0 + 2 * KT, N, tid, stA);
+      consume(j0);
+      if (j0 + KT >= c1) break;
+      __syncthreads();
+      ktile_store<T, D>(lds, tid, stB);
+      __syncthreads();
+      if (j0 + 3 * KT < c1) ktile_load<T, D>(kb, j0 + 3 * KT, N, tid, stB);
+      consume(j0 + KT);
     }
     // merge the four lane groups that hold the same row
 #pragma unroll
     for (int mt = 0; mt < MTW; ++mt) {
-      if (tile0 + wv + 4 * mt >= a.n_tiles) continue;
       float m = mrow[mt], s = srow[mt];
       const float mx = fmaxf(fmaxf(m, shfl_xor_f<16>(m)), fmaxf(shfl_xor_f<32>(m), shfl_xor_f<48>(m)));
       s *= rescale(m, mx);
@@ -240,7 +264,11 @@ template <typename T, int D, int MTW>
 __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int units = a.n_chunks * a.n_kv_heads * a.batch;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int chunk = unit % a.n_chunks, h = (unit / a.n_chunks) % a.n_kv_heads,
+            b = unit / (a.n_chunks * a.n_kv_heads);
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
   const int c0 = chunk * a.chunk_keys;
@@ -268,38 +296,45 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int m = (tile0 + wv + 4 * mt) * 16 + 4 * g16 + t;
-        cr[mt][t] = m < a.M ? rowc[m] : INFINITY;
+        if (a.lse_in != nullptr) {
+          const int g = m / a.n_rows, r = m - (m / a.n_rows) * a.n_rows;
+          cr[mt][t] = m < a.M ? a.lse_in[(int64_t)(h * a.G + g) * (a.q_head_stride / D) +
+                                         b * a.n_rows + r] * kLog2e
+                              : INFINITY;
+        } else {
+          cr[mt][t] = m < a.M ? rowc[m] : INFINITY;
+        }
         pos[mt][t] = p0 + (m < a.M ? m % a.n_rows : 0);
       }
 
-    uint4 st[KTl::kPerThread];
-    ktile_load<T, D>(kb, c0, N, tid, st);
-    for (int j0 = c0; j0 < c1; j0 += KT) {
-      __syncthreads();
-      ktile_store<T, D>(lds, tid, st);
-      __syncthreads();
-      if (j0 + KT < c1) ktile_load<T, D>(kb, j0 + KT, N, tid, st);
+    uint4 stA[KTl::kPerThread], stB[KTl::kPerThread];
+    ktile_load<T, D>(kb, c0, N, tid, stA);
+    if (c0 + KT < c1) ktile_load<T, D>(kb, c0 + KT, N, tid, stB);
+    auto consume = [&](int j0) {
       const bool need_mask = (j0 + KT - 1 > p0);
-#pragma unroll
+#pragma unroll 2
       for (int sub = 0; sub < KT / 16; ++sub) {
         uint4 kf[NS];
 #pragma unroll
         for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
+        f32x4_t acc[MTW];
+#pragma unroll
+        for (int mt = 0; mt < MTW; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+          for (int mt = 0; mt < MTW; ++mt) acc[mt] = mma_step(T{}, qf[mt][s], kf[s], acc[mt]);
+        // acc[mt][t] = logit of row (tile*16 + 4*g16 + t) for key j0 + sub*16 + c16
         const int j = j0 + sub * 16 + c16;
         float colp = 0.0f;
 #pragma unroll
-        for (int mt = 0; mt < MTW; ++mt) {
-          if (tile0 + wv + 4 * mt >= a.n_tiles) continue;   // wave-uniform
-          f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s = 0; s < NS; ++s) acc = mma_step(T{}, qf[mt][s], kf[s], acc);
+        for (int mt = 0; mt < MTW; ++mt)
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            float p = fast_exp2(fmaf(acc[t], a.scale_log2, -cr[mt][t]));
+            float p = fast_exp2(fmaf(acc[mt][t], a.scale_log2, -cr[mt][t]));
             if (need_mask) p = (j < N && j <= pos[mt][t]) ? p : 0.0f;
             colp += p;
           }
-        }
         colp += shfl_xor_f<16>(colp);
         colp += shfl_xor_f<32>(colp);
         if (g16 == 0) red[wv][sub * 16 + c16] = colp;
@@ -310,6 +345,19 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
         if (grp == 0) out[j0 + tid] = v * a.inv_G;
         else out[j0 + tid] += v * a.inv_G;
       }
+    };
+    for (int j0 = c0; j0 < c1; j0 += 2 * KT) {
+      __syncthreads();
+      ktile_store<T, D>(lds, tid, stA);
+      __syncthreads();
+      if (j0 + 2 * KT < c1) ktile_load<T, D>(kb, j0 + 2 * KT, N, tid, stA);
+      consume(j0);
+      if (j0 + KT >= c1) break;
+      __syncthreads();
+      ktile_store<T, D>(lds, tid, stB);
+      __syncthreads();
+      if (j0 + 3 * KT < c1) ktile_load<T, D>(kb, j0 + 3 * KT, N, tid, stB);
+      consume(j0 + KT);
     }
     __syncthreads();
   }
@@ -317,7 +365,11 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
 
 template <typename T, int D, int MTW>
 hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st) {
-  dim3 grid(a.n_chunks, g.n_kv_heads, g.batch);
+  const dim3 grid(xcd_grid(a.n_chunks * g.n_kv_heads * g.batch));
+  if (a.lse_in != nullptr) {   // normalisers supplied: one pass over K
+    hipLaunchKernelGGL((score_colsum_kernel<T, D, MTW>), grid, dim3(kThreads), 0, st, a);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((score_stats_kernel<T, D, MTW>), grid, dim3(kThreads), 0, st, a);
   hipLaunchKernelGGL(score_reduce_kernel, dim3(a.M_pad / 4, g.n_kv_heads, g.batch), dim3(256), 0,
                      st, a);
@@ -350,6 +402,15 @@ int max_mtw(const dge_geom_t& g) {
 
 }  // namespace
 
+SeqOffsets seq_offsets(const dge_geom_t& g) {
+  SeqOffsets o{};
+  o.dev = g.kv_offsets;
+  o.batch = g.batch;
+  if (g.batch <= kInlineSeqs)
+    for (int b = 0; b <= g.batch; ++b) o.inl[b] = g.kv_offsets_host[b];
+  return o;
+}
+
 int64_t total_rows(const dge_geom_t& g) { return g.kv_offsets_host[g.batch]; }
 
 int64_t max_seq_rows(const dge_geom_t& g) {
@@ -377,10 +438,10 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
   p.groups = per_wave <= cap ? 1 : (per_wave + cap - 1) / cap;
   p.mt = (per_wave + p.groups - 1) / p.groups;
   if (p.mt < 1) p.mt = 1;
-  // Enough workgroups to cover the chip a few times; more keys per workgroup once the
-  // layer is large (amortises the query-fragment loads).
+  // About one resident round of workgroups (two per compute unit): every workgroup
+  // loads its query fragments once and streams several 64-key tiles with two in flight.
   const int64_t tiles_total = (int64_t)g.n_kv_heads * ((total_rows(g) + KT - 1) / KT);
-  int iters = (int)(tiles_total / 1024);
+  int iters = (int)((tiles_total + 511) / 512);
   iters = iters < 1 ? 1 : (iters > 16 ? 16 : iters);
   p.tiles_per_wave = iters;
   p.chunk_keys = KT * iters;
@@ -396,20 +457,23 @@ size_t score_workspace_bytes(const dge_geom_t& g, const ScorePlan& p) {
 }
 
 hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, const void* k,
-                        float* raw, void* ws, hipStream_t st) {
+                        const float* row_lse, float* raw, void* ws, hipStream_t st) {
   ScoreArgs a{};
+  a.lse_in = row_lse;
   a.q = q;
   a.k = k;
   a.raw = raw;
   const size_t units = (size_t)g.batch * g.n_kv_heads;
   a.partial = reinterpret_cast<float2*>(ws);
-  a.rowc = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
-                                    units * p.n_chunks * p.M_pad * sizeof(float2));
-  a.offs = g.kv_offsets;
+  a.rowc = ws == nullptr ? nullptr
+                         : reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
+                                                    units * p.n_chunks * p.M_pad * sizeof(float2));
+  a.offs = seq_offsets(g);
   a.kv_head_stride = g.kv_head_stride;
   a.q_head_stride = (int64_t)g.batch * p.n_rows * g.head_dim;
   a.total_rows = total_rows(g);
   a.n_kv_heads = g.n_kv_heads;
+  a.batch = g.batch;
   a.G = g.n_q_heads / g.n_kv_heads;
   a.n_rows = p.n_rows;
   a.p0_from_end = p.p0_from_end;

@@ -22,10 +22,10 @@ struct SelectArgs {
   uint32_t* keys;        // workspace [batch][H_kv][key_stride]
   int32_t* idx;          // [batch][H_kv][n_select]
   int32_t* n_kept;       // [batch]
-  const int64_t* offs;
+  SeqOffsets offs;
   int64_t total_rows;
   int64_t key_stride;
-  int n_kv_heads, pool_half, n_tail, n_select;
+  int n_kv_heads, batch, pool_half, n_tail, n_select;
   // fused compaction (k_out == nullptr: selection only)
   const char* k;
   const char* v;
@@ -35,7 +35,7 @@ struct SelectArgs {
   int row_bytes, n_out, replicas, rows_per_rep;
 };
 
-constexpr int kMaxRowsPerRep = 1024;
+constexpr int kMaxRowsPerRep = 512;
 constexpr int kPoolHalo = 8;   // register path handles pool kernels up to 2*8+1
 
 __global__ __launch_bounds__(kSelThreads) void select_topb_kernel(SelectArgs a) {
@@ -180,11 +180,42 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* sh) {
   return before + inc - x;
 }
 
+// Find the digit d of a histogram at which the count from the top first reaches
+// `remaining`: above(d) < remaining <= above(d) + hist[d], above(d) = sum of the bins
+// above d.  Thread t scans bin group (THREADS-1-t), so an ordinary prefix sum over the
+// threads counts the keys above each group.  Writes {d, above(d)} to out[0..1].
+template <int THREADS>
+__device__ __forceinline__ void radix_find_digit(const uint32_t* hist, int nbins, int remaining,
+                                                uint32_t* scan_sh, int* out) {
+  const int per = nbins >= THREADS ? nbins / THREADS : 1;
+  const int grp = THREADS - 1 - (int)threadIdx.x;
+  const int b0 = grp * per;
+  uint32_t cnt = 0;
+  if (b0 < nbins)
+    for (int i = 0; i < per; ++i) cnt += hist[b0 + i];
+  uint32_t above = block_excl_scan<THREADS>(cnt, scan_sh);
+  if (b0 < nbins && cnt > 0) {
+    for (int i = per - 1; i >= 0; --i) {
+      const uint32_t c = hist[b0 + i];
+      if (above < (uint32_t)remaining && above + c >= (uint32_t)remaining) {
+        out[0] = b0 + i;
+        out[1] = (int)above;
+      }
+      above += c;
+    }
+  }
+  __syncthreads();
+}
+
 template <int THREADS, int KPT>
 __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) {
   constexpr int WAVES = THREADS / kWave;
   extern __shared__ __attribute__((aligned(16))) float stage[];
-  const int h = blockIdx.x / a.replicas, rep = blockIdx.x % a.replicas, b = blockIdx.y;
+  const int units = a.replicas * a.n_kv_heads * a.batch;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int rep = unit % a.replicas, h = (unit / a.replicas) % a.n_kv_heads,
+            b = unit / (a.replicas * a.n_kv_heads);
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
@@ -196,12 +227,13 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   if (writer)
     for (int r = nsel + tid; r < a.n_select; r += THREADS) out[r] = -1;
   // this replica's slice of output rows and the kept index of each
-  const int r0 = rep * a.rows_per_rep;
-  const int r1 = min(a.n_out, r0 + a.rows_per_rep);
   __shared__ int slice[kMaxRowsPerRep];
   __shared__ uint32_t scan_sh[WAVES];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t sh_digit, sh_above;
+  __shared__ uint32_t hist[4096];
+  __shared__ int sh_digit_above[2];
+  if (tid == 0) { sh_digit_above[0] = 0; sh_digit_above[1] = 0; }
+  const int r0 = rep * a.rows_per_rep;
+  const int r1 = min(a.n_out, r0 + a.rows_per_rep);
 
   if (nsel == C) {
     // every candidate is kept, in order
@@ -213,7 +245,18 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
     const int base = tid * KPT;
     uint32_t key[KPT];
     if (a.pool_half > 0) {
-      for (int j = tid; j < C; j += THREADS) stage[stage_pos(j)] = src[j];
+      // all of this thread's staging loads in flight at once, then the LDS stores
+      float sv[KPT];
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const int j = tid + THREADS * i;
+        sv[i] = j < C ? src[j] : 0.0f;
+      }
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const int j = tid + THREADS * i;
+        if (j < C) stage[stage_pos(j)] = sv[i];
+      }
       __syncthreads();
       // the segment and a halo of kPoolHalo on each side, indices clamped into [0, C):
       // a clamped index repeats a candidate that is inside the window anyway, so the
@@ -228,72 +271,35 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
 #pragma unroll
         for (int q = 1; q <= kPoolHalo; ++q)
           if (q <= a.pool_half) m = fmaxf(m, fmaxf(w[i + kPoolHalo - q], w[i + kPoolHalo + q]));
-        key[i] = __float_as_uint(m);
+        key[i] = __float_as_uint(m) & 0x7fffffffu;
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < KPT; ++i) key[i] = base + i < C ? __float_as_uint(src[base + i]) : 0u;
+      for (int i = 0; i < KPT; ++i)
+        key[i] = base + i < C ? (__float_as_uint(src[base + i]) & 0x7fffffffu) : 0u;
     }
 
-    if (tid == 0) { sh_digit = 0; sh_above = 0; }
-    uint32_t prefix = 0, mask = 0;
+    // three radix passes over bits 30..19, 18..9 and 8..0 (bit 31 is zero for
+    // non-negative scores); the wide first digit splits every binade into 16 bins, so
+    // clustered scores do not pile onto a few histogram addresses
+    uint32_t prefix = 0, mask = 0x80000000u;
     int remaining = nsel;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      if (tid < 256) hist[tid] = 0;
+#pragma unroll
+    for (int pass = 0; pass < 3; ++pass) {
+      const int shift = pass == 0 ? 19 : (pass == 1 ? 9 : 0);
+      const int nbins = pass == 0 ? 4096 : (pass == 1 ? 1024 : 512);
+      for (int i = tid; i < nbins; i += THREADS) hist[i] = 0;
       __syncthreads();
-      if (shift == 24) {
-        // leading digit: nearly every score shares one or a few values, so same-address
-        // atomics would serialise; count each distinct digit of a wavefront with one
-        // ballot (at most four rounds), then fall back to per-lane atomics
 #pragma unroll
-        for (int i = 0; i < KPT; ++i) {
-          bool pend = base + i < C;
-          const uint32_t dg = key[i] >> 24;
-#pragma unroll
-          for (int round = 0; round < 4; ++round) {
-            const uint64_t pm = __ballot(pend);
-            if (pm == 0) break;
-            const uint32_t lead = __builtin_amdgcn_readlane(dg, __builtin_ctzll(pm));
-            const uint64_t sm = __ballot(pend && dg == lead);
-            if (lane == 0) atomicAdd(&hist[lead], (uint32_t)__popcll(sm));
-            pend = pend && dg != lead;
-          }
-          if (pend) atomicAdd(&hist[dg], 1u);
-        }
-      } else {
-        // later digits are spread out: independent per-lane atomics (no return value)
-#pragma unroll
-        for (int i = 0; i < KPT; ++i) {
-          const bool in = base + i < C && (key[i] & mask) == prefix;
-          if (in) atomicAdd(&hist[(key[i] >> shift) & 255u], 1u);
-        }
+      for (int i = 0; i < KPT; ++i) {
+        const bool in = base + i < C && (key[i] & mask) == prefix;
+        if (in) atomicAdd(&hist[(key[i] >> shift) & (uint32_t)(nbins - 1)], 1u);
       }
       __syncthreads();
-      if (wv == 0) {
-        uint32_t c[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) c[i] = hist[4 * lane + i];
-        const uint32_t tot = c[0] + c[1] + c[2] + c[3];
-        uint32_t suf = tot;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const uint32_t v = __shfl_down(suf, o, 64);
-          if (lane + o < 64) suf += v;
-        }
-        uint32_t above = suf - tot;
-#pragma unroll
-        for (int i = 3; i >= 0; --i) {
-          if (above < (uint32_t)remaining && above + c[i] >= (uint32_t)remaining) {
-            sh_digit = 4 * lane + i;
-            sh_above = above;
-          }
-          above += c[i];
-        }
-      }
-      __syncthreads();
-      remaining -= (int)sh_above;
-      prefix |= sh_digit << shift;
-      mask |= 255u << shift;
+      radix_find_digit<THREADS>(hist, nbins, remaining, scan_sh, sh_digit_above);
+      remaining -= sh_digit_above[1];
+      prefix |= (uint32_t)sh_digit_above[0] << shift;
+      mask |= (uint32_t)(nbins - 1) << shift;
       __syncthreads();
     }
     const uint32_t thr = prefix;   // the nsel-th largest key
@@ -353,7 +359,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
 }
 
 __global__ __launch_bounds__(256) void select_streaming_kernel(int32_t* idx, int32_t* n_kept,
-                                                                const int64_t* offs, int n_kv_heads,
+                                                                SeqOffsets offs, int n_kv_heads,
                                                                 int n_sink, int n_recent) {
   const int h = blockIdx.x, b = blockIdx.y;
   const int N = (int)(offs[b + 1] - offs[b]);
@@ -383,10 +389,11 @@ SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, 
   a.keys = reinterpret_cast<uint32_t*>(ws);
   a.idx = idx;
   a.n_kept = n_kept;
-  a.offs = g.kv_offsets;
+  a.offs = seq_offsets(g);
   a.total_rows = total_rows(g);
   a.key_stride = (max_seq_rows(g) + 63) / 64 * 64;
   a.n_kv_heads = g.n_kv_heads;
+  a.batch = g.batch;
   a.pool_half = pool_kernel / 2;
   a.n_tail = n_tail;
   a.n_select = n_select;
@@ -401,7 +408,7 @@ SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, 
 bool launch_fast(const SelectArgs& a, const dge_geom_t& g, int64_t cmax, hipStream_t st,
                  hipError_t* err) {
   if (a.pool_half > kPoolHalo) return false;
-  const dim3 grid(g.n_kv_heads * a.replicas, g.batch);
+  const dim3 grid(xcd_grid(a.replicas * g.n_kv_heads * g.batch));
   const size_t lds = a.pool_half > 0 ? (size_t)stage_pos((int)(cmax > 0 ? cmax : 1)) * 4 + 64 : 0;
   if (cmax <= 1024) *err = launch_seg<256, 4>(a, grid, lds, st);
   else if (cmax <= 2048) *err = launch_seg<256, 8>(a, grid, lds, st);
@@ -470,7 +477,7 @@ hipError_t launch_select_compact(const dge_geom_t& g, const float* scores, int p
 hipError_t launch_select_streaming(const dge_geom_t& g, int n_sink, int n_recent, int32_t* idx,
                                    int32_t* n_kept, hipStream_t st) {
   hipLaunchKernelGGL(select_streaming_kernel, dim3(g.n_kv_heads, g.batch), dim3(256), 0, st, idx,
-                     n_kept, g.kv_offsets, g.n_kv_heads, n_sink, n_recent);
+                     n_kept, seq_offsets(g), g.n_kv_heads, n_sink, n_recent);
   return hipGetLastError();
 }
 

@@ -118,6 +118,9 @@ def test_score_validation(L):
     g.offs[1], g.offs[2] = 80, 70
     assert _score(L, g) == _lib.DGE_ERR_INVALID                          # decreasing offsets
     assert L.dge_score(None, 0, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == _lib.DGE_ERR_INVALID
+    assert L.dge_score_lse(_G().p, 0, FAKE, FAKE, None, FAKE, None) == _lib.DGE_ERR_INVALID
+    assert L.dge_score_lse(_G(d=96).p, 0, FAKE, FAKE, FAKE, FAKE, None) == _lib.DGE_ERR_UNSUPPORTED
+    assert L.dge_score_lse(_G(lens=(100, 9)).p, 0, FAKE, FAKE, FAKE, FAKE, None) == _lib.DGE_ERR_INVALID
 
 
 def test_workspace_size(L):

@@ -122,6 +122,22 @@ def test_score_c3_layer():
     check_scores(got, want, "c3/l5")
 
 
+@pytest.mark.parametrize("case", ["c2", "c2_ragged", "c1"])
+def test_score_lse_single_pass(case):
+    wl = {"c2": di.WORKLOADS["c2"], "c2_ragged": SCORE_CASES["c2_ragged"], "c1": di.WORKLOADS["c1"]}[case]
+    _log(f"score with supplied row LSE {case}")
+    x = di.make_layer(wl, with_v=False)
+    g = geom_of(wl)
+    lse = oracle.scoring_row_lse(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                 wl.k_draft)
+    q, k = to_dev(x.q_bits, wl.dtype), to_dev(x.k_bits, wl.dtype)
+    raw = dge.score_lse(g, dge.ROWS_WINDOW_DRAFT, q, k, torch.from_numpy(lse.astype(np.float32)).to(DEV))
+    torch.cuda.synchronize()
+    want = oracle.window_scores(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                wl.k_draft)
+    check_scores(raw.cpu().numpy(), want, f"score_lse {case}")
+
+
 def test_score_deterministic():
     wl = di.small_variant("c2", [2000, 900])
     x = di.make_layer(wl, with_v=False)

@@ -25,7 +25,7 @@ def _rand(shape, seed, scale=1.0):
 
 
 # ----------------------------------------------------------------------------------
-# PyramidKV: the paper's five worked examples (app:analysis)
+# PyramidKV: the paper's five worked examples (App. "Additional analysis")
 # ----------------------------------------------------------------------------------
 def test_pyramid_worked_examples():
     cases = json.load(open(os.path.join(GOLDEN, "pyramidkv_worked_examples.json")))["cases"]
@@ -113,6 +113,27 @@ def test_score_matches_torch_sdpa(mode):
             assert np.allclose(raw[h, s0:s0 + N], np.mean(cols, axis=0), rtol=1e-12, atol=1e-15)
 
 
+@pytest.mark.parametrize("mode", [oracle.ROWS_WINDOW_DRAFT, oracle.ROWS_DRAFT, oracle.ROWS_WINDOW])
+def test_scoring_row_lse_matches_torch_logsumexp(mode):
+    Hq, Hkv, d, w, kd = 4, 2, 16, 5, 2
+    offs = [0, 20, 51]
+    G = Hq // Hkv
+    nr = oracle.scoring_rows(10, w, kd, mode)[1]
+    q = _rand((Hq, 2 * nr, d), 24, 2.0)
+    k = _rand((Hkv, offs[-1], d), 25, 2.0)
+    lse = oracle.scoring_row_lse(q, k, offs, Hq, Hkv, w, kd, mode)
+    for b in range(2):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        p0, _ = oracle.scoring_rows(N, w, kd, mode)
+        for hq in range(Hq):
+            Q = torch.tensor(q[hq, b * nr:(b + 1) * nr])
+            K = torch.tensor(k[hq // G, s0:s0 + N])
+            x = (Q @ K.T) / math.sqrt(d)
+            mask = torch.arange(N)[None, :] > (p0 + torch.arange(nr))[:, None]
+            want = torch.logsumexp(x.masked_fill(mask, float("-inf")), dim=1).numpy()
+            assert np.allclose(lse[hq, b * nr:(b + 1) * nr], want, rtol=1e-13)
+
+
 def test_dgew_timing_invariance():
     # DGE-W keeps the window scorer and only moves the eviction step: the window rows'
     # scores of the prompt keys do not change when k draft rows are appended to the cache
@@ -187,7 +208,7 @@ def test_streaming_closed_form_c5():
 
 
 # ----------------------------------------------------------------------------------
-# Compaction: exact identities of Eq. 1 / eq:evict-mass and eq:match
+# Compaction: exact identities of Eq. 1, the eviction-mass equation and the attention-matching-loss equation
 # ----------------------------------------------------------------------------------
 def test_compaction_attention_identities():
     Hq, Hkv, d, w, kd, L = 4, 1, 16, 4, 2, 60
@@ -270,8 +291,8 @@ def test_bf16_rounding_matches_torch():
 
 
 def test_byte_accounting_pins_bf16_storage():
-    # app:complexity: 3.79 GiB (KV repeated to 32 heads) vs 0.95 GiB (8 KV heads) at L = 7762;
-    # intro: ~16 GiB for an 8B model at 128K; app:dg: ~60 MB of prompt queries per layer
+    # App. "Complexity and overheads": 3.79 GiB (KV repeated to 32 heads) vs 0.95 GiB (8 KV heads) at L = 7762;
+    # intro: ~16 GiB for an 8B model at 128K; App. "Draft-guided eviction implementation": ~60 MB of prompt queries per layer
     def kv_bytes(layers, H, L, d=128, elt=2):
         return layers * 2 * H * L * d * elt
     assert round(kv_bytes(32, 32, 7762) / 2 ** 30, 2) == 3.79
