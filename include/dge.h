@@ -95,7 +95,8 @@ const char *dge_status_string(int status);
 /* Bytes of device workspace the given operation needs for this geometry.
  * DGE_OP_SCORE: per-row softmax partials of dge_score (sized for w + k scoring rows).
  * DGE_OP_SELECT: radix keys of dge_select_topb.
- * DGE_OP_H2O: per-row log-sum-exp of dge_h2o_colsum when the caller supplies none.
+ * DGE_OP_H2O: partial column sums of dge_h2o_colsum, plus the per-row log-sum-exp
+ *             for calls where the caller supplies none.
  * Writes *bytes (host pointer).  Errors: DGE_ERR_INVALID for a bad geometry. */
 dge_status_t dge_workspace_size(const dge_geom_t *geom, int32_t op, size_t *bytes);
 
@@ -191,8 +192,10 @@ dge_status_t dge_compact(const dge_geom_t *geom, const int32_t *idx, const int32
  *            supplied by the caller (e.g. from its attention forward); when NULL the
  *            library computes it first into the workspace.
  *   colsum : [H_kv][T] float32 output; each sequence's colsum sums to N_b.
- *   ws     : dge_workspace_size(geom, DGE_OP_H2O) bytes when lse == NULL (else may be NULL).
- * Only bfloat16 inputs are supported (DGE_ERR_UNSUPPORTED otherwise). */
+ *   ws     : dge_workspace_size(geom, DGE_OP_H2O) bytes (per-segment partial column sums,
+ *            and the row LSE when lse == NULL).
+ * Only bfloat16 inputs with head_dim 128 are supported, and computing the LSE in the
+ * library needs G <= 4 query heads per KV head (DGE_ERR_UNSUPPORTED otherwise). */
 dge_status_t dge_h2o_colsum(const dge_geom_t *geom, const void *q_all, const void *k,
                             const float *lse, float *colsum, void *ws, size_t ws_bytes,
                             hipStream_t stream);

@@ -203,9 +203,8 @@ def h2o_colsum(geom: Geometry, q_all, k, lse=None, colsum=None, ws=None, stream=
     if colsum is None:
         colsum = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32,
                              device=geom.device)
-    if lse is None:
-        ws = _workspace(geom, OP_H2O, ws)
-    nbytes = 0 if ws is None else ws.numel()
+    ws = _workspace(geom, OP_H2O, ws)
+    nbytes = ws.numel()
     _lib.check(_lib.lib().dge_h2o_colsum(ctypes.byref(geom.c), _ptr(q_all), _ptr(k), _ptr(lse),
                                          _ptr(colsum), _ptr(ws), nbytes, _stream(stream)),
                "dge_h2o_colsum")

@@ -192,8 +192,8 @@ dge_status_t dge_h2o_colsum(const dge_geom_t* geom, const void* q_all, const voi
   if (!q_all || !k || !colsum || !aligned16(q_all) || !aligned16(k) || !aligned16(colsum) ||
       (lse && !aligned16(lse)))
     return DGE_ERR_INVALID;
-  if (lse == nullptr &&
-      (ws == nullptr || !aligned16(ws) || ws_bytes < dge::h2o_workspace_bytes(*geom)))
+  if (lse == nullptr && geom->n_q_heads / geom->n_kv_heads > 4) return DGE_ERR_UNSUPPORTED;
+  if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::h2o_workspace_bytes(*geom))
     return DGE_ERR_WORKSPACE;
   return hip_status(dge::launch_h2o(*geom, q_all, k, lse, colsum, ws, stream));
 }

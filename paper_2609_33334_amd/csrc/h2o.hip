@@ -1,15 +1,25 @@
-// H2O accumulated attention (Table "Complexity and measured overhead", footnote a): the causal softmax of every
-// cached row, summed down each key column and meaned over the GQA group,
+// H2O accumulated attention (Table "Complexity and measured overhead", footnote a): the
+// causal softmax of every cached row, summed down each key column and meaned over the
+// GQA group,
 //   colsum[h][j] = (1/G) sum_g sum_{p >= j} exp(q_{g,p} . k_j / sqrt(d) - lse_{g,p}).
 //
-// Two launches, both on the bf16 matrix cores:
-//   lse    (skipped when the caller passes its own): one wavefront per 16 query rows
-//          walks the keys j <= p with an online (max, sum) per row;
-//   colsum : one wavefront per 16-key tile keeps its K fragment in registers and walks
-//          the query rows p >= j of all G heads of its group; the column sum of P stays
-//          in the lanes (each lane owns 4 rows of one key column) until the very end,
-//          so the inner loop is MFMA + exp2 + add with no cross-lane traffic.
-// Workgroups with the longest column (small j) are issued first.
+// Two kernels on the bf16 matrix cores (v_mfma_f32_16x16x32_bf16):
+//
+// lse (skipped when the caller supplies it): a workgroup owns a pair of 64-row blocks
+//   (one from each end of the sequence, so every workgroup does the same causal work)
+//   of one KV head; wavefront g is query head g of the group and keeps its 4 row tiles
+//   of Q in registers.  64-key tiles of K are staged once in XOR-swizzled LDS and read
+//   by all G wavefronts.  The product is taken transposed (A = keys, B = query rows) so
+//   a lane holds 4 keys of one row and keeps that row's (max, sum) in registers.
+//
+// colsum: a workgroup owns a 128-key block and a 512-row segment of one KV head; each
+//   wavefront keeps two 16-key tiles of K in registers.  For every query head of the
+//   group, 64-row blocks of Q and their log-sum-exp are staged in LDS (double-buffered,
+//   next block prefetched into registers) and shared by the four wavefronts.  With
+//   A = query rows, a lane holds 4 rows of one key: P = 2^(x - lse) is summed in the
+//   lane and crosses lanes once, at the end of the segment.  A small reduction adds
+//   the segments' partial sums in a fixed order.
+// No atomics: every partial column sum is owned by exactly one wavefront.
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
 
@@ -17,7 +27,12 @@ namespace dge {
 namespace {
 
 constexpr int D = 128;
-constexpr int NS = RowChunks<bf16_t, D>::kSteps;
+constexpr int NS = RowChunks<bf16_t, D>::kSteps;   // 4 chunk steps of 32 elements
+constexpr int RB = 64;                              // rows per Q block (colsum) / lse block
+constexpr int KB = 128;                             // keys per colsum key block
+constexpr int KTL = 64;                             // keys per K tile (lse)
+constexpr int RowBytes = D * 2;
+constexpr int kMaxG = 4;                            // lse kernel: one wavefront per head
 
 struct H2oArgs {
   const bf16_t* q;      // [H_q][T][D]
@@ -28,108 +43,263 @@ struct H2oArgs {
   SeqOffsets offs;
   int64_t kv_head_stride;
   int64_t total_rows;
-  int n_q_heads, n_kv_heads, G;
+  int n_q_heads, n_kv_heads, G, batch;
+  int n_pairs;          // block pairs per (sequence, KV head)
   float scale_log2;
   float inv_G;
 };
 
-__global__ __launch_bounds__(256) void h2o_lse_kernel(H2oArgs a) {
-  const int rb = blockIdx.x, hq = blockIdx.y, b = blockIdx.z;
-  const int64_t s0 = a.offs[b];
-  const int N = (int)(a.offs[b + 1] - s0);
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int g16 = lane >> 4, c16 = lane & 15;
-  const int r0 = rb * 64 + wv * 16;
-  if (r0 >= N) return;
-  const int h = hq / a.G;
-  const bf16_t* qrow = a.q + (int64_t)hq * a.total_rows * D + (s0 + min(r0 + c16, N - 1)) * D;
-  uint4 qf[NS];
-#pragma unroll
-  for (int s = 0; s < NS; ++s) qf[s] = load16(qrow + chunk_elem<bf16_t, D>(s, g16));
-  const bf16_t* kb = a.k + (int64_t)h * a.kv_head_stride + s0 * D;
-  float m[4], sm[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { m[i] = -INFINITY; sm[i] = 0.0f; }
-  const int last = min(r0 + 15, N - 1);
-  for (int j0 = 0; j0 <= last; j0 += 16) {
-    const int j = j0 + c16;
-    const bf16_t* krow = kb + (int64_t)min(j, N - 1) * D;
-    uint4 kf[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) kf[s] = load16(krow + chunk_elem<bf16_t, D>(s, g16));
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < NS; ++s) acc = mma_step(bf16_t{}, qf[s], kf[s], acc);
-    const bool diag = j0 + 15 > r0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float x = acc[i] * a.scale_log2;
-      const int p = r0 + 4 * g16 + i;
-      if (!diag || j <= p) online_push(x, m[i], sm[i]);
-    }
-  }
+// 64 rows x 256 B staged with the 16-byte unit u of row r at u ^ (r % 16).
+__device__ __forceinline__ int swz(int r, int u) { return r * RowBytes + ((u ^ (r & 15)) * 16); }
+
+__device__ __forceinline__ uint4 lds_frag(const char* lds, int r, int s, int g16) {
+  return *reinterpret_cast<const uint4*>(lds + swz(r, s * 4 + g16));
+}
+
+// Global loads of a 64-row block (rows clamped to the sequence); 4 units per thread.
+__device__ __forceinline__ void block_load(const char* base, int r0, int N, int tid, uint4 (&st)[4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    float mm = m[i], ss = sm[i];
-    online_merge(mm, ss, shfl_xor_f<1>(mm), shfl_xor_f<1>(ss));
-    online_merge(mm, ss, shfl_xor_f<2>(mm), shfl_xor_f<2>(ss));
-    online_merge(mm, ss, shfl_xor_f<4>(mm), shfl_xor_f<4>(ss));
-    online_merge(mm, ss, shfl_xor_f<8>(mm), shfl_xor_f<8>(ss));
-    const int p = r0 + 4 * g16 + i;
-    if (c16 == 0 && p < N)
-      a.lse_out[(int64_t)hq * a.total_rows + s0 + p] = (mm + log2f(ss)) * 0.6931471805599453f;
+    const int e = tid + 256 * i;
+    const int r = e >> 4, u = e & 15;
+    st[i] = load16(base + (int64_t)min(r0 + r, N - 1) * RowBytes + u * 16);
   }
 }
 
-__global__ __launch_bounds__(256) void h2o_colsum_kernel(H2oArgs a, int n_blocks) {
-  const int kbk = n_blocks - 1 - (int)blockIdx.x;   // longest columns first
-  const int h = blockIdx.y, b = blockIdx.z;
+__device__ __forceinline__ void block_store(char* lds, int tid, const uint4 (&st)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = tid + 256 * i;
+    *reinterpret_cast<uint4*>(lds + swz(e >> 4, e & 15)) = st[i];
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Row log-sum-exp: one (row-block pair, KV head, sequence) per workgroup.
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void h2o_lse_kernel(H2oArgs a) {
+  const int units = a.n_pairs * a.n_kv_heads * a.batch;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int pair = unit % a.n_pairs, h = (unit / a.n_pairs) % a.n_kv_heads,
+            b = unit / (a.n_pairs * a.n_kv_heads);
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int nrb = (N + RB - 1) / RB;
+  if (pair >= (nrb + 1) / 2) return;        // a shorter sequence of a ragged batch
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g16 = lane >> 4, c16 = lane & 15;
-  const int j0 = kbk * 64 + wv * 16;
-  if (j0 >= N) return;
-  const int j = j0 + c16;
-  const bf16_t* krow = a.k + (int64_t)h * a.kv_head_stride + (s0 + min(j, N - 1)) * D;
-  uint4 kf[NS];
+  const bool active = wv < a.G;             // wavefront wv = query head h*G + wv
+  const int hq = h * a.G + (active ? wv : 0);
+  const char* kb = reinterpret_cast<const char*>(a.k + (int64_t)h * a.kv_head_stride + s0 * D);
+  const char* qb = reinterpret_cast<const char*>(a.q + (int64_t)hq * a.total_rows * D + s0 * D);
+  __shared__ __attribute__((aligned(16))) char lds[2][KTL * RowBytes];
+
+  for (int side = 0; side < 2; ++side) {
+    const int rb = side == 0 ? pair : nrb - 1 - pair;
+    if (side == 1 && rb == pair) break;     // odd count: the middle block once
+    if (rb >= nrb || rb < 0) break;
+    const int r0 = rb * RB;
+    // Q fragments of this wavefront's 4 row tiles (B operand: lane supplies row c16)
+    uint4 qf[4][NS];
 #pragma unroll
-  for (int s = 0; s < NS; ++s) kf[s] = load16(krow + chunk_elem<bf16_t, D>(s, g16));
-  float colp = 0.0f;
-  for (int g = 0; g < a.G; ++g) {
-    const int hq = h * a.G + g;
-    const bf16_t* qb = a.q + (int64_t)hq * a.total_rows * D + s0 * D;
-    const float* lb = a.lse + (int64_t)hq * a.total_rows + s0;
-    for (int p0 = j0; p0 < N; p0 += 16) {
-      const bf16_t* qrow = qb + (int64_t)min(p0 + c16, N - 1) * D;
-      uint4 qf[NS];
+    for (int rt = 0; rt < 4; ++rt) {
+      const char* row = qb + (int64_t)min(r0 + rt * 16 + c16, N - 1) * RowBytes;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) qf[s] = load16(qrow + chunk_elem<bf16_t, D>(s, g16));
-      float l2[4];
+      for (int s = 0; s < NS; ++s) qf[rt][s] = load16(row + (s * 4 + g16) * 16);
+    }
+    float m[4], sm[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) l2[i] = lb[min(p0 + 4 * g16 + i, N - 1)] * kLog2e;
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    for (int rt = 0; rt < 4; ++rt) { m[rt] = -INFINITY; sm[rt] = 0.0f; }
+    const int last = min(r0 + RB, N);       // keys [0, last) can be seen by this block
+    const int ntile = (last + KTL - 1) / KTL;
+    uint4 st[4];
+    block_load(kb, 0, N, tid, st);
+    for (int t = 0; t < ntile; ++t) {
+      char* buf = lds[t & 1];
+      block_store(buf, tid, st);
+      __syncthreads();
+      if (t + 1 < ntile) block_load(kb, (t + 1) * KTL, N, tid, st);
+      const int j0 = t * KTL;
+      const bool diag = j0 + KTL > r0;      // some key may be past some row
+      if (active) {
+#pragma unroll 2
+        for (int sub = 0; sub < KTL / 16; ++sub) {
+          uint4 kf[NS];
 #pragma unroll
-      for (int s = 0; s < NS; ++s) acc = mma_step(bf16_t{}, qf[s], kf[s], acc);
-      const bool edge = (p0 == j0) || (p0 + 15 >= N);
+          for (int s = 0; s < NS; ++s) kf[s] = lds_frag(buf, sub * 16 + c16, s, g16);
+          f32x4_t acc[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int p = p0 + 4 * g16 + i;
-        float pr = exp2f(fmaf(acc[i], a.scale_log2, -l2[i]));
-        if (edge) pr = (p < N && j <= p && j < N) ? pr : 0.0f;
-        colp += pr;
+          for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) acc[rt] = mma_step(bf16_t{}, kf[s], qf[rt][s], acc[rt]);
+          // acc[rt][i] = logit of key j0 + sub*16 + 4*g16 + i for row r0 + rt*16 + c16
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt) {
+            const int p = r0 + rt * 16 + c16;
+            float x[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              x[i] = acc[rt][i] * a.scale_log2;
+              if (diag) {
+                const int j = j0 + sub * 16 + 4 * g16 + i;
+                x[i] = (j <= p && j < N) ? x[i] : -INFINITY;
+              }
+            }
+            const float mx = fmaxf(fmaxf(m[rt], fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
+            const float base = mx == -INFINITY ? 0.0f : mx;
+            sm[rt] = sm[rt] * fast_exp2(m[rt] - base) + fast_exp2(x[0] - base) +
+                     fast_exp2(x[1] - base) + fast_exp2(x[2] - base) + fast_exp2(x[3] - base);
+            m[rt] = mx;
+          }
+        }
+      }
+      __syncthreads();
+    }
+    if (active) {
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        float mm = m[rt], ss = sm[rt];
+        const float mx = fmaxf(fmaxf(mm, shfl_xor_f<16>(mm)), fmaxf(shfl_xor_f<32>(mm), shfl_xor_f<48>(mm)));
+        ss *= rescale(mm, mx);
+        ss += shfl_xor_f<16>(ss);
+        ss += shfl_xor_f<32>(ss);
+        const int p = r0 + rt * 16 + c16;
+        if (g16 == 0 && p < N)
+          a.lse_out[(int64_t)hq * a.total_rows + s0 + p] = (mx + __log2f(ss)) * 0.6931471805599453f;
       }
     }
   }
-  colp += shfl_xor_f<16>(colp);
-  colp += shfl_xor_f<32>(colp);
-  if (g16 == 0 && j < N) a.colsum[(int64_t)h * a.total_rows + s0 + j] = colp * a.inv_G;
+}
+
+// ------------------------------------------------------------------------------------
+// Column sums.  Work unit = (128-key block kb, 512-row segment s, KV head, sequence):
+// the rows p >= 128*kb of segment s, for all G query heads of the group.  Units whose
+// segment ends before the key block starts, or starts past the sequence, exit at once;
+// every other unit is at most SEG rows x G heads, so the ~half of a causal grid that
+// has work is evenly loaded.  Each unit writes the partial column sums of its 128 keys
+// to part[s][h][j]; h2o_reduce_kernel adds the segments in a fixed order.
+// ------------------------------------------------------------------------------------
+constexpr int SEG = 512;
+
+__global__ __launch_bounds__(256) void h2o_colsum_kernel(H2oArgs a, float* part, int nkb_max,
+                                                         int nseg_max) {
+  const int units = nkb_max * nseg_max * a.n_kv_heads * a.batch;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int kblk = unit % nkb_max, seg = (unit / nkb_max) % nseg_max;
+  const int h = (unit / (nkb_max * nseg_max)) % a.n_kv_heads,
+            b = unit / (nkb_max * nseg_max * a.n_kv_heads);
+  const int64_t s0 = a.offs[b];
+  const int N = (int)(a.offs[b + 1] - s0);
+  const int k0 = kblk * KB;
+  const int seg_lo = seg * SEG, seg_hi = min(N, seg_lo + SEG);
+  if (k0 >= N || seg_lo >= N || seg_hi <= k0) return;     // no rows p >= k0 here
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int g16 = lane >> 4, c16 = lane & 15;
+  __shared__ __attribute__((aligned(16))) char qlds[2][RB * RowBytes];
+  __shared__ __attribute__((aligned(16))) float llds[2][RB];
+
+  // this wavefront's two 16-key tiles of K (B operand: lane supplies key c16)
+  const int ja = k0 + wv * 32 + c16, jb = ja + 16;
+  uint4 kfa[NS], kfb[NS];
+  {
+    const bf16_t* kh = a.k + (int64_t)h * a.kv_head_stride + s0 * D;
+    const char* ra = reinterpret_cast<const char*>(kh + (int64_t)min(ja, N - 1) * D);
+    const char* rbp = reinterpret_cast<const char*>(kh + (int64_t)min(jb, N - 1) * D);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      kfa[s] = load16(ra + (s * 4 + g16) * 16);
+      kfb[s] = load16(rbp + (s * 4 + g16) * 16);
+    }
+  }
+  float cola = 0.0f, colb = 0.0f;
+  const int rlo = max(seg_lo, k0 / RB * RB);   // first 64-row block with rows >= k0
+  const int per = (seg_hi - rlo + RB - 1) / RB;
+  const int nblk = per * a.G;                  // (head, row block) iterations
+  const int64_t qstride = a.total_rows * D;
+  const bf16_t* qh = a.q + (int64_t)(h * a.G) * qstride + s0 * D;
+  const float* lh = a.lse + (int64_t)(h * a.G) * a.total_rows + s0;
+  uint4 st[4];
+  float lst = 0.0f;
+  block_load(reinterpret_cast<const char*>(qh), rlo, N, tid, st);
+  if (tid < RB) lst = lh[min(rlo + tid, N - 1)];
+  for (int it = 0; it < nblk; ++it) {
+    const int cur = it & 1;
+    block_store(qlds[cur], tid, st);
+    if (tid < RB) llds[cur][tid] = lst * kLog2e;
+    __syncthreads();
+    const int r0 = rlo + (it % per) * RB;
+    if (it + 1 < nblk) {
+      const int g1 = (it + 1) / per, r1 = rlo + ((it + 1) % per) * RB;
+      block_load(reinterpret_cast<const char*>(qh + (int64_t)g1 * qstride), r1, N, tid, st);
+      if (tid < RB) lst = lh[(int64_t)g1 * a.total_rows + min(r1 + tid, N - 1)];
+    }
+    // rows that can be masked: below the key block, or past the segment / sequence
+    const bool edge = (r0 < k0 + KB) || (r0 + RB > seg_hi);
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      uint4 qf[NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) qf[s] = lds_frag(qlds[cur], rt * 16 + c16, s, g16);
+      f32x4_t acca = {0.f, 0.f, 0.f, 0.f}, accb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        acca = mma_step(bf16_t{}, qf[s], kfa[s], acca);
+        accb = mma_step(bf16_t{}, qf[s], kfb[s], accb);
+      }
+      // acc[i] = logit of row r0 + rt*16 + 4*g16 + i for key ja (jb)
+      const float4 l4 = *reinterpret_cast<const float4*>(&llds[cur][rt * 16 + 4 * g16]);
+      const float l2[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float pa = fast_exp2(fmaf(acca[i], a.scale_log2, -l2[i]));
+        float pb = fast_exp2(fmaf(accb[i], a.scale_log2, -l2[i]));
+        if (edge) {
+          const int p = r0 + rt * 16 + 4 * g16 + i;
+          pa = (p < seg_hi && ja <= p) ? pa : 0.0f;
+          pb = (p < seg_hi && jb <= p) ? pb : 0.0f;
+        }
+        cola += pa;
+        colb += pb;
+      }
+    }
+    __syncthreads();
+  }
+  cola += shfl_xor_f<16>(cola);
+  colb += shfl_xor_f<16>(colb);
+  cola += shfl_xor_f<32>(cola);
+  colb += shfl_xor_f<32>(colb);
+  if (g16 == 0) {
+    float* out = part + ((int64_t)seg * a.n_kv_heads + h) * a.total_rows + s0;
+    if (ja < N) out[ja] = cola;
+    if (jb < N) out[jb] = colb;
+  }
+}
+
+// colsum[h][j] = (1/G) * sum over the segments that hold rows >= j's key block, in order.
+__global__ __launch_bounds__(256) void h2o_reduce_kernel(H2oArgs a, const float* part) {
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int64_t s0 = a.offs[b];
+  const int N = (int)(a.offs[b + 1] - s0);
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= N) return;
+  const int nseg = (N + SEG - 1) / SEG;
+  float acc = 0.0f;
+  for (int s = (j / KB) * KB / SEG; s < nseg; ++s)
+    acc += part[((int64_t)s * a.n_kv_heads + h) * a.total_rows + s0 + j];
+  a.colsum[(int64_t)h * a.total_rows + s0 + j] = acc * a.inv_G;
 }
 
 }  // namespace
 
 size_t h2o_workspace_bytes(const dge_geom_t& g) {
-  return (size_t)g.n_q_heads * (size_t)total_rows(g) * sizeof(float) + 256;
+  // row LSE [H_q][T] (when computed here) + segment partials [nseg][H_kv][T]
+  const size_t T = (size_t)total_rows(g);
+  const size_t nseg = (size_t)((max_seq_rows(g) + SEG - 1) / SEG);
+  return (size_t)g.n_q_heads * T * sizeof(float) + nseg * g.n_kv_heads * T * sizeof(float) + 512;
 }
 
 hipError_t launch_h2o(const dge_geom_t& g, const void* q_all, const void* k, const float* lse,
@@ -144,19 +314,30 @@ hipError_t launch_h2o(const dge_geom_t& g, const void* q_all, const void* k, con
   a.n_q_heads = g.n_q_heads;
   a.n_kv_heads = g.n_kv_heads;
   a.G = g.n_q_heads / g.n_kv_heads;
+  a.batch = g.batch;
   a.scale_log2 = kLog2e / sqrtf((float)D);
   a.inv_G = 1.0f / (float)a.G;
-  const int nblk = (int)((max_seq_rows(g) + 63) / 64);
-  if (nblk == 0) return hipSuccess;
+  const int64_t nmax = max_seq_rows(g);
+  if (nmax == 0) return hipSuccess;
   if (lse == nullptr) {
+    if (a.G > kMaxG) return hipErrorInvalidValue;
     a.lse_out = reinterpret_cast<float*>(ws);
-    hipLaunchKernelGGL(h2o_lse_kernel, dim3(nblk, g.n_q_heads, g.batch), dim3(256), 0, st, a);
+    const int nrb = (int)((nmax + RB - 1) / RB);
+    a.n_pairs = (nrb + 1) / 2;
+    hipLaunchKernelGGL(h2o_lse_kernel, dim3(xcd_grid(a.n_pairs * g.n_kv_heads * g.batch)),
+                       dim3(256), 0, st, a);
     a.lse = a.lse_out;
   } else {
     a.lse = lse;
   }
-  hipLaunchKernelGGL(h2o_colsum_kernel, dim3(nblk, g.n_kv_heads, g.batch), dim3(256), 0, st, a,
-                     nblk);
+  const int nkb = (int)((nmax + KB - 1) / KB);
+  const int nseg = (int)((nmax + SEG - 1) / SEG);
+  const size_t lse_bytes = ((size_t)g.n_q_heads * (size_t)a.total_rows * sizeof(float) + 255) / 256 * 256;
+  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + lse_bytes);
+  hipLaunchKernelGGL(h2o_colsum_kernel, dim3(xcd_grid(nkb * nseg * g.n_kv_heads * g.batch)),
+                     dim3(256), 0, st, a, part, nkb, nseg);
+  hipLaunchKernelGGL(h2o_reduce_kernel, dim3((unsigned)((nmax + 255) / 256), g.n_kv_heads, g.batch),
+                     dim3(256), 0, st, a, part);
   return hipGetLastError();
 }
 

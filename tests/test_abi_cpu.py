@@ -156,3 +156,5 @@ def test_streaming_compact_h2o_validation(L):
     assert L.dge_h2o_colsum(_G(dtype=1).p, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None) == _lib.DGE_ERR_UNSUPPORTED
     assert L.dge_h2o_colsum(_G(d=64).p, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None) == _lib.DGE_ERR_UNSUPPORTED
     assert L.dge_h2o_colsum(g.p, FAKE, FAKE, None, FAKE, None, 0, None) == _lib.DGE_ERR_WORKSPACE
+    assert L.dge_h2o_colsum(g.p, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.DGE_ERR_WORKSPACE
+    assert L.dge_h2o_colsum(_G(hq=16, hkv=2).p, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None) == _lib.DGE_ERR_UNSUPPORTED

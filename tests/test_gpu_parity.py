@@ -301,9 +301,10 @@ def test_streaming_closed_form():
 # H2O accumulated attention
 # ------------------------------------------------------------------------------------------
 @pytest.mark.parametrize("supply_lse", [False, True])
-def test_h2o_parity_small(supply_lse):
-    wl = di.small_variant("c5", [300, 77, 1000])
-    _log(f"h2o small supply_lse={supply_lse}")
+@pytest.mark.parametrize("lens", [(300, 77, 1000), (5, 640, 129)])
+def test_h2o_parity_small(supply_lse, lens):
+    wl = di.small_variant("c5", list(lens))
+    _log(f"h2o small lens={lens} supply_lse={supply_lse}")
     x = di.make_layer(wl, with_v=False)
     g = geom_of(wl)
     lse = None
