@@ -94,6 +94,83 @@ __device__ __forceinline__ float rescale(float m, float mx) {
   return m == mx ? 1.0f : fast_exp2(m - mx);
 }
 
+// Waits and barriers for pipelines that keep global->LDS copies in flight across
+// workgroup barriers (__syncthreads() would drain every outstanding load).
+// s_waitcnt immediate on gfx9: vmcnt[3:0] + vmcnt[5:4] at [15:14], expcnt[6:4],
+// lgkmcnt[11:8]; fields not waited on are set to their maximum.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));
+}
+// Workgroup barrier for LDS traffic only: this wave's LDS reads/writes are done, then
+// s_barrier.  Outstanding global loads (including global->LDS copies) stay in flight.
+// The empty asm statements keep the compiler from moving memory accesses across the
+// barrier (the s_barrier builtin itself is not a memory operation to the optimiser).
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void lds_barrier() {
+  wait_lgkmcnt0();
+  wg_barrier();
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) const void* global_ptr_t;
+
+// 16 bytes per lane from global memory straight into LDS: lane l of the wavefront
+// writes lds_wave_base + 16 * l (lds_wave_base must be the same for the whole wave).
+// Issued from asm so that the compiler's own wait insertion, which cannot tell the
+// ring buffers apart, does not drain every copy in flight before each LDS read; the
+// callers order these copies with explicit vmcnt waits and workgroup barriers.  M0
+// (the LDS base) is saved and restored around the copy; the s_nop covers the wait
+// state required between an M0 write and an LDS-DMA load.
+__device__ __forceinline__ void dma16(const void* g, void* lds_wave_base) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(lds_ptr_t)lds_wave_base);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(base)
+      : "memory");
+}
+
+// Register loads issued from asm, for kernels that keep global->LDS copies in flight
+// with explicit vmcnt waits: the compiler does not track these loads, so it inserts no
+// wait of its own (which would also drain the copies).  The caller waits (vmcnt) and
+// then passes the values through reg_fence() before any use, so that nothing reads the
+// registers while the load is outstanding.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4_t async_load16(const void* p) {
+  u32x4_t v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ float async_load4(const void* p) {
+  float v;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ void reg_fence(u32x4_t& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ uint4 as_uint4(const u32x4_t& v) { return __builtin_bit_cast(uint4, v); }
+__device__ __forceinline__ void reg_fence(float& v) { asm volatile("" : "+v"(v)); }
+// vmcnt wait as an asm statement, ordered with the loads and fences above.
+template <int N>
+__device__ __forceinline__ void asm_wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
 // XCD-aware work mapping.  The command processor hands workgroups to the 8 XCDs of an
 // MI355X round-robin by linear block id, and each XCD has its own L2.  Grids that use
 // this mapping are 1-D with a multiple of 8 blocks; block L runs on XCD L % 8 and takes
@@ -116,8 +193,13 @@ struct SeqOffsets {
   const int64_t* dev;
   int64_t inl[kInlineSeqs + 1];
   int batch;
+  // i must be the same for the whole wavefront; the result is then wave-uniform (held
+  // in scalar registers, so that everything derived from it branches uniformly)
   __device__ __forceinline__ int64_t operator[](int i) const {
-    return batch <= kInlineSeqs ? inl[i] : dev[i];
+    const int64_t v = batch <= kInlineSeqs ? inl[i] : dev[i];
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
   }
 };
 

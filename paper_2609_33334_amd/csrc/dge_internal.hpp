@@ -16,8 +16,9 @@ struct ScorePlan {
   int M;               // G * n_rows query rows per KV head and sequence
   int M_pad;           // M rounded up to 16
   int n_tiles;         // 16-row tiles (M_pad / 16)
-  int mt;              // row tiles each wavefront holds in registers at once
-  int groups;          // row groups of 4 * mt tiles covering all tiles
+  int ft;              // row tiles each wavefront owns in a row group (all keys)
+  int rt;              // shared row tiles, split across wavefronts by key subtile
+  int groups;          // row groups of 4 * ft + rt tiles covering all tiles
   int tiles_per_wave;  // 64-key iterations per workgroup
   int chunk_keys;      // keys per workgroup (4 wavefronts)
   int n_chunks;        // workgroups per (sequence, KV head)

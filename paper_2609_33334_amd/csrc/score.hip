@@ -12,6 +12,10 @@
 //   3. colsum: each workgroup streams its chunk again, P = 2^(x - c_r), sums over all
 //              rows of the group and writes raw[] (the K slab of one layer, 8-34 MB at
 //              Llama-3-8B geometry, is still in the 256 MB Infinity Cache).
+// With caller-supplied row LSEs (dge_score_lse) only the colsum pass runs.
+// (A single launch that waits in-kernel for the other chunks of a head was measured
+// slower on MI355X: device-scope atomics and coherent loads cost microseconds each,
+// more than the two kernel boundaries they replace.)
 //
 // Workgroups are laid out XCD-aware (see xcd_unit): the chunks of one KV head share an
 // XCD, so its query block is fetched into one L2, and the colsum pass finds each chunk
@@ -21,11 +25,12 @@
 // - The G * n_rows query rows form 16-row tiles; wavefront w owns tiles w, w+4, w+8...
 //   Its query fragments stay in registers for the whole chunk (<= 48 VGPRs at
 //   Llama-3-8B geometry), so several workgroups fit on a compute unit.
-// - Each 64-key tile of K is read from HBM once per workgroup with 16-byte loads, one
-//   coalesced row per 16 threads, and staged in LDS with the 16-byte units of row r
-//   XOR-swizzled by r: the 16 lanes that read one fragment column hit 16 different
-//   bank groups.  The next tile's global loads are in flight while the current tile
-//   is on the matrix cores.
+// - Each 64-key tile of K is copied from HBM straight into LDS (global_load_lds, 16
+//   bytes per lane, a row per 16 lanes) with the 16-byte units of row r XOR-swizzled
+//   by r, so the 16 lanes that read one fragment column hit 16 different bank groups.
+//   Up to three tiles are in flight (a 4-stage ring of 16 KB buffers) while one is on
+//   the matrix cores; the loop's barriers wait on LDS traffic only, so the copies are
+//   never drained early.
 // - stats uses the transposed product (A = keys, B = query rows): a lane then holds
 //   4 keys of ONE row, so the per-row max/sum is mostly in-lane and needs two
 //   cross-lane steps per row tile at the end of the chunk.
@@ -61,35 +66,41 @@ template <typename T, int D>
 struct KTile {
   static constexpr int kRowBytes = D * Elem<T>::kBytes;
   static constexpr int kUnits = kRowBytes / 16;                // 16-byte units per row
-  static constexpr int kPerThread = KT * kUnits / kThreads;    // units each thread stages
+  static constexpr int kInstr = KT * kUnits / kThreads;        // copy instructions per wave
   static constexpr int kBytes = KT * kRowBytes;
+  // pipeline depth: up to 64 KB of LDS per workgroup, at most 4 tiles (3 in flight)
+  static constexpr int kStages = kBytes <= 16384 ? 4 : 2;
 };
 
-// Issue the global loads of one 64-key tile (rows past the sequence are clamped to
-// its last row; their logits are masked later).
+// Global->LDS copy of one 64-key tile, issued by all 4 wavefronts: wavefront w's
+// instruction i fills bytes [(w*kInstr + i) KB, +1 KB) of the tile, lane l the 16 bytes
+// at offset 16*l of that kilobyte.  Each lane fetches the global unit that belongs at
+// its LDS position under the XOR swizzle (unit u of row r at position u ^ (r % kUnits)),
+// so a fragment read later hits 16 different bank groups.  Rows past the sequence are
+// clamped to its last row (their logits are masked).  A dummy copy (real == false)
+// issues the same instructions with every lane reading the 16 bytes at kb: it keeps
+// the number of copies in flight constant at the end of a chunk, so that every wait
+// below has a fixed count, and costs one cached line.
 template <typename T, int D>
-__device__ __forceinline__ void ktile_load(const char* kb, int j0, int N, int tid,
-                                           uint4 (&st)[KTile<T, D>::kPerThread]) {
+__device__ __forceinline__ void ktile_dma(const char* kb, int j0, int N, char* tile, int wv,
+                                          int lane, bool real) {
   using KTl = KTile<T, D>;
 #pragma unroll
-  for (int i = 0; i < KTl::kPerThread; ++i) {
-    const int e = tid + kThreads * i;
-    const int r = e / KTl::kUnits, u = e % KTl::kUnits;
-    const int j = min(j0 + r, N - 1);
-    st[i] = load16(kb + (int64_t)j * KTl::kRowBytes + u * 16);
+  for (int i = 0; i < KTl::kInstr; ++i) {
+    const int e = (wv * KTl::kInstr + i) * kWave + lane;
+    const int r = e / KTl::kUnits, p = e % KTl::kUnits;
+    const int u = p ^ (r % KTl::kUnits);
+    const char* src = kb + (int64_t)min(j0 + r, N - 1) * KTl::kRowBytes + u * 16;
+    dma16(real ? src : kb, tile + (wv * KTl::kInstr + i) * (kWave * 16));
   }
 }
 
+// With S - 1 tiles always in flight, tile t has landed once at most S - 2 younger
+// tiles (and whatever was issued after them) are outstanding; loads issued before it
+// are complete too.
 template <typename T, int D>
-__device__ __forceinline__ void ktile_store(char* lds, int tid,
-                                            const uint4 (&st)[KTile<T, D>::kPerThread]) {
-  using KTl = KTile<T, D>;
-#pragma unroll
-  for (int i = 0; i < KTl::kPerThread; ++i) {
-    const int e = tid + kThreads * i;
-    const int r = e / KTl::kUnits, u = e % KTl::kUnits;
-    *reinterpret_cast<uint4*>(lds + r * KTl::kRowBytes + ((u ^ (r % KTl::kUnits)) * 16)) = st[i];
-  }
+__device__ __forceinline__ void ktile_wait() {
+  asm_wait_vmcnt<(KTile<T, D>::kStages - 2) * KTile<T, D>::kInstr>();
 }
 
 // Fragment of key row r (0..63 within the tile) for chunk step s and lane group g16.
@@ -100,33 +111,328 @@ __device__ __forceinline__ uint4 ktile_frag(const char* lds, int r, int s, int g
   return *reinterpret_cast<const uint4*>(lds + r * KTl::kRowBytes + ((u ^ (r % KTl::kUnits)) * 16));
 }
 
-// Query fragments of the row tiles owned by wavefront wv in row group grp.
-template <typename T, int D, int MTW>
+// Row tiles of one row group (first tile tile0) as wavefront wv sees them:
+//   slot i <  FT : tile tile0 + wv + 4 i, for every key of every K tile ("own" tiles);
+//   slot FT + r  : tile tile0 + 4 FT + r, shared by the four wavefronts -- wavefront wv
+//                  takes only the 16 keys of subtile wv of each 64-key K tile.
+// With T tiles in the group, FT = T / 4 and RT = T % 4 give every wavefront the same
+// number of (row tile, 16-key subtile) products, 4 FT + RT per K tile; the plain
+// "tile w + 4i" ownership would leave three wavefronts computing a padding tile.
+template <int FT>
+__device__ __forceinline__ int slot_tile(int tile0, int wv, int i) {
+  return i < FT ? tile0 + wv + 4 * i : tile0 + 4 * FT + (i - FT);
+}
+
+// Register loads before the K copies: from asm (untracked by the compiler, so the first
+// tile wait covers them and later tiles keep streaming) when the wavefront holds at
+// most kAsyncSlots slots; with more, register pressure makes the compiler copy values
+// between registers before they can have landed, so those instances use ordinary loads
+// and one full wait before the stream.
+constexpr int kAsyncSlots = 6;
+template <int NQ>
+__device__ __forceinline__ u32x4_t slot_load16(const void* p) {
+  if constexpr (NQ <= kAsyncSlots) return async_load16(p);
+  else return __builtin_bit_cast(u32x4_t, load16(p));
+}
+template <int NQ>
+__device__ __forceinline__ float slot_load4(const float* p) {
+  if constexpr (NQ <= kAsyncSlots) return async_load4(p);
+  else return *p;
+}
+
+// Query fragments of the wavefront's slots (slot_load16): valid only after the first
+// tile wait and q_fence().  Padding rows (m >= M) read row M - 1; their logits are
+// masked (stats) or weighted by 2^-inf (colsum).
+template <typename T, int D, int FT, int NQ>
 __device__ __forceinline__ void load_q_frags(const ScoreArgs& a, int h, int b, int tile0, int wv,
                                              int c16, int g16,
-                                             uint4 (&qf)[MTW][RowChunks<T, D>::kSteps]) {
+                                             u32x4_t (&qf)[NQ][RowChunks<T, D>::kSteps]) {
   constexpr int NS = RowChunks<T, D>::kSteps;
   const T* qb = reinterpret_cast<const T*>(a.q);
 #pragma unroll
-  for (int mt = 0; mt < MTW; ++mt) {
-    const int m = (tile0 + wv + 4 * mt) * 16 + c16;   // lane supplies row l % 16
-    if (m < a.M) {
-      const int g = m / a.n_rows;
-      const int r = m - g * a.n_rows;
-      const T* row = qb + (int64_t)(h * a.G + g) * a.q_head_stride + (int64_t)(b * a.n_rows + r) * D;
+  for (int i = 0; i < NQ; ++i) {
+    const int m = min(slot_tile<FT>(tile0, wv, i) * 16 + c16, a.M - 1);   // lane: row l % 16
+    const int g = m / a.n_rows;
+    const int r = m - g * a.n_rows;
+    const T* row = qb + (int64_t)(h * a.G + g) * a.q_head_stride + (int64_t)(b * a.n_rows + r) * D;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) qf[mt][s] = load16(row + chunk_elem<T, D>(s, g16));
-    } else {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) qf[mt][s] = make_uint4(0, 0, 0, 0);
-    }
+    for (int s = 0; s < NS; ++s) qf[i][s] = slot_load16<NQ>(row + chunk_elem<T, D>(s, g16));
   }
 }
 
-template <typename T, int D, int MTW>
+// After the first tile wait: the slot registers may be read from here on.
+template <int NQ, int NS>
+__device__ __forceinline__ void q_fence(u32x4_t (&qf)[NQ][NS]) {
+  if constexpr (NQ <= kAsyncSlots) {
+#pragma unroll
+    for (int i = 0; i < NQ; ++i)
+#pragma unroll
+      for (int s = 0; s < NS; ++s) reg_fence(qf[i][s]);
+  } else {
+    wait_vmcnt<0>();         // compiler-visible: no wait of its own inside the stream
+  }
+}
+template <int NQ>
+__device__ __forceinline__ void cr_fence(float (&cr)[NQ][4]) {
+  if constexpr (NQ <= kAsyncSlots) {
+#pragma unroll
+    for (int i = 0; i < NQ; ++i)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) reg_fence(cr[i][t]);
+  }
+}
+
+// Copies of tiles 0..S-2 of a chunk (dummies past its end), then the wait for tile 0:
+// every load issued before the copies (query fragments, normalisers) has landed too.
+template <typename T, int D>
+__device__ __forceinline__ void ktile_prologue(const char* kb, int c0, int ntiles, int N,
+                                               char (*buf)[KTile<T, D>::kBytes], int wv,
+                                               int lane) {
+  constexpr int S = KTile<T, D>::kStages;
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t) ktile_dma<T, D>(kb, c0 + t * KT, N, buf[t], wv, lane, t < ntiles);
+  ktile_wait<T, D>();
+}
+
+// consume(tile, j0) for the tiles of [c0, c0 + ntiles * KT), ntiles >= 1, after the
+// prologue.  Tile t lands in buffer t % S; S - 1 copies stay in flight (dummies past
+// the chunk's end) and all of them have landed when this returns.
+template <typename T, int D, typename F>
+__device__ __forceinline__ void ktile_stream(const char* kb, int c0, int ntiles, int N,
+                                             char (*buf)[KTile<T, D>::kBytes], int wv, int lane,
+                                             F&& consume) {
+  constexpr int S = KTile<T, D>::kStages;
+  int t = 0;
+  do {
+    if (t > 0) ktile_wait<T, D>();
+    wg_barrier();            // tile t landed everywhere; buffer (t - 1) % S and red[] free
+    const int tn = t + S - 1;
+    ktile_dma<T, D>(kb, c0 + tn * KT, N, buf[tn % S], wv, lane, tn < ntiles);
+    consume(buf[t % S], c0 + t * KT);
+  } while (++t < ntiles);
+  asm_wait_vmcnt<0>();       // no copy still writes into the buffers
+}
+
+// Per-wavefront row state of the stats pass: lane (c16, g16) holds row c16 of each
+// slot's tile and keys 4*g16..4*g16+3 of a 16-key subtile.  The sum is kept relative to
+// a reference mref (log2 domain) that only moves when a logit exceeds it by more than
+// 2^kLazyBound: the common update is then fma + exp + add per logit, with no rescale.
+// mref starts finite and very negative so that fully masked subtiles add exactly 0.
+constexpr float kLazyBound = 64.0f;
+constexpr float kRefInit = -1.0e30f;
+
+template <int NQ>
+struct StatsRows {
+  int pos[NQ];
+  bool live[NQ];
+  float mref[NQ], srow[NQ];
+};
+
+template <int FT, int NQ>
+__device__ __forceinline__ void stats_rows_init(const ScoreArgs& a, int tile0, int wv, int c16,
+                                                int p0, StatsRows<NQ>& st) {
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const int m = slot_tile<FT>(tile0, wv, i) * 16 + c16;
+    st.live[i] = m < a.M;
+    st.pos[i] = p0 + (st.live[i] ? m % a.n_rows : 0);
+    st.mref[i] = kRefInit;
+    st.srow[i] = 0.0f;
+  }
+}
+
+// acc[t] = logit (unscaled) of key jb + t for this lane's row.  MASK: the tile reaches
+// past the sequence or past some row's position (the last tiles of a sequence only).
+template <bool MASK>
+__device__ __forceinline__ void stats_update(const f32x4_t& acc, int jb, bool live, int pos,
+                                             int N, float scale, float& mref, float& srow) {
+  float x[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    x[t] = acc[t];
+    if constexpr (MASK) x[t] = (live && jb + t < N && jb + t <= pos) ? x[t] : -INFINITY;
+  }
+  const float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])) * scale;
+  if (__any(mx > mref + kLazyBound)) {     // rare and wave-uniform: exact rescale
+    const float nr = fmaxf(mref, mx);
+    srow *= fast_exp2(mref - nr);
+    mref = nr;
+  }
+  srow += (fast_exp2(fmaf(x[0], scale, -mref)) + fast_exp2(fmaf(x[1], scale, -mref))) +
+          (fast_exp2(fmaf(x[2], scale, -mref)) + fast_exp2(fmaf(x[3], scale, -mref)));
+}
+
+// Running sums of one 64-key tile for the wavefront's slots.
+template <typename T, int D, int FT, int RT, bool MASK>
+__device__ __forceinline__ void stats_tile_body(const ScoreArgs& a, const char* lds, int j0, int N,
+                                                int wv, int c16, int g16,
+                                                const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
+                                                StatsRows<FT + RT>& st) {
+  constexpr int NS = RowChunks<T, D>::kSteps;
+  if constexpr (FT > 0) {
+#pragma unroll 2
+    for (int sub = 0; sub < KT / 16; ++sub) {
+      uint4 kf[NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
+      // FT independent accumulation chains, issued k-step-major (A = keys, B = rows)
+      f32x4_t acc[FT];
+#pragma unroll
+      for (int i = 0; i < FT; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int i = 0; i < FT; ++i) acc[i] = mma_step(T{}, kf[s], as_uint4(qf[i][s]), acc[i]);
+#pragma unroll
+      for (int i = 0; i < FT; ++i)
+        stats_update<MASK>(acc[i], j0 + sub * 16 + 4 * g16, st.live[i], st.pos[i], N,
+                           a.scale_log2, st.mref[i], st.srow[i]);
+    }
+  }
+  if constexpr (RT > 0) {                  // shared tiles: subtile wv only
+    uint4 kf[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, wv * 16 + c16, s, g16);
+    f32x4_t acc[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) acc[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int r = 0; r < RT; ++r) acc[r] = mma_step(T{}, kf[s], as_uint4(qf[FT + r][s]), acc[r]);
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+      stats_update<MASK>(acc[r], j0 + wv * 16 + 4 * g16, st.live[FT + r], st.pos[FT + r], N,
+                         a.scale_log2, st.mref[FT + r], st.srow[FT + r]);
+  }
+}
+
+template <typename T, int D, int FT, int RT>
+__device__ __forceinline__ void stats_tile(const ScoreArgs& a, const char* lds, int j0, int N,
+                                           int p0, int wv, int c16, int g16,
+                                           const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
+                                           StatsRows<FT + RT>& st) {
+  // masking only where the tile reaches past the first scoring position: padding rows
+  // (not live) elsewhere accumulate harmless sums that are never stored
+  if (j0 + KT - 1 > p0) stats_tile_body<T, D, FT, RT, true>(a, lds, j0, N, wv, c16, g16, qf, st);
+  else stats_tile_body<T, D, FT, RT, false>(a, lds, j0, N, wv, c16, g16, qf, st);
+}
+
+// Merge the four lane groups that hold the same row: every lane ends with its row's
+// (reference, sum) over the keys the wavefront has seen.
+template <int NQ>
+__device__ __forceinline__ void stats_rows_merge(StatsRows<NQ>& st) {
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const float m = st.mref[i];
+    float s = st.srow[i];
+    const float mx = fmaxf(fmaxf(m, shfl_xor_f<16>(m)), fmaxf(shfl_xor_f<32>(m), shfl_xor_f<48>(m)));
+    s *= rescale(m, mx);
+    s += shfl_xor_f<16>(s);
+    s += shfl_xor_f<32>(s);
+    st.mref[i] = mx;
+    st.srow[i] = s;
+  }
+}
+
+// Column sums of one 64-key tile: lane (c16, g16) holds rows 4*g16..4*g16+3 of each
+// slot's tile for key c16 of a 16-key subtile.  cr = log2 normaliser of each row (+inf
+// for padding rows, whose terms are then exactly 0).  Ends with wavefront 0 adding the
+// tile's sums into out[].  MASK: the tile reaches past the first scoring position.
+template <typename T, int D, int FT, int RT, bool MASK>
+__device__ __forceinline__ void colsum_tile_body(const ScoreArgs& a, const char* lds, int j0,
+                                                 int N, int wv, int c16, int g16,
+                                                 const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
+                                                 const float (&cr)[FT + RT][4],
+                                                 const int (&pos)[FT + RT][4], float (*red)[KT]) {
+  constexpr int NS = RowChunks<T, D>::kSteps;
+#pragma unroll 2
+  for (int sub = 0; sub < KT / 16; ++sub) {
+    uint4 kf[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
+    const int j = j0 + sub * 16 + c16;
+    float colp = 0.0f;
+    // acc[i][t] = logit of row (slot tile*16 + 4*g16 + t) for key j (A = rows, B = keys)
+    if constexpr (FT > 0) {
+      f32x4_t acc[FT];
+#pragma unroll
+      for (int i = 0; i < FT; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int i = 0; i < FT; ++i) acc[i] = mma_step(T{}, as_uint4(qf[i][s]), kf[s], acc[i]);
+#pragma unroll
+      for (int i = 0; i < FT; ++i)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          float p = fast_exp2(fmaf(acc[i][t], a.scale_log2, -cr[i][t]));
+          if constexpr (MASK) p = (j < N && j <= pos[i][t]) ? p : 0.0f;
+          colp += p;
+        }
+    }
+    if constexpr (RT > 0) {
+      if (sub == wv) {                     // shared tiles: this wavefront's subtile
+        f32x4_t acc[RT];
+#pragma unroll
+        for (int r = 0; r < RT; ++r) acc[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+          for (int r = 0; r < RT; ++r) acc[r] = mma_step(T{}, as_uint4(qf[FT + r][s]), kf[s], acc[r]);
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            float p = fast_exp2(fmaf(acc[r][t], a.scale_log2, -cr[FT + r][t]));
+            if constexpr (MASK) p = (j < N && j <= pos[FT + r][t]) ? p : 0.0f;
+            colp += p;
+          }
+      }
+    }
+    colp += shfl_xor_f<16>(colp);
+    colp += shfl_xor_f<32>(colp);
+    if (g16 == 0) red[wv][sub * 16 + c16] = colp;
+  }
+}
+
+template <typename T, int D, int FT, int RT>
+__device__ __forceinline__ void colsum_tile(const ScoreArgs& a, const char* lds, int j0, int c1,
+                                            int N, int tid, int wv, int c16, int g16,
+                                            const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
+                                            const float (&cr)[FT + RT][4],
+                                            const int (&pos)[FT + RT][4], const int p0,
+                                            float (*red)[KT], float* out, bool accumulate) {
+  if (j0 + KT - 1 > p0)
+    colsum_tile_body<T, D, FT, RT, true>(a, lds, j0, N, wv, c16, g16, qf, cr, pos, red);
+  else
+    colsum_tile_body<T, D, FT, RT, false>(a, lds, j0, N, wv, c16, g16, qf, cr, pos, red);
+  lds_barrier();                           // column partials of all 4 wavefronts
+  if (tid < KT && j0 + tid < c1) {
+    const float v = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
+    if (accumulate) out[j0 + tid] += v * a.inv_G;
+    else out[j0 + tid] = v * a.inv_G;
+  }
+}
+
+// Positions of the colsum rows (4 per lane per slot).
+template <int FT, int NQ>
+__device__ __forceinline__ void colsum_positions(const ScoreArgs& a, int tile0, int wv, int g16,
+                                                 int p0, int (&pos)[NQ][4]) {
+#pragma unroll
+  for (int i = 0; i < NQ; ++i)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
+      pos[i][t] = p0 + min(m, a.M - 1) % a.n_rows;
+    }
+}
+
+template <typename T, int D, int FT, int RT>
 __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
+  constexpr int NQ = FT + RT;
   const int units = a.n_chunks * a.n_kv_heads * a.batch;
   const int unit = xcd_unit(units);
   if (unit >= units) return;
@@ -140,93 +446,49 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
   const int g16 = lane >> 4, c16 = lane & 15;
   const int p0 = N - a.p0_from_end;
   const int c1 = min(N, c0 + a.chunk_keys);
+  const int ntiles = (c1 - c0 + KT - 1) / KT;
   const char* kb = reinterpret_cast<const char*>(a.k) +
                    ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
-  __shared__ __attribute__((aligned(16))) char lds[KTl::kBytes];
+  float2* part = a.partial + ((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad;
+  __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
+  __shared__ float2 xch[4][(RT > 0 ? RT : 1) * 16];   // shared-tile partials per wavefront
 
   for (int grp = 0; grp < a.groups; ++grp) {
-    const int tile0 = grp * 4 * MTW;
-    uint4 qf[MTW][NS];
-    load_q_frags<T, D, MTW>(a, h, b, tile0, wv, c16, g16, qf);
-    // this lane's row in each owned tile, and that row's position
-    int pos[MTW];
-    bool live[MTW];
+    const int tile0 = grp * 4 * FT;
+    // query fragments first, then the K copies: the first tile wait covers both, and
+    // later tiles keep landing while the first ones are on the matrix cores
+    lds_barrier();                         // previous row group done with the buffers
+    u32x4_t qf[NQ][NS];
+    load_q_frags<T, D, FT, NQ>(a, h, b, tile0, wv, c16, g16, qf);
+    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane);
+    q_fence(qf);                           // landed with the first tile
+    StatsRows<NQ> st;
+    stats_rows_init<FT, NQ>(a, tile0, wv, c16, p0, st);
+    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane,
+                       [&](const char* lds, int j0) {
+                         stats_tile<T, D, FT, RT>(a, lds, j0, N, p0, wv, c16, g16, qf, st);
+                       });
+    stats_rows_merge<NQ>(st);
 #pragma unroll
-    for (int mt = 0; mt < MTW; ++mt) {
-      const int m = (tile0 + wv + 4 * mt) * 16 + c16;
-      live[mt] = m < a.M;
-      pos[mt] = p0 + (live[mt] ? m % a.n_rows : 0);
+    for (int i = 0; i < FT; ++i) {
+      const int row = slot_tile<FT>(tile0, wv, i) * 16 + c16;
+      if (g16 == 0 && row < a.M) part[row] = make_float2(st.mref[i], st.srow[i]);
     }
-    float mrow[MTW], srow[MTW];
+    if constexpr (RT > 0) {                // the four wavefronts' shares of each shared row
+      if (g16 == 0)
 #pragma unroll
-    for (int mt = 0; mt < MTW; ++mt) { mrow[mt] = -INFINITY; srow[mt] = 0.0f; }
-
-    // two K tiles in flight per workgroup: tile t+2 loads while tile t is consumed
-    uint4 stA[KTl::kPerThread], stB[KTl::kPerThread];
-    ktile_load<T, D>(kb, c0, N, tid, stA);
-    if (c0 + KT < c1) ktile_load<T, D>(kb, c0 + KT, N, tid, stB);
-    auto consume = [&](int j0) {
-      // no key of this tile is past the sequence or beyond any row's position
-      const bool need_mask = (j0 + KT - 1 > p0);
-#pragma unroll 2
-      for (int sub = 0; sub < KT / 16; ++sub) {
-        uint4 kf[NS];
+        for (int r = 0; r < RT; ++r) xch[wv][r * 16 + c16] = make_float2(st.mref[FT + r], st.srow[FT + r]);
+      lds_barrier();
+      if (tid < RT * 16) {
+        const int r = tid / 16, row = (tile0 + 4 * FT + r) * 16 + (tid % 16);
+        float m = xch[0][tid].x;
 #pragma unroll
-        for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
-        // MTW independent accumulation chains, issued k-step-major
-        f32x4_t acc[MTW];
+        for (int w = 1; w < 4; ++w) m = fmaxf(m, xch[w][tid].x);
+        float sum = 0.0f;
 #pragma unroll
-        for (int mt = 0; mt < MTW; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < NS; ++s)
-#pragma unroll
-          for (int mt = 0; mt < MTW; ++mt) acc[mt] = mma_step(T{}, kf[s], qf[mt][s], acc[mt]);
-        // acc[mt][t] = logit of key j0 + sub*16 + 4*g16 + t for this lane's row
-#pragma unroll
-        for (int mt = 0; mt < MTW; ++mt) {
-          float x[4];
-#pragma unroll
-          for (int t = 0; t < 4; ++t) x[t] = acc[mt][t] * a.scale_log2;
-          if (need_mask) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              const int j = j0 + sub * 16 + 4 * g16 + t;
-              x[t] = (live[mt] && j < N && j <= pos[mt]) ? x[t] : -INFINITY;
-            }
-          }
-          const float mx = fmaxf(fmaxf(mrow[mt], fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
-          const float base = mx == -INFINITY ? 0.0f : mx;
-          srow[mt] = srow[mt] * fast_exp2(mrow[mt] - base) + fast_exp2(x[0] - base) +
-                     fast_exp2(x[1] - base) + fast_exp2(x[2] - base) + fast_exp2(x[3] - base);
-          mrow[mt] = mx;
-        }
+        for (int w = 0; w < 4; ++w) sum += xch[w][tid].y * rescale(xch[w][tid].x, m);
+        if (row < a.M) part[row] = make_float2(m, sum);
       }
-    };
-    for (int j0 = c0; j0 < c1; j0 += 2 * KT) {
-      __syncthreads();
-      ktile_store<T, D>(lds, tid, stA);
-      __syncthreads();
-      if (j0 + 2 * KT < c1) ktile_load<T, D>(kb, j0 + 2 * KT, N, tid, stA);
-      consume(j0);
-      if (j0 + KT >= c1) break;
-      __syncthreads();
-      ktile_store<T, D>(lds, tid, stB);
-      __syncthreads();
-      if (j0 + 3 * KT < c1) ktile_load<T, D>(kb, j0 + 3 * KT, N, tid, stB);
-      consume(j0 + KT);
-    }
-    // merge the four lane groups that hold the same row
-#pragma unroll
-    for (int mt = 0; mt < MTW; ++mt) {
-      float m = mrow[mt], s = srow[mt];
-      const float mx = fmaxf(fmaxf(m, shfl_xor_f<16>(m)), fmaxf(shfl_xor_f<32>(m), shfl_xor_f<48>(m)));
-      s *= rescale(m, mx);
-      s += shfl_xor_f<16>(s);
-      s += shfl_xor_f<32>(s);
-      const int row = (tile0 + wv + 4 * mt) * 16 + c16;
-      if (g16 == 0 && row < a.M)
-        a.partial[((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad + row] =
-            make_float2(mx, s);
     }
   }
 }
@@ -260,10 +522,11 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
   if (lane == 0) a.rowc[base * a.M_pad + m] = mx + __log2f(ss);
 }
 
-template <typename T, int D, int MTW>
+template <typename T, int D, int FT, int RT>
 __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
+  constexpr int NQ = FT + RT;
   const int units = a.n_chunks * a.n_kv_heads * a.batch;
   const int unit = xcd_unit(units);
   if (unit >= units) return;
@@ -277,120 +540,90 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   const int g16 = lane >> 4, c16 = lane & 15;
   const int p0 = N - a.p0_from_end;
   const int c1 = min(N, c0 + a.chunk_keys);
+  const int ntiles = (c1 - c0 + KT - 1) / KT;
   const char* kb = reinterpret_cast<const char*>(a.k) +
                    ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
   const float* rowc = a.rowc + (int64_t)(b * a.n_kv_heads + h) * a.M_pad;
+  // row normalisers: natural-log LSE supplied by the caller, or log2-domain rowc
+  const float* lse_in = a.lse_in;
+  const float cr_scale = lse_in != nullptr ? kLog2e : 1.0f;
   float* out = a.raw + (int64_t)h * a.total_rows + s0;
-  __shared__ __attribute__((aligned(16))) char lds[KTl::kBytes];
+  __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
   __shared__ float red[4][KT];
 
   for (int grp = 0; grp < a.groups; ++grp) {
-    const int tile0 = grp * 4 * MTW;
-    uint4 qf[MTW][NS];
-    load_q_frags<T, D, MTW>(a, h, b, tile0, wv, c16, g16, qf);
-    // normalisers and positions of this lane's 4 rows in each owned tile
-    float cr[MTW][4];
-    int pos[MTW][4];
+    const int tile0 = grp * 4 * FT;
+    lds_barrier();                         // previous row group done with the buffers
+    // query fragments and row normalisers first (asm loads, clamped rows), then the K
+    // copies; the first tile wait covers all of them
+    u32x4_t qf[NQ][NS];
+    load_q_frags<T, D, FT, NQ>(a, h, b, tile0, wv, c16, g16, qf);
+    float cr[NQ][4];
 #pragma unroll
-    for (int mt = 0; mt < MTW; ++mt)
+    for (int i = 0; i < NQ; ++i)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int m = (tile0 + wv + 4 * mt) * 16 + 4 * g16 + t;
-        if (a.lse_in != nullptr) {
-          const int g = m / a.n_rows, r = m - (m / a.n_rows) * a.n_rows;
-          cr[mt][t] = m < a.M ? a.lse_in[(int64_t)(h * a.G + g) * (a.q_head_stride / D) +
-                                         b * a.n_rows + r] * kLog2e
-                              : INFINITY;
-        } else {
-          cr[mt][t] = m < a.M ? rowc[m] : INFINITY;
-        }
-        pos[mt][t] = p0 + (m < a.M ? m % a.n_rows : 0);
+        const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
+        const int mm = min(m, a.M - 1);
+        const int g = mm / a.n_rows, r = mm - g * a.n_rows;
+        const float* src = lse_in != nullptr
+                               ? lse_in + (int64_t)(h * a.G + g) * (a.q_head_stride / D) +
+                                     b * a.n_rows + r
+                               : rowc + mm;
+        cr[i][t] = slot_load4<NQ>(src);
       }
-
-    uint4 stA[KTl::kPerThread], stB[KTl::kPerThread];
-    ktile_load<T, D>(kb, c0, N, tid, stA);
-    if (c0 + KT < c1) ktile_load<T, D>(kb, c0 + KT, N, tid, stB);
-    auto consume = [&](int j0) {
-      const bool need_mask = (j0 + KT - 1 > p0);
-#pragma unroll 2
-      for (int sub = 0; sub < KT / 16; ++sub) {
-        uint4 kf[NS];
+    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane);
+    q_fence(qf);                           // landed with the first tile
+    cr_fence<NQ>(cr);
 #pragma unroll
-        for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
-        f32x4_t acc[MTW];
+    for (int i = 0; i < NQ; ++i)
 #pragma unroll
-        for (int mt = 0; mt < MTW; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < NS; ++s)
-#pragma unroll
-          for (int mt = 0; mt < MTW; ++mt) acc[mt] = mma_step(T{}, qf[mt][s], kf[s], acc[mt]);
-        // acc[mt][t] = logit of row (tile*16 + 4*g16 + t) for key j0 + sub*16 + c16
-        const int j = j0 + sub * 16 + c16;
-        float colp = 0.0f;
-#pragma unroll
-        for (int mt = 0; mt < MTW; ++mt)
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            float p = fast_exp2(fmaf(acc[mt][t], a.scale_log2, -cr[mt][t]));
-            if (need_mask) p = (j < N && j <= pos[mt][t]) ? p : 0.0f;
-            colp += p;
-          }
-        colp += shfl_xor_f<16>(colp);
-        colp += shfl_xor_f<32>(colp);
-        if (g16 == 0) red[wv][sub * 16 + c16] = colp;
+      for (int t = 0; t < 4; ++t) {
+        const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
+        cr[i][t] = m < a.M ? cr[i][t] * cr_scale : INFINITY;
       }
-      __syncthreads();
-      if (tid < KT && j0 + tid < c1) {
-        const float v = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
-        if (grp == 0) out[j0 + tid] = v * a.inv_G;
-        else out[j0 + tid] += v * a.inv_G;
-      }
-    };
-    for (int j0 = c0; j0 < c1; j0 += 2 * KT) {
-      __syncthreads();
-      ktile_store<T, D>(lds, tid, stA);
-      __syncthreads();
-      if (j0 + 2 * KT < c1) ktile_load<T, D>(kb, j0 + 2 * KT, N, tid, stA);
-      consume(j0);
-      if (j0 + KT >= c1) break;
-      __syncthreads();
-      ktile_store<T, D>(lds, tid, stB);
-      __syncthreads();
-      if (j0 + 3 * KT < c1) ktile_load<T, D>(kb, j0 + 3 * KT, N, tid, stB);
-      consume(j0 + KT);
-    }
-    __syncthreads();
+    int pos[NQ][4];
+    colsum_positions<FT, NQ>(a, tile0, wv, g16, p0, pos);
+    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane,
+                       [&](const char* lds, int j0) {
+                         colsum_tile<T, D, FT, RT>(a, lds, j0, c1, N, tid, wv, c16, g16, qf, cr,
+                                                   pos, p0, red, out, grp > 0);
+                       });
   }
 }
 
-template <typename T, int D, int MTW>
+template <typename T, int D, int FT, int RT>
 hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st) {
   const dim3 grid(xcd_grid(a.n_chunks * g.n_kv_heads * g.batch));
   if (a.lse_in != nullptr) {   // normalisers supplied: one pass over K
-    hipLaunchKernelGGL((score_colsum_kernel<T, D, MTW>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((score_stats_kernel<T, D, MTW>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((score_stats_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
   hipLaunchKernelGGL(score_reduce_kernel, dim3(a.M_pad / 4, g.n_kv_heads, g.batch), dim3(256), 0,
                      st, a);
-  hipLaunchKernelGGL((score_colsum_kernel<T, D, MTW>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
+// (FT, RT): own tiles per wavefront and shared tiles per row group.  Instantiated for
+// RT = 0 with FT = 1..9, and for FT <= 3 with RT = 1..3, within the register budget of
+// 36 16-byte query fragments per lane (FT + RT <= 36 / steps).
 template <typename T, int D>
-hipError_t launch_mt(const ScoreArgs& a, const dge_geom_t& g, int mtw, hipStream_t st) {
-  switch (mtw) {
-    case 1: return launch_typed<T, D, 1>(a, g, st);
-    case 2: return launch_typed<T, D, 2>(a, g, st);
-    case 3: return launch_typed<T, D, 3>(a, g, st);
-    case 4: return launch_typed<T, D, 4>(a, g, st);
-    case 5: return launch_typed<T, D, 5>(a, g, st);
-    case 6: return launch_typed<T, D, 6>(a, g, st);
-    case 7: return launch_typed<T, D, 7>(a, g, st);
-    case 8: return launch_typed<T, D, 8>(a, g, st);
-    case 9: return launch_typed<T, D, 9>(a, g, st);
-    default: return hipErrorInvalidValue;
+hipError_t launch_split(const ScoreArgs& a, const dge_geom_t& g, int ft, int rt, hipStream_t st) {
+  constexpr int kSlots = 36 / RowChunks<T, D>::kSteps;
+#define DGE_SPLIT(F, R)                                                  \
+  if constexpr ((F) + (R) <= kSlots) {                                  \
+    if (ft == (F) && rt == (R)) return launch_typed<T, D, F, R>(a, g, st); \
   }
+  DGE_SPLIT(1, 0) DGE_SPLIT(2, 0) DGE_SPLIT(3, 0) DGE_SPLIT(4, 0) DGE_SPLIT(5, 0)
+  DGE_SPLIT(6, 0) DGE_SPLIT(7, 0) DGE_SPLIT(8, 0) DGE_SPLIT(9, 0)
+  DGE_SPLIT(0, 1) DGE_SPLIT(0, 2) DGE_SPLIT(0, 3)
+  DGE_SPLIT(1, 1) DGE_SPLIT(1, 2) DGE_SPLIT(1, 3)
+  DGE_SPLIT(2, 1) DGE_SPLIT(2, 2) DGE_SPLIT(2, 3)
+  DGE_SPLIT(3, 1) DGE_SPLIT(3, 2) DGE_SPLIT(3, 3)
+#undef DGE_SPLIT
+  return hipErrorInvalidValue;
 }
 
 // Register budget for query fragments: tiles-per-wavefront * steps <= 36 16-byte chunks.
@@ -434,18 +667,25 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
   p.M_pad = (p.M + 15) / 16 * 16;
   p.n_tiles = p.M_pad / 16;
   const int cap = max_mtw(g);
-  const int per_wave = (p.n_tiles + 3) / 4;
-  p.groups = per_wave <= cap ? 1 : (per_wave + cap - 1) / cap;
-  p.mt = (per_wave + p.groups - 1) / p.groups;
-  if (p.mt < 1) p.mt = 1;
+  const int T = p.n_tiles, ft = T / 4, rt = T % 4;
+  if (rt == 0 && ft <= cap) {              // every wavefront owns T / 4 tiles
+    p.groups = 1; p.ft = ft; p.rt = 0;
+  } else if (ft <= 3 && ft + rt <= cap) {  // own tiles + subtile-split shared tiles
+    p.groups = 1; p.ft = ft; p.rt = rt;
+  } else {                                 // row groups of 4 * ft tiles, padding in the last
+    const int per_wave = (T + 3) / 4;
+    p.groups = per_wave <= cap ? 1 : (per_wave + cap - 1) / cap;
+    p.ft = (per_wave + p.groups - 1) / p.groups;
+    p.rt = 0;
+  }
   // About one resident round of workgroups (two per compute unit): every workgroup
-  // loads its query fragments once and streams several 64-key tiles with two in flight.
+  // loads its query fragments once and streams several 64-key tiles.
   const int64_t tiles_total = (int64_t)g.n_kv_heads * ((total_rows(g) + KT - 1) / KT);
+  const int64_t nmax = max_seq_rows(g);
   int iters = (int)((tiles_total + 511) / 512);
   iters = iters < 1 ? 1 : (iters > 16 ? 16 : iters);
   p.tiles_per_wave = iters;
   p.chunk_keys = KT * iters;
-  const int64_t nmax = max_seq_rows(g);
   p.n_chunks = (int)((nmax + p.chunk_keys - 1) / p.chunk_keys);
   if (p.n_chunks < 1) p.n_chunks = 1;
   return p;
@@ -487,11 +727,11 @@ hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, 
   a.scale_log2 = kLog2e / sqrtf((float)g.head_dim);
   a.inv_G = 1.0f / (float)a.G;
   if (g.dtype == DGE_BF16) {
-    return g.head_dim == 128 ? launch_mt<bf16_t, 128>(a, g, p.mt, st)
-                             : launch_mt<bf16_t, 64>(a, g, p.mt, st);
+    return g.head_dim == 128 ? launch_split<bf16_t, 128>(a, g, p.ft, p.rt, st)
+                             : launch_split<bf16_t, 64>(a, g, p.ft, p.rt, st);
   }
-  return g.head_dim == 128 ? launch_mt<float, 128>(a, g, p.mt, st)
-                           : launch_mt<float, 64>(a, g, p.mt, st);
+  return g.head_dim == 128 ? launch_split<float, 128>(a, g, p.ft, p.rt, st)
+                           : launch_split<float, 64>(a, g, p.ft, p.rt, st);
 }
 
 }  // namespace dge

@@ -81,6 +81,13 @@ SCORE_CASES = {
     "bf16_d64": di.small_variant("c1", [400, 129], dtype="bf16"),
     "big_M": di.small_variant("c2", [260], n_q_heads=64, window=64, k_draft=8, plant="none"),
     "w0": di.small_variant("c2", [96], window=0, k_draft=3, plant="none"),
+    # row-tile splits across the 4 wavefronts: 7 tiles (1 own + 3 shared), 14 tiles
+    # (3 own + 2 shared), fp32 with 13 tiles (3 + 1), and 52 tiles in two row groups
+    "t7": di.small_variant("c2", [611, 130], window=24, k_draft=4, plant="none"),
+    "t14": di.small_variant("c2", [777], window=48, k_draft=8, plant="none"),
+    "f32_t13": di.small_variant("c2", [300], dtype="f32", window=46, k_draft=6, plant="none"),
+    "groups2": di.small_variant("c2", [450, 200], n_q_heads=64, window=96, k_draft=8,
+                                plant="none"),
 }
 
 
@@ -147,6 +154,7 @@ def test_score_deterministic():
     b = dge.score(g, 0, q, k)
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
 
 
 # ------------------------------------------------------------------------------------------
