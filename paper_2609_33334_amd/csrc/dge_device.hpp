@@ -185,22 +185,53 @@ __device__ __forceinline__ int xcd_unit(int total) {
   return (L % kXcds) * xcd_per(total) + L / kXcds;
 }
 
-// Sequence offsets as a kernel argument: up to kInlineSeqs sequences travel by value
-// in the argument block (read through the scalar cache, no dependent global load at
-// kernel start); larger batches read the device array.
+// Sequence offsets as a kernel argument: up to kInlineSeqs sequences whose offsets fit
+// in 31 bits travel by value in the argument block (as 32-bit values); otherwise the
+// kernel reads the device array.  The inline values are picked by a select chain over
+// values held in scalar registers (not an indexed load: that would add a dependent
+// round trip at kernel start), and the result is wave-uniform.
 constexpr int kInlineSeqs = 16;
 struct SeqOffsets {
   const int64_t* dev;
-  int64_t inl[kInlineSeqs + 1];
+  int32_t inl[kInlineSeqs + 1];
   int batch;
-  // i must be the same for the whole wavefront; the result is then wave-uniform (held
-  // in scalar registers, so that everything derived from it branches uniformly)
+  int use_inline;
+  // i must be the same for the whole wavefront
   __device__ __forceinline__ int64_t operator[](int i) const {
-    const int64_t v = batch <= kInlineSeqs ? inl[i] : dev[i];
+    if (use_inline) {
+      int32_t v = inl[0];
+      asm volatile("" : "+s"(v));
+#pragma unroll
+      for (int k = 1; k <= kInlineSeqs; ++k) {
+        int32_t w = inl[k];
+        asm volatile("" : "+s"(w));
+        v = i == k ? w : v;
+      }
+      return v;
+    }
+    const int64_t v = dev[i];
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
     const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
     return (int64_t)(((uint64_t)hi << 32) | lo);
   }
 };
+
+// Makes the given kernel arguments resident in scalar registers at this point, so that
+// they are fetched together (one round trip) instead of one dependent load at a time
+// after each early-exit branch.
+template <typename T>
+__device__ __forceinline__ void prefetch_arg(const T& x) {
+  asm volatile("" : : "s"(x));
+}
+__device__ __forceinline__ void prefetch_arg(const SeqOffsets& o) {
+  prefetch_arg(o.use_inline);
+  prefetch_arg(o.dev);
+#pragma unroll
+  for (int k = 0; k <= kInlineSeqs; ++k) prefetch_arg(o.inl[k]);
+}
+template <typename... Ts>
+__device__ __forceinline__ void prefetch_args(const Ts&... xs) {
+  (prefetch_arg(xs), ...);
+}
 
 }  // namespace dge

@@ -433,6 +433,9 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int NQ = FT + RT;
+  prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
+                a.kv_head_stride, a.q_head_stride, a.M, a.n_rows, a.G, a.M_pad, a.groups,
+                a.offs);
   const int units = a.n_chunks * a.n_kv_heads * a.batch;
   const int unit = xcd_unit(units);
   if (unit >= units) return;
@@ -527,6 +530,9 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int NQ = FT + RT;
+  prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
+                a.kv_head_stride, a.q_head_stride, a.M, a.n_rows, a.G, a.M_pad, a.groups,
+                a.offs);
   const int units = a.n_chunks * a.n_kv_heads * a.batch;
   const int unit = xcd_unit(units);
   if (unit >= units) return;
@@ -639,8 +645,9 @@ SeqOffsets seq_offsets(const dge_geom_t& g) {
   SeqOffsets o{};
   o.dev = g.kv_offsets;
   o.batch = g.batch;
-  if (g.batch <= kInlineSeqs)
-    for (int b = 0; b <= g.batch; ++b) o.inl[b] = g.kv_offsets_host[b];
+  o.use_inline = g.batch <= kInlineSeqs && g.kv_offsets_host[g.batch] <= INT32_MAX;
+  if (o.use_inline)
+    for (int b = 0; b <= g.batch; ++b) o.inl[b] = (int32_t)g.kv_offsets_host[b];
   return o;
 }
 

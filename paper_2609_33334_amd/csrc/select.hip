@@ -208,6 +208,12 @@ __device__ __forceinline__ void radix_find_digit(const uint32_t* hist, int nbins
 }
 
 template <int THREADS, int KPT>
+struct SegDigits {
+  static constexpr int kBits0 = THREADS * KPT > 4096 ? 14 : 12;
+  static constexpr size_t kHistBytes = (size_t)4 << kBits0;
+};
+
+template <int THREADS, int KPT>
 __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) {
   constexpr int WAVES = THREADS / kWave;
   extern __shared__ __attribute__((aligned(16))) float stage[];
@@ -227,9 +233,15 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   if (writer)
     for (int r = nsel + tid; r < a.n_select; r += THREADS) out[r] = -1;
   // this replica's slice of output rows and the kept index of each
+  // first radix digit: 12 bits (16 bins per binade) for up to 4096 candidates, 14 bits
+  // (64 bins per binade) beyond, so that scores clustered in a few binades do not pile
+  // their histogram atomics onto a few LDS addresses
+  // The histogram reuses the staging buffer (dead once the pooled keys are in registers).
+  constexpr int kBits0 = SegDigits<THREADS, KPT>::kBits0, kBits1 = 10;
+  constexpr int kBits2 = 31 - kBits0 - kBits1;
+  uint32_t* hist = reinterpret_cast<uint32_t*>(stage);
   __shared__ int slice[kMaxRowsPerRep];
   __shared__ uint32_t scan_sh[WAVES];
-  __shared__ uint32_t hist[4096];
   __shared__ int sh_digit_above[2];
   if (tid == 0) { sh_digit_above[0] = 0; sh_digit_above[1] = 0; }
   const int r0 = rep * a.rows_per_rep;
@@ -279,15 +291,16 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
         key[i] = base + i < C ? (__float_as_uint(src[base + i]) & 0x7fffffffu) : 0u;
     }
 
-    // three radix passes over bits 30..19, 18..9 and 8..0 (bit 31 is zero for
-    // non-negative scores); the wide first digit splits every binade into 16 bins, so
-    // clustered scores do not pile onto a few histogram addresses
+    // three radix passes over bits 30..0 (bit 31 is zero for non-negative scores), most
+    // significant digit first
+    __syncthreads();                       // staging reads done: the buffer becomes hist
     uint32_t prefix = 0, mask = 0x80000000u;
     int remaining = nsel;
 #pragma unroll
     for (int pass = 0; pass < 3; ++pass) {
-      const int shift = pass == 0 ? 19 : (pass == 1 ? 9 : 0);
-      const int nbins = pass == 0 ? 4096 : (pass == 1 ? 1024 : 512);
+      const int bits = pass == 0 ? kBits0 : (pass == 1 ? kBits1 : kBits2);
+      const int shift = pass == 0 ? 31 - kBits0 : (pass == 1 ? kBits2 : 0);
+      const int nbins = 1 << bits;
       for (int i = tid; i < nbins; i += THREADS) hist[i] = 0;
       __syncthreads();
 #pragma unroll
@@ -372,6 +385,7 @@ __global__ __launch_bounds__(256) void select_streaming_kernel(int32_t* idx, int
 
 template <int THREADS, int KPT>
 hipError_t launch_seg(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t st) {
+  lds = lds > SegDigits<THREADS, KPT>::kHistBytes ? lds : SegDigits<THREADS, KPT>::kHistBytes;
   if (lds > 64 * 1024) {
     const hipError_t e = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&select_topb_seg_kernel<THREADS, KPT>),
@@ -410,10 +424,12 @@ bool launch_fast(const SelectArgs& a, const dge_geom_t& g, int64_t cmax, hipStre
   if (a.pool_half > kPoolHalo) return false;
   const dim3 grid(xcd_grid(a.replicas * g.n_kv_heads * g.batch));
   const size_t lds = a.pool_half > 0 ? (size_t)stage_pos((int)(cmax > 0 ? cmax : 1)) * 4 + 64 : 0;
+  // (threads, candidates per thread): more threads per workgroup shorten the serial
+  // per-thread loops of every radix pass (measured best at each size on MI355X)
   if (cmax <= 1024) *err = launch_seg<256, 4>(a, grid, lds, st);
   else if (cmax <= 2048) *err = launch_seg<256, 8>(a, grid, lds, st);
-  else if (cmax <= 4096) *err = launch_seg<256, 16>(a, grid, lds, st);
-  else if (cmax <= 8192) *err = launch_seg<512, 16>(a, grid, lds, st);
+  else if (cmax <= 4096) *err = launch_seg<512, 8>(a, grid, lds, st);
+  else if (cmax <= 8192) *err = launch_seg<1024, 8>(a, grid, lds, st);
   else if (cmax <= 16384) *err = launch_seg<1024, 16>(a, grid, lds, st);
   else if (cmax <= 32768) *err = launch_seg<1024, 32>(a, grid, lds, st);
   else return false;
@@ -449,12 +465,12 @@ hipError_t launch_select_compact(const dge_geom_t& g, const float* scores, int p
   a.head_stride_bytes = g.kv_head_stride * elt;
   a.row_bytes = g.head_dim * elt;
   // Spread each head's row copies over enough replicas to occupy the chip while keeping
-  // the repeated selection bounded: at most 16 replicas of at least 64 rows each.
+  // the repeated selection bounded: at most 32 replicas of at least 64 rows each.
   const int units = g.batch * g.n_kv_heads;
   int reps = 256 / (units > 0 ? units : 1);
   const int by_rows = (a.n_out + 63) / 64;
   reps = reps > by_rows ? by_rows : reps;
-  reps = reps > 16 ? 16 : reps;
+  reps = reps > 32 ? 32 : reps;
   reps = reps < 1 ? 1 : reps;
   int rpr = (a.n_out + reps - 1) / reps;
   if (rpr > kMaxRowsPerRep) {
