@@ -35,7 +35,12 @@ WORKLOAD_TEXT = {
           "window 32 + k=2 draft rows, B=512, max-pool 7",
     "c3": "c3: 32 Llama-3-8B-shaped layers, 32q/8kv heads, d=128, batch 1, L=16384, "
           "window 32 + k=2, PyramidKV-style budgets 2048 -> 256, max-pool 7",
+    "c4": "c4: 32 Llama-3-8B-shaped layers, 32q/8kv heads, d=128, ragged batch of 8 with "
+          "L_b in [16384, 32768], window 32 + k=2, B=2048, max-pool 7",
+    "c5": "c5: H2O on one Llama-3-8B-shaped layer, 32q/8kv heads, d=128, L=8192 + k=2, "
+          "all 8194 rows scored, 512 heavy + 512 recent",
 }
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix peak
 GRAPH_STEPS = 8
 
 
@@ -64,9 +69,9 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(every step is independent per KV head and sequence, see the sharding notes "
-              "in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: runs on one GPU; --gpus {args.gpus} is not supported (every step "
+              "is independent per KV head and sequence: tensor- or batch-parallel sharding "
+              "needs no exchange)", file=sys.stderr)
         sys.exit(2)
     import torch
     import dge_inputs as di
@@ -86,11 +91,13 @@ def main():
         sys.exit(2)
     dev = "cuda:0"
     wl = di.WORKLOADS[args.workload]
-    if wl.h2o or wl.batch != 1:
-        print("bench.py: workloads c1, c2 and c3 are timed here", file=sys.stderr)
+    if args.lse and wl.batch != 1:
+        print("bench.py: --lse is implemented for single-sequence workloads", file=sys.stderr)
         sys.exit(2)
     log(f"[bench] workload {wl.name}: generating inputs")
-    x = di.make_layer(wl)
+    x = di.make_layer(wl, with_v=True)
+    if wl.h2o:
+        return bench_h2o(args, wl, x, dev)
     is_bf16 = wl.dtype == "bf16"
     elt = 2 if is_bf16 else 4
 
@@ -108,6 +115,7 @@ def main():
     budgets = [wl.budget_of_layer(l) for l in range(L_layers)]
     # one step = every layer once; single-layer workloads rotate over --sets copies so that
     # no step finds its inputs in the Infinity Cache, multi-layer ones are large enough
+    # (each layer gets its own copy of the generated layer's tensors)
     S = max(1, args.sets) if L_layers == 1 else 1
     ws_score = torch.empty(dge.workspace_size(geom, dge.OP_SCORE), dtype=torch.uint8, device=dev)
     ws_sel = torch.empty(dge.workspace_size(geom, dge.OP_SELECT), dtype=torch.uint8, device=dev)
@@ -265,6 +273,148 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def bench_h2o(args, wl, x, dev):
+    """H2O step on one layer (Sec. 6 baselines; App. H2O complexity): accumulated attention
+    of every cached row (dge_h2o_colsum, row LSE computed in the library unless --lse),
+    then the top-(B - n_recent) heavy rows plus the n_recent most recent ones
+    (dge_select_compact with pool 1).  The dominant kernel is MFMA-bound."""
+    import torch
+    import paper_2609_33334_amd as dge
+
+    def dev_t(bits):
+        t = torch.from_numpy(np.ascontiguousarray(bits))
+        return t.view(torch.int16).view(torch.bfloat16).to(dev)
+
+    geom = dge.Geometry(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.window, wl.k_draft,
+                        wl.cached_lens, dtype=dge.DGE_BF16, device=dev)
+    qa0, k0, v0 = dev_t(x.q_all_bits), dev_t(x.k_bits), dev_t(x.v_bits)
+    n_tail, n_sel = wl.n_recent, wl.budget - wl.n_recent
+    lse = None
+    if args.lse:   # natural-log LSE of every cached row, prepared outside the timed region
+        N = wl.cached_lens[0]
+        rows = []
+        for hq in range(wl.n_q_heads):
+            qq = qa0[hq].float()
+            kk = k0[hq // wl.group].float()
+            xx = (qq @ kk.t()) / (wl.head_dim ** 0.5)
+            xx = xx.masked_fill(torch.ones(N, N, device=dev, dtype=torch.bool).triu(1), float("-inf"))
+            rows.append(torch.logsumexp(xx, dim=1))
+            del xx
+        lse = torch.stack(rows).contiguous()
+    S = 4
+    ws_h2o = torch.empty(dge.workspace_size(geom, dge.OP_H2O), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(dge.workspace_size(geom, dge.OP_SELECT), dtype=torch.uint8, device=dev)
+    sets = []
+    for _ in range(S):
+        out = dict(col=torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=dev),
+                   idx=torch.empty(1, geom.n_kv_heads, n_sel, dtype=torch.int32, device=dev),
+                   n_kept=torch.zeros(4, dtype=torch.int32, device=dev),
+                   k=torch.empty(1, geom.n_kv_heads, n_sel + n_tail, wl.head_dim, dtype=k0.dtype, device=dev),
+                   v=torch.empty(1, geom.n_kv_heads, n_sel + n_tail, wl.head_dim, dtype=k0.dtype, device=dev))
+        sets.append((qa0.clone(), k0.clone(), v0.clone(), out))
+
+    def h2o_only(i):
+        qa, k, v, out = sets[i % S]
+        dge.h2o_colsum(geom, qa, k, lse=lse, colsum=out["col"], ws=ws_h2o)
+
+    def step(i):
+        qa, k, v, out = sets[i % S]
+        h2o_only(i)
+        dge.select_compact(geom, out["col"], 1, n_tail, n_sel, k, v, idx=out["idx"],
+                           n_kept=out["n_kept"], k_out=out["k"], v_out=out["v"], ws=ws_sel)
+
+    for i in range(max(args.warmup, S)):
+        step(i)
+    torch.cuda.synchronize()
+    ref = {kk: vv.clone() for kk, vv in sets[0][3].items()}
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for j in range(S):
+                step(j)
+        sg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(sg, stream=stream):
+            for j in range(S):
+                h2o_only(j)
+    torch.cuda.synchronize()
+    for kk in ref:
+        sets[0][3][kk].zero_()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    for kk in ref:
+        assert torch.equal(sets[0][3][kk], ref[kk]), f"graph replay differs from eager ({kk})"
+    n_rep = max(1, (args.steps + S - 1) // S)
+    K = n_rep * S
+    g.replay()
+    torch.cuda.synchronize()
+
+    def timed(graph):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(n_rep):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
+    log(f"[bench] timing {K} H2O steps ({n_rep} replays of {S})")
+    ms_per_step = timed(g)
+    h2o_ms = timed(sg)
+    N = wl.cached_lens[0]
+    passes = 1 if lse is not None else 2       # the LSE pass repeats QK^T
+    flops = passes * (N * (N + 1) // 2) * 2 * wl.head_dim * wl.n_q_heads
+    achieved = flops / (h2o_ms * 1e-3) / 1e12
+    log(f"[bench] {ms_per_step * 1e3:.1f} us/step; dge_h2o_colsum {h2o_ms * 1e3:.1f} us/call, "
+        f"{achieved:.0f} TFLOP/s executed")
+    units = N * wl.n_kv_heads
+    roofline = {"kernel": "dge_h2o_colsum (" + ("LSE supplied" if lse is not None else
+                                                "row LSE computed in the library") + ")",
+                "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFS,
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4),
+                "traffic": None, "flops_per_launch": flops, "us_per_launch": round(h2o_ms * 1e3, 3)}
+    cpu = None if args.no_cpu_baseline else cpu_baseline_h2o(wl, x, args.cpu_seconds)
+    line = {
+        "metric": "cached tokens x KV heads scored+compacted per second (H2O eviction step)",
+        "value": round(units / (ms_per_step * 1e-3), 1), "unit": "token*kvhead/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian Q/K/V; no model weights)",
+        "config": {"workload": WORKLOAD_TEXT[wl.name], "global_batch": 1, "seq_len": N,
+                   "layers": 1, "parallelism": "single GPU",
+                   "step": "dge_h2o_colsum -> dge_select_compact (512 heavy + 512 recent)",
+                   "buffer_sets": S},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline_h2o(wl, x, seconds):
+    """The float64 oracle's H2O colsum on a bounded sample: the query heads of the first
+    KV head (one GQA group), scaled to all 8 KV heads."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    G = wl.group
+    q = x.q_all[:G]
+    k = x.k[:1]
+    t0 = time.perf_counter()
+    oracle.h2o_colsum(q, k, wl.kv_offsets, G, 1)
+    el = time.perf_counter() - t0
+    N = wl.cached_lens[0]
+    rate = N / el                      # one KV head of N tokens in el seconds
+    log(f"[bench] cpu oracle: one GQA group of H2O colsum in {el:.1f}s -> {rate:.3g} token*kvhead/s")
+    return {"value": round(rate, 1), "unit": "token*kvhead/s", "cores": cores, "kind": "oracle",
+            "sample": f"H2O colsum of one KV head's GQA group ({G} query heads x {N} rows) in "
+                      f"float64 numpy, {el:.1f} s; select/compact not included"}
 
 
 SCORE_SOURCES = ("paper_2609_33334_amd/csrc/score.hip", "paper_2609_33334_amd/csrc/dge_device.hpp")

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_score_asm_loads_waited_on_every_path():
     from paper_2609_33334_amd import build
     src = os.path.join(build.CSRC, "score.hip")
-    flags = [f for f in build.CFLAGS if f != "-fPIC"]
+    flags = [f for f in build.flags_for(src) if f != "-fPIC"]
     with tempfile.TemporaryDirectory() as tmp:
         out = os.path.join(tmp, "score.s")
         r = subprocess.run([build.HIPCC, *flags, "-S", "--cuda-device-only", src, "-o", out],
