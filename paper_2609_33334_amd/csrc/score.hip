@@ -22,15 +22,20 @@
 // in the L2 that streamed it during the stats pass.
 //
 // Work split inside a workgroup (4 wavefronts, one KV head, one chunk of keys):
-// - The G * n_rows query rows form 16-row tiles; wavefront w owns tiles w, w+4, w+8...
-//   Its query fragments stay in registers for the whole chunk (<= 48 VGPRs at
-//   Llama-3-8B geometry), so several workgroups fit on a compute unit.
+// - The G * n_rows query rows form T 16-row tiles.  Each wavefront owns T/4 of them
+//   for every key and takes the T%4 leftover tiles only for its own 16-key subtile of
+//   each K tile (see slot_tile), so the four wavefronts do equal work and none computes
+//   a padding tile.  Query fragments stay in registers for the whole chunk (48 VGPRs at
+//   Llama-3-8B geometry), so two workgroups fit on a compute unit.
 // - Each 64-key tile of K is copied from HBM straight into LDS (global_load_lds, 16
 //   bytes per lane, a row per 16 lanes) with the 16-byte units of row r XOR-swizzled
 //   by r, so the 16 lanes that read one fragment column hit 16 different bank groups.
-//   Up to three tiles are in flight (a 4-stage ring of 16 KB buffers) while one is on
-//   the matrix cores; the loop's barriers wait on LDS traffic only, so the copies are
-//   never drained early.
+//   Three tiles are always in flight (a 4-stage ring of 16 KB buffers; dummy copies
+//   past the end of a chunk keep every wait count fixed) while one is on the matrix
+//   cores; the loop's barriers wait on LDS traffic only, so the copies are never
+//   drained early.
+// - stats keeps each row's sum relative to a lazily moved reference and runs a masked
+//   tile body only where a tile reaches past the first scoring position.
 // - stats uses the transposed product (A = keys, B = query rows): a lane then holds
 //   4 keys of ONE row, so the per-row max/sum is mostly in-lane and needs two
 //   cross-lane steps per row tile at the end of the chunk.
