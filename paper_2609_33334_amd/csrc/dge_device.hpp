@@ -94,6 +94,26 @@ __device__ __forceinline__ float rescale(float m, float mx) {
   return m == mx ? 1.0f : fast_exp2(m - mx);
 }
 
+// Online sum of 2^x over a stream of logits, kept relative to a reference mref (log2
+// domain) that moves only when a logit exceeds it by more than 2^kLazyBound: the
+// common update is fma + exp2 + add per logit, with no rescale.  mref starts finite and
+// very negative (kLazyRefInit) so that fully masked groups (-inf) add exactly 0; the
+// result (mref, srow) merges with others like any (max, sum) pair.  x are unscaled
+// logits, scale = log2(e)/sqrt(d).  The rescale branch is wave-uniform.
+constexpr float kLazyBound = 64.0f;
+constexpr float kLazyRefInit = -1.0e30f;
+__device__ __forceinline__ void lazy_lse_update4(const float (&x)[4], float scale, float& mref,
+                                                 float& srow) {
+  const float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])) * scale;
+  if (__any(mx > mref + kLazyBound)) {
+    const float nr = fmaxf(mref, mx);
+    srow *= fast_exp2(mref - nr);
+    mref = nr;
+  }
+  srow += (fast_exp2(fmaf(x[0], scale, -mref)) + fast_exp2(fmaf(x[1], scale, -mref))) +
+          (fast_exp2(fmaf(x[2], scale, -mref)) + fast_exp2(fmaf(x[3], scale, -mref)));
+}
+
 // Waits and barriers for pipelines that keep global->LDS copies in flight across
 // workgroup barriers (__syncthreads() would drain every outstanding load).
 // s_waitcnt immediate on gfx9: vmcnt[3:0] + vmcnt[5:4] at [15:14], expcnt[6:4],

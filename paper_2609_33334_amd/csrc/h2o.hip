@@ -77,6 +77,41 @@ __device__ __forceinline__ void block_store(char* lds, int tid, const uint4 (&st
 // ------------------------------------------------------------------------------------
 // Row log-sum-exp: one (row-block pair, KV head, sequence) per workgroup.
 // ------------------------------------------------------------------------------------
+// One 64-key tile for the wavefront's four 16-row tiles (rows r0 + rt*16 + c16): the
+// transposed product (A = keys) puts 4 keys of one row in each lane.
+template <bool MASK>
+__device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N, int c16,
+                                         int g16, const uint4 (&qf)[4][NS], float scale,
+                                         float (&m)[4], float (&sm)[4]) {
+#pragma unroll 2
+  for (int sub = 0; sub < KTL / 16; ++sub) {
+    uint4 kf[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) kf[s] = lds_frag(buf, sub * 16 + c16, s, g16);
+    f32x4_t acc[4];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) acc[rt] = mma_step(bf16_t{}, kf[s], qf[rt][s], acc[rt]);
+    // acc[rt][i] = logit of key j0 + sub*16 + 4*g16 + i for row r0 + rt*16 + c16
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      float x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[i] = acc[rt][i];
+        if constexpr (MASK) {
+          const int p = r0 + rt * 16 + c16, j = j0 + sub * 16 + 4 * g16 + i;
+          x[i] = (j <= p && j < N) ? x[i] : -INFINITY;
+        }
+      }
+      lazy_lse_update4(x, scale, m[rt], sm[rt]);
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void h2o_lse_kernel(H2oArgs a) {
   const int units = a.n_pairs * a.n_kv_heads * a.batch;
   const int unit = xcd_unit(units);
@@ -108,9 +143,9 @@ __global__ __launch_bounds__(256) void h2o_lse_kernel(H2oArgs a) {
 #pragma unroll
       for (int s = 0; s < NS; ++s) qf[rt][s] = load16(row + (s * 4 + g16) * 16);
     }
-    float m[4], sm[4];
+    float m[4], sm[4];                      // lazy reference and sum (lazy_lse_update4)
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) { m[rt] = -INFINITY; sm[rt] = 0.0f; }
+    for (int rt = 0; rt < 4; ++rt) { m[rt] = kLazyRefInit; sm[rt] = 0.0f; }
     const int last = min(r0 + RB, N);       // keys [0, last) can be seen by this block
     const int ntile = (last + KTL - 1) / KTL;
     uint4 st[4];
@@ -121,40 +156,10 @@ __global__ __launch_bounds__(256) void h2o_lse_kernel(H2oArgs a) {
       __syncthreads();
       if (t + 1 < ntile) block_load(kb, (t + 1) * KTL, N, tid, st);
       const int j0 = t * KTL;
-      const bool diag = j0 + KTL > r0;      // some key may be past some row
       if (active) {
-#pragma unroll 2
-        for (int sub = 0; sub < KTL / 16; ++sub) {
-          uint4 kf[NS];
-#pragma unroll
-          for (int s = 0; s < NS; ++s) kf[s] = lds_frag(buf, sub * 16 + c16, s, g16);
-          f32x4_t acc[4];
-#pragma unroll
-          for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s = 0; s < NS; ++s)
-#pragma unroll
-            for (int rt = 0; rt < 4; ++rt) acc[rt] = mma_step(bf16_t{}, kf[s], qf[rt][s], acc[rt]);
-          // acc[rt][i] = logit of key j0 + sub*16 + 4*g16 + i for row r0 + rt*16 + c16
-#pragma unroll
-          for (int rt = 0; rt < 4; ++rt) {
-            const int p = r0 + rt * 16 + c16;
-            float x[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              x[i] = acc[rt][i] * a.scale_log2;
-              if (diag) {
-                const int j = j0 + sub * 16 + 4 * g16 + i;
-                x[i] = (j <= p && j < N) ? x[i] : -INFINITY;
-              }
-            }
-            const float mx = fmaxf(fmaxf(m[rt], fmaxf(x[0], x[1])), fmaxf(x[2], x[3]));
-            const float base = mx == -INFINITY ? 0.0f : mx;
-            sm[rt] = sm[rt] * fast_exp2(m[rt] - base) + fast_exp2(x[0] - base) +
-                     fast_exp2(x[1] - base) + fast_exp2(x[2] - base) + fast_exp2(x[3] - base);
-            m[rt] = mx;
-          }
-        }
+        // tiles that reach the block's diagonal (or the sequence end) run the masked body
+        if (j0 + KTL > r0) lse_tile<true>(buf, j0, r0, N, c16, g16, qf, a.scale_log2, m, sm);
+        else lse_tile<false>(buf, j0, r0, N, c16, g16, qf, a.scale_log2, m, sm);
       }
       __syncthreads();
     }

@@ -219,12 +219,9 @@ __device__ __forceinline__ void ktile_stream(const char* kb, int c0, int ntiles,
 }
 
 // Per-wavefront row state of the stats pass: lane (c16, g16) holds row c16 of each
-// slot's tile and keys 4*g16..4*g16+3 of a 16-key subtile.  The sum is kept relative to
-// a reference mref (log2 domain) that only moves when a logit exceeds it by more than
-// 2^kLazyBound: the common update is then fma + exp + add per logit, with no rescale.
-// mref starts finite and very negative so that fully masked subtiles add exactly 0.
-constexpr float kLazyBound = 64.0f;
-constexpr float kRefInit = -1.0e30f;
+// slot's tile and keys 4*g16..4*g16+3 of a 16-key subtile; the sums use the lazy
+// reference of lazy_lse_update4.
+constexpr float kRefInit = kLazyRefInit;
 
 template <int NQ>
 struct StatsRows {
@@ -257,14 +254,7 @@ __device__ __forceinline__ void stats_update(const f32x4_t& acc, int jb, bool li
     x[t] = acc[t];
     if constexpr (MASK) x[t] = (live && jb + t < N && jb + t <= pos) ? x[t] : -INFINITY;
   }
-  const float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])) * scale;
-  if (__any(mx > mref + kLazyBound)) {     // rare and wave-uniform: exact rescale
-    const float nr = fmaxf(mref, mx);
-    srow *= fast_exp2(mref - nr);
-    mref = nr;
-  }
-  srow += (fast_exp2(fmaf(x[0], scale, -mref)) + fast_exp2(fmaf(x[1], scale, -mref))) +
-          (fast_exp2(fmaf(x[2], scale, -mref)) + fast_exp2(fmaf(x[3], scale, -mref)));
+  lazy_lse_update4(x, scale, mref, srow);
 }
 
 // Running sums of one 64-key tile for the wavefront's slots.
