@@ -285,3 +285,41 @@ def log_partition(qrow: np.ndarray, keys: np.ndarray) -> float:
     x = keys @ as_f64(qrow) / math.sqrt(d)
     m = x.max()
     return float(m + np.log(np.exp(x - m).sum()))
+
+
+def cache_attention(q, k_c, v_c, n_kept, n_tail: int, q_from_end: int, n_q_heads: int,
+                    n_kv_heads: int):
+    """Attention of query rows over compacted caches: the check of a continuation on the
+    evicted cache (Alg. 1 step C's output; Sec. 3 Eq. 1; the eviction-mass equation of
+    App. "Why deferral can recover FullKV").
+
+    q: [H_q][batch * n_q][d]; k_c, v_c: [batch][H_kv][n_out][d], laid out as
+    [retained past rows (n_kept[b])] || [tail (n_tail)] || padding.  Query row r of
+    sequence b sits at position N_b - q_from_end + r; it attends every retained past row
+    (all precede the tail) and the tail rows t <= n_tail - q_from_end + r, i.e. the tail
+    rows at positions not after its own.  Returns out [H_q][batch * n_q][d] and the
+    natural-log partition lse [H_q][batch * n_q] over the attended rows.
+    """
+    q = as_f64(q)
+    k_c = as_f64(k_c)
+    v_c = as_f64(v_c)
+    G = n_q_heads // n_kv_heads
+    batch = k_c.shape[0]
+    n_q = q.shape[1] // batch
+    d = q.shape[2]
+    out = np.zeros((n_q_heads, batch * n_q, d), np.float64)
+    lse = np.full((n_q_heads, batch * n_q), -np.inf, np.float64)
+    for b in range(batch):
+        nk = int(n_kept[b])
+        for hq in range(n_q_heads):
+            keys, vals = k_c[b, hq // G], v_c[b, hq // G]
+            for r in range(n_q):
+                n_vis_tail = min(n_tail, max(0, n_tail - q_from_end + r + 1))
+                rows = np.concatenate([np.arange(nk), nk + np.arange(n_vis_tail)]).astype(np.int64)
+                if rows.size == 0:
+                    continue
+                qr = q[hq, b * n_q + r]
+                out[hq, b * n_q + r] = attention_output(qr, keys[rows], vals[rows])
+                lse[hq, b * n_q + r] = log_partition(qr, keys[rows])
+    return out, lse
+

@@ -235,6 +235,90 @@ def test_compaction_attention_identities():
 
 
 # ----------------------------------------------------------------------------------
+# Attention over a compacted cache (continuation check)
+# ----------------------------------------------------------------------------------
+def _compacted(k, v, idx_per_seq, n_tail, offs, n_out):
+    """[batch][H_kv][n_out][d] caches: retained rows || tail || zero padding."""
+    Hkv, _, d = k.shape
+    batch = len(offs) - 1
+    kc = np.zeros((batch, Hkv, n_out, d))
+    vc = np.zeros((batch, Hkv, n_out, d))
+    for b in range(batch):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        rows = np.concatenate([idx_per_seq[b], np.arange(N - n_tail, N)]).astype(int)
+        kc[b, :, :len(rows)] = k[:, s0 + rows]
+        vc[b, :, :len(rows)] = v[:, s0 + rows]
+    return kc, vc
+
+
+def test_cache_attention_matches_sdpa_with_explicit_mask():
+    # torch SDPA (float64, CPU) with a boolean mask built independently from positions
+    Hq, Hkv, d, n_tail, n_q, q_from_end = 6, 2, 16, 5, 7, 5
+    offs = [0, 40, 71]
+    k = _rand((Hkv, 71, d), 31, 1.3)
+    v = _rand((Hkv, 71, d), 32)
+    idx = [np.array([1, 4, 9, 20, 33]), np.array([0, 2, 3, 17])]
+    n_kept = [5, 4]
+    kc, vc = _compacted(k, v, idx, n_tail, offs, 12)
+    q = _rand((Hq, 2 * n_q, d), 33, 1.3)
+    out, lse = oracle.cache_attention(q, kc, vc, n_kept, n_tail, q_from_end, Hq, Hkv)
+    G = Hq // Hkv
+    for b in range(2):
+        N = offs[b + 1] - offs[b]
+        pos_rows = np.concatenate([idx[b], np.arange(N - n_tail, N)])       # original positions
+        pos_rows = np.concatenate([pos_rows, np.full(12 - len(pos_rows), 10 ** 9)])  # padding never seen
+        qpos = N - q_from_end + np.arange(n_q)
+        mask = torch.from_numpy(pos_rows[None, :] <= qpos[:, None])
+        for hq in range(Hq):
+            Q = torch.from_numpy(q[hq, b * n_q:(b + 1) * n_q])[None]
+            K = torch.from_numpy(kc[b, hq // G])[None]
+            V = torch.from_numpy(vc[b, hq // G])[None]
+            ref = torch.nn.functional.scaled_dot_product_attention(Q, K, V, attn_mask=mask)[0].numpy()
+            assert np.allclose(out[hq, b * n_q:(b + 1) * n_q], ref, rtol=1e-10, atol=1e-12)
+            x = (Q[0] @ K[0].T) / math.sqrt(d)
+            ref_lse = torch.logsumexp(x.masked_fill(~mask, float("-inf")), dim=1).numpy()
+            assert np.allclose(lse[hq, b * n_q:(b + 1) * n_q], ref_lse, rtol=1e-12, atol=1e-12)
+
+
+def test_cache_attention_keep_all_reproduces_scoring_row_lse():
+    # keep-all compaction + the scoring rows (q_from_end = w + k) sees exactly the causal
+    # keys of each scoring row: its log-partition is the scoring pass's row LSE
+    Hq, Hkv, d, w, kd = 4, 2, 8, 5, 2
+    offs = [0, 30, 47]
+    k = _rand((Hkv, 47, d), 34, 1.2)
+    v = _rand((Hkv, 47, d), 35)
+    q = _rand((Hq, 2 * (w + kd), d), 36, 1.2)
+    n_tail = w + kd
+    idx = [np.arange(30 - n_tail), np.arange(17 - n_tail)]
+    kc, vc = _compacted(k, v, idx, n_tail, offs, 30)
+    _, lse = oracle.cache_attention(q, kc, vc, [len(i) for i in idx], n_tail, n_tail, Hq, Hkv)
+    want = oracle.scoring_row_lse(q, k, offs, Hq, Hkv, w, kd)
+    assert np.allclose(lse, want, rtol=1e-12, atol=1e-12)
+
+
+def test_cache_attention_decomposes_over_keep_and_evict():
+    # Eq. 1: a decode query's full output is (1 - m) * output over R + m * output over E,
+    # with m = 1 - exp(lse_R - lse_full); and lse_full = logaddexp(lse_R, lse_E)
+    Hq, Hkv, d, n_tail, N = 4, 2, 8, 3, 25
+    k = _rand((Hkv, N, d), 37, 1.5)
+    v = _rand((Hkv, N, d), 38)
+    q = _rand((Hq, 2, d), 39, 1.5)
+    C = N - n_tail
+    keep = np.array([0, 3, 7, 8, 15])
+    ev = np.setdiff1d(np.arange(C), keep)
+    full_k, full_v = _compacted(k, v, [np.arange(C)], n_tail, [0, N], N)
+    r_k, r_v = _compacted(k, v, [keep], n_tail, [0, N], N)
+    e_k, e_v = _compacted(k, v, [ev], 0, [0, N], N)
+    o_f, l_f = oracle.cache_attention(q, full_k, full_v, [C], n_tail, 0, Hq, Hkv)
+    o_r, l_r = oracle.cache_attention(q, r_k, r_v, [len(keep)], n_tail, 0, Hq, Hkv)
+    o_e, l_e = oracle.cache_attention(q, e_k, e_v, [len(ev)], 0, 0, Hq, Hkv)
+    m = 1.0 - np.exp(l_r - l_f)
+    assert np.allclose(o_f, (1 - m)[..., None] * o_r + m[..., None] * o_e, rtol=1e-12, atol=1e-13)
+    assert np.allclose(l_f, np.logaddexp(l_r, l_e), rtol=1e-13, atol=1e-13)
+    assert np.all((m > 0) & (m < 1))
+
+
+# ----------------------------------------------------------------------------------
 # H2O accumulated attention
 # ----------------------------------------------------------------------------------
 def test_h2o_uniform_is_harmonic():
