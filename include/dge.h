@@ -183,6 +183,33 @@ dge_status_t dge_compact(const dge_geom_t *geom, const int32_t *idx, const int32
                          int32_t n_select, int32_t n_tail, const void *k, const void *v,
                          void *k_out, void *v_out, hipStream_t stream);
 
+/* Continuation check on the evicted cache (Sec. 3 Eq. 1; App. "Why deferral can recover
+ * FullKV", the eviction-mass equation; App. "Attention-matching loss"): attention of
+ * query rows over the compacted caches that dge_compact / dge_select_compact write.
+ * For sequence b, KV head h and each of its G = H_q / H_kv query heads, query row r
+ * (position N_b - q_from_end + r) attends
+ *   the retained past rows  k_c[b][h][0 .. n_kept[b])      (all precede the tail), and
+ *   the tail rows           k_c[b][h][n_kept[b] + t], t <= n_tail - q_from_end + r
+ *                           (tail row t sits at position N_b - n_tail + t),
+ * with weights softmax_j(q . k_j / sqrt(d)) in float32:
+ *   out[hq][b * n_q + r][:] = sum_j a_j v_j,
+ *   lse[hq][b * n_q + r]    = log sum_j exp(q . k_j / sqrt(d))  (natural log; -inf and a
+ *                             zero output when the row attends nothing).
+ * q_from_end = n_tail gives the window + draft scoring rows (their evicted mass is
+ * rho_q = 1 - exp(lse_R - lse_full), lse_full from a keep-all compaction); q_from_end <= 0
+ * gives continuation (decode) queries, which attend every kept row.
+ *   q        : [H_q][batch * n_q][d], the cache's element type.
+ *   k_c, v_c : [batch][H_kv][n_select + n_tail][d] (dge_compact layout).
+ *   n_kept   : [batch] int32 (clamped to [0, n_select]).
+ *   out      : [H_q][batch * n_q][d] float32 output;  lse : [H_q][batch * n_q] float32 output.
+ * No workspace.  Errors: DGE_ERR_INVALID for n_q < 1, n_select < 0, n_tail < 0,
+ * q_from_end > n_tail, n_select + n_tail < 1 or a NULL / misaligned pointer;
+ * DGE_ERR_UNSUPPORTED for more than 8 query heads per KV head. */
+dge_status_t dge_cache_attention(const dge_geom_t *geom, const void *q, int32_t n_q,
+                                 int32_t q_from_end, const void *k_c, const void *v_c,
+                                 int32_t n_select, int32_t n_tail, const int32_t *n_kept,
+                                 float *out, float *lse, hipStream_t stream);
+
 /* H2O accumulated attention, kept running through the draft rows
  * (Table "Complexity and measured overhead", footnote a; App. "Draft-guided eviction implementation" on H2O's prompt-query buffer):
  *   colsum[h][j] = (1/G) sum_{g in group h} sum_{p = j}^{N_b - 1} softmax_j(q_{g,p} . k_j / sqrt(d))

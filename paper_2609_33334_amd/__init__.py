@@ -197,6 +197,25 @@ def compact(geom: Geometry, idx, n_kept, n_select: int, n_tail: int, k, v, k_out
     return k_out, v_out
 
 
+def cache_attention(geom: Geometry, q, n_q: int, q_from_end: int, k_c, v_c, n_select: int,
+                    n_tail: int, n_kept, out=None, lse=None, stream=None):
+    """dge_cache_attention: attention of query rows over compacted caches (the layout of
+    compact / select_compact).  Returns (out [H_q][batch*n_q][d] float32,
+    lse [H_q][batch*n_q] float32, natural log)."""
+    torch = _torch()
+    rows = geom.batch * n_q
+    if out is None:
+        out = torch.empty(geom.n_q_heads, rows, geom.head_dim, dtype=torch.float32,
+                          device=geom.device)
+    if lse is None:
+        lse = torch.empty(geom.n_q_heads, rows, dtype=torch.float32, device=geom.device)
+    _lib.check(_lib.lib().dge_cache_attention(ctypes.byref(geom.c), _ptr(q), n_q, q_from_end,
+                                              _ptr(k_c), _ptr(v_c), n_select, n_tail,
+                                              _ptr(n_kept), _ptr(out), _ptr(lse),
+                                              _stream(stream)), "dge_cache_attention")
+    return out, lse
+
+
 def h2o_colsum(geom: Geometry, q_all, k, lse=None, colsum=None, ws=None, stream=None):
     """dge_h2o_colsum: H2O accumulated attention.  Returns colsum [H_kv][T] float32."""
     torch = _torch()

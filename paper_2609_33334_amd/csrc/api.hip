@@ -183,6 +183,24 @@ dge_status_t dge_compact(const dge_geom_t* geom, const int32_t* idx, const int32
       dge::launch_compact(*geom, idx, n_kept, n_select, n_tail, k, v, k_out, v_out, stream));
 }
 
+dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t n_q,
+                                 int32_t q_from_end, const void* k_c, const void* v_c,
+                                 int32_t n_select, int32_t n_tail, const int32_t* n_kept,
+                                 float* out, float* lse, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (n_q < 1 || n_select < 0 || n_tail < 0 || q_from_end > n_tail || n_select + n_tail < 1)
+    return DGE_ERR_INVALID;
+  if (!q || !k_c || !v_c || !n_kept || !out || !lse || !aligned16(q) || !aligned16(k_c) ||
+      !aligned16(v_c) || !aligned16(out) || (reinterpret_cast<uintptr_t>(n_kept) & 3) ||
+      (reinterpret_cast<uintptr_t>(lse) & 3))
+    return DGE_ERR_INVALID;
+  if (geom->n_q_heads / geom->n_kv_heads > dge::cache_attention_max_group())
+    return DGE_ERR_UNSUPPORTED;
+  return hip_status(dge::launch_cache_attention(*geom, q, n_q, q_from_end, k_c, v_c, n_select,
+                                                n_tail, n_kept, out, lse, stream));
+}
+
 dge_status_t dge_h2o_colsum(const dge_geom_t* geom, const void* q_all, const void* k,
                             const float* lse, float* colsum, void* ws, size_t ws_bytes,
                             hipStream_t stream) {

@@ -49,6 +49,12 @@ hipError_t launch_compact(const dge_geom_t& g, const int32_t* idx, const int32_t
                           int n_select, int n_tail, const void* k, const void* v, void* k_out,
                           void* v_out, hipStream_t stream);
 
+int cache_attention_max_group();
+hipError_t launch_cache_attention(const dge_geom_t& g, const void* q, int n_q, int q_from_end,
+                                  const void* k_c, const void* v_c, int n_select, int n_tail,
+                                  const int32_t* n_kept, float* out, float* lse,
+                                  hipStream_t stream);
+
 size_t h2o_workspace_bytes(const dge_geom_t& g);
 hipError_t launch_h2o(const dge_geom_t& g, const void* q_all, const void* k, const float* lse,
                       float* colsum, void* ws, hipStream_t stream);

@@ -158,3 +158,21 @@ def test_streaming_compact_h2o_validation(L):
     assert L.dge_h2o_colsum(g.p, FAKE, FAKE, None, FAKE, None, 0, None) == _lib.DGE_ERR_WORKSPACE
     assert L.dge_h2o_colsum(g.p, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.DGE_ERR_WORKSPACE
     assert L.dge_h2o_colsum(_G(hq=16, hkv=2).p, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None) == _lib.DGE_ERR_UNSUPPORTED
+
+
+def test_cache_attention_validation(L):
+    g = _G()
+    def att(geom=g, q=FAKE, n_q=3, q_from_end=0, kc=FAKE, vc=FAKE, n_select=20, n_tail=10,
+            nk=FAKE, out=FAKE, lse=FAKE):
+        return L.dge_cache_attention(geom.p, q, n_q, q_from_end, kc, vc, n_select, n_tail, nk,
+                                     out, lse, None)
+    assert att(n_q=0) == _lib.DGE_ERR_INVALID
+    assert att(n_select=-1) == _lib.DGE_ERR_INVALID
+    assert att(n_tail=-1) == _lib.DGE_ERR_INVALID
+    assert att(q_from_end=11) == _lib.DGE_ERR_INVALID        # rows before the tail start
+    assert att(n_select=0, n_tail=0, q_from_end=0) == _lib.DGE_ERR_INVALID
+    assert att(q=None) == _lib.DGE_ERR_INVALID
+    assert att(kc=FAKE + 4) == _lib.DGE_ERR_INVALID
+    assert att(lse=FAKE + 2) == _lib.DGE_ERR_INVALID
+    assert att(geom=_G(hq=18, hkv=2)) == _lib.DGE_ERR_UNSUPPORTED   # 9 query heads per KV head
+    assert att(geom=_G(d=96)) == _lib.DGE_ERR_UNSUPPORTED

@@ -352,3 +352,127 @@ def test_h2o_c5_two_heads_and_select():
         must = set(np.nonzero(want[:N - wl.n_recent] > t * (1 + 1e-3))[0].tolist())
         never = set(np.nonzero(want[:N - wl.n_recent] < t * (1 - 1e-3))[0].tolist())
         assert must <= gi and not (never & gi)
+
+
+# ------------------------------------------------------------------------------------------
+# Attention over the compacted cache (continuation check, Eq. 1 / eviction-mass equation)
+# ------------------------------------------------------------------------------------------
+def _evicted_cache(wl, x, g):
+    """GPU eviction of one layer: (idx, n_kept, k_c, v_c) on the device."""
+    n_tail = wl.window + wl.k_draft
+    n_sel = wl.budget - wl.window
+    q, k, v = to_dev(x.q_bits, wl.dtype), to_dev(x.k_bits, wl.dtype), to_dev(x.v_bits, wl.dtype)
+    raw = dge.score(g, dge.ROWS_WINDOW_DRAFT, q, k)
+    idx, nk, kc, vc = dge.select_compact(g, raw, wl.pool, n_tail, n_sel, k, v)
+    torch.cuda.synchronize()
+    return idx, nk, kc, vc, k, v, n_sel, n_tail
+
+
+def _host_f64(t, dtype):
+    t = t.cpu()
+    if dtype == "bf16":
+        return di.bf16_bits_to_f32(t.view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
+    return t.numpy().astype(np.float64)
+
+
+def _check_att(got_o, got_l, want_o, want_l, what):
+    got_o, got_l = got_o.cpu().numpy().astype(np.float64), got_l.cpu().numpy().astype(np.float64)
+    fin = np.isfinite(want_l)
+    assert np.array_equal(fin, np.isfinite(got_l)), f"{what}: attended-nothing rows differ"
+    lerr = float(np.abs(got_l[fin] - want_l[fin]).max()) if fin.any() else 0.0
+    oerr = float(np.abs(got_o - want_o).max())
+    _log(f"  {what}: max |lse err| {lerr:.2e}, max |out err| {oerr:.2e}")
+    assert lerr <= 1e-4, f"{what}: lse error {lerr}"
+    assert np.all(np.abs(got_o - want_o) <= 1e-4 + 1e-3 * np.abs(want_o)), f"{what}: output error {oerr}"
+
+
+ATT_CASES = {
+    "c2_700": di.small_variant("c2", [700]),
+    "ragged": di.small_variant("c2", [300, 517, 1029, 70]),
+    "f32_d64": di.WORKLOADS["c1"],
+}
+
+
+@pytest.mark.parametrize("case", list(ATT_CASES))
+def test_cache_attention_parity(case):
+    wl = ATT_CASES[case]
+    _log(f"cache attention parity {case} lens={wl.prompt_lens}")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    idx, nk, kc, vc, _, _, n_sel, n_tail = _evicted_cache(wl, x, g)
+    kc64, vc64 = _host_f64(kc, wl.dtype), _host_f64(vc, wl.dtype)
+    n_kept = nk.cpu().numpy()[:wl.batch]
+    # decode queries (positions N_b, N_b + 1, N_b + 2: every kept row visible)
+    rng = np.random.default_rng(77)
+    qd = rng.standard_normal((wl.n_q_heads, wl.batch * 3, wl.head_dim)).astype(np.float32)
+    qd_bits = di.f32_to_bf16_bits(qd) if wl.dtype == "bf16" else qd
+    qd64 = di.bf16_bits_to_f32(qd_bits).astype(np.float64) if wl.dtype == "bf16" else qd.astype(np.float64)
+    out, lse = dge.cache_attention(g, to_dev(qd_bits, wl.dtype), 3, 0, kc, vc, n_sel, n_tail, nk)
+    torch.cuda.synchronize()
+    wo, wlse = oracle.cache_attention(qd64, kc64, vc64, n_kept, n_tail, 0, wl.n_q_heads, wl.n_kv_heads)
+    _check_att(out, lse, wo, wlse, f"{case} decode")
+    # the scoring rows themselves (causal inside the tail)
+    out, lse = dge.cache_attention(g, to_dev(x.q_bits, wl.dtype), n_tail, n_tail, kc, vc, n_sel,
+                                   n_tail, nk)
+    torch.cuda.synchronize()
+    wo, wlse = oracle.cache_attention(x.q, kc64, vc64, n_kept, n_tail, n_tail, wl.n_q_heads,
+                                      wl.n_kv_heads)
+    _check_att(out, lse, wo, wlse, f"{case} scoring rows")
+
+
+def test_cache_attention_eq1_and_evicted_mass():
+    """Eq. 1 on GPU outputs alone (keep-all, kept and evicted compactions of the same
+    layer), and the scoring rows' evicted mass rho_q against the oracle's."""
+    wl = di.small_variant("c2", [900, 1400])
+    _log("cache attention Eq. 1 decomposition and evicted mass")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    idx, nk, kc, vc, k, v, n_sel, n_tail = _evicted_cache(wl, x, g)
+    C = [n - n_tail for n in wl.cached_lens]
+    n_kept = nk.cpu().numpy()[:wl.batch]
+    idx_h = idx.cpu().numpy()
+    # keep-all compaction and the complement (evicted rows only, no tail)
+    n_all = max(C)
+    idx_all = np.full((wl.batch, wl.n_kv_heads, n_all), -1, np.int32)
+    n_ev = max(C[b] - int(n_kept[b]) for b in range(wl.batch))
+    idx_ev = np.full((wl.batch, wl.n_kv_heads, n_ev), -1, np.int32)
+    for b in range(wl.batch):
+        for h in range(wl.n_kv_heads):
+            idx_all[b, h, :C[b]] = np.arange(C[b])
+            ev = np.setdiff1d(np.arange(C[b]), idx_h[b, h, :n_kept[b]])
+            idx_ev[b, h, :len(ev)] = ev
+    nk_all = torch.tensor(C, dtype=torch.int32, device=DEV)
+    nk_ev = torch.tensor([C[b] - int(n_kept[b]) for b in range(wl.batch)], dtype=torch.int32,
+                         device=DEV)
+    kf, vf = dge.compact(g, torch.from_numpy(idx_all).to(DEV), nk_all, n_all, n_tail, k, v)
+    ke, ve = dge.compact(g, torch.from_numpy(idx_ev).to(DEV), nk_ev, n_ev, 0, k, v)
+    rng = np.random.default_rng(78)
+    qd = di.f32_to_bf16_bits(rng.standard_normal((wl.n_q_heads, wl.batch * 2, wl.head_dim)).astype(np.float32))
+    qdd = to_dev(qd, "bf16")
+    o_f, l_f = dge.cache_attention(g, qdd, 2, 0, kf, vf, n_all, n_tail, nk_all)
+    o_r, l_r = dge.cache_attention(g, qdd, 2, 0, kc, vc, n_sel, n_tail, nk)
+    o_e, l_e = dge.cache_attention(g, qdd, 2, 0, ke, ve, n_ev, 0, nk_ev)
+    torch.cuda.synchronize()
+    o_f, l_f, o_r, l_r, o_e, l_e = (t.cpu().double().numpy() for t in (o_f, l_f, o_r, l_r, o_e, l_e))
+    m = 1.0 - np.exp(l_r - l_f)
+    recon = (1 - m)[..., None] * o_r + m[..., None] * o_e
+    err_o = float(np.abs(o_f - recon).max())
+    err_l = float(np.abs(l_f - np.logaddexp(l_r, l_e)).max())
+    _log(f"  Eq. 1: max |o_full - ((1-m) o_R + m o_E)| {err_o:.2e}; log-partition {err_l:.2e}; "
+         f"evicted mass of the decode queries in [{m.min():.3g}, {m.max():.3g}]")
+    assert err_o < 1e-4 and err_l < 1e-4
+    # evicted mass rho_q of the scoring rows (observation queries of the matching loss)
+    qs = to_dev(x.q_bits, "bf16")
+    _, lf_s = dge.cache_attention(g, qs, n_tail, n_tail, kf, vf, n_all, n_tail, nk_all)
+    _, lr_s = dge.cache_attention(g, qs, n_tail, n_tail, kc, vc, n_sel, n_tail, nk)
+    torch.cuda.synchronize()
+    rho = 1.0 - np.exp(lr_s.cpu().double().numpy() - lf_s.cpu().double().numpy())
+    kc64, vc64 = _host_f64(kc, "bf16"), _host_f64(vc, "bf16")
+    _, w_r = oracle.cache_attention(x.q, kc64, vc64, n_kept, n_tail, n_tail, wl.n_q_heads, wl.n_kv_heads)
+    w_f = oracle.scoring_row_lse(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                 wl.k_draft)
+    rho_want = 1.0 - np.exp(w_r - w_f)
+    err = float(np.abs(rho - rho_want).max())
+    _log(f"  scoring rows: evicted mass max |err| {err:.2e}; matching loss "
+         f"{float(np.mean(-np.log1p(-rho))):.4f} (oracle {float(np.mean(-np.log1p(-rho_want))):.4f})")
+    assert err < 2e-4
