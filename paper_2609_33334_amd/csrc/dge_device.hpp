@@ -114,6 +114,57 @@ __device__ __forceinline__ void lazy_lse_update4(const float (&x)[4], float scal
           (fast_exp2(fmaf(x[2], scale, -mref)) + fast_exp2(fmaf(x[3], scale, -mref)));
 }
 
+// Online (max, sum) update with NV logits of one row at once, branch-free: the
+// reference becomes the running maximum, the old sum is rescaled once (one exp2 per NV
+// logits) and every logit adds 2^(x*scale - m).  m starts finite (kLazyRefInit), so
+// masked logits (-inf) add exactly 0 and a fully masked batch leaves (m, s) unchanged.
+template <int NV>
+__device__ __forceinline__ void online_lse_update(const float (&x)[NV], float scale, float& m,
+                                                  float& s) {
+  float mx = x[0];
+#pragma unroll
+  for (int i = 1; i < NV; ++i) mx = fmaxf(mx, x[i]);
+  const float nm = fmaxf(m, mx * scale);
+  float e[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) e[i] = fast_exp2(fmaf(x[i], scale, -nm));
+#pragma unroll
+  for (int w = 1; w < NV; w *= 2)
+#pragma unroll
+    for (int i = 0; i + w < NV; i += 2 * w) e[i] += e[i + w];
+  s = fmaf(s, fast_exp2(m - nm), e[0]);
+  m = nm;
+}
+
+// Sum of v over the four lane groups (lanes l, l^16, l^32, l^48), returned in every
+// lane.  v_permlane32_swap exchanges the upper half of one copy with the lower half of
+// the other, so the two results add to the sum over l and l^32; v_permlane16_swap does
+// the same for odd/even rows of 16 lanes.  Both are VALU operations (no LDS round trip).
+__device__ __forceinline__ float sum_lane_groups(float v) {
+  const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  v = __uint_as_float(h[0]) + __uint_as_float(h[1]);
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Reduce-scatter over the four lane groups: lane group g returns, for its position
+// c = l % 16, the sum of v[g] over lanes c, c+16, c+32, c+48.  The first two swaps
+// leave the half-sums of v[0] / v[1] in lanes 0-31 and of v[2] / v[3] in lanes 32-63;
+// the row swap then pairs rows (0,1) and (2,3).
+__device__ __forceinline__ float reduce_scatter_lane_groups(const float (&v)[4]) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[0]), __float_as_uint(v[2]),
+                                                  false, false);
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[1]), __float_as_uint(v[3]),
+                                                  false, false);
+  const float a = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  const float b = __uint_as_float(q[0]) + __uint_as_float(q[1]);
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Waits and barriers for pipelines that keep global->LDS copies in flight across
 // workgroup barriers (__syncthreads() would drain every outstanding load).
 // s_waitcnt immediate on gfx9: vmcnt[3:0] + vmcnt[5:4] at [15:14], expcnt[6:4],

@@ -6,16 +6,18 @@
 // A column sum needs every scoring row's global normaliser first, so one layer runs
 // as three launches over the same split of the keys into chunks:
 //   1. stats : each workgroup streams its chunk of K and keeps, per query row, the
-//              running (max, sum of 2^(x - max)) of its logits (log2 domain);
+//              running (max, sum of 2^(x - max)) of its logits (log2 domain), stored
+//              as one log2-sum-exp per row and chunk;
 //   2. reduce: one wavefront per (row, sequence, KV head) merges the chunk partials
 //              into c_r = log2 Z_r;
 //   3. colsum: each workgroup streams its chunk again, P = 2^(x - c_r), sums over all
 //              rows of the group and writes raw[] (the K slab of one layer, 8-34 MB at
 //              Llama-3-8B geometry, is still in the 256 MB Infinity Cache).
 // With caller-supplied row LSEs (dge_score_lse) only the colsum pass runs.
-// (A single launch that waits in-kernel for the other chunks of a head was measured
-// slower on MI355X: device-scope atomics and coherent loads cost microseconds each,
-// more than the two kernel boundaries they replace.)
+// (Measured slower on MI355X, and not used: a single launch that waits in-kernel for
+// the other chunks of a head -- device-scope atomics and coherent loads cost
+// microseconds each -- and merging the chunk partials inside every colsum workgroup,
+// whose extra loads join the burst of query and K loads at kernel start.)
 //
 // Workgroups are laid out XCD-aware (see xcd_unit): the chunks of one KV head share an
 // XCD, so its query block is fetched into one L2, and the colsum pass finds each chunk
@@ -34,13 +36,16 @@
 //   past the end of a chunk keep every wait count fixed) while one is on the matrix
 //   cores; the loop's barriers wait on LDS traffic only, so the copies are never
 //   drained early.
-// - stats keeps each row's sum relative to a lazily moved reference and runs a masked
-//   tile body only where a tile reaches past the first scoring position.
+// - Tile bodies are branch-free: all products of a tile (or of a group of subtiles)
+//   are issued before their results are used, so the exp2 work overlaps the matrix
+//   cores; a separate masked body runs only where a tile reaches past the first
+//   scoring position.
 // - stats uses the transposed product (A = keys, B = query rows): a lane then holds
-//   4 keys of ONE row, so the per-row max/sum is mostly in-lane and needs two
-//   cross-lane steps per row tile at the end of the chunk.
+//   4 keys of ONE row, so the per-row max/sum is in-lane (one running-max update per
+//   group of subtiles) and needs cross-lane steps only at the end of the chunk.
 // - colsum uses A = query rows, B = keys: a lane holds 4 rows of ONE key, the sum
-//   over rows is in-lane, then across the 4 lane groups and the 4 wavefronts.
+//   over rows is in-lane, then across the 4 lane groups (permlane swaps) and the 4
+//   wavefronts (LDS, double-buffered, flushed after the next tile's barrier).
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
 
@@ -54,7 +59,7 @@ struct ScoreArgs {
   const void* q;
   const void* k;
   float* raw;
-  float2* partial;   // [batch][H_kv][n_chunks][M_pad] (max, sum) per chunk, log2 domain
+  float* partial;    // [batch][H_kv][n_chunks][M_pad] log2-sum-exp of each row per chunk
   float* rowc;       // [batch][H_kv][M_pad]  log2 of each row's softmax normaliser
   const float* lse_in;      // optional [H_q][batch * n_rows] natural-log row LSE
   SeqOffsets offs;
@@ -128,11 +133,12 @@ __device__ __forceinline__ int slot_tile(int tile0, int wv, int i) {
   return i < FT ? tile0 + wv + 4 * i : tile0 + 4 * FT + (i - FT);
 }
 
-// Register loads before the K copies: from asm (untracked by the compiler, so the first
-// tile wait covers them and later tiles keep streaming) when the wavefront holds at
-// most kAsyncSlots slots; with more, register pressure makes the compiler copy values
+// Register loads before the K copies (query fragments, the colsum pass's row
+// normalisers): from asm (untracked by the compiler, so an explicit vmcnt wait
+// covers them and the K tiles keep streaming) when the wavefront holds at most
+// kAsyncSlots slots; with more, register pressure makes the compiler copy values
 // between registers before they can have landed, so those instances use ordinary loads
-// and one full wait before the stream.
+// and the compiler's own waits.
 constexpr int kAsyncSlots = 6;
 template <int NQ>
 __device__ __forceinline__ u32x4_t slot_load16(const void* p) {
@@ -177,6 +183,7 @@ __device__ __forceinline__ void q_fence(u32x4_t (&qf)[NQ][NS]) {
     wait_vmcnt<0>();         // compiler-visible: no wait of its own inside the stream
   }
 }
+
 template <int NQ>
 __device__ __forceinline__ void cr_fence(float (&cr)[NQ][4]) {
   if constexpr (NQ <= kAsyncSlots) {
@@ -187,21 +194,30 @@ __device__ __forceinline__ void cr_fence(float (&cr)[NQ][4]) {
   }
 }
 
-// Copies of tiles 0..S-2 of a chunk (dummies past its end), then the wait for tile 0:
-// every load issued before the copies (query fragments, normalisers) has landed too.
+// Copies of tiles 0..S-2 of a chunk (dummies past its end).
+template <typename T, int D>
+__device__ __forceinline__ void ktile_issue(const char* kb, int c0, int ntiles, int N,
+                                            char (*buf)[KTile<T, D>::kBytes], int wv, int lane) {
+  constexpr int S = KTile<T, D>::kStages;
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t) ktile_dma<T, D>(kb, c0 + t * KT, N, buf[t], wv, lane, t < ntiles);
+}
+
+// The copies, then the wait for tile 0: every load issued before the copies (query
+// fragments) has landed too.
 template <typename T, int D>
 __device__ __forceinline__ void ktile_prologue(const char* kb, int c0, int ntiles, int N,
                                                char (*buf)[KTile<T, D>::kBytes], int wv,
                                                int lane) {
-  constexpr int S = KTile<T, D>::kStages;
-#pragma unroll
-  for (int t = 0; t < S - 1; ++t) ktile_dma<T, D>(kb, c0 + t * KT, N, buf[t], wv, lane, t < ntiles);
+  ktile_issue<T, D>(kb, c0, ntiles, N, buf, wv, lane);
   ktile_wait<T, D>();
 }
 
-// consume(tile, j0) for the tiles of [c0, c0 + ntiles * KT), ntiles >= 1, after the
-// prologue.  Tile t lands in buffer t % S; S - 1 copies stay in flight (dummies past
-// the chunk's end) and all of them have landed when this returns.
+// consume(tile, j0, t) for the tiles t of [c0, c0 + ntiles * KT), ntiles >= 1, after
+// the prologue.  Tile t lands in buffer t % S; S - 1 copies stay in flight (dummies
+// past the chunk's end) and all of them have landed when this returns.  The barrier
+// at the top of each iteration also waits for the wavefront's own LDS traffic, so
+// whatever consume(t - 1) wrote to LDS is visible to every wavefront in consume(t).
 template <typename T, int D, typename F>
 __device__ __forceinline__ void ktile_stream(const char* kb, int c0, int ntiles, int N,
                                              char (*buf)[KTile<T, D>::kBytes], int wv, int lane,
@@ -210,19 +226,37 @@ __device__ __forceinline__ void ktile_stream(const char* kb, int c0, int ntiles,
   int t = 0;
   do {
     if (t > 0) ktile_wait<T, D>();
-    wg_barrier();            // tile t landed everywhere; buffer (t - 1) % S and red[] free
+    lds_barrier();           // tile t landed everywhere; buffer (t - 1) % S free
     const int tn = t + S - 1;
     ktile_dma<T, D>(kb, c0 + tn * KT, N, buf[tn % S], wv, lane, tn < ntiles);
-    consume(buf[t % S], c0 + t * KT);
+    consume(buf[t % S], c0 + t * KT, t);
   } while (++t < ntiles);
   asm_wait_vmcnt<0>();       // no copy still writes into the buffers
 }
 
-// Per-wavefront row state of the stats pass: lane (c16, g16) holds row c16 of each
-// slot's tile and keys 4*g16..4*g16+3 of a 16-key subtile; the sums use the lazy
-// reference of lazy_lse_update4.
-constexpr float kRefInit = kLazyRefInit;
+// Subtiles of a 64-key tile whose products the stats pass issues together before their
+// results are used (16 registers per own tile per subtile); the running maxima are
+// updated once per group (one rescale per 4 * group logits of a row).  The products of
+// one group are independent of the exp2 work of the previous one, so the matrix cores
+// and the vector ALUs overlap.
+template <int FT>
+constexpr int sub_group() { return FT <= 2 ? 4 : (FT <= 4 ? 2 : 1); }
 
+// Wavefronts per SIMD the score kernels are compiled for: two (256 registers each, so
+// two workgroups share a compute unit) while a wavefront holds at most 12 16-byte query
+// chunks, owns at most two row tiles and shares at most two (every Llama-3-8B-shaped
+// scoring geometry); larger row sets get the whole register file and one wavefront per
+// SIMD instead of spilling.
+template <typename T, int D, int FT, int RT>
+constexpr int score_waves() {
+  constexpr int NS = RowChunks<T, D>::kSteps;
+  return (FT + RT) * NS <= 12 && FT < 3 && RT < 3 && NS <= 4 ? 2 : 1;
+}
+
+// Per-wavefront row state of the stats pass: lane (c16, g16) holds row c16 of each
+// slot's tile and keys 4*g16..4*g16+3 of every 16-key subtile; (mref, srow) is the
+// running (max, sum of 2^(x - max)) of those logits in the log2 domain, mref starting
+// finite (see online_lse_update).
 template <int NQ>
 struct StatsRows {
   int pos[NQ];
@@ -238,67 +272,81 @@ __device__ __forceinline__ void stats_rows_init(const ScoreArgs& a, int tile0, i
     const int m = slot_tile<FT>(tile0, wv, i) * 16 + c16;
     st.live[i] = m < a.M;
     st.pos[i] = p0 + (st.live[i] ? m % a.n_rows : 0);
-    st.mref[i] = kRefInit;
+    st.mref[i] = kLazyRefInit;
     st.srow[i] = 0.0f;
   }
 }
 
-// acc[t] = logit (unscaled) of key jb + t for this lane's row.  MASK: the tile reaches
-// past the sequence or past some row's position (the last tiles of a sequence only).
-template <bool MASK>
-__device__ __forceinline__ void stats_update(const f32x4_t& acc, int jb, bool live, int pos,
-                                             int N, float scale, float& mref, float& srow) {
-  float x[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    x[t] = acc[t];
-    if constexpr (MASK) x[t] = (live && jb + t < N && jb + t <= pos) ? x[t] : -INFINITY;
-  }
-  lazy_lse_update4(x, scale, mref, srow);
+// Logit of key j for a row at position pos, -inf where it is masked.  MASK bodies run
+// only on tiles that reach past the sequence or past the first scoring position.
+__device__ __forceinline__ float stats_mask(float x, int j, bool live, int pos, int N) {
+  return (live && j < N && j <= pos) ? x : -INFINITY;
 }
 
-// Running sums of one 64-key tile for the wavefront's slots.
+// Running sums of one 64-key tile for the wavefront's slots (A = keys, B = query rows).
 template <typename T, int D, int FT, int RT, bool MASK>
 __device__ __forceinline__ void stats_tile_body(const ScoreArgs& a, const char* lds, int j0, int N,
                                                 int wv, int c16, int g16,
                                                 const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
                                                 StatsRows<FT + RT>& st) {
   constexpr int NS = RowChunks<T, D>::kSteps;
-  if constexpr (FT > 0) {
-#pragma unroll 2
-    for (int sub = 0; sub < KT / 16; ++sub) {
-      uint4 kf[NS];
-#pragma unroll
-      for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
-      // FT independent accumulation chains, issued k-step-major (A = keys, B = rows)
-      f32x4_t acc[FT];
-#pragma unroll
-      for (int i = 0; i < FT; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-#pragma unroll
-        for (int i = 0; i < FT; ++i) acc[i] = mma_step(T{}, kf[s], as_uint4(qf[i][s]), acc[i]);
-#pragma unroll
-      for (int i = 0; i < FT; ++i)
-        stats_update<MASK>(acc[i], j0 + sub * 16 + 4 * g16, st.live[i], st.pos[i], N,
-                           a.scale_log2, st.mref[i], st.srow[i]);
-    }
-  }
+  constexpr int SG = sub_group<FT>();
+  f32x4_t accr[RT > 0 ? RT : 1];
   if constexpr (RT > 0) {                  // shared tiles: subtile wv only
     uint4 kf[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, wv * 16 + c16, s, g16);
-    f32x4_t acc[RT];
 #pragma unroll
-    for (int r = 0; r < RT; ++r) acc[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int r = 0; r < RT; ++r) accr[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int r = 0; r < RT; ++r) acc[r] = mma_step(T{}, kf[s], as_uint4(qf[FT + r][s]), acc[r]);
+      for (int r = 0; r < RT; ++r) accr[r] = mma_step(T{}, kf[s], as_uint4(qf[FT + r][s]), accr[r]);
+  }
+  if constexpr (FT > 0) {
 #pragma unroll
-    for (int r = 0; r < RT; ++r)
-      stats_update<MASK>(acc[r], j0 + wv * 16 + 4 * g16, st.live[FT + r], st.pos[FT + r], N,
-                         a.scale_log2, st.mref[FT + r], st.srow[FT + r]);
+    for (int sg = 0; sg < KT / 16; sg += SG) {
+      f32x4_t acc[SG][FT];
+#pragma unroll
+      for (int u = 0; u < SG; ++u) {
+        uint4 kf[NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, (sg + u) * 16 + c16, s, g16);
+#pragma unroll
+        for (int i = 0; i < FT; ++i) acc[u][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+          for (int i = 0; i < FT; ++i) acc[u][i] = mma_step(T{}, kf[s], as_uint4(qf[i][s]), acc[u][i]);
+      }
+#pragma unroll
+      for (int i = 0; i < FT; ++i) {
+        float x[4 * SG];
+#pragma unroll
+        for (int u = 0; u < SG; ++u)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            x[4 * u + t] = acc[u][i][t];
+            if constexpr (MASK)
+              x[4 * u + t] = stats_mask(x[4 * u + t], j0 + (sg + u) * 16 + 4 * g16 + t,
+                                        st.live[i], st.pos[i], N);
+          }
+        online_lse_update<4 * SG>(x, a.scale_log2, st.mref[i], st.srow[i]);
+      }
+    }
+  }
+  if constexpr (RT > 0) {
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      float x[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        x[t] = accr[r][t];
+        if constexpr (MASK)
+          x[t] = stats_mask(x[t], j0 + wv * 16 + 4 * g16 + t, st.live[FT + r], st.pos[FT + r], N);
+      }
+      online_lse_update<4>(x, a.scale_log2, st.mref[FT + r], st.srow[FT + r]);
+    }
   }
 }
 
@@ -330,26 +378,31 @@ __device__ __forceinline__ void stats_rows_merge(StatsRows<NQ>& st) {
   }
 }
 
-// Column sums of one 64-key tile: lane (c16, g16) holds rows 4*g16..4*g16+3 of each
-// slot's tile for key c16 of a 16-key subtile.  cr = log2 normaliser of each row (+inf
-// for padding rows, whose terms are then exactly 0).  Ends with wavefront 0 adding the
-// tile's sums into out[].  MASK: the tile reaches past the first scoring position.
+// Column sums of one 64-key tile (A = query rows, B = keys): for subtile u, lane
+// (c16, g16) holds rows 4*g16..4*g16+3 of each slot's tile for key u*16 + c16.  cr = log2
+// normaliser of each row (+inf for padding rows, whose terms are then exactly 0).  The
+// subtiles are independent straight-line code, so the products of one overlap the exp2
+// work of the previous one.  Ends with lane group g16 of every wavefront writing the
+// wavefront's sums of subtile g16 to redw[g16 * 16 + c16].  MASK: the tile reaches past
+// the first scoring position; pos(i, t) is then the position of row (slot i, 4*g16 + t).
 template <typename T, int D, int FT, int RT, bool MASK>
 __device__ __forceinline__ void colsum_tile_body(const ScoreArgs& a, const char* lds, int j0,
-                                                 int N, int wv, int c16, int g16,
+                                                 int N, int p0, int tile0, int wv, int c16,
+                                                 int g16,
                                                  const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
-                                                 const float (&cr)[FT + RT][4],
-                                                 const int (&pos)[FT + RT][4], float (*red)[KT]) {
+                                                 const float (&cr)[FT + RT][4], float* redw) {
   constexpr int NS = RowChunks<T, D>::kSteps;
-#pragma unroll 2
-  for (int sub = 0; sub < KT / 16; ++sub) {
-    uint4 kf[NS];
+  auto pos = [&](int i, int t) {
+    const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
+    return p0 + min(m, a.M - 1) % a.n_rows;
+  };
+  float colp[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (FT > 0) {
 #pragma unroll
-    for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, sub * 16 + c16, s, g16);
-    const int j = j0 + sub * 16 + c16;
-    float colp = 0.0f;
-    // acc[i][t] = logit of row (slot tile*16 + 4*g16 + t) for key j (A = rows, B = keys)
-    if constexpr (FT > 0) {
+    for (int u = 0; u < KT / 16; ++u) {
+      uint4 kf[NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, u * 16 + c16, s, g16);
       f32x4_t acc[FT];
 #pragma unroll
       for (int i = 0; i < FT; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -357,74 +410,74 @@ __device__ __forceinline__ void colsum_tile_body(const ScoreArgs& a, const char*
       for (int s = 0; s < NS; ++s)
 #pragma unroll
         for (int i = 0; i < FT; ++i) acc[i] = mma_step(T{}, as_uint4(qf[i][s]), kf[s], acc[i]);
+      const int j = j0 + u * 16 + c16;
 #pragma unroll
-      for (int i = 0; i < FT; ++i)
+      for (int i = 0; i < FT; ++i) {
+        float e[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          float p = fast_exp2(fmaf(acc[i][t], a.scale_log2, -cr[i][t]));
-          if constexpr (MASK) p = (j < N && j <= pos[i][t]) ? p : 0.0f;
-          colp += p;
+          e[t] = fast_exp2(fmaf(acc[i][t], a.scale_log2, -cr[i][t]));
+          if constexpr (MASK) e[t] = (j < N && j <= pos(i, t)) ? e[t] : 0.0f;
         }
-    }
-    if constexpr (RT > 0) {
-      if (sub == wv) {                     // shared tiles: this wavefront's subtile
-        f32x4_t acc[RT];
-#pragma unroll
-        for (int r = 0; r < RT; ++r) acc[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < NS; ++s)
-#pragma unroll
-          for (int r = 0; r < RT; ++r) acc[r] = mma_step(T{}, as_uint4(qf[FT + r][s]), kf[s], acc[r]);
-#pragma unroll
-        for (int r = 0; r < RT; ++r)
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            float p = fast_exp2(fmaf(acc[r][t], a.scale_log2, -cr[FT + r][t]));
-            if constexpr (MASK) p = (j < N && j <= pos[FT + r][t]) ? p : 0.0f;
-            colp += p;
-          }
+        colp[u] += (e[0] + e[1]) + (e[2] + e[3]);
       }
     }
-    colp += shfl_xor_f<16>(colp);
-    colp += shfl_xor_f<32>(colp);
-    if (g16 == 0) red[wv][sub * 16 + c16] = colp;
   }
-}
-
-template <typename T, int D, int FT, int RT>
-__device__ __forceinline__ void colsum_tile(const ScoreArgs& a, const char* lds, int j0, int c1,
-                                            int N, int tid, int wv, int c16, int g16,
-                                            const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
-                                            const float (&cr)[FT + RT][4],
-                                            const int (&pos)[FT + RT][4], const int p0,
-                                            float (*red)[KT], float* out, bool accumulate) {
-  if (j0 + KT - 1 > p0)
-    colsum_tile_body<T, D, FT, RT, true>(a, lds, j0, N, wv, c16, g16, qf, cr, pos, red);
-  else
-    colsum_tile_body<T, D, FT, RT, false>(a, lds, j0, N, wv, c16, g16, qf, cr, pos, red);
-  lds_barrier();                           // column partials of all 4 wavefronts
-  if (tid < KT && j0 + tid < c1) {
-    const float v = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
-    if (accumulate) out[j0 + tid] += v * a.inv_G;
-    else out[j0 + tid] = v * a.inv_G;
-  }
-}
-
-// Positions of the colsum rows (4 per lane per slot).
-template <int FT, int NQ>
-__device__ __forceinline__ void colsum_positions(const ScoreArgs& a, int tile0, int wv, int g16,
-                                                 int p0, int (&pos)[NQ][4]) {
+  if constexpr (RT > 0) {                  // shared tiles: this wavefront's subtile only
+    uint4 kf[NS];
 #pragma unroll
-  for (int i = 0; i < NQ; ++i)
+    for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, wv * 16 + c16, s, g16);
+    f32x4_t accr[RT];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
-      pos[i][t] = p0 + min(m, a.M - 1) % a.n_rows;
+    for (int r = 0; r < RT; ++r) accr[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int r = 0; r < RT; ++r) accr[r] = mma_step(T{}, as_uint4(qf[FT + r][s]), kf[s], accr[r]);
+    const int j = j0 + wv * 16 + c16;
+    float cp = 0.0f;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      float e[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        e[t] = fast_exp2(fmaf(accr[r][t], a.scale_log2, -cr[FT + r][t]));
+        if constexpr (MASK) e[t] = (j < N && j <= pos(FT + r, t)) ? e[t] : 0.0f;
+      }
+      cp += (e[0] + e[1]) + (e[2] + e[3]);
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) colp[u] += u == wv ? cp : 0.0f;
+  }
+  redw[g16 * 16 + c16] = reduce_scatter_lane_groups(colp);
+}
+
+// Column sums of the tile at j0 from the four wavefronts' partials (red[w][key]):
+// lanes 0..15 of wavefront w store keys w*16..w*16+15.
+__device__ __forceinline__ void colsum_flush(const ScoreArgs& a, const float (*red)[KT], int j0,
+                                             int c1, int wv, int lane, float* out,
+                                             bool accumulate) {
+  const int key = wv * 16 + lane;
+  if (lane < 16 && j0 + key < c1) {
+    const float v = ((red[0][key] + red[1][key]) + (red[2][key] + red[3][key])) * a.inv_G;
+    if (accumulate) out[j0 + key] += v;
+    else out[j0 + key] = v;
+  }
 }
 
 template <typename T, int D, int FT, int RT>
-__global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
+__device__ __forceinline__ void colsum_tile(const ScoreArgs& a, const char* lds, int j0, int N,
+                                            int p0, int tile0, int wv, int c16, int g16,
+                                            const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
+                                            const float (&cr)[FT + RT][4], float* redw) {
+  if (j0 + KT - 1 > p0)
+    colsum_tile_body<T, D, FT, RT, true>(a, lds, j0, N, p0, tile0, wv, c16, g16, qf, cr, redw);
+  else
+    colsum_tile_body<T, D, FT, RT, false>(a, lds, j0, N, p0, tile0, wv, c16, g16, qf, cr, redw);
+}
+
+template <typename T, int D, int FT, int RT>
+__global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score_stats_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int NQ = FT + RT;
@@ -447,7 +500,7 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
   const int ntiles = (c1 - c0 + KT - 1) / KT;
   const char* kb = reinterpret_cast<const char*>(a.k) +
                    ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
-  float2* part = a.partial + ((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad;
+  float* part = a.partial + ((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad;
   __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
   __shared__ float2 xch[4][(RT > 0 ? RT : 1) * 16];   // shared-tile partials per wavefront
 
@@ -463,14 +516,14 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
     StatsRows<NQ> st;
     stats_rows_init<FT, NQ>(a, tile0, wv, c16, p0, st);
     ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane,
-                       [&](const char* lds, int j0) {
+                       [&](const char* lds, int j0, int) {
                          stats_tile<T, D, FT, RT>(a, lds, j0, N, p0, wv, c16, g16, qf, st);
                        });
     stats_rows_merge<NQ>(st);
 #pragma unroll
     for (int i = 0; i < FT; ++i) {
       const int row = slot_tile<FT>(tile0, wv, i) * 16 + c16;
-      if (g16 == 0 && row < a.M) part[row] = make_float2(st.mref[i], st.srow[i]);
+      if (g16 == 0 && row < a.M) part[row] = st.mref[i] + __log2f(st.srow[i]);
     }
     if constexpr (RT > 0) {                // the four wavefronts' shares of each shared row
       if (g16 == 0)
@@ -485,13 +538,14 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreArgs a) {
         float sum = 0.0f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) sum += xch[w][tid].y * rescale(xch[w][tid].x, m);
-        if (row < a.M) part[row] = make_float2(m, sum);
+        if (row < a.M) part[row] = m + __log2f(sum);
       }
     }
   }
 }
 
-// One wavefront per query row: merge that row's chunk partials.
+// One wavefront per query row: merge that row's chunk partials (log2-sum-exps, -inf
+// for a chunk whose keys are all masked for the row) into log2 of its normaliser.
 __global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
   const int lane = threadIdx.x & 63;
   const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -506,9 +560,9 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
   const int nch = (N + a.chunk_keys - 1) / a.chunk_keys;
   float mm = -INFINITY, ss = 0.0f;
   for (int ch = lane; ch < nch; ch += 64) {
-    const float2 p = a.partial[(base * a.n_chunks + ch) * a.M_pad + m];
-    const float mx = fmaxf(mm, p.x);
-    ss = ss * rescale(mm, mx) + p.y * rescale(p.x, mx);
+    const float p = a.partial[(base * a.n_chunks + ch) * a.M_pad + m];
+    const float mx = fmaxf(mm, p);
+    ss = ss * rescale(mm, mx) + (p > -INFINITY ? fast_exp2(p - mx) : 0.0f);
     mm = mx;
   }
   float mx = mm;
@@ -521,7 +575,7 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
 }
 
 template <typename T, int D, int FT, int RT>
-__global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score_colsum_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int NQ = FT + RT;
@@ -550,7 +604,7 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
   const float cr_scale = lse_in != nullptr ? kLog2e : 1.0f;
   float* out = a.raw + (int64_t)h * a.total_rows + s0;
   __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
-  __shared__ float red[4][KT];
+  __shared__ float red[2][4][KT];          // per-wavefront column partials, double-buffered
 
   for (int grp = 0; grp < a.groups; ++grp) {
     const int tile0 = grp * 4 * FT;
@@ -564,13 +618,12 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
     for (int i = 0; i < NQ; ++i)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
-        const int mm = min(m, a.M - 1);
-        const int g = mm / a.n_rows, r = mm - g * a.n_rows;
+        const int m = min(slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t, a.M - 1);
+        const int g = m / a.n_rows, r = m - g * a.n_rows;
         const float* src = lse_in != nullptr
                                ? lse_in + (int64_t)(h * a.G + g) * (a.q_head_stride / D) +
                                      b * a.n_rows + r
-                               : rowc + mm;
+                               : rowc + m;
         cr[i][t] = slot_load4<NQ>(src);
       }
     ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane);
@@ -581,28 +634,30 @@ __global__ __launch_bounds__(kThreads) void score_colsum_kernel(ScoreArgs a) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
-        cr[i][t] = m < a.M ? cr[i][t] * cr_scale : INFINITY;
+        cr[i][t] = m < a.M ? cr[i][t] * cr_scale : INFINITY;   // padding rows add 0
       }
-    int pos[NQ][4];
-    colsum_positions<FT, NQ>(a, tile0, wv, g16, p0, pos);
+    int prev_j0 = c0;
     ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane,
-                       [&](const char* lds, int j0) {
-                         colsum_tile<T, D, FT, RT>(a, lds, j0, c1, N, tid, wv, c16, g16, qf, cr,
-                                                   pos, p0, red, out, grp > 0);
+                       [&](const char* lds, int j0, int t) {
+                         // the previous tile's partials are visible after the stream's barrier
+                         if (t > 0) colsum_flush(a, red[(t - 1) & 1], prev_j0, c1, wv, lane, out, grp > 0);
+                         colsum_tile<T, D, FT, RT>(a, lds, j0, N, p0, tile0, wv, c16, g16, qf,
+                                                   cr, red[t & 1][wv]);
+                         prev_j0 = j0;
                        });
+    lds_barrier();
+    colsum_flush(a, red[(ntiles - 1) & 1], prev_j0, c1, wv, lane, out, grp > 0);
   }
 }
 
 template <typename T, int D, int FT, int RT>
 hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st) {
   const dim3 grid(xcd_grid(a.n_chunks * g.n_kv_heads * g.batch));
-  if (a.lse_in != nullptr) {   // normalisers supplied: one pass over K
-    hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
-    return hipGetLastError();
+  if (a.lse_in == nullptr) {   // normalisers computed here: stats and reduce first
+    hipLaunchKernelGGL((score_stats_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL(score_reduce_kernel, dim3(a.M_pad / 4, g.n_kv_heads, g.batch), dim3(256),
+                       0, st, a);
   }
-  hipLaunchKernelGGL((score_stats_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
-  hipLaunchKernelGGL(score_reduce_kernel, dim3(a.M_pad / 4, g.n_kv_heads, g.batch), dim3(256), 0,
-                     st, a);
   hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
@@ -695,7 +750,7 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
 
 size_t score_workspace_bytes(const dge_geom_t& g, const ScorePlan& p) {
   const size_t units = (size_t)g.batch * g.n_kv_heads;
-  return units * p.n_chunks * p.M_pad * sizeof(float2) + units * p.M_pad * sizeof(float) + 256;
+  return units * p.n_chunks * p.M_pad * sizeof(float) + units * p.M_pad * sizeof(float) + 256;
 }
 
 hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, const void* k,
@@ -706,10 +761,8 @@ hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, 
   a.k = k;
   a.raw = raw;
   const size_t units = (size_t)g.batch * g.n_kv_heads;
-  a.partial = reinterpret_cast<float2*>(ws);
-  a.rowc = ws == nullptr ? nullptr
-                         : reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
-                                                    units * p.n_chunks * p.M_pad * sizeof(float2));
+  a.partial = reinterpret_cast<float*>(ws);
+  a.rowc = ws == nullptr ? nullptr : a.partial + units * p.n_chunks * p.M_pad;
   a.offs = seq_offsets(g);
   a.kv_head_stride = g.kv_head_stride;
   a.q_head_stride = (int64_t)g.batch * p.n_rows * g.head_dim;

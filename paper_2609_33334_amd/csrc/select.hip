@@ -180,30 +180,64 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* sh) {
   return before + inc - x;
 }
 
-// Find the digit d of a histogram at which the count from the top first reaches
-// `remaining`: above(d) < remaining <= above(d) + hist[d], above(d) = sum of the bins
-// above d.  Thread t scans bin group (THREADS-1-t), so an ordinary prefix sum over the
-// threads counts the keys above each group.  Writes {d, above(d)} to out[0..1].
-template <int THREADS>
-__device__ __forceinline__ void radix_find_digit(const uint32_t* hist, int nbins, int remaining,
+// Find the digit d of a histogram of NB bins at which the count from the top first
+// reaches `remaining`: above(d) < remaining <= above(d) + hist[d], above(d) = sum of the
+// bins above d.  Thread t holds bin group (THREADS-1-t) in registers (16-byte LDS reads
+// when the group spans 4 or more bins), so an ordinary prefix sum over the threads
+// counts the keys above each group.  Writes {d, above(d)} to out[0..1].
+template <int THREADS, int NB>
+__device__ __forceinline__ void radix_find_digit(const uint32_t* hist, int remaining,
                                                 uint32_t* scan_sh, int* out) {
-  const int per = nbins >= THREADS ? nbins / THREADS : 1;
+  constexpr int PER = NB >= THREADS ? NB / THREADS : 1;
   const int grp = THREADS - 1 - (int)threadIdx.x;
-  const int b0 = grp * per;
+  const int b0 = grp * PER;
+  uint32_t c[PER];
+  if constexpr (PER % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < PER; i += 4) {
+      const uint4 v = *reinterpret_cast<const uint4*>(hist + b0 + i);
+      c[i] = v.x; c[i + 1] = v.y; c[i + 2] = v.z; c[i + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) c[i] = b0 < NB ? hist[b0 + i] : 0u;
+  }
   uint32_t cnt = 0;
-  if (b0 < nbins)
-    for (int i = 0; i < per; ++i) cnt += hist[b0 + i];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) cnt += c[i];
   uint32_t above = block_excl_scan<THREADS>(cnt, scan_sh);
-  if (b0 < nbins && cnt > 0) {
-    for (int i = per - 1; i >= 0; --i) {
-      const uint32_t c = hist[b0 + i];
-      if (above < (uint32_t)remaining && above + c >= (uint32_t)remaining) {
+  if (cnt > 0) {
+#pragma unroll
+    for (int i = PER - 1; i >= 0; --i) {
+      if (above < (uint32_t)remaining && above + c[i] >= (uint32_t)remaining) {
         out[0] = b0 + i;
         out[1] = (int)above;
       }
-      above += c;
+      above += c[i];
     }
   }
+  __syncthreads();
+}
+
+// One radix pass over the BITS-bit digit at SHIFT of the keys that match `prefix` under
+// `mask`: histogram (LDS atomics), then the digit holding the remaining-th largest key.
+template <int THREADS, int KPT, int BITS, int SHIFT>
+__device__ __forceinline__ void radix_pass(const uint32_t (&key)[KPT], int base, int C,
+                                           uint32_t* hist, uint32_t* scan_sh, int* digit_above,
+                                           uint32_t& prefix, uint32_t& mask, int& remaining) {
+  constexpr int NB = 1 << BITS;
+  for (int i = threadIdx.x; i < NB; i += THREADS) hist[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const bool in = base + i < C && (key[i] & mask) == prefix;
+    if (in) atomicAdd(&hist[(key[i] >> SHIFT) & (uint32_t)(NB - 1)], 1u);
+  }
+  __syncthreads();
+  radix_find_digit<THREADS, NB>(hist, remaining, scan_sh, digit_above);
+  remaining -= digit_above[1];
+  prefix |= (uint32_t)digit_above[0] << SHIFT;
+  mask |= (uint32_t)(NB - 1) << SHIFT;
   __syncthreads();
 }
 
@@ -213,7 +247,9 @@ struct SegDigits {
   static constexpr size_t kHistBytes = (size_t)4 << kBits0;
 };
 
-template <int THREADS, int KPT>
+// PH: max-pool radius fixed at compile time (2 or 3: kernels 5 and 7), or 0 for any
+// radius up to kPoolHalo read from the arguments.
+template <int THREADS, int KPT, int PH>
 __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) {
   constexpr int WAVES = THREADS / kWave;
   extern __shared__ __attribute__((aligned(16))) float stage[];
@@ -222,7 +258,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   if (unit >= units) return;
   const int rep = unit % a.replicas, h = (unit / a.replicas) % a.n_kv_heads,
             b = unit / (a.replicas * a.n_kv_heads);
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int tid = threadIdx.x;
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
   const int C = N - a.n_tail;
@@ -257,7 +293,9 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
     const int base = tid * KPT;
     uint32_t key[KPT];
     if (a.pool_half > 0) {
-      // all of this thread's staging loads in flight at once, then the LDS stores
+      // all of this thread's staging loads in flight at once, then the LDS stores;
+      // candidate j sits at stage_pos(j + kPoolHalo), with kPoolHalo zeros on each side:
+      // scores are non-negative, so a zero inside a window never changes its maximum
       float sv[KPT];
 #pragma unroll
       for (int i = 0; i < KPT; ++i) {
@@ -267,22 +305,25 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
 #pragma unroll
       for (int i = 0; i < KPT; ++i) {
         const int j = tid + THREADS * i;
-        if (j < C) stage[stage_pos(j)] = sv[i];
+        if (j < C) stage[stage_pos(j + kPoolHalo)] = sv[i];
       }
+      if (tid < 2 * kPoolHalo)
+        stage[stage_pos(tid < kPoolHalo ? tid : C + tid)] = 0.0f;
       __syncthreads();
-      // the segment and a halo of kPoolHalo on each side, indices clamped into [0, C):
-      // a clamped index repeats a candidate that is inside the window anyway, so the
-      // maximum is unchanged and the loads need no guards
-      float w[KPT + 2 * kPoolHalo];
+      // the segment and a halo of H on each side (H = PH, or kPoolHalo with the radius
+      // checked at run time); reads past the zero padding are clamped into it
+      constexpr int H = PH > 0 ? PH : kPoolHalo;
+      const int last = C + 2 * kPoolHalo - 1;
+      float w[KPT + 2 * H];
 #pragma unroll
-      for (int i = 0; i < KPT + 2 * kPoolHalo; ++i)
-        w[i] = stage[stage_pos(min(max(base + i - kPoolHalo, 0), C - 1))];
+      for (int i = 0; i < KPT + 2 * H; ++i)
+        w[i] = stage[stage_pos(min(base + i + kPoolHalo - H, last))];
 #pragma unroll
       for (int i = 0; i < KPT; ++i) {
-        float m = w[i + kPoolHalo];
+        float m = w[i + H];
 #pragma unroll
-        for (int q = 1; q <= kPoolHalo; ++q)
-          if (q <= a.pool_half) m = fmaxf(m, fmaxf(w[i + kPoolHalo - q], w[i + kPoolHalo + q]));
+        for (int q = 1; q <= H; ++q)
+          if (PH > 0 || q <= a.pool_half) m = fmaxf(m, fmaxf(w[i + H - q], w[i + H + q]));
         key[i] = __float_as_uint(m) & 0x7fffffffu;
       }
     } else {
@@ -296,25 +337,12 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
     __syncthreads();                       // staging reads done: the buffer becomes hist
     uint32_t prefix = 0, mask = 0x80000000u;
     int remaining = nsel;
-#pragma unroll
-    for (int pass = 0; pass < 3; ++pass) {
-      const int bits = pass == 0 ? kBits0 : (pass == 1 ? kBits1 : kBits2);
-      const int shift = pass == 0 ? 31 - kBits0 : (pass == 1 ? kBits2 : 0);
-      const int nbins = 1 << bits;
-      for (int i = tid; i < nbins; i += THREADS) hist[i] = 0;
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < KPT; ++i) {
-        const bool in = base + i < C && (key[i] & mask) == prefix;
-        if (in) atomicAdd(&hist[(key[i] >> shift) & (uint32_t)(nbins - 1)], 1u);
-      }
-      __syncthreads();
-      radix_find_digit<THREADS>(hist, nbins, remaining, scan_sh, sh_digit_above);
-      remaining -= sh_digit_above[1];
-      prefix |= (uint32_t)sh_digit_above[0] << shift;
-      mask |= (uint32_t)(nbins - 1) << shift;
-      __syncthreads();
-    }
+    radix_pass<THREADS, KPT, kBits0, 31 - kBits0>(key, base, C, hist, scan_sh, sh_digit_above,
+                                                  prefix, mask, remaining);
+    radix_pass<THREADS, KPT, kBits1, kBits2>(key, base, C, hist, scan_sh, sh_digit_above, prefix,
+                                             mask, remaining);
+    radix_pass<THREADS, KPT, kBits2, 0>(key, base, C, hist, scan_sh, sh_digit_above, prefix, mask,
+                                        remaining);
     const uint32_t thr = prefix;   // the nsel-th largest key
     const int need = remaining;    // keys equal to thr that are kept
 
@@ -329,25 +357,32 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
     // C <= 32768, so neither half of the packed prefix overflows 16 bits
     const uint32_t before = block_excl_scan<THREADS>(packed, scan_sh);
     const int gt_before = (int)(before & 0xffffu), tie_before = (int)(before >> 16);
+    // output position of each kept candidate of the segment, without branches; ties
+    // are kept in index order up to the quota
     int pos = gt_before + min(tie_before, need);
     int trank = tie_before;
+    int kp[KPT];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const bool valid = base + i < C;
-      bool keep = valid && key[i] > thr;
-      if (valid && key[i] == thr) {
-        keep = trank < need;
-        ++trank;
-      }
-      if (keep && pos < nsel) {
-        if (writer) out[pos] = base + i;
-        if (pos >= r0 && pos < r1) slice[pos - r0] = base + i;
-        ++pos;
+      const bool gt = valid && key[i] > thr;
+      const bool eq = valid && key[i] == thr;
+      const bool keep = gt || (eq && trank < need);
+      trank += eq ? 1 : 0;
+      kp[i] = keep ? pos : -1;
+      pos += keep ? 1 : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int q = kp[i];
+      if (q >= 0 && q < nsel) {
+        if (writer) out[q] = base + i;
+        if (q >= r0 && q < r1) slice[q - r0] = base + i;
       }
     }
   }
   if (a.k_out == nullptr) return;
-  __syncthreads();
+  lds_barrier();                           // slice[] written; the index stores need not land
 
   // compaction of output rows [r0, r1): kept rows, then the tail, then zero rows
   const int tpr = a.row_bytes / 16;
@@ -383,17 +418,24 @@ __global__ __launch_bounds__(256) void select_streaming_kernel(int32_t* idx, int
   if (h == 0 && threadIdx.x == 0) n_kept[b] = nk;
 }
 
-template <int THREADS, int KPT>
-hipError_t launch_seg(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t st) {
+template <int THREADS, int KPT, int PH>
+hipError_t launch_seg_ph(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t st) {
   lds = lds > SegDigits<THREADS, KPT>::kHistBytes ? lds : SegDigits<THREADS, KPT>::kHistBytes;
   if (lds > 64 * 1024) {
     const hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&select_topb_seg_kernel<THREADS, KPT>),
+        reinterpret_cast<const void*>(&select_topb_seg_kernel<THREADS, KPT, PH>),
         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((select_topb_seg_kernel<THREADS, KPT>), grid, dim3(THREADS), lds, st, a);
+  hipLaunchKernelGGL((select_topb_seg_kernel<THREADS, KPT, PH>), grid, dim3(THREADS), lds, st, a);
   return hipGetLastError();
+}
+
+template <int THREADS, int KPT>
+hipError_t launch_seg(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t st) {
+  if (a.pool_half == 2) return launch_seg_ph<THREADS, KPT, 2>(a, grid, lds, st);
+  if (a.pool_half == 3) return launch_seg_ph<THREADS, KPT, 3>(a, grid, lds, st);
+  return launch_seg_ph<THREADS, KPT, 0>(a, grid, lds, st);
 }
 
 SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, int n_tail,
@@ -423,7 +465,8 @@ bool launch_fast(const SelectArgs& a, const dge_geom_t& g, int64_t cmax, hipStre
                  hipError_t* err) {
   if (a.pool_half > kPoolHalo) return false;
   const dim3 grid(xcd_grid(a.replicas * g.n_kv_heads * g.batch));
-  const size_t lds = a.pool_half > 0 ? (size_t)stage_pos((int)(cmax > 0 ? cmax : 1)) * 4 + 64 : 0;
+  const size_t lds =
+      a.pool_half > 0 ? (size_t)stage_pos((int)(cmax > 0 ? cmax : 1) + 2 * kPoolHalo) * 4 + 64 : 0;
   // (threads, candidates per thread): more threads per workgroup shorten the serial
   // per-thread loops of every radix pass (measured best at each size on MI355X)
   if (cmax <= 1024) *err = launch_seg<256, 4>(a, grid, lds, st);
