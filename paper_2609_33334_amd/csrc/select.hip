@@ -35,7 +35,7 @@ struct SelectArgs {
   int row_bytes, n_out, replicas, rows_per_rep;
 };
 
-constexpr int kMaxRowsPerRep = 512;
+constexpr int kMaxRowsPerRep = 1024;
 constexpr int kPoolHalo = 8;   // register path handles pool kernels up to 2*8+1
 
 __global__ __launch_bounds__(kSelThreads) void select_topb_kernel(SelectArgs a) {
@@ -384,25 +384,41 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   if (a.k_out == nullptr) return;
   lds_barrier();                           // slice[] written; the index stores need not land
 
-  // compaction of output rows [r0, r1): kept rows, then the tail, then zero rows
+  // compaction of output rows [r0, r1): kept rows, then the tail, then zero rows; the
+  // loads of kCopyBatch rows per thread are issued before their stores, so a thread
+  // waits for one round trip per batch rather than per row
+  constexpr int kCopyBatch = 4;
   const int tpr = a.row_bytes / 16;
   const int rpp = THREADS / tpr;
   const int part = tid % tpr;
   const int64_t obase = ((int64_t)b * a.n_kv_heads + h) * a.n_out;
-  for (int r = r0 + tid / tpr; r < r1; r += rpp) {
-    int srow;
-    if (r < nsel) srow = slice[r - r0];
-    else if (r < nsel + a.n_tail) srow = C + (r - nsel);
-    else srow = -1;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (srow >= 0) {
-      const int64_t in = h * a.head_stride_bytes + (s0 + srow) * a.row_bytes + part * 16;
-      kv = load16(a.k + in);
-      vv = load16(a.v + in);
+  for (int rb = r0 + tid / tpr; rb < r1; rb += kCopyBatch * rpp) {
+    uint4 kv[kCopyBatch], vv[kCopyBatch];
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) {
+      const int r = rb + u * rpp;
+      int srow = -1;
+      if (r < r1) {
+        if (r < nsel) srow = slice[r - r0];
+        else if (r < nsel + a.n_tail) srow = C + (r - nsel);
+      }
+      kv[u] = make_uint4(0, 0, 0, 0);
+      vv[u] = make_uint4(0, 0, 0, 0);
+      if (srow >= 0) {
+        const int64_t in = h * a.head_stride_bytes + (s0 + srow) * a.row_bytes + part * 16;
+        kv[u] = load16(a.k + in);
+        vv[u] = load16(a.v + in);
+      }
     }
-    const int64_t o = (obase + r) * a.row_bytes + part * 16;
-    *reinterpret_cast<uint4*>(a.k_out + o) = kv;
-    *reinterpret_cast<uint4*>(a.v_out + o) = vv;
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) {
+      const int r = rb + u * rpp;
+      if (r < r1) {
+        const int64_t o = (obase + r) * a.row_bytes + part * 16;
+        *reinterpret_cast<uint4*>(a.k_out + o) = kv[u];
+        *reinterpret_cast<uint4*>(a.v_out + o) = vv[u];
+      }
+    }
   }
 }
 
