@@ -29,11 +29,12 @@ CFLAGS = [
 ]
 
 
-# Per-file additions.  score.hip: MFMA accumulators in ordinary VGPRs, which saves the
+# Per-file additions.  score.hip, h2o.hip: MFMA accumulators in ordinary VGPRs, which saves the
 # accumulator-to-VGPR copies before every softmax update (measured faster on MI355X), and
 # no NaN semantics (inputs are finite; fmaxf then needs no canonicalising moves).
 FILE_FLAGS = {
     "score.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"],
+    "h2o.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"],
 }
 
 

@@ -78,12 +78,14 @@ __device__ __forceinline__ void block_store(char* lds, int tid, const uint4 (&st
 // Row log-sum-exp: one (row-block pair, KV head, sequence) per workgroup.
 // ------------------------------------------------------------------------------------
 // One 64-key tile for the wavefront's four 16-row tiles (rows r0 + rt*16 + c16): the
-// transposed product (A = keys) puts 4 keys of one row in each lane.
+// transposed product (A = keys) puts 4 keys of one row in each lane.  The four rows'
+// sums are kept relative to lazy references (as lazy_lse_update4); one wave-uniform
+// check per 16-key subtile moves them, so the common path has no branch per row.
 template <bool MASK>
 __device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N, int c16,
                                          int g16, const uint4 (&qf)[4][NS], float scale,
                                          float (&m)[4], float (&sm)[4]) {
-#pragma unroll 2
+#pragma unroll 1
   for (int sub = 0; sub < KTL / 16; ++sub) {
     uint4 kf[NS];
 #pragma unroll
@@ -96,23 +98,39 @@ __device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N,
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) acc[rt] = mma_step(bf16_t{}, kf[s], qf[rt][s], acc[rt]);
     // acc[rt][i] = logit of key j0 + sub*16 + 4*g16 + i for row r0 + rt*16 + c16
+    float x[4][4], mx[4];
+    bool up = false;
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
-      float x[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        x[i] = acc[rt][i];
+        x[rt][i] = acc[rt][i];
         if constexpr (MASK) {
           const int p = r0 + rt * 16 + c16, j = j0 + sub * 16 + 4 * g16 + i;
-          x[i] = (j <= p && j < N) ? x[i] : -INFINITY;
+          x[rt][i] = (j <= p && j < N) ? x[rt][i] : -INFINITY;
         }
       }
-      lazy_lse_update4(x, scale, m[rt], sm[rt]);
+      mx[rt] = fmaxf(fmaxf(x[rt][0], x[rt][1]), fmaxf(x[rt][2], x[rt][3])) * scale;
+      up = up || mx[rt] > m[rt] + kLazyBound;
     }
+    if (__any(up)) {
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        const float nr = fmaxf(m[rt], mx[rt]);
+        sm[rt] *= fast_exp2(m[rt] - nr);
+        m[rt] = nr;
+      }
+    }
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+      sm[rt] += (fast_exp2(fmaf(x[rt][0], scale, -m[rt])) + fast_exp2(fmaf(x[rt][1], scale, -m[rt]))) +
+                (fast_exp2(fmaf(x[rt][2], scale, -m[rt])) + fast_exp2(fmaf(x[rt][3], scale, -m[rt])));
   }
 }
 
-__global__ __launch_bounds__(256) void h2o_lse_kernel(H2oArgs a) {
+// Three workgroups per compute unit (168 registers): every block pair of the
+// Llama-3-8B-shaped layer (65 pairs x 8 KV heads) is resident in one round.
+__global__ __launch_bounds__(256, 3) void h2o_lse_kernel(H2oArgs a) {
   const int units = a.n_pairs * a.n_kv_heads * a.batch;
   const int unit = xcd_unit(units);
   if (unit >= units) return;
