@@ -216,6 +216,23 @@ __device__ __forceinline__ void dma16(const void* g, void* lds_wave_base) {
       : "memory");
 }
 
+// As dma16, with the global address split into a wave-uniform base (an SGPR pair) and a
+// 32-bit per-lane byte offset (the saddr form of the instruction): no 64-bit address
+// arithmetic per lane.  lds_wave_base must already be wave-uniform.
+__device__ __forceinline__ void dma16_sbase(const void* sbase, uint32_t voff,
+                                            uint32_t lds_wave_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(sbase), "s"(lds_wave_base)
+      : "memory");
+}
+
 // Register loads issued from asm, for kernels that keep global->LDS copies in flight
 // with explicit vmcnt waits: the compiler does not track these loads, so it inserts no
 // wait of its own (which would also drain the copies).  The caller waits (vmcnt) and

@@ -86,23 +86,42 @@ struct KTile {
 // instruction i fills bytes [(w*kInstr + i) KB, +1 KB) of the tile, lane l the 16 bytes
 // at offset 16*l of that kilobyte.  Each lane fetches the global unit that belongs at
 // its LDS position under the XOR swizzle (unit u of row r at position u ^ (r % kUnits)),
-// so a fragment read later hits 16 different bank groups.  Rows past the sequence are
-// clamped to its last row (their logits are masked).  A dummy copy (real == false)
-// issues the same instructions with every lane reading the 16 bytes at kb: it keeps
+// so a fragment read later hits 16 different bank groups.  The lane's row and column
+// within a tile (KCopy) are computed once; a copy is then a wave-uniform base plus a
+// 32-bit lane offset whose row is clamped to the sequence's last row (their logits are
+// masked).  A dummy copy (real == false) reads tile 0 of the sequence again: it keeps
 // the number of copies in flight constant at the end of a chunk, so that every wait
-// below has a fixed count, and costs one cached line.
+// below has a fixed count, and hits the cache.  Nothing here branches, so every path
+// through the kernel issues the same copies.
 template <typename T, int D>
-__device__ __forceinline__ void ktile_dma(const char* kb, int j0, int N, char* tile, int wv,
-                                          int lane, bool real) {
+struct KCopy {
   using KTl = KTile<T, D>;
+  uint32_t row[KTl::kInstr];     // row of this lane's unit within a tile
+  uint32_t col[KTl::kInstr];     // byte offset of the unit within its row
+  uint32_t lds_base;             // wave-uniform LDS offset of this wavefront's first KB
+  __device__ __forceinline__ KCopy(int wv, int lane) {
 #pragma unroll
-  for (int i = 0; i < KTl::kInstr; ++i) {
-    const int e = (wv * KTl::kInstr + i) * kWave + lane;
-    const int r = e / KTl::kUnits, p = e % KTl::kUnits;
-    const int u = p ^ (r % KTl::kUnits);
-    const char* src = kb + (int64_t)min(j0 + r, N - 1) * KTl::kRowBytes + u * 16;
-    dma16(real ? src : kb, tile + (wv * KTl::kInstr + i) * (kWave * 16));
+    for (int i = 0; i < KTl::kInstr; ++i) {
+      const int e = (wv * KTl::kInstr + i) * kWave + lane;
+      const int r = e / KTl::kUnits, p = e % KTl::kUnits;
+      row[i] = (uint32_t)r;
+      col[i] = (uint32_t)((p ^ (r % KTl::kUnits)) * 16);
+    }
+    lds_base = __builtin_amdgcn_readfirstlane((uint32_t)(wv * KTl::kInstr * kWave * 16));
   }
+};
+
+template <typename T, int D>
+__device__ __forceinline__ void ktile_dma(const char* kb, int j0, int N, char* tile,
+                                          const KCopy<T, D>& cp, bool real) {
+  using KTl = KTile<T, D>;
+  const int j0e = real ? j0 : 0;
+  const uint32_t lim = (uint32_t)(N - 1 - j0e);     // last row of the sequence, tile-relative
+  const char* base = kb + (int64_t)j0e * KTl::kRowBytes;
+  const uint32_t lds = (uint32_t)(uintptr_t)(lds_ptr_t)tile + cp.lds_base;
+#pragma unroll
+  for (int i = 0; i < KTl::kInstr; ++i)
+    dma16_sbase(base, min(cp.row[i], lim) * KTl::kRowBytes + cp.col[i], lds + i * kWave * 16);
 }
 
 // With S - 1 tiles always in flight, tile t has landed once at most S - 2 younger
@@ -197,19 +216,20 @@ __device__ __forceinline__ void cr_fence(float (&cr)[NQ][4]) {
 // Copies of tiles 0..S-2 of a chunk (dummies past its end).
 template <typename T, int D>
 __device__ __forceinline__ void ktile_issue(const char* kb, int c0, int ntiles, int N,
-                                            char (*buf)[KTile<T, D>::kBytes], int wv, int lane) {
+                                            char (*buf)[KTile<T, D>::kBytes],
+                                            const KCopy<T, D>& cp) {
   constexpr int S = KTile<T, D>::kStages;
 #pragma unroll
-  for (int t = 0; t < S - 1; ++t) ktile_dma<T, D>(kb, c0 + t * KT, N, buf[t], wv, lane, t < ntiles);
+  for (int t = 0; t < S - 1; ++t) ktile_dma<T, D>(kb, c0 + t * KT, N, buf[t], cp, t < ntiles);
 }
 
 // The copies, then the wait for tile 0: every load issued before the copies (query
 // fragments) has landed too.
 template <typename T, int D>
 __device__ __forceinline__ void ktile_prologue(const char* kb, int c0, int ntiles, int N,
-                                               char (*buf)[KTile<T, D>::kBytes], int wv,
-                                               int lane) {
-  ktile_issue<T, D>(kb, c0, ntiles, N, buf, wv, lane);
+                                               char (*buf)[KTile<T, D>::kBytes],
+                                               const KCopy<T, D>& cp) {
+  ktile_issue<T, D>(kb, c0, ntiles, N, buf, cp);
   ktile_wait<T, D>();
 }
 
@@ -220,15 +240,15 @@ __device__ __forceinline__ void ktile_prologue(const char* kb, int c0, int ntile
 // whatever consume(t - 1) wrote to LDS is visible to every wavefront in consume(t).
 template <typename T, int D, typename F>
 __device__ __forceinline__ void ktile_stream(const char* kb, int c0, int ntiles, int N,
-                                             char (*buf)[KTile<T, D>::kBytes], int wv, int lane,
-                                             F&& consume) {
+                                             char (*buf)[KTile<T, D>::kBytes],
+                                             const KCopy<T, D>& cp, F&& consume) {
   constexpr int S = KTile<T, D>::kStages;
   int t = 0;
   do {
     if (t > 0) ktile_wait<T, D>();
     lds_barrier();           // tile t landed everywhere; buffer (t - 1) % S free
     const int tn = t + S - 1;
-    ktile_dma<T, D>(kb, c0 + tn * KT, N, buf[tn % S], wv, lane, tn < ntiles);
+    ktile_dma<T, D>(kb, c0 + tn * KT, N, buf[tn % S], cp, tn < ntiles);
     consume(buf[t % S], c0 + t * KT, t);
   } while (++t < ntiles);
   asm_wait_vmcnt<0>();       // no copy still writes into the buffers
@@ -503,6 +523,7 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
   float* part = a.partial + ((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad;
   __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
   __shared__ float2 xch[4][(RT > 0 ? RT : 1) * 16];   // shared-tile partials per wavefront
+  const KCopy<T, D> kcp(wv, lane);
 
   for (int grp = 0; grp < a.groups; ++grp) {
     const int tile0 = grp * 4 * FT;
@@ -511,11 +532,11 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
     lds_barrier();                         // previous row group done with the buffers
     u32x4_t qf[NQ][NS];
     load_q_frags<T, D, FT, NQ>(a, h, b, tile0, wv, c16, g16, qf);
-    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane);
+    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, kcp);
     q_fence(qf);                           // landed with the first tile
     StatsRows<NQ> st;
     stats_rows_init<FT, NQ>(a, tile0, wv, c16, p0, st);
-    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane,
+    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, kcp,
                        [&](const char* lds, int j0, int) {
                          stats_tile<T, D, FT, RT>(a, lds, j0, N, p0, wv, c16, g16, qf, st);
                        });
@@ -605,6 +626,7 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
   float* out = a.raw + (int64_t)h * a.total_rows + s0;
   __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
   __shared__ float red[2][4][KT];          // per-wavefront column partials, double-buffered
+  const KCopy<T, D> kcp(wv, lane);
 
   for (int grp = 0; grp < a.groups; ++grp) {
     const int tile0 = grp * 4 * FT;
@@ -626,7 +648,7 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
                                : rowc + m;
         cr[i][t] = slot_load4<NQ>(src);
       }
-    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane);
+    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, kcp);
     q_fence(qf);                           // landed with the first tile
     cr_fence<NQ>(cr);
 #pragma unroll
@@ -637,7 +659,7 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
         cr[i][t] = m < a.M ? cr[i][t] * cr_scale : INFINITY;   // padding rows add 0
       }
     int prev_j0 = c0;
-    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, wv, lane,
+    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, kcp,
                        [&](const char* lds, int j0, int t) {
                          // the previous tile's partials are visible after the stream's barrier
                          if (t > 0) colsum_flush(a, red[(t - 1) & 1], prev_j0, c1, wv, lane, out, grp > 0);
