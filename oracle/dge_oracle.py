@@ -323,3 +323,24 @@ def cache_attention(q, k_c, v_c, n_kept, n_tail: int, q_from_end: int, n_q_heads
                 lse[hq, b * n_q + r] = log_partition(qr, keys[rows])
     return out, lse
 
+
+def retained_runs(idx) -> tuple:
+    """Contiguity of a retained set: (number of runs, mean run length).
+
+    The selection diagnostics (Sec. 4, "Selection trades coverage for contiguity";
+    Table "Selection decomposition", column "run len."; App. "Diagnostic details") report
+    how contiguous a retention rule's kept positions are: a run is a maximal block of
+    consecutive retained positions, the run length the mean block size.  Measured over the
+    selected past keys: the protected window/draft tail is one block under every rule and
+    is not counted.  idx: selected positions (any order; duplicates count once).  An empty
+    set gives (0, 0.0).
+    """
+    pos = sorted({int(i) for i in idx})
+    if not pos:
+        return 0, 0.0
+    runs = 1
+    for a, b in zip(pos, pos[1:]):
+        if b != a + 1:
+            runs += 1
+    return runs, len(pos) / runs
+

@@ -395,3 +395,44 @@ def test_c1_planted_keys_survive():
         kept = set(out[(0, h)]["idx"].tolist())
         hits = sum(int(r) in kept for r in x.planted[(0, h)])
         assert hits >= 6, (h, hits)
+
+
+# ----------------------------------------------------------------------------------
+# Retained-set contiguity (Sec. 4; Table "Selection decomposition", "run len.")
+# ----------------------------------------------------------------------------------
+def test_retained_runs_closed_forms():
+    # one block of n consecutive positions; every other position; the empty set
+    for n in (1, 5, 64):
+        assert oracle.retained_runs(range(7, 7 + n)) == (1, float(n))
+        assert oracle.retained_runs(range(0, 2 * n, 2)) == (n, 1.0)
+    assert oracle.retained_runs([]) == (0, 0.0)
+    # order and duplicates do not matter
+    assert oracle.retained_runs([9, 3, 4, 10, 3, 11]) == (2, 2.5)
+
+
+def test_retained_runs_match_rising_edges_of_the_mask():
+    # an independent count: runs are the 0 -> 1 transitions of the retained 0/1 mask
+    rng = np.random.default_rng(17)
+    for trial in range(200):
+        C = int(rng.integers(1, 60))
+        keep = rng.random(C) < rng.random()
+        idx = np.flatnonzero(keep)
+        mask = np.concatenate([[0], keep.astype(int)])
+        edges = int(np.sum((mask[1:] == 1) & (mask[:-1] == 0)))
+        runs, mean = oracle.retained_runs(idx)
+        assert runs == edges
+        assert (mean == 0.0) if edges == 0 else math.isclose(mean, keep.sum() / edges)
+
+
+def test_maxpool_plateau_is_one_run():
+    # a single positive raw score at position j spreads, after max-pooling with an odd
+    # kernel kappa, over the kappa candidates around j (clipped at the ends); selecting
+    # exactly that many keeps one run of that length -- the contiguity the paper credits
+    # to SnapKV's pooling
+    for C, j, kappa in ((40, 20, 7), (40, 1, 7), (40, 39, 5), (12, 6, 1)):
+        raw = np.zeros(C + 3)
+        raw[j] = 1.0
+        pooled = oracle.maxpool(raw, C, kappa)
+        width = min(C - 1, j + kappa // 2) - max(0, j - kappa // 2) + 1
+        idx = oracle.select_topb(pooled, width)
+        assert oracle.retained_runs(idx) == (1, float(width))
