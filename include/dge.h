@@ -210,6 +210,24 @@ dge_status_t dge_cache_attention(const dge_geom_t *geom, const void *q, int32_t 
                                  int32_t n_select, int32_t n_tail, const int32_t *n_kept,
                                  float *out, float *lse, hipStream_t stream);
 
+/* Contiguity of the retained sets (Sec. 4, "Selection trades coverage for contiguity";
+ * Table "Selection decomposition", column "run len."): for sequence b and KV head h,
+ *   runs[b][h]     = number of maximal runs of consecutive positions among the first
+ *                    n_kept[b] entries of idx[b][h][.] (0 when none is kept),
+ *   mean_len[b][h] = n_kept[b] / runs[b][h] (float32; 0 when none is kept).
+ * Counted over the selected past keys; the protected window/draft tail, one run under
+ * every rule, is not included.
+ *   idx      : [batch][H_kv][n_select] int32, strictly ascending within each row's kept
+ *              prefix (as dge_select_topb and dge_select_streaming write it); entries past
+ *              n_kept[b] are ignored.  Unsorted or repeated entries give a count that is
+ *              not the run count (no error is raised).
+ *   n_kept   : [batch] int32 (clamped to [0, n_select]).
+ *   runs     : [batch][H_kv] int32 output;  mean_len : [batch][H_kv] float32 output.
+ * No workspace.  Errors: DGE_ERR_INVALID for n_select < 0 or a NULL / misaligned pointer. */
+dge_status_t dge_retained_runs(const dge_geom_t *geom, const int32_t *idx, const int32_t *n_kept,
+                               int32_t n_select, int32_t *runs, float *mean_len,
+                               hipStream_t stream);
+
 /* H2O accumulated attention, kept running through the draft rows
  * (Table "Complexity and measured overhead", footnote a; App. "Draft-guided eviction implementation" on H2O's prompt-query buffer):
  *   colsum[h][j] = (1/G) sum_{g in group h} sum_{p = j}^{N_b - 1} softmax_j(q_{g,p} . k_j / sqrt(d))

@@ -22,7 +22,8 @@ from . import _lib
 from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  # noqa: F401
                    ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
 
-__all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact", "select_streaming", "compact", "h2o_colsum",
+__all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact", "select_streaming", "compact",
+           "cache_attention", "retained_runs", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
 
@@ -214,6 +215,23 @@ def cache_attention(geom: Geometry, q, n_q: int, q_from_end: int, k_c, v_c, n_se
                                               _ptr(n_kept), _ptr(out), _ptr(lse),
                                               _stream(stream)), "dge_cache_attention")
     return out, lse
+
+
+def retained_runs(geom: Geometry, idx, n_kept, runs=None, mean_len=None, stream=None):
+    """dge_retained_runs: contiguity of the selected sets.  idx [batch][H_kv][n_select]
+    int32 (ascending rows, as select_topb writes them), n_kept [batch].  Returns
+    (runs [batch][H_kv] int32, mean_len [batch][H_kv] float32)."""
+    torch = _torch()
+    n_select = int(idx.shape[-1])
+    if runs is None:
+        runs = torch.empty(geom.batch, geom.n_kv_heads, dtype=torch.int32, device=geom.device)
+    if mean_len is None:
+        mean_len = torch.empty(geom.batch, geom.n_kv_heads, dtype=torch.float32,
+                               device=geom.device)
+    _lib.check(_lib.lib().dge_retained_runs(ctypes.byref(geom.c), _ptr(idx), _ptr(n_kept),
+                                            n_select, _ptr(runs), _ptr(mean_len),
+                                            _stream(stream)), "dge_retained_runs")
+    return runs, mean_len
 
 
 def h2o_colsum(geom: Geometry, q_all, k, lse=None, colsum=None, ws=None, stream=None):

@@ -20,7 +20,7 @@ ABI_VERSION = 1
 # every entry point declared in include/dge.h
 EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_score", "dge_score_lse",
            "dge_select_topb", "dge_select_compact", "dge_select_streaming", "dge_compact",
-           "dge_cache_attention", "dge_h2o_colsum",
+           "dge_cache_attention", "dge_retained_runs", "dge_h2o_colsum",
            "dge_pyramid_budgets")
 
 
@@ -87,6 +87,8 @@ def lib() -> ctypes.CDLL:
                                       c_int32, c_void_p, c_void_p, c_void_p, c_void_p]
     L.dge_h2o_colsum.argtypes = [GP, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                  c_void_p]
+    L.dge_retained_runs.restype = c_int
+    L.dge_retained_runs.argtypes = [GP, c_void_p, c_void_p, c_int32, c_void_p, c_void_p, c_void_p]
     L.dge_pyramid_budgets.restype = c_int
     L.dge_pyramid_budgets.argtypes = [c_int32, c_int32, c_int32, c_int32, POINTER(c_int32)]
     if L.dge_abi_version() != ABI_VERSION:

@@ -201,6 +201,18 @@ dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t 
                                                 n_tail, n_kept, out, lse, stream));
 }
 
+dge_status_t dge_retained_runs(const dge_geom_t* geom, const int32_t* idx, const int32_t* n_kept,
+                               int32_t n_select, int32_t* runs, float* mean_len,
+                               hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (n_select < 0 || !n_kept || !runs || !mean_len || (n_select > 0 && !idx)) return DGE_ERR_INVALID;
+  if ((reinterpret_cast<uintptr_t>(idx) & 3) || (reinterpret_cast<uintptr_t>(n_kept) & 3) ||
+      (reinterpret_cast<uintptr_t>(runs) & 3) || (reinterpret_cast<uintptr_t>(mean_len) & 3))
+    return DGE_ERR_INVALID;
+  return hip_status(dge::launch_retained_runs(*geom, idx, n_kept, n_select, runs, mean_len, stream));
+}
+
 dge_status_t dge_h2o_colsum(const dge_geom_t* geom, const void* q_all, const void* k,
                             const float* lse, float* colsum, void* ws, size_t ws_bytes,
                             hipStream_t stream) {

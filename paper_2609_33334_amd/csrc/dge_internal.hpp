@@ -55,6 +55,9 @@ hipError_t launch_cache_attention(const dge_geom_t& g, const void* q, int n_q, i
                                   const int32_t* n_kept, float* out, float* lse,
                                   hipStream_t stream);
 
+hipError_t launch_retained_runs(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,
+                                int n_select, int32_t* runs, float* mean_len, hipStream_t stream);
+
 size_t h2o_workspace_bytes(const dge_geom_t& g);
 hipError_t launch_h2o(const dge_geom_t& g, const void* q_all, const void* k, const float* lse,
                       float* colsum, void* ws, hipStream_t stream);

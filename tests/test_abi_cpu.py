@@ -176,3 +176,15 @@ def test_cache_attention_validation(L):
     assert att(lse=FAKE + 2) == _lib.DGE_ERR_INVALID
     assert att(geom=_G(hq=18, hkv=2)) == _lib.DGE_ERR_UNSUPPORTED   # 9 query heads per KV head
     assert att(geom=_G(d=96)) == _lib.DGE_ERR_UNSUPPORTED
+
+
+def test_retained_runs_validation(L):
+    g = _G()
+    def runs(geom=g, idx=FAKE, nk=FAKE, n_select=20, out=FAKE, mean=FAKE):
+        return L.dge_retained_runs(geom.p, idx, nk, n_select, out, mean, None)
+    assert runs(n_select=-1) == _lib.DGE_ERR_INVALID
+    assert runs(idx=None) == _lib.DGE_ERR_INVALID
+    assert runs(nk=None) == _lib.DGE_ERR_INVALID
+    assert runs(out=None) == _lib.DGE_ERR_INVALID
+    assert runs(mean=FAKE + 2) == _lib.DGE_ERR_INVALID
+    assert runs(idx=FAKE + 1) == _lib.DGE_ERR_INVALID

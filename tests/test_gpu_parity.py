@@ -476,3 +476,56 @@ def test_cache_attention_eq1_and_evicted_mass():
     _log(f"  scoring rows: evicted mass max |err| {err:.2e}; matching loss "
          f"{float(np.mean(-np.log1p(-rho))):.4f} (oracle {float(np.mean(-np.log1p(-rho_want))):.4f})")
     assert err < 2e-4
+
+
+# ----------------------------------------------------------------------------------
+# Retained-set contiguity (dge_retained_runs) against the oracle: exact counts, and the
+# float32 mean n_kept / runs
+# ----------------------------------------------------------------------------------
+def _runs_check(geom, idx, n_kept, what):
+    runs, mean = dge.retained_runs(geom, torch.from_numpy(idx).to(DEV),
+                                   torch.from_numpy(n_kept).to(DEV))
+    torch.cuda.synchronize()
+    runs, mean = runs.cpu().numpy(), mean.cpu().numpy()
+    for b in range(idx.shape[0]):
+        for h in range(idx.shape[1]):
+            n = int(min(max(n_kept[b], 0), idx.shape[2]))
+            want_runs, want_mean = oracle.retained_runs(idx[b, h, :n])
+            assert runs[b, h] == want_runs, (what, b, h, runs[b, h], want_runs)
+            assert mean[b, h] == np.float32(n / want_runs if want_runs else 0.0), (what, b, h)
+    return runs, mean
+
+
+def test_retained_runs_synthetic():
+    _log("retained runs: synthetic index sets")
+    rng = np.random.default_rng(29)
+    n_select = 700
+    g = dge.Geometry(8, 4, 128, 8, 2, [900, 1000, 800, 1200], device=DEV)
+    idx = np.full((4, 4, n_select), -1, np.int32)
+    n_kept = np.array([n_select, 0, 350, 1], np.int32)
+    for h in range(4):
+        idx[0, h] = np.arange(n_select) + 5 * h                       # one run
+        idx[2, h, :350] = np.arange(0, 700, 2)                         # 350 runs of one
+        idx[3, h, :1] = 17 + h
+    # random ascending subsets, including a row whose kept prefix is shorter than the row
+    for h in range(4):
+        pick = np.sort(rng.choice(1100, n_select, replace=False)).astype(np.int32)
+        idx[1, h] = pick
+    _runs_check(g, idx, n_kept, "structured")
+    n_kept2 = np.array([n_select, 600, 350, 1], np.int32)
+    _runs_check(g, idx, n_kept2, "random subsets")
+
+
+@pytest.mark.parametrize("pool", [1, 7])
+def test_retained_runs_on_gpu_selection(pool):
+    wl = di.WORKLOADS["c2"]
+    _log(f"retained runs on the c2 selection, pool {pool}")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    out = dge.evict_layer(g, to_dev(x.q_bits, "bf16"), to_dev(x.k_bits, "bf16"),
+                          to_dev(x.v_bits, "bf16"), wl.budget, pool)
+    torch.cuda.synchronize()
+    idx = out["idx"].cpu().numpy().astype(np.int32)
+    n_kept = out["n_kept"].cpu().numpy().astype(np.int32)[: g.batch]
+    runs, mean = _runs_check(g, idx, n_kept, f"pool {pool}")
+    _log(f"  mean run length per head: {np.round(mean[0], 2).tolist()}")
