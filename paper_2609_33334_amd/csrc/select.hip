@@ -149,28 +149,73 @@ __global__ __launch_bounds__(kSelThreads) void select_topb_kernel(SelectArgs a) 
 // [t*KPT, (t+1)*KPT): their pooled keys stay in registers through the radix passes, and
 // one workgroup-wide exclusive scan of (greater, tied) counts gives every thread the
 // output position of its first kept candidate, so kept indices come out ascending
-// without a sort.  Raw scores are staged in LDS for the max-pool, padded by one word
-// every 16 so that the threads' consecutive segments fall in different banks.
+// without a sort.
 //
 // With `a.k_out` set, the workgroup also performs the compaction of its slice of
 // output rows (replica `rep` of `a.replicas` per head): every replica repeats the
 // selection (cheap, from L2) and copies rows [rep*rows_per_rep, (rep+1)*rows_per_rep)
 // of [kept rows || tail || zero rows], so the row copies of one head spread over
 // several compute units.
-__host__ __device__ __forceinline__ int stage_pos(int j) { return j + (j >> 4); }
 
-// Workgroup-wide exclusive prefix sum of one int per thread.  Counts here stay
-// below 2^16 per half, so two counters can share one packed word.
+// Staging layout of the generic pool radius (up to kPoolHalo): candidate j at
+// stage_pos(j + kPoolHalo), one pad word every 16 so that consecutive segments of the
+// threads fall in different banks.
+__host__ __device__ constexpr int stage_pos(int j) { return j + (j >> 4); }
+
+// Staging layout of pool radius 2 and 3 (pool kernels 5 and 7): thread t's KPT
+// candidates fill slot t+1 of kSlot words; slot 0 and slot THREADS+1 provide the zero
+// halo of the first and the last thread.  A slot is a whole number of 16-byte units and
+// that number is odd, so the 16-byte reads of eight consecutive lanes hit distinct banks.
+template <int KPT>
+struct PoolSlots {
+  static constexpr int kSlot = ((KPT + 4) / 4) % 2 == 1 ? KPT + 4 : KPT + 8;
+};
+
+constexpr int kLdsBytesMax = 160 * 1024;
+constexpr int kSegStaticLds = 512;   // scan and digit slots
+
+// Dynamic LDS of one segment-kernel instance: the staging buffer and the three radix
+// histograms (first digit: 12 bits, 16 bins per binade, up to 4096 candidates; 14 bits,
+// 64 bins per binade, beyond, so that scores clustered in a few binades do not pile
+// their atomics onto a few LDS addresses; then 10 bits and the rest).  The histograms
+// sit beside the staging buffer when both fit, so they are cleared before the first
+// barrier; otherwise they reuse the staging buffer once the pooled keys are in registers.
+template <int THREADS, int KPT, int PH>
+struct SegLds {
+  static constexpr int kBits0 = THREADS * KPT > 4096 ? 14 : 12;
+  static constexpr int kBits1 = 10;
+  static constexpr int kBits2 = 31 - kBits0 - kBits1;
+  static constexpr int kHistWords = (1 << kBits0) + (1 << kBits1) + (1 << kBits2);
+  static constexpr int kStageWords = PH > 0 ? (THREADS + 2) * PoolSlots<KPT>::kSlot
+                                            : stage_pos(THREADS * KPT + 2 * kPoolHalo) + 1;
+  static constexpr bool kApart =
+      (size_t)4 * ((kStageWords + 3) / 4 * 4 + kHistWords) + kSegStaticLds <= kLdsBytesMax;
+  static constexpr int kHistOff = kApart ? (kStageWords + 3) / 4 * 4 : 0;
+  static constexpr size_t kBytes =
+      (size_t)4 * (kApart ? kHistOff + kHistWords
+                          : (kStageWords > kHistWords ? kStageWords : kHistWords));
+};
+
+// Inclusive prefix sum over the 64 lanes of a wavefront: DPP row shifts by 1, 2, 4 and 8
+// within each row of 16 lanes, then the row broadcasts of lane 15 (into rows 1 and 3)
+// and lane 31 (into rows 2 and 3).  Lanes without a source add the zero `old` value.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
+// Workgroup-wide exclusive prefix sum of one int per thread (one barrier).  Counts here
+// stay below 2^16 per half, so two counters can share one packed word.
 template <int THREADS>
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* sh) {
   constexpr int WAVES = THREADS / kWave;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  uint32_t inc = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t v = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += v;
-  }
+  const uint32_t inc = wave_incl_scan(x);
   if (lane == 63) sh[wv] = inc;
   __syncthreads();
   uint32_t before = 0;
@@ -184,7 +229,8 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* sh) {
 // reaches `remaining`: above(d) < remaining <= above(d) + hist[d], above(d) = sum of the
 // bins above d.  Thread t holds bin group (THREADS-1-t) in registers (16-byte LDS reads
 // when the group spans 4 or more bins), so an ordinary prefix sum over the threads
-// counts the keys above each group.  Writes {d, above(d)} to out[0..1].
+// counts the keys above each group.  Writes {d, above(d), hist[d]} to out[0..2]; ends
+// with a barrier, so every thread can read them.
 template <int THREADS, int NB>
 __device__ __forceinline__ void radix_find_digit(const uint32_t* hist, int remaining,
                                                 uint32_t* scan_sh, int* out) {
@@ -212,6 +258,7 @@ __device__ __forceinline__ void radix_find_digit(const uint32_t* hist, int remai
       if (above < (uint32_t)remaining && above + c[i] >= (uint32_t)remaining) {
         out[0] = b0 + i;
         out[1] = (int)above;
+        out[2] = (int)c[i];
       }
       above += c[i];
     }
@@ -220,38 +267,40 @@ __device__ __forceinline__ void radix_find_digit(const uint32_t* hist, int remai
 }
 
 // One radix pass over the BITS-bit digit at SHIFT of the keys that match `prefix` under
-// `mask`: histogram (LDS atomics), then the digit holding the remaining-th largest key.
+// `mask`: histogram (LDS atomics into a cleared histogram), then the digit holding the
+// remaining-th largest key.  Returns true when that digit's bin holds exactly the keys
+// still to take: every key of the bin is kept, and the lower bits need no more passes.
 template <int THREADS, int KPT, int BITS, int SHIFT>
-__device__ __forceinline__ void radix_pass(const uint32_t (&key)[KPT], int base, int C,
-                                           uint32_t* hist, uint32_t* scan_sh, int* digit_above,
+__device__ __forceinline__ bool radix_pass(const uint32_t (&key)[KPT], int base, int C,
+                                           uint32_t* hist, uint32_t* scan_sh, int* dig,
                                            uint32_t& prefix, uint32_t& mask, int& remaining) {
   constexpr int NB = 1 << BITS;
-  for (int i = threadIdx.x; i < NB; i += THREADS) hist[i] = 0;
-  __syncthreads();
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     const bool in = base + i < C && (key[i] & mask) == prefix;
     if (in) atomicAdd(&hist[(key[i] >> SHIFT) & (uint32_t)(NB - 1)], 1u);
   }
   __syncthreads();
-  radix_find_digit<THREADS, NB>(hist, remaining, scan_sh, digit_above);
-  remaining -= digit_above[1];
-  prefix |= (uint32_t)digit_above[0] << SHIFT;
+  radix_find_digit<THREADS, NB>(hist, remaining, scan_sh, dig);
+  remaining -= dig[1];
+  prefix |= (uint32_t)dig[0] << SHIFT;
   mask |= (uint32_t)(NB - 1) << SHIFT;
-  __syncthreads();
+  return dig[2] == remaining;
 }
 
-template <int THREADS, int KPT>
-struct SegDigits {
-  static constexpr int kBits0 = THREADS * KPT > 4096 ? 14 : 12;
-  static constexpr size_t kHistBytes = (size_t)4 << kBits0;
-};
+template <int THREADS>
+__device__ __forceinline__ void clear_words(uint32_t* p, int n) {
+  for (int i = 4 * (int)threadIdx.x; i < n; i += 4 * THREADS)
+    *reinterpret_cast<uint4*>(p + i) = make_uint4(0, 0, 0, 0);
+}
 
 // PH: max-pool radius fixed at compile time (2 or 3: kernels 5 and 7), or 0 for any
 // radius up to kPoolHalo read from the arguments.
 template <int THREADS, int KPT, int PH>
 __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) {
+  using Lds = SegLds<THREADS, KPT, PH>;
   constexpr int WAVES = THREADS / kWave;
+  static_assert(KPT <= 32, "kept-candidate bit mask is 32 bits");
   extern __shared__ __attribute__((aligned(16))) float stage[];
   const int units = a.replicas * a.n_kv_heads * a.batch;
   const int unit = xcd_unit(units);
@@ -268,34 +317,66 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   if (writer && h == 0 && tid == 0) a.n_kept[b] = nsel;
   if (writer)
     for (int r = nsel + tid; r < a.n_select; r += THREADS) out[r] = -1;
-  // this replica's slice of output rows and the kept index of each
-  // first radix digit: 12 bits (16 bins per binade) for up to 4096 candidates, 14 bits
-  // (64 bins per binade) beyond, so that scores clustered in a few binades do not pile
-  // their histogram atomics onto a few LDS addresses
-  // The histogram reuses the staging buffer (dead once the pooled keys are in registers).
-  constexpr int kBits0 = SegDigits<THREADS, KPT>::kBits0, kBits1 = 10;
-  constexpr int kBits2 = 31 - kBits0 - kBits1;
-  uint32_t* hist = reinterpret_cast<uint32_t*>(stage);
-  __shared__ int slice[kMaxRowsPerRep];
+  uint32_t* const hist0 = reinterpret_cast<uint32_t*>(stage) + Lds::kHistOff;
+  uint32_t* const hist1 = hist0 + (1 << Lds::kBits0);
+  uint32_t* const hist2 = hist1 + (1 << Lds::kBits1);
+  // the kept candidates in output order, written over the staging buffer (and the
+  // histograms on top of it) once those are dead; nsel <= C <= THREADS * KPT words
+  int32_t* const sel = reinterpret_cast<int32_t*>(stage);
   __shared__ uint32_t scan_sh[WAVES];
-  __shared__ int sh_digit_above[2];
-  if (tid == 0) { sh_digit_above[0] = 0; sh_digit_above[1] = 0; }
+  __shared__ int sh_digit[3][4];
   const int r0 = rep * a.rows_per_rep;
   const int r1 = min(a.n_out, r0 + a.rows_per_rep);
+  const bool keep_all = nsel == C;
 
-  if (nsel == C) {
+  if (keep_all) {
     // every candidate is kept, in order
     if (writer)
       for (int r = tid; r < C; r += THREADS) out[r] = r;
-    for (int r = r0 + tid; r < min(r1, nsel); r += THREADS) slice[r - r0] = r;
   } else if (nsel > 0) {
     const float* src = a.scores + (int64_t)h * a.total_rows + s0;
     const int base = tid * KPT;
+    if constexpr (Lds::kApart) clear_words<THREADS>(hist0, Lds::kHistWords);
     uint32_t key[KPT];
-    if (a.pool_half > 0) {
-      // all of this thread's staging loads in flight at once, then the LDS stores;
-      // candidate j sits at stage_pos(j + kPoolHalo), with kPoolHalo zeros on each side:
-      // scores are non-negative, so a zero inside a window never changes its maximum
+    bool staged = true;   // a barrier has followed the histogram clearing
+    if constexpr (PH > 0) {
+      // all of this thread's staging loads in flight at once, then the LDS stores into
+      // the slot layout (candidates past C are zeros: scores are non-negative, so a zero
+      // inside a window never changes its maximum)
+      constexpr int S = PoolSlots<KPT>::kSlot;
+      float sv[KPT];
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const int j = tid + THREADS * i;
+        sv[i] = j < C ? src[j] : 0.0f;
+      }
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const int j = tid + THREADS * i;
+        stage[(j / KPT + 1) * S + j % KPT] = sv[i];
+      }
+      if (tid < 8) stage[tid < 4 ? KPT - 4 + tid : (THREADS + 1) * S + tid - 4] = 0.0f;
+      __syncthreads();
+      // the segment and four values of halo on each side, in 16-byte reads
+      float w[KPT + 8];
+      const float4 lh = *reinterpret_cast<const float4*>(stage + tid * S + KPT - 4);
+      w[0] = lh.x; w[1] = lh.y; w[2] = lh.z; w[3] = lh.w;
+#pragma unroll
+      for (int k = 0; k < KPT / 4; ++k) {
+        const float4 o = *reinterpret_cast<const float4*>(stage + (tid + 1) * S + 4 * k);
+        w[4 + 4 * k] = o.x; w[5 + 4 * k] = o.y; w[6 + 4 * k] = o.z; w[7 + 4 * k] = o.w;
+      }
+      const float4 rh = *reinterpret_cast<const float4*>(stage + (tid + 2) * S);
+      w[KPT + 4] = rh.x; w[KPT + 5] = rh.y; w[KPT + 6] = rh.z; w[KPT + 7] = rh.w;
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        float m = w[i + 4];
+#pragma unroll
+        for (int q = 1; q <= PH; ++q) m = fmaxf(m, fmaxf(w[i + 4 - q], w[i + 4 + q]));
+        key[i] = __float_as_uint(m) & 0x7fffffffu;
+      }
+    } else if (a.pool_half > 0) {
+      // generic radius: candidate j at stage_pos(j + kPoolHalo), kPoolHalo zeros on each side
       float sv[KPT];
 #pragma unroll
       for (int i = 0; i < KPT; ++i) {
@@ -310,79 +391,85 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
       if (tid < 2 * kPoolHalo)
         stage[stage_pos(tid < kPoolHalo ? tid : C + tid)] = 0.0f;
       __syncthreads();
-      // the segment and a halo of H on each side (H = PH, or kPoolHalo with the radius
-      // checked at run time); reads past the zero padding are clamped into it
-      constexpr int H = PH > 0 ? PH : kPoolHalo;
+      // the segment and a halo of kPoolHalo on each side; reads past the zero padding
+      // are clamped into it
       const int last = C + 2 * kPoolHalo - 1;
-      float w[KPT + 2 * H];
+      float w[KPT + 2 * kPoolHalo];
 #pragma unroll
-      for (int i = 0; i < KPT + 2 * H; ++i)
-        w[i] = stage[stage_pos(min(base + i + kPoolHalo - H, last))];
+      for (int i = 0; i < KPT + 2 * kPoolHalo; ++i)
+        w[i] = stage[stage_pos(min(base + i, last))];
 #pragma unroll
       for (int i = 0; i < KPT; ++i) {
-        float m = w[i + H];
+        float m = w[i + kPoolHalo];
 #pragma unroll
-        for (int q = 1; q <= H; ++q)
-          if (PH > 0 || q <= a.pool_half) m = fmaxf(m, fmaxf(w[i + H - q], w[i + H + q]));
+        for (int q = 1; q <= kPoolHalo; ++q)
+          if (q <= a.pool_half) m = fmaxf(m, fmaxf(w[i + kPoolHalo - q], w[i + kPoolHalo + q]));
         key[i] = __float_as_uint(m) & 0x7fffffffu;
       }
     } else {
 #pragma unroll
       for (int i = 0; i < KPT; ++i)
         key[i] = base + i < C ? (__float_as_uint(src[base + i]) & 0x7fffffffu) : 0u;
+      staged = false;
+    }
+    if constexpr (!Lds::kApart) {
+      __syncthreads();                     // staging reads done: the buffer becomes hist
+      clear_words<THREADS>(hist0, Lds::kHistWords);
+      __syncthreads();
+    } else {
+      if (!staged) __syncthreads();
     }
 
-    // three radix passes over bits 30..0 (bit 31 is zero for non-negative scores), most
-    // significant digit first
-    __syncthreads();                       // staging reads done: the buffer becomes hist
+    // radix passes over bits 30..0 (bit 31 is zero for non-negative scores), most
+    // significant digit first, until the digit's bin holds exactly the keys still to take
     uint32_t prefix = 0, mask = 0x80000000u;
     int remaining = nsel;
-    radix_pass<THREADS, KPT, kBits0, 31 - kBits0>(key, base, C, hist, scan_sh, sh_digit_above,
-                                                  prefix, mask, remaining);
-    radix_pass<THREADS, KPT, kBits1, kBits2>(key, base, C, hist, scan_sh, sh_digit_above, prefix,
-                                             mask, remaining);
-    radix_pass<THREADS, KPT, kBits2, 0>(key, base, C, hist, scan_sh, sh_digit_above, prefix, mask,
-                                        remaining);
-    const uint32_t thr = prefix;   // the nsel-th largest key
-    const int need = remaining;    // keys equal to thr that are kept
+    const bool done = radix_pass<THREADS, KPT, Lds::kBits0, 31 - Lds::kBits0>(
+        key, base, C, hist0, scan_sh, sh_digit[0], prefix, mask, remaining);
+    if (!done) {
+      const bool done1 = radix_pass<THREADS, KPT, Lds::kBits1, Lds::kBits2>(
+          key, base, C, hist1, scan_sh, sh_digit[1], prefix, mask, remaining);
+      if (!done1)
+        radix_pass<THREADS, KPT, Lds::kBits2, 0>(key, base, C, hist2, scan_sh, sh_digit[2],
+                                                 prefix, mask, remaining);
+    }
+    // kept: keys above the threshold prefix, and `need` of the keys on it (index order)
+    const uint32_t thr = prefix;
+    const int need = remaining;
 
     // (greater, tied) counts of this thread's segment, packed into one scanned word
     uint32_t packed = 0;
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const bool valid = base + i < C;
-      packed += (valid && key[i] > thr) ? 1u : 0u;
-      packed += (valid && key[i] == thr) ? (1u << 16) : 0u;
+      const uint32_t km = key[i] & mask;
+      packed += (valid && km > thr) ? 1u : 0u;
+      packed += (valid && km == thr) ? (1u << 16) : 0u;
     }
     // C <= 32768, so neither half of the packed prefix overflows 16 bits
     const uint32_t before = block_excl_scan<THREADS>(packed, scan_sh);
     const int gt_before = (int)(before & 0xffffu), tie_before = (int)(before >> 16);
-    // output position of each kept candidate of the segment, without branches; ties
-    // are kept in index order up to the quota
-    int pos = gt_before + min(tie_before, need);
+    // the kept candidates of the segment take consecutive output positions; ties are
+    // kept in index order up to the quota.  The scan's barrier has retired every read of
+    // the staging buffer and the histograms, so sel[] may overwrite them.
+    int q = gt_before + min(tie_before, need);
     int trank = tie_before;
-    int kp[KPT];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const bool valid = base + i < C;
-      const bool gt = valid && key[i] > thr;
-      const bool eq = valid && key[i] == thr;
+      const uint32_t km = key[i] & mask;
+      const bool gt = valid && km > thr;
+      const bool eq = valid && km == thr;
       const bool keep = gt || (eq && trank < need);
       trank += eq ? 1 : 0;
-      kp[i] = keep ? pos : -1;
-      pos += keep ? 1 : 0;
-    }
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int q = kp[i];
-      if (q >= 0 && q < nsel) {
-        if (writer) out[q] = base + i;
-        if (q >= r0 && q < r1) slice[q - r0] = base + i;
-      }
+      if (keep && q < nsel) sel[q] = base + i;
+      q += keep ? 1 : 0;
     }
   }
+  lds_barrier();                           // sel[] complete
+  if (writer && !keep_all)
+    for (int r = tid; r < nsel; r += THREADS) out[r] = sel[r];
   if (a.k_out == nullptr) return;
-  lds_barrier();                           // slice[] written; the index stores need not land
 
   // compaction of output rows [r0, r1): kept rows, then the tail, then zero rows; the
   // loads of kCopyBatch rows per thread are issued before their stores, so a thread
@@ -399,7 +486,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
       const int r = rb + u * rpp;
       int srow = -1;
       if (r < r1) {
-        if (r < nsel) srow = slice[r - r0];
+        if (r < nsel) srow = keep_all ? r : sel[r];
         else if (r < nsel + a.n_tail) srow = C + (r - nsel);
       }
       kv[u] = make_uint4(0, 0, 0, 0);
@@ -435,8 +522,9 @@ __global__ __launch_bounds__(256) void select_streaming_kernel(int32_t* idx, int
 }
 
 template <int THREADS, int KPT, int PH>
-hipError_t launch_seg_ph(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t st) {
-  lds = lds > SegDigits<THREADS, KPT>::kHistBytes ? lds : SegDigits<THREADS, KPT>::kHistBytes;
+hipError_t launch_seg_ph(const SelectArgs& a, dim3 grid, hipStream_t st) {
+  constexpr size_t lds = SegLds<THREADS, KPT, PH>::kBytes;
+  static_assert(lds + kSegStaticLds <= kLdsBytesMax, "segment kernel LDS");
   if (lds > 64 * 1024) {
     const hipError_t e = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&select_topb_seg_kernel<THREADS, KPT, PH>),
@@ -448,10 +536,10 @@ hipError_t launch_seg_ph(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t
 }
 
 template <int THREADS, int KPT>
-hipError_t launch_seg(const SelectArgs& a, dim3 grid, size_t lds, hipStream_t st) {
-  if (a.pool_half == 2) return launch_seg_ph<THREADS, KPT, 2>(a, grid, lds, st);
-  if (a.pool_half == 3) return launch_seg_ph<THREADS, KPT, 3>(a, grid, lds, st);
-  return launch_seg_ph<THREADS, KPT, 0>(a, grid, lds, st);
+hipError_t launch_seg(const SelectArgs& a, dim3 grid, hipStream_t st) {
+  if (a.pool_half == 2) return launch_seg_ph<THREADS, KPT, 2>(a, grid, st);
+  if (a.pool_half == 3) return launch_seg_ph<THREADS, KPT, 3>(a, grid, st);
+  return launch_seg_ph<THREADS, KPT, 0>(a, grid, st);
 }
 
 SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, int n_tail,
@@ -481,16 +569,14 @@ bool launch_fast(const SelectArgs& a, const dge_geom_t& g, int64_t cmax, hipStre
                  hipError_t* err) {
   if (a.pool_half > kPoolHalo) return false;
   const dim3 grid(xcd_grid(a.replicas * g.n_kv_heads * g.batch));
-  const size_t lds =
-      a.pool_half > 0 ? (size_t)stage_pos((int)(cmax > 0 ? cmax : 1) + 2 * kPoolHalo) * 4 + 64 : 0;
   // (threads, candidates per thread): more threads per workgroup shorten the serial
   // per-thread loops of every radix pass (measured best at each size on MI355X)
-  if (cmax <= 1024) *err = launch_seg<256, 4>(a, grid, lds, st);
-  else if (cmax <= 2048) *err = launch_seg<256, 8>(a, grid, lds, st);
-  else if (cmax <= 4096) *err = launch_seg<512, 8>(a, grid, lds, st);
-  else if (cmax <= 8192) *err = launch_seg<1024, 8>(a, grid, lds, st);
-  else if (cmax <= 16384) *err = launch_seg<1024, 16>(a, grid, lds, st);
-  else if (cmax <= 32768) *err = launch_seg<1024, 32>(a, grid, lds, st);
+  if (cmax <= 1024) *err = launch_seg<256, 4>(a, grid, st);
+  else if (cmax <= 2048) *err = launch_seg<256, 8>(a, grid, st);
+  else if (cmax <= 4096) *err = launch_seg<512, 8>(a, grid, st);
+  else if (cmax <= 8192) *err = launch_seg<1024, 8>(a, grid, st);
+  else if (cmax <= 16384) *err = launch_seg<1024, 16>(a, grid, st);
+  else if (cmax <= 32768) *err = launch_seg<1024, 32>(a, grid, st);
   else return false;
   return true;
 }
