@@ -117,22 +117,45 @@ def main():
     # no step finds its inputs in the Infinity Cache, multi-layer ones are large enough
     # (each layer gets its own copy of the generated layer's tensors)
     S = max(1, args.sets) if L_layers == 1 else 1
-    ws_score = torch.empty(dge.workspace_size(geom, dge.OP_SCORE), dtype=torch.uint8, device=dev)
+    # A multi-layer cache is held layer-major ([layer][KV head][row][d], queries likewise):
+    # the layers' KV heads are then consecutive heads of one geometry, and a single
+    # dge_score call scores every layer (each layer keeps its own copy of the tensors).
+    Hq, Hkv = wl.n_q_heads, wl.n_kv_heads
+    geom_all = geom if L_layers == 1 else dge.Geometry(
+        Hq * L_layers, Hkv * L_layers, wl.head_dim, wl.window, wl.k_draft, wl.cached_lens,
+        dtype=geom.dtype, device=dev)
+    ws_score = torch.empty(dge.workspace_size(geom_all, dge.OP_SCORE), dtype=torch.uint8, device=dev)
     ws_sel = torch.empty(dge.workspace_size(geom, dge.OP_SELECT), dtype=torch.uint8, device=dev)
-    layers = []   # layers[set][layer] = (q, k, v, out, budget)
+    sets = []     # sets[set] = (q_all, k_all, v_all, raw_all, per-layer [(q, k, v, out, budget)])
     for i in range(S):
+        q_all = q0.repeat(L_layers, 1, 1)
+        k_all = k0.repeat(L_layers, 1, 1)
+        v_all = v0.repeat(L_layers, 1, 1)
+        raw_all = torch.empty(Hkv * L_layers, geom.total_rows, dtype=torch.float32, device=dev)
+        # outputs packed layer after layer (the layout of dge_select_compact_layers)
+        nb = geom.batch * Hkv
+        n_sels = [B - wl.window for B in budgets]
+        flat = dict(idx=torch.empty(max(4, nb * sum(n_sels)), dtype=torch.int32, device=dev),
+                    n_kept=torch.zeros(max(4, L_layers * geom.batch), dtype=torch.int32, device=dev),
+                    k=torch.empty(nb * sum(x + n_tail for x in n_sels), wl.head_dim,
+                                  dtype=k0.dtype, device=dev),
+                    v=torch.empty(nb * sum(x + n_tail for x in n_sels), wl.head_dim,
+                                  dtype=k0.dtype, device=dev))
         row = []
+        io = ro = 0
         for l in range(L_layers):
-            n_sel = budgets[l] - wl.window
-            out = dict(raw=torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=dev),
-                       idx=torch.empty(geom.batch, geom.n_kv_heads, n_sel, dtype=torch.int32, device=dev),
-                       n_kept=torch.zeros(max(geom.batch, 4), dtype=torch.int32, device=dev),
-                       k=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
-                                     dtype=k0.dtype, device=dev),
-                       v=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
-                                     dtype=k0.dtype, device=dev))
-            row.append((q0.clone(), k0.clone(), v0.clone(), out, budgets[l]))
-        layers.append(row)
+            n_sel = n_sels[l]
+            rows = nb * (n_sel + n_tail)
+            shape = (geom.batch, Hkv, n_sel + n_tail, wl.head_dim)
+            out = dict(raw=raw_all[l * Hkv:(l + 1) * Hkv],
+                       idx=flat["idx"][io:io + nb * n_sel].view(geom.batch, Hkv, n_sel),
+                       n_kept=flat["n_kept"][l * geom.batch:(l + 1) * geom.batch],
+                       k=flat["k"][ro:ro + rows].view(shape), v=flat["v"][ro:ro + rows].view(shape))
+            io += nb * n_sel
+            ro += rows
+            row.append((q_all[l * Hq:(l + 1) * Hq], k_all[l * Hkv:(l + 1) * Hkv],
+                        v_all[l * Hkv:(l + 1) * Hkv], out, budgets[l]))
+        sets.append((q_all, k_all, v_all, raw_all, row, flat))
     torch.cuda.synchronize()
     row_lse = None
     if args.lse:
@@ -145,31 +168,40 @@ def main():
         x = torch.einsum("hrd,hnd->hrn", qq, kk.repeat_interleave(G, dim=0)) / (wl.head_dim ** 0.5)
         pos = torch.arange(N - nr, N, device=dev)
         x = x.masked_fill(torch.arange(N, device=dev)[None, None, :] > pos[None, :, None], float("-inf"))
-        row_lse = torch.logsumexp(x, dim=2).contiguous()
+        row_lse = torch.logsumexp(x, dim=2).repeat(L_layers, 1).contiguous()
         del x, kk, qq
 
-    def score_call(q, k, out):
+    def score_call(i):
+        q_all, k_all, _, raw_all, _, _ = sets[i % S]
         if row_lse is not None:
-            dge.score_lse(geom, dge.ROWS_WINDOW_DRAFT, q, k, row_lse, raw=out["raw"])
+            dge.score_lse(geom_all, dge.ROWS_WINDOW_DRAFT, q_all, k_all, row_lse, raw=raw_all)
         else:
-            dge.score(geom, dge.ROWS_WINDOW_DRAFT, q, k, raw=out["raw"], ws=ws_score)
+            dge.score(geom_all, dge.ROWS_WINDOW_DRAFT, q_all, k_all, raw=raw_all, ws=ws_score)
 
     def step(i):
-        for (q, k, v, out, B) in layers[i % S]:
-            score_call(q, k, out)
+        score_call(i)
+        _, k_all, v_all, raw_all, row, flat = sets[i % S]
+        if L_layers == 1:
+            q, k, v, out, B = row[0]
             dge.select_compact(geom, out["raw"], wl.pool, n_tail, B - wl.window, k, v,
                                idx=out["idx"], n_kept=out["n_kept"], k_out=out["k"],
                                v_out=out["v"], ws=ws_sel)
+        else:   # every layer, each with its own budget, in one launch
+            dge.select_compact_layers(geom, raw_all, wl.pool, n_tail,
+                                      [B - wl.window for B in budgets], k_all, v_all,
+                                      idx=flat["idx"], n_kept=flat["n_kept"], k_out=flat["k"],
+                                      v_out=flat["v"], ws=ws_sel)
 
     def score_only(i):
-        for (q, k, v, out, B) in layers[i % S]:
-            score_call(q, k, out)
+        score_call(i)
 
     # eager warmup and reference result
     for i in range(max(args.warmup, S)):
         step(i)
     torch.cuda.synchronize()
-    ref = {kk: vv.clone() for kk, vv in layers[0][0][3].items()}
+    # set 0's outputs: the scores of every layer and the packed selections / caches
+    outs0 = dict(sets[0][5], raw=sets[0][3])
+    ref = {kk: vv.clone() for kk, vv in outs0.items()}
 
     # HIP graphs of GRAPH_STEPS consecutive steps, covering every buffer set
     gsteps = GRAPH_STEPS if L_layers == 1 else 1
@@ -189,14 +221,14 @@ def main():
                     score_only(gi * gsteps + j)
             sgraphs.append(sg)
     torch.cuda.synchronize()
-    # graph replays must reproduce the eager result (layer 0 of set 0 is in graph 0)
+    # graph replays must reproduce the eager result (set 0 is in graph 0)
     for kk in ref:
-        layers[0][0][3][kk].zero_()
+        outs0[kk].zero_()
     torch.cuda.synchronize()
     graphs[0].replay()
     torch.cuda.synchronize()
     for kk in ref:
-        assert torch.equal(layers[0][0][3][kk], ref[kk]), f"graph replay differs from eager ({kk})"
+        assert torch.equal(outs0[kk], ref[kk]), f"graph replay differs from eager ({kk})"
 
     K = args.steps
     n_rep = (K + gsteps - 1) // gsteps
@@ -227,9 +259,9 @@ def main():
         sgraphs[r % n_graphs].replay()
     es1.record()
     torch.cuda.synchronize()
-    score_us = es0.elapsed_time(es1) * 1e3 / (K * L_layers)
+    score_us = es0.elapsed_time(es1) * 1e3 / K      # one dge_score launch per step
     log(f"[bench] {ms_per_step * 1e3:.2f} us/step (event), wall {wall * 1e6 / K:.2f} us/step; "
-        f"dge_score {score_us:.2f} us/call")
+        f"dge_score {score_us:.2f} us/call ({L_layers} layers per call)")
 
     L = sum(wl.prompt_lens)
     units = L * wl.n_kv_heads * L_layers          # prefix tokens x KV heads per step
@@ -237,14 +269,15 @@ def main():
     # algorithmic bytes of one dge_score call: K once + the scoring queries
     n_rows = wl.window + wl.k_draft
     score_bytes = (wl.n_kv_heads * geom.total_rows * wl.head_dim * elt
-                   + wl.n_q_heads * wl.batch * n_rows * wl.head_dim * elt)
-    achieved = score_bytes / (score_us * 1e-6) / 1e9
+                   + wl.n_q_heads * wl.batch * n_rows * wl.head_dim * elt)   # per layer
+    achieved = score_bytes * L_layers / (score_us * 1e-6) / 1e9
     roofline = {"kernel": ("dge_score_lse (colsum launch)" if args.lse else
                            "dge_score (stats + reduce + colsum launches)"), "bound": "hbm",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": measured_traffic(wl.name, args.lse),
-                "bytes_per_launch": int(score_bytes), "us_per_launch": round(score_us, 3)}
+                "traffic": measured_traffic(wl.name, args.lse, L_layers),
+                "bytes_per_launch": int(score_bytes * L_layers), "us_per_launch": round(score_us, 3),
+                "layers_per_launch": L_layers}
     # whole step against its own algorithmic bytes (score + compaction + indices)
     step_bytes = 0
     for B in budgets:
@@ -265,9 +298,11 @@ def main():
         "config": {"workload": WORKLOAD_TEXT.get(wl.name, wl.name),
                    "global_batch": wl.batch, "seq_len": L, "layers": L_layers,
                    "parallelism": "single GPU",
-                   "step": ("per layer: dge_score_lse (row LSE supplied) -> dge_select_compact"
-                            if args.lse else
-                            "per layer: dge_score -> dge_select_compact (pool, top-(B-w), gather)"),
+                   "step": (("dge_score_lse (row LSE supplied)" if args.lse else "dge_score")
+                            + (" over all layers (layer-major cache) -> dge_select_compact_layers"
+                               " (every layer's pool, top-(B_l-w), gather in one launch)"
+                               if L_layers > 1 else
+                               " -> dge_select_compact (pool, top-(B-w), gather)")),
                    "step_hbm_frac": round(step_frac, 4), "buffer_sets": S},
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -434,9 +469,10 @@ def score_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str, lse: bool):
+def measured_traffic(workload: str, lse: bool, layers_per_call: int):
     """HBM bytes per dge_score call from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    summary, or None when there is none or the score kernels changed since it was taken."""
+    summary, or None when there is none, it was taken with another number of layers per
+    call, or the score kernels changed since it was taken."""
     path = os.path.join(ROOT, "profiles", f"score_traffic_{workload}{'_lse' if lse else ''}.json")
     try:
         with open(path) as fh:
@@ -444,6 +480,8 @@ def measured_traffic(workload: str, lse: bool):
     except (OSError, ValueError):
         return None
     if rec.get("source_sha256") != score_source_hash():
+        return None
+    if rec.get("layers_per_call", 1) != layers_per_call:
         return None
     return rec.get("hbm_bytes_per_call")
 

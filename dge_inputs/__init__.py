@@ -231,7 +231,9 @@ def random_scores(shape, seed: int, kind: str = "continuous") -> np.ndarray:
     """Non-negative float32 score arrays for selection tests.
 
     ``continuous`` is tie-free with probability ~1; ``plateau`` repeats values in
-    short runs (as max-pooling does); ``ints`` draws small integers (many ties).
+    short runs (as max-pooling does); ``ints`` draws small integers (many ties);
+    ``ulps`` draws values a few thousand units in the last place above 1.0, so that
+    distinct values share every leading bit but the last dozen (and some repeat).
     """
     rng = np.random.default_rng(np.random.SeedSequence([99, seed]))
     if kind == "continuous":
@@ -244,4 +246,7 @@ def random_scores(shape, seed: int, kind: str = "continuous") -> np.ndarray:
         runs = rng.integers(1, 6, size=n)
         idx = np.repeat(np.arange(n), runs)[:n]
         return np.ascontiguousarray(base[..., idx])
+    if kind == "ulps":
+        off = rng.integers(0, 3000, size=shape).astype(np.uint32)
+        return (np.uint32(0x3F800000) + off).view(np.float32)
     raise ValueError(kind)

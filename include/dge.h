@@ -160,6 +160,29 @@ dge_status_t dge_select_compact(const dge_geom_t *geom, const float *scores, int
                                 const void *k, const void *v, void *k_out, void *v_out, void *ws,
                                 size_t ws_bytes, hipStream_t stream);
 
+/* dge_select_compact for n_layers layers in one launch (Alg. 1 steps B-C run for every
+ * layer at once after drafting), each layer with its own budget.  The caches are
+ * layer-major: layer l's scores are heads [l*H_kv, (l+1)*H_kv) of a [n_layers*H_kv][T]
+ * array (one dge_score call over the layer-major geometry writes them), and its K and V
+ * heads start at element l * H_kv * kv_head_stride of k and v.  geom describes one layer.
+ * Outputs are packed layer after layer, with nb = batch * H_kv:
+ *   idx    : layer l's [batch][H_kv][n_select_host[l]] block starts at int32 element
+ *            nb * (n_select_host[0] + ... + n_select_host[l-1]);
+ *   n_kept : [n_layers][batch];
+ *   k_out, v_out : layer l's [batch][H_kv][n_select_host[l] + n_tail][head_dim] block
+ *            starts at row nb * sum over l' < l of (n_select_host[l'] + n_tail).
+ * Every block equals what dge_select_compact writes for that layer's slices.
+ *   n_select_host : host array [n_layers], each >= 0 (B_l - w for per-layer budgets).
+ *   ws     : the DGE_OP_SELECT workspace of one layer.
+ * Errors: those of dge_select_compact; DGE_ERR_INVALID for n_layers < 1, a NULL
+ * n_select_host or a negative entry. */
+dge_status_t dge_select_compact_layers(const dge_geom_t *geom, int32_t n_layers,
+                                       const float *scores, int32_t pool_kernel, int32_t n_tail,
+                                       const int32_t *n_select_host, int32_t *idx,
+                                       int32_t *n_kept, const void *k, const void *v, void *k_out,
+                                       void *v_out, void *ws, size_t ws_bytes,
+                                       hipStream_t stream);
+
 /* StreamingLLM retention (Sec. 6; App. "Additional analysis": four sinks and a recency window):
  * idx[b][h][0 .. n_kept[b]) = 0, 1, ..., n_kept[b]-1 with n_kept[b] = min(n_sink, N_b - n_recent);
  * remaining entries up to n_sink are -1.  The n_recent rows are the tail passed to

@@ -22,8 +22,9 @@ from . import _lib
 from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  # noqa: F401
                    ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
 
-__all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact", "select_streaming", "compact",
-           "cache_attention", "retained_runs", "h2o_colsum",
+__all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact",
+           "select_compact_layers", "select_streaming", "compact", "cache_attention",
+           "retained_runs", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
 
@@ -165,6 +166,47 @@ def select_compact(geom: Geometry, scores, pool_kernel: int, n_tail: int, n_sele
                                              _ptr(v), _ptr(k_out), _ptr(v_out), _ptr(ws),
                                              ws.numel(), _stream(stream)), "dge_select_compact")
     return idx, n_kept[:geom.batch], k_out, v_out
+
+
+def select_compact_layers(geom: Geometry, scores, pool_kernel: int, n_tail: int, n_select,
+                          k, v, idx=None, n_kept=None, k_out=None, v_out=None, ws=None,
+                          stream=None):
+    """dge_select_compact_layers: select + compact for len(n_select) layers of a
+    layer-major cache in one launch (geom describes one layer).  Returns lists of
+    per-layer views (idx [batch][H_kv][n_select[l]], k_out / v_out
+    [batch][H_kv][n_select[l] + n_tail][d]) and n_kept [n_layers][batch]; the packed
+    buffers may be passed in as flat tensors."""
+    torch = _torch()
+    n_sel = [int(x) for x in n_select]
+    nl = len(n_sel)
+    nb = geom.batch * geom.n_kv_heads
+    tot_idx = nb * sum(n_sel)
+    tot_rows = nb * sum(x + n_tail for x in n_sel)
+    if idx is None:
+        idx = torch.empty(max(tot_idx, 4), dtype=torch.int32, device=geom.device)
+    if n_kept is None:
+        n_kept = torch.empty(max(nl * geom.batch, 4), dtype=torch.int32, device=geom.device)
+    if k_out is None:
+        k_out = torch.empty(tot_rows, geom.head_dim, dtype=k.dtype, device=geom.device)
+    if v_out is None:
+        v_out = torch.empty(tot_rows, geom.head_dim, dtype=v.dtype, device=geom.device)
+    ws = _workspace(geom, OP_SELECT, ws)
+    arr = (ctypes.c_int32 * nl)(*n_sel)
+    _lib.check(_lib.lib().dge_select_compact_layers(
+        ctypes.byref(geom.c), nl, _ptr(scores), pool_kernel, n_tail, arr, _ptr(idx),
+        _ptr(n_kept), _ptr(k), _ptr(v), _ptr(k_out), _ptr(v_out), _ptr(ws), ws.numel(),
+        _stream(stream)), "dge_select_compact_layers")
+    idx_l, k_l, v_l = [], [], []
+    io = ro = 0
+    for x in n_sel:
+        idx_l.append(idx[io:io + nb * x].view(geom.batch, geom.n_kv_heads, x))
+        rows = nb * (x + n_tail)
+        shape = (geom.batch, geom.n_kv_heads, x + n_tail, geom.head_dim)
+        k_l.append(k_out.view(-1, geom.head_dim)[ro:ro + rows].view(shape))
+        v_l.append(v_out.view(-1, geom.head_dim)[ro:ro + rows].view(shape))
+        io += nb * x
+        ro += rows
+    return idx_l, n_kept[:nl * geom.batch].view(nl, geom.batch), k_l, v_l
 
 
 def select_streaming(geom: Geometry, n_sink: int, n_recent: int, idx=None, n_kept=None,

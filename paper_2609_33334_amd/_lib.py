@@ -19,7 +19,8 @@ ABI_VERSION = 1
 
 # every entry point declared in include/dge.h
 EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_score", "dge_score_lse",
-           "dge_select_topb", "dge_select_compact", "dge_select_streaming", "dge_compact",
+           "dge_select_topb", "dge_select_compact", "dge_select_compact_layers",
+           "dge_select_streaming", "dge_compact",
            "dge_cache_attention", "dge_retained_runs", "dge_h2o_colsum",
            "dge_pyramid_budgets")
 
@@ -76,6 +77,11 @@ def lib() -> ctypes.CDLL:
     L.dge_select_compact.argtypes = [GP, c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                      c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                      c_void_p]
+    L.dge_select_compact_layers.restype = c_int
+    L.dge_select_compact_layers.argtypes = [GP, c_int32, c_void_p, c_int32, c_int32,
+                                            POINTER(c_int32), c_void_p, c_void_p, c_void_p,
+                                            c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                            c_void_p]
     L.dge_select_streaming.restype = c_int
     L.dge_select_streaming.argtypes = [GP, c_int32, c_int32, c_void_p, c_void_p, c_void_p]
     L.dge_compact.restype = c_int

@@ -157,6 +157,34 @@ dge_status_t dge_select_compact(const dge_geom_t* geom, const float* scores, int
                                                n_kept, k, v, k_out, v_out, ws, stream));
 }
 
+dge_status_t dge_select_compact_layers(const dge_geom_t* geom, int32_t n_layers,
+                                       const float* scores, int32_t pool_kernel, int32_t n_tail,
+                                       const int32_t* n_select_host, int32_t* idx, int32_t* n_kept,
+                                       const void* k, const void* v, void* k_out, void* v_out,
+                                       void* ws, size_t ws_bytes, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (n_layers < 1 || !n_select_host) return DGE_ERR_INVALID;
+  if (pool_kernel < 1 || (pool_kernel & 1) == 0) return DGE_ERR_INVALID;
+  bool any_sel = false;
+  for (int l = 0; l < n_layers; ++l) {
+    if (n_select_host[l] < 0) return DGE_ERR_INVALID;
+    any_sel = any_sel || n_select_host[l] > 0;
+  }
+  if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
+  if (!scores || !n_kept || (any_sel && !idx) || !aligned16(scores) || !aligned16(idx) ||
+      !aligned16(n_kept))
+    return DGE_ERR_INVALID;
+  if (!k || !v || !k_out || !v_out || !aligned16(k) || !aligned16(v) || !aligned16(k_out) ||
+      !aligned16(v_out))
+    return DGE_ERR_INVALID;
+  if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::select_workspace_bytes(*geom))
+    return DGE_ERR_WORKSPACE;
+  return hip_status(dge::launch_select_compact_layers(*geom, n_layers, scores, pool_kernel, n_tail,
+                                                      n_select_host, idx, n_kept, k, v, k_out,
+                                                      v_out, ws, stream));
+}
+
 dge_status_t dge_select_streaming(const dge_geom_t* geom, int32_t n_sink, int32_t n_recent,
                                   int32_t* idx, int32_t* n_kept, hipStream_t stream) {
   dge_status_t st = check_geom(geom);

@@ -42,6 +42,10 @@ hipError_t launch_select_compact(const dge_geom_t& g, const float* scores, int p
                                  int n_tail, int n_select, int32_t* idx, int32_t* n_kept,
                                  const void* k, const void* v, void* k_out, void* v_out, void* ws,
                                  hipStream_t stream);
+hipError_t launch_select_compact_layers(const dge_geom_t& g, int n_layers, const float* scores,
+                                        int pool_kernel, int n_tail, const int32_t* n_select_host,
+                                        int32_t* idx, int32_t* n_kept, const void* k, const void* v,
+                                        void* k_out, void* v_out, void* ws, hipStream_t stream);
 hipError_t launch_select_streaming(const dge_geom_t& g, int n_sink, int n_recent, int32_t* idx,
                                    int32_t* n_kept, hipStream_t stream);
 

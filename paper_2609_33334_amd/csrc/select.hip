@@ -16,6 +16,7 @@ namespace {
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
+constexpr int kMaxLayers = 64;   // layers per multi-layer launch
 
 struct SelectArgs {
   const float* scores;
@@ -33,9 +34,16 @@ struct SelectArgs {
   char* v_out;
   int64_t head_stride_bytes;
   int row_bytes, n_out, replicas, rows_per_rep;
+  // Several layers of a layer-major cache in one launch (segment kernel only): layer l
+  // reads score/K/V heads [l*H_kv, (l+1)*H_kv), selects lay_nsel[l] rows and writes its
+  // idx block at lay_idx_off[l] (int32 elements), n_kept at l*batch and its compacted
+  // rows at row lay_out_off[l] of k_out / v_out.  One layer: n_layers = 1, offsets 0.
+  int n_layers;
+  int32_t lay_nsel[kMaxLayers];
+  int64_t lay_idx_off[kMaxLayers];
+  int64_t lay_out_off[kMaxLayers];
 };
 
-constexpr int kMaxRowsPerRep = 1024;
 constexpr int kPoolHalo = 8;   // register path handles pool kernels up to 2*8+1
 
 __global__ __launch_bounds__(kSelThreads) void select_topb_kernel(SelectArgs a) {
@@ -302,21 +310,26 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   constexpr int WAVES = THREADS / kWave;
   static_assert(KPT <= 32, "kept-candidate bit mask is 32 bits");
   extern __shared__ __attribute__((aligned(16))) float stage[];
-  const int units = a.replicas * a.n_kv_heads * a.batch;
+  const int per_layer = a.replicas * a.n_kv_heads * a.batch;
+  const int units = per_layer * a.n_layers;
   const int unit = xcd_unit(units);
   if (unit >= units) return;
-  const int rep = unit % a.replicas, h = (unit / a.replicas) % a.n_kv_heads,
-            b = unit / (a.replicas * a.n_kv_heads);
+  const int layer = unit / per_layer, lu = unit - layer * per_layer;
+  const int rep = lu % a.replicas, h = (lu / a.replicas) % a.n_kv_heads,
+            b = lu / (a.replicas * a.n_kv_heads);
+  const int hh = layer * a.n_kv_heads + h;   // head of the layer-major scores, K and V
+  const int n_select = a.lay_nsel[layer];
+  const int n_out = n_select + a.n_tail;
   const int tid = threadIdx.x;
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
   const int C = N - a.n_tail;
-  const int nsel = max(0, min(a.n_select, C));
+  const int nsel = max(0, min(n_select, C));
   const bool writer = rep == 0;
-  int32_t* out = a.idx + ((int64_t)b * a.n_kv_heads + h) * a.n_select;
-  if (writer && h == 0 && tid == 0) a.n_kept[b] = nsel;
+  int32_t* out = a.idx + a.lay_idx_off[layer] + ((int64_t)b * a.n_kv_heads + h) * n_select;
+  if (writer && h == 0 && tid == 0) a.n_kept[layer * a.batch + b] = nsel;
   if (writer)
-    for (int r = nsel + tid; r < a.n_select; r += THREADS) out[r] = -1;
+    for (int r = nsel + tid; r < n_select; r += THREADS) out[r] = -1;
   uint32_t* const hist0 = reinterpret_cast<uint32_t*>(stage) + Lds::kHistOff;
   uint32_t* const hist1 = hist0 + (1 << Lds::kBits0);
   uint32_t* const hist2 = hist1 + (1 << Lds::kBits1);
@@ -326,7 +339,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   __shared__ uint32_t scan_sh[WAVES];
   __shared__ int sh_digit[3][4];
   const int r0 = rep * a.rows_per_rep;
-  const int r1 = min(a.n_out, r0 + a.rows_per_rep);
+  const int r1 = min(n_out, r0 + a.rows_per_rep);
   const bool keep_all = nsel == C;
 
   if (keep_all) {
@@ -334,7 +347,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
     if (writer)
       for (int r = tid; r < C; r += THREADS) out[r] = r;
   } else if (nsel > 0) {
-    const float* src = a.scores + (int64_t)h * a.total_rows + s0;
+    const float* src = a.scores + (int64_t)hh * a.total_rows + s0;
     const int base = tid * KPT;
     if constexpr (Lds::kApart) clear_words<THREADS>(hist0, Lds::kHistWords);
     uint32_t key[KPT];
@@ -478,7 +491,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   const int tpr = a.row_bytes / 16;
   const int rpp = THREADS / tpr;
   const int part = tid % tpr;
-  const int64_t obase = ((int64_t)b * a.n_kv_heads + h) * a.n_out;
+  const int64_t obase = a.lay_out_off[layer] + ((int64_t)b * a.n_kv_heads + h) * n_out;
   for (int rb = r0 + tid / tpr; rb < r1; rb += kCopyBatch * rpp) {
     uint4 kv[kCopyBatch], vv[kCopyBatch];
 #pragma unroll
@@ -492,7 +505,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
       kv[u] = make_uint4(0, 0, 0, 0);
       vv[u] = make_uint4(0, 0, 0, 0);
       if (srow >= 0) {
-        const int64_t in = h * a.head_stride_bytes + (s0 + srow) * a.row_bytes + part * 16;
+        const int64_t in = hh * a.head_stride_bytes + (s0 + srow) * a.row_bytes + part * 16;
         kv[u] = load16(a.k + in);
         vv[u] = load16(a.v + in);
       }
@@ -559,8 +572,25 @@ SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, 
   a.n_select = n_select;
   a.n_out = n_select + n_tail;
   a.replicas = 1;
-  a.rows_per_rep = kMaxRowsPerRep;
+  a.rows_per_rep = n_select + n_tail > 0 ? n_select + n_tail : 1;
+  a.n_layers = 1;
+  a.lay_nsel[0] = n_select;
+  a.lay_idx_off[0] = 0;
+  a.lay_out_off[0] = 0;
   return a;
+}
+
+// Spread each head's row copies over enough replicas to occupy the chip while keeping
+// the repeated selection bounded: at most 32 replicas of at least 64 rows each.
+void set_replicas(SelectArgs& a, int units, int n_out) {
+  int reps = 256 / (units > 0 ? units : 1);
+  const int by_rows = (n_out + 63) / 64;
+  reps = reps > by_rows ? by_rows : reps;
+  reps = reps > 32 ? 32 : reps;
+  reps = reps < 1 ? 1 : reps;
+  const int rpr = (n_out + reps - 1) / reps;
+  a.replicas = reps;
+  a.rows_per_rep = rpr > 0 ? rpr : 1;
 }
 
 // Launch the segment kernel when the largest candidate set fits; returns false when
@@ -568,7 +598,7 @@ SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, 
 bool launch_fast(const SelectArgs& a, const dge_geom_t& g, int64_t cmax, hipStream_t st,
                  hipError_t* err) {
   if (a.pool_half > kPoolHalo) return false;
-  const dim3 grid(xcd_grid(a.replicas * g.n_kv_heads * g.batch));
+  const dim3 grid(xcd_grid(a.replicas * g.n_kv_heads * g.batch * a.n_layers));
   // (threads, candidates per thread): more threads per workgroup shorten the serial
   // per-thread loops of every radix pass (measured best at each size on MI355X)
   if (cmax <= 1024) *err = launch_seg<256, 4>(a, grid, st);
@@ -609,21 +639,7 @@ hipError_t launch_select_compact(const dge_geom_t& g, const float* scores, int p
   a.v_out = reinterpret_cast<char*>(v_out);
   a.head_stride_bytes = g.kv_head_stride * elt;
   a.row_bytes = g.head_dim * elt;
-  // Spread each head's row copies over enough replicas to occupy the chip while keeping
-  // the repeated selection bounded: at most 32 replicas of at least 64 rows each.
-  const int units = g.batch * g.n_kv_heads;
-  int reps = 256 / (units > 0 ? units : 1);
-  const int by_rows = (a.n_out + 63) / 64;
-  reps = reps > by_rows ? by_rows : reps;
-  reps = reps > 32 ? 32 : reps;
-  reps = reps < 1 ? 1 : reps;
-  int rpr = (a.n_out + reps - 1) / reps;
-  if (rpr > kMaxRowsPerRep) {
-    rpr = kMaxRowsPerRep;
-    reps = (a.n_out + rpr - 1) / rpr;
-  }
-  a.replicas = reps;
-  a.rows_per_rep = rpr > 0 ? rpr : 1;
+  set_replicas(a, g.batch * g.n_kv_heads, a.n_out);
   hipError_t err = hipSuccess;
   if (launch_fast(a, g, max_seq_rows(g) - n_tail, st, &err)) return err;
   // candidate sets beyond the register path: select, then the separate row gather
@@ -633,6 +649,68 @@ hipError_t launch_select_compact(const dge_geom_t& g, const float* scores, int p
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   return launch_compact(g, idx, n_kept, n_select, n_tail, k, v, k_out, v_out, st);
+}
+
+hipError_t launch_select_compact_layers(const dge_geom_t& g, int n_layers, const float* scores,
+                                        int pool_kernel, int n_tail, const int32_t* n_select_host,
+                                        int32_t* idx, int32_t* n_kept, const void* k, const void* v,
+                                        void* k_out, void* v_out, void* ws, hipStream_t st) {
+  const int elt = g.dtype == DGE_BF16 ? 2 : 4;
+  const int64_t heads = (int64_t)g.batch * g.n_kv_heads;
+  const int64_t cmax = max_seq_rows(g) - n_tail;
+  const int64_t hsz = (int64_t)g.n_kv_heads * g.kv_head_stride * elt;   // bytes per layer
+  const int64_t ssz = (int64_t)g.n_kv_heads * total_rows(g);             // scores per layer
+  const char* kc = static_cast<const char*>(k);
+  const char* vc = static_cast<const char*>(v);
+  char* koc = static_cast<char*>(k_out);
+  char* voc = static_cast<char*>(v_out);
+  const int row_bytes = g.head_dim * elt;
+  int64_t io = 0, oo = 0;   // packed idx elements and output rows of the layers before
+  if (pool_kernel / 2 <= kPoolHalo && cmax <= 32768) {
+    // groups of up to kMaxLayers layers, one launch each
+    for (int l0 = 0; l0 < n_layers; l0 += kMaxLayers) {
+      const int nl = n_layers - l0 < kMaxLayers ? n_layers - l0 : kMaxLayers;
+      int max_sel = 0;
+      for (int l = 0; l < nl; ++l)
+        max_sel = max_sel > n_select_host[l0 + l] ? max_sel : n_select_host[l0 + l];
+      SelectArgs a = make_args(g, scores + l0 * ssz, pool_kernel, n_tail, max_sel, idx + io,
+                               n_kept + (int64_t)l0 * g.batch, ws);
+      a.k = kc + l0 * hsz;
+      a.v = vc + l0 * hsz;
+      a.k_out = koc + oo * row_bytes;
+      a.v_out = voc + oo * row_bytes;
+      a.head_stride_bytes = g.kv_head_stride * elt;
+      a.row_bytes = row_bytes;
+      a.n_layers = nl;
+      int64_t gio = 0, goo = 0;
+      for (int l = 0; l < nl; ++l) {
+        a.lay_nsel[l] = n_select_host[l0 + l];
+        a.lay_idx_off[l] = gio;
+        a.lay_out_off[l] = goo;
+        gio += heads * n_select_host[l0 + l];
+        goo += heads * (n_select_host[l0 + l] + n_tail);
+      }
+      set_replicas(a, (int)(heads * nl), max_sel + n_tail);
+      hipError_t err = hipSuccess;
+      if (!launch_fast(a, g, cmax, st, &err)) return hipErrorInvalidValue;   // excluded above
+      if (err != hipSuccess) return err;
+      io += gio;
+      oo += goo;
+    }
+    return hipSuccess;
+  }
+  // pool radius beyond the register halo or candidate sets beyond the register path:
+  // one launch per layer on that layer's slices
+  for (int l = 0; l < n_layers; ++l) {
+    const int ns = n_select_host[l];
+    const hipError_t err = launch_select_compact(
+        g, scores + l * ssz, pool_kernel, n_tail, ns, idx + io, n_kept + (int64_t)l * g.batch,
+        kc + l * hsz, vc + l * hsz, koc + oo * row_bytes, voc + oo * row_bytes, ws, st);
+    if (err != hipSuccess) return err;
+    io += heads * ns;
+    oo += heads * (ns + n_tail);
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_select_streaming(const dge_geom_t& g, int n_sink, int n_recent, int32_t* idx,

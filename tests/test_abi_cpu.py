@@ -188,3 +188,20 @@ def test_retained_runs_validation(L):
     assert runs(out=None) == _lib.DGE_ERR_INVALID
     assert runs(mean=FAKE + 2) == _lib.DGE_ERR_INVALID
     assert runs(idx=FAKE + 1) == _lib.DGE_ERR_INVALID
+
+
+def test_select_compact_layers_validation(L):
+    g = _G()
+    ns = (ctypes.c_int32 * 3)(10, 20, 5)
+    def call(n_layers=3, arr=ns, pool=7, tail=10, idx=FAKE, ws=FAKE, nbytes=1 << 40, k=FAKE):
+        return L.dge_select_compact_layers(g.p, n_layers, FAKE, pool, tail, arr, idx, FAKE, k,
+                                           FAKE, FAKE, FAKE, ws, nbytes, None)
+    assert call(n_layers=0) == _lib.DGE_ERR_INVALID
+    assert call(arr=None) == _lib.DGE_ERR_INVALID
+    assert call(arr=(ctypes.c_int32 * 3)(10, -1, 5)) == _lib.DGE_ERR_INVALID
+    assert call(pool=4) == _lib.DGE_ERR_INVALID
+    assert call(tail=61) == _lib.DGE_ERR_INVALID          # longer than the 60-row sequence
+    assert call(idx=None) == _lib.DGE_ERR_INVALID
+    assert call(k=FAKE + 8) == _lib.DGE_ERR_INVALID
+    assert call(ws=None) == _lib.DGE_ERR_WORKSPACE
+    assert call(nbytes=16) == _lib.DGE_ERR_WORKSPACE

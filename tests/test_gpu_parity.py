@@ -174,6 +174,10 @@ SELECT_CASES = [
     ((40000, 300), "plateau", 7, 34, 2016),     # beyond the register path: global fallback
     ((3000, 700), "continuous", 19, 34, 300),   # pool wider than the register halo
     ((32768 + 34, 5000), "ints", 17, 34, 2016), # largest register-path candidate set
+    # values that differ only in their lowest bits: the last radix digit decides
+    ((4098, 1200), "ulps", 7, 34, 480),
+    ((16418,), "ulps", 1, 34, 2016),
+    ((30000, 9000), "ulps", 5, 34, 1500),
 ]
 
 
@@ -529,3 +533,49 @@ def test_retained_runs_on_gpu_selection(pool):
     n_kept = out["n_kept"].cpu().numpy().astype(np.int32)[: g.batch]
     runs, mean = _runs_check(g, idx, n_kept, f"pool {pool}")
     _log(f"  mean run length per head: {np.round(mean[0], 2).tolist()}")
+
+
+# ----------------------------------------------------------------------------------
+# Select + compact over several layers in one launch: bit-identical to one
+# dge_select_compact call per layer slice
+# ----------------------------------------------------------------------------------
+LAYER_CASES = {
+    # name: (lens, H_kv, head_dim, dtype, n_select per layer, pool, n_tail, score kind)
+    "ragged_budgets": ((3000, 700), 4, 128, "bf16", [600, 64, 0, 2000], 7, 34, "plateau"),
+    "pool5_f32": ((1500, 260, 900), 2, 64, "f32", [100, 250, 17], 5, 10, "ints"),
+    "no_pool_ulps": ((5000,), 8, 128, "bf16", [480, 2016, 1000], 1, 34, "ulps"),
+    "wide_pool": ((2000,), 2, 128, "bf16", [300, 40], 19, 34, "continuous"),     # per-layer launches
+    "beyond_register_path": ((33000, 400), 2, 128, "bf16", [100, 2016], 7, 34, "plateau"),
+    "many_layers": ((200, 90), 1, 64, "f32", [(7 * l) % 150 for l in range(130)], 3, 8, "continuous"),
+}
+
+
+@pytest.mark.parametrize("case", list(LAYER_CASES))
+def test_select_compact_layers_equals_per_layer(case):
+    lens, H, d, dtype, n_sel, pool, n_tail, kind = LAYER_CASES[case]
+    _log(f"select_compact_layers {case}: lens={lens} H={H} layers={len(n_sel)}")
+    nl, T = len(n_sel), sum(lens)
+    rng = np.random.default_rng(np.random.SeedSequence([7, len(case)]))
+    scores = torch.from_numpy(di.random_scores((nl * H, T), seed=len(case), kind=kind)).to(DEV)
+    if dtype == "bf16":
+        k = to_dev(rng.integers(0, 1 << 16, size=(nl * H, T, d), dtype=np.uint16), "bf16")
+        v = to_dev(rng.integers(0, 1 << 16, size=(nl * H, T, d), dtype=np.uint16), "bf16")
+    else:
+        k = torch.from_numpy(rng.standard_normal((nl * H, T, d), dtype=np.float32)).to(DEV)
+        v = torch.from_numpy(rng.standard_normal((nl * H, T, d), dtype=np.float32)).to(DEV)
+    g = dge.Geometry(2 * H, H, d, 0, 0, lens, dtype=dge.DGE_BF16 if dtype == "bf16" else dge.DGE_F32,
+                     device=DEV)
+    idx_l, nk, k_l, v_l = dge.select_compact_layers(g, scores, pool, n_tail, n_sel, k, v)
+    torch.cuda.synchronize()
+    for l in range(nl):
+        sl = slice(l * H, (l + 1) * H)
+        # fresh (aligned) copies of the layer's slices for the one-layer call
+        ri, rn, rk, rv = dge.select_compact(g, scores[sl].clone(), pool, n_tail, n_sel[l],
+                                            k[sl].clone(), v[sl].clone())
+        torch.cuda.synchronize()
+        assert torch.equal(nk[l], rn), (case, l)
+        assert torch.equal(idx_l[l], ri), (case, l)
+        assert torch.equal(k_l[l].view(torch.int16 if dtype == "bf16" else torch.int32),
+                           rk.view(torch.int16 if dtype == "bf16" else torch.int32)), (case, l)
+        assert torch.equal(v_l[l].view(torch.int16 if dtype == "bf16" else torch.int32),
+                           rv.view(torch.int16 if dtype == "bf16" else torch.int32)), (case, l)
