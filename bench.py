@@ -63,6 +63,9 @@ def parse():
                    help="score with the scoring rows' log-sum-exp supplied (dge_score_lse); the "
                         "LSE is prepared outside the timed region, as an attention forward would")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--compact-cmp", action="store_true",
+                   help="only time dge_compact (out of place) against dge_compact_inplace on one "
+                        "layer of the workload, the cache restored outside the timed events")
     return p.parse_args()
 
 
@@ -96,6 +99,8 @@ def main():
         sys.exit(2)
     log(f"[bench] workload {wl.name}: generating inputs")
     x = di.make_layer(wl, with_v=True)
+    if args.compact_cmp:
+        return bench_compact_cmp(args, wl, x, dev)
     if wl.h2o:
         return bench_h2o(args, wl, x, dev)
     is_bf16 = wl.dtype == "bf16"
@@ -308,6 +313,53 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def bench_compact_cmp(args, wl, x, dev):
+    """Compaction of one layer (Alg. 1 step C) into a separate buffer (dge_compact) and as an
+    edit of the cache itself (dge_compact_inplace), from the same selection.  Each call is
+    bracketed by HIP events on the stream it runs on; the in-place call's cache is restored
+    by a device copy before the first event.  Prints one JSON line."""
+    import torch
+    import paper_2609_33334_amd as dge
+
+    def dev_t(bits):
+        t = torch.from_numpy(np.ascontiguousarray(bits))
+        return t.view(torch.int16).view(torch.bfloat16).to(dev)
+
+    geom = dge.Geometry(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.window, wl.k_draft,
+                        wl.cached_lens, device=dev)
+    q, k, v = dev_t(x.q_bits), dev_t(x.k_bits), dev_t(x.v_bits)
+    n_tail = wl.window + wl.k_draft
+    n_sel = wl.budget_of_layer(0) - wl.window
+    raw = dge.score(geom, dge.ROWS_WINDOW_DRAFT, q, k)
+    idx, nk = dge.select_topb(geom, raw, wl.pool, n_tail, n_sel)
+    k_out, v_out = dge.compact(geom, idx, nk, n_sel, n_tail, k, v)
+    kw, vw = k.clone(), v.clone()
+    torch.cuda.synchronize()
+    reps = max(1, min(args.steps, 200))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    t_out, t_in = [], []
+    for _ in range(reps):
+        ev[0].record()
+        dge.compact(geom, idx, nk, n_sel, n_tail, k, v, k_out=k_out, v_out=v_out)
+        ev[1].record()
+        kw.copy_(k)
+        vw.copy_(v)
+        ev[2].record()
+        dge.compact_inplace(geom, idx, nk, n_sel, n_tail, kw, vw)
+        ev[3].record()
+        torch.cuda.synchronize()
+        t_out.append(ev[0].elapsed_time(ev[1]) * 1e3)
+        t_in.append(ev[2].elapsed_time(ev[3]) * 1e3)
+    nk_h = nk.cpu().numpy()
+    rows = int(sum(int(nk_h[b]) + n_tail for b in range(wl.batch))) * wl.n_kv_heads
+    moved = 2 * 2 * rows * wl.head_dim * 2        # K and V, read + write, bf16
+    med_out, med_in = float(np.median(t_out)), float(np.median(t_in))
+    print(json.dumps({"workload": wl.name, "compacted_rows": rows, "bytes_moved": moved,
+                      "dge_compact_us": round(med_out, 3), "dge_compact_inplace_us": round(med_in, 3),
+                      "compact_GBps": round(moved / med_out / 1e3, 1),
+                      "inplace_GBps": round(moved / med_in / 1e3, 1), "reps": reps}), flush=True)
 
 
 def bench_h2o(args, wl, x, dev):

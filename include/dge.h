@@ -206,6 +206,26 @@ dge_status_t dge_compact(const dge_geom_t *geom, const int32_t *idx, const int32
                          int32_t n_select, int32_t n_tail, const void *k, const void *v,
                          void *k_out, void *v_out, hipStream_t stream);
 
+/* Step 3 as an edit of the live cache (Alg. 1 step C rewrites the cache the continuation
+ * decodes from): for every (b, h), with C_b = N_b - n_tail and nk = n_kept[b],
+ *   K[h][off_b + r] <- K[h][off_b + idx[b][h][r]]   for r < nk
+ *   K[h][off_b + nk + t] <- K[h][off_b + C_b + t]   for t < n_tail
+ * and the same for V, with every source read before it is overwritten: afterwards the
+ * first nk + n_tail rows of each segment hold exactly the rows dge_compact writes to
+ * out[b][h][0 .. nk + n_tail).  Rows from nk + n_tail to N_b keep stale contents, and no
+ * zero rows are written; the caller's new sequence length is nk + n_tail (the segment
+ * offsets are unchanged).
+ *   idx, n_kept : dge_select_topb / dge_select_streaming output: ascending, so that
+ *                 idx[b][h][r] >= r (an entry below r is raised to r, one past C_b - 1
+ *                 lowered to C_b - 1; rows are never moved upwards).
+ *   k, v        : the cache, layout above; distinct buffers.
+ * No workspace; one workgroup per (KV head, sequence) copies its rows in order.
+ * Errors: DGE_ERR_INVALID for n_select < 0, n_tail outside [0, N_b], k == v or a NULL /
+ * misaligned pointer. */
+dge_status_t dge_compact_inplace(const dge_geom_t *geom, const int32_t *idx,
+                                 const int32_t *n_kept, int32_t n_select, int32_t n_tail,
+                                 void *k, void *v, hipStream_t stream);
+
 /* Continuation check on the evicted cache (Sec. 3 Eq. 1; App. "Why deferral can recover
  * FullKV", the eviction-mass equation; App. "Attention-matching loss"): attention of
  * query rows over the compacted caches that dge_compact / dge_select_compact write.

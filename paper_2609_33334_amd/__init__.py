@@ -23,7 +23,8 @@ from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  
                    ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
 
 __all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact",
-           "select_compact_layers", "select_streaming", "compact", "cache_attention",
+           "select_compact_layers", "select_streaming", "compact", "compact_inplace",
+           "cache_attention",
            "retained_runs", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
@@ -238,6 +239,16 @@ def compact(geom: Geometry, idx, n_kept, n_select: int, n_tail: int, k, v, k_out
                                       n_tail, _ptr(k), _ptr(v), _ptr(k_out), _ptr(v_out),
                                       _stream(stream)), "dge_compact")
     return k_out, v_out
+
+
+def compact_inplace(geom: Geometry, idx, n_kept, n_select: int, n_tail: int, k, v,
+                    stream=None):
+    """dge_compact_inplace: the compacted rows overwrite the first n_kept[b] + n_tail rows
+    of each (sequence, KV head) segment of k and v.  Returns (k, v)."""
+    _lib.check(_lib.lib().dge_compact_inplace(ctypes.byref(geom.c), _ptr(idx), _ptr(n_kept),
+                                              n_select, n_tail, _ptr(k), _ptr(v),
+                                              _stream(stream)), "dge_compact_inplace")
+    return k, v
 
 
 def cache_attention(geom: Geometry, q, n_q: int, q_from_end: int, k_c, v_c, n_select: int,

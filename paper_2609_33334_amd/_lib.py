@@ -20,7 +20,7 @@ ABI_VERSION = 1
 # every entry point declared in include/dge.h
 EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_score", "dge_score_lse",
            "dge_select_topb", "dge_select_compact", "dge_select_compact_layers",
-           "dge_select_streaming", "dge_compact",
+           "dge_select_streaming", "dge_compact", "dge_compact_inplace",
            "dge_cache_attention", "dge_retained_runs", "dge_h2o_colsum",
            "dge_pyramid_budgets")
 
@@ -87,6 +87,9 @@ def lib() -> ctypes.CDLL:
     L.dge_compact.restype = c_int
     L.dge_compact.argtypes = [GP, c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p,
                               c_void_p, c_void_p, c_void_p]
+    L.dge_compact_inplace.restype = c_int
+    L.dge_compact_inplace.argtypes = [GP, c_void_p, c_void_p, c_int32, c_int32, c_void_p,
+                                      c_void_p, c_void_p]
     L.dge_h2o_colsum.restype = c_int
     L.dge_cache_attention.restype = c_int
     L.dge_cache_attention.argtypes = [GP, c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_int32,

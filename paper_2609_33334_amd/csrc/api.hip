@@ -211,6 +211,19 @@ dge_status_t dge_compact(const dge_geom_t* geom, const int32_t* idx, const int32
       dge::launch_compact(*geom, idx, n_kept, n_select, n_tail, k, v, k_out, v_out, stream));
 }
 
+dge_status_t dge_compact_inplace(const dge_geom_t* geom, const int32_t* idx,
+                                 const int32_t* n_kept, int32_t n_select, int32_t n_tail, void* k,
+                                 void* v, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (n_select < 0) return DGE_ERR_INVALID;
+  if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
+  if (!n_kept || !k || !v || (n_select > 0 && !idx) || k == v) return DGE_ERR_INVALID;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(n_kept) || (idx && !aligned16(idx)))
+    return DGE_ERR_INVALID;
+  return hip_status(dge::launch_compact_inplace(*geom, idx, n_kept, n_select, n_tail, k, v, stream));
+}
+
 dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t n_q,
                                  int32_t q_from_end, const void* k_c, const void* v_c,
                                  int32_t n_select, int32_t n_tail, const int32_t* n_kept,

@@ -63,7 +63,87 @@ hipError_t launch_rb(const CompactArgs& a, const dge_geom_t& g, hipStream_t st) 
   return hipGetLastError();
 }
 
+// In-place compaction: the compacted rows of (b, h) overwrite the first n_kept + n_tail
+// rows of that head's own segment of the cache.  Every retained row moves down or stays
+// (idx is ascending, so idx[r] >= r; tail row t moves from C + t to n_kept + t).  One
+// workgroup per (KV head, sequence) walks the output rows in chunks: it reads every
+// source row of a chunk, meets a barrier, then writes the chunk.  The rows a chunk
+// writes lie below every source of the later chunks (a source is never below its own
+// output row), and the sources of this and the earlier chunks were read before the
+// barrier, so no row is overwritten before it has been read.
+constexpr int kInplaceThreads = 1024;
+constexpr int kInplaceUnroll = 8;
+
+template <int RB>
+__global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(CompactArgs a,
+                                                                         char* k, char* v) {
+  constexpr int TPR = RB / 16;                    // threads per row
+  constexpr int RPP = kInplaceThreads / TPR;      // rows per pass
+  constexpr int CHUNK = RPP * kInplaceUnroll;     // rows read before each barrier
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int sub = threadIdx.x / TPR, part = threadIdx.x % TPR;
+  const int64_t s0 = a.offs[b];
+  const int N = (int)(a.offs[b + 1] - s0);
+  const int C = N - a.n_tail;
+  const int nk = max(0, min(a.n_kept[b], min(a.n_select, C)));
+  const int n_out = nk + a.n_tail;
+  const int32_t* ix = a.idx + ((int64_t)b * a.n_kv_heads + h) * a.n_select;
+  const int64_t base = h * a.head_stride_bytes + s0 * RB + part * 16;
+  for (int c0 = 0; c0 < n_out; c0 += CHUNK) {
+    uint4 kv[kInplaceUnroll], vv[kInplaceUnroll];
+    int src[kInplaceUnroll];
+#pragma unroll
+    for (int u = 0; u < kInplaceUnroll; ++u) {
+      const int r = c0 + u * RPP + sub;
+      int s = -1;
+      if (r < nk)
+        s = max(r, min(ix[r], C - 1));   // a malformed index never moves a row upwards
+      else if (r < n_out)
+        s = C + (r - nk);
+      src[u] = s == r ? -1 : s;          // a row already in place is not copied
+      if (src[u] >= 0) {
+        kv[u] = load16(k + base + (int64_t)src[u] * RB);
+        vv[u] = load16(v + base + (int64_t)src[u] * RB);
+      }
+    }
+    __syncthreads();   // every source row of this chunk has been read
+#pragma unroll
+    for (int u = 0; u < kInplaceUnroll; ++u) {
+      if (src[u] >= 0) {
+        const int r = c0 + u * RPP + sub;
+        *reinterpret_cast<uint4*>(k + base + (int64_t)r * RB) = kv[u];
+        *reinterpret_cast<uint4*>(v + base + (int64_t)r * RB) = vv[u];
+      }
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_compact_inplace(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,
+                                  int n_select, int n_tail, void* k, void* v, hipStream_t st) {
+  CompactArgs a{};
+  const int elt = g.dtype == DGE_BF16 ? 2 : 4;
+  const int rb = g.head_dim * elt;
+  a.idx = idx;
+  a.n_kept = n_kept;
+  a.offs = seq_offsets(g);
+  a.head_stride_bytes = g.kv_head_stride * elt;
+  a.n_kv_heads = g.n_kv_heads;
+  a.n_select = n_select;
+  a.n_tail = n_tail;
+  a.n_out = n_select + n_tail;
+  char* kc = static_cast<char*>(k);
+  char* vc = static_cast<char*>(v);
+  const dim3 grid(g.n_kv_heads, g.batch);
+  switch (rb) {
+    case 128: hipLaunchKernelGGL((compact_inplace_kernel<128>), grid, dim3(kInplaceThreads), 0, st, a, kc, vc); break;
+    case 256: hipLaunchKernelGGL((compact_inplace_kernel<256>), grid, dim3(kInplaceThreads), 0, st, a, kc, vc); break;
+    case 512: hipLaunchKernelGGL((compact_inplace_kernel<512>), grid, dim3(kInplaceThreads), 0, st, a, kc, vc); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_compact(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,
                           int n_select, int n_tail, const void* k, const void* v, void* k_out,

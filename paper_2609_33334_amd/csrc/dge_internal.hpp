@@ -52,6 +52,8 @@ hipError_t launch_select_streaming(const dge_geom_t& g, int n_sink, int n_recent
 hipError_t launch_compact(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,
                           int n_select, int n_tail, const void* k, const void* v, void* k_out,
                           void* v_out, hipStream_t stream);
+hipError_t launch_compact_inplace(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,
+                                  int n_select, int n_tail, void* k, void* v, hipStream_t stream);
 
 int cache_attention_max_group();
 hipError_t launch_cache_attention(const dge_geom_t& g, const void* q, int n_q, int q_from_end,

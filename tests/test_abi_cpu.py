@@ -205,3 +205,15 @@ def test_select_compact_layers_validation(L):
     assert call(k=FAKE + 8) == _lib.DGE_ERR_INVALID
     assert call(ws=None) == _lib.DGE_ERR_WORKSPACE
     assert call(nbytes=16) == _lib.DGE_ERR_WORKSPACE
+
+
+def test_compact_inplace_validation(L):
+    g = _G()
+    def call(n_select=20, n_tail=10, idx=FAKE, nk=FAKE, k=FAKE, v=FAKE + 4096):
+        return L.dge_compact_inplace(g.p, idx, nk, n_select, n_tail, k, v, None)
+    assert call(n_select=-1) == _lib.DGE_ERR_INVALID
+    assert call(n_tail=61) == _lib.DGE_ERR_INVALID
+    assert call(v=FAKE) == _lib.DGE_ERR_INVALID            # k and v must be distinct
+    assert call(nk=None) == _lib.DGE_ERR_INVALID
+    assert call(idx=None) == _lib.DGE_ERR_INVALID
+    assert call(k=FAKE + 8) == _lib.DGE_ERR_INVALID

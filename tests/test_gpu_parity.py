@@ -579,3 +579,53 @@ def test_select_compact_layers_equals_per_layer(case):
                            rk.view(torch.int16 if dtype == "bf16" else torch.int32)), (case, l)
         assert torch.equal(v_l[l].view(torch.int16 if dtype == "bf16" else torch.int32),
                            rv.view(torch.int16 if dtype == "bf16" else torch.int32)), (case, l)
+
+
+# ----------------------------------------------------------------------------------
+# In-place compaction: the first n_kept + n_tail rows of every segment equal the
+# out-of-place compaction, the rest of the segment is untouched
+# ----------------------------------------------------------------------------------
+INPLACE_CASES = {
+    # name: (lens, H_kv, head_dim, dtype, n_select, n_tail, pool, selector)
+    "ragged_bf16": ((3000, 700, 90), 4, 128, "bf16", 480, 34, 7, "topb"),
+    "keep_all": ((600, 1200), 2, 128, "bf16", 5000, 34, 7, "topb"),
+    "tail_only": ((800,), 2, 128, "bf16", 0, 34, 7, "topb"),
+    "f32_d64": ((2500, 333), 2, 64, "f32", 300, 8, 5, "topb"),
+    "streaming": ((4098, 2000), 8, 128, "bf16", 4, 1020, 1, "streaming"),
+    "c4_length": ((32802,), 1, 128, "bf16", 2016, 34, 7, "topb"),
+}
+
+
+@pytest.mark.parametrize("case", list(INPLACE_CASES))
+def test_compact_inplace_equals_compact(case):
+    lens, H, d, dtype, n_select, n_tail, pool, selector = INPLACE_CASES[case]
+    _log(f"compact_inplace {case}: lens={lens} H={H} sel={n_select} tail={n_tail}")
+    T = sum(lens)
+    rng = np.random.default_rng(np.random.SeedSequence([11, len(case)]))
+    g = dge.Geometry(2 * H, H, d, 0, 0, lens, dtype=dge.DGE_BF16 if dtype == "bf16" else dge.DGE_F32,
+                     device=DEV)
+    if dtype == "bf16":
+        k = to_dev(rng.integers(0, 1 << 16, size=(H, T, d), dtype=np.uint16), "bf16")
+        v = to_dev(rng.integers(0, 1 << 16, size=(H, T, d), dtype=np.uint16), "bf16")
+        bits = torch.int16
+    else:
+        k = torch.from_numpy(rng.standard_normal((H, T, d), dtype=np.float32)).to(DEV)
+        v = torch.from_numpy(rng.standard_normal((H, T, d), dtype=np.float32)).to(DEV)
+        bits = torch.int32
+    if selector == "topb":
+        scores = torch.from_numpy(di.random_scores((H, T), seed=len(case), kind="plateau")).to(DEV)
+        idx, nk = dge.select_topb(g, scores, pool, n_tail, n_select)
+    else:
+        idx, nk = dge.select_streaming(g, n_select, n_tail)
+    k_out, v_out = dge.compact(g, idx, nk, n_select, n_tail, k, v)
+    k0, v0 = k.clone(), v.clone()
+    dge.compact_inplace(g, idx, nk, n_select, n_tail, k, v)
+    torch.cuda.synchronize()
+    nk = nk.cpu().numpy()
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    for b, N in enumerate(lens):
+        m = int(nk[b]) + n_tail
+        for name, got, want, orig in (("k", k, k_out, k0), ("v", v, v_out, v0)):
+            seg = got[:, offs[b]:offs[b] + N].view(bits)
+            assert torch.equal(seg[:, :m], want[b, :, :m].view(bits)), (case, b, name)
+            assert torch.equal(seg[:, m:], orig[:, offs[b] + m:offs[b] + N].view(bits)), (case, b, name)
