@@ -129,6 +129,28 @@ def test_score_c3_layer():
     check_scores(got, want, "c3/l5")
 
 
+def test_score_layer_major_long_walks():
+    # eight copies of a c3 layer scored as one layer-major geometry (64 KV heads): every
+    # workgroup walks the longest chunk (64 tiles of 64 keys); each copy must match the
+    # oracle of the layer
+    wl = di.WORKLOADS["c3"]
+    _log("score parity: 8 stacked c3 layers in one call")
+    x = di.make_layer(wl, layer=2, with_v=False)
+    nl = 8
+    g = dge.Geometry(wl.n_q_heads * nl, wl.n_kv_heads * nl, wl.head_dim, wl.window, wl.k_draft,
+                     wl.cached_lens, device=DEV)
+    q = to_dev(x.q_bits, "bf16").repeat(nl, 1, 1)
+    k = to_dev(x.k_bits, "bf16").repeat(nl, 1, 1)
+    raw = dge.score(g, oracle.ROWS_WINDOW_DRAFT, q, k)
+    torch.cuda.synchronize()
+    raw = raw.cpu().numpy()
+    want = oracle.window_scores(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                wl.k_draft, oracle.ROWS_WINDOW_DRAFT)
+    H = wl.n_kv_heads
+    for l in range(nl):
+        check_scores(raw[l * H:(l + 1) * H], want, f"layer copy {l}")
+
+
 @pytest.mark.parametrize("case", ["c2", "c2_ragged", "c1"])
 def test_score_lse_single_pass(case):
     wl = {"c2": di.WORKLOADS["c2"], "c2_ragged": SCORE_CASES["c2_ragged"], "c1": di.WORKLOADS["c1"]}[case]
