@@ -63,6 +63,9 @@ def parse():
                    help="score with the scoring rows' log-sum-exp supplied (dge_score_lse); the "
                         "LSE is prepared outside the timed region, as an attention forward would")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--repeat-kv", action="store_true",
+                   help="the prototype's layout: every KV head repeated to the G query heads of its "
+                        "group, scored and selected per query head (no group mean); one layer")
     p.add_argument("--compact-cmp", action="store_true",
                    help="only time dge_compact (out of place) against dge_compact_inplace on one "
                         "layer of the workload, the cache restored outside the timed events")
@@ -101,6 +104,8 @@ def main():
     x = di.make_layer(wl, with_v=True)
     if args.compact_cmp:
         return bench_compact_cmp(args, wl, x, dev)
+    if args.repeat_kv:
+        return bench_repeat_kv(args, wl, x, dev)
     if wl.h2o:
         return bench_h2o(args, wl, x, dev)
     is_bf16 = wl.dtype == "bf16"
@@ -313,6 +318,82 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def bench_repeat_kv(args, wl, x, dev):
+    """The eviction step on the repeated-KV layout the paper's prototype uses (App.
+    "Complexity and overheads"): K and V copied to all H_q query heads, dge_score with one
+    query head per cache head (no group mean), dge_select_compact per query head.  Same
+    timing method as the main path (HIP graphs over rotating buffer sets); `value` counts
+    prefix tokens x cache heads (H_q here).  Prints one JSON line."""
+    import torch
+    import paper_2609_33334_amd as dge
+
+    def dev_t(bits):
+        t = torch.from_numpy(np.ascontiguousarray(bits))
+        return t.view(torch.int16).view(torch.bfloat16).to(dev)
+
+    G = wl.n_q_heads // wl.n_kv_heads
+    H = wl.n_q_heads
+    g1 = dge.Geometry(H, H, wl.head_dim, wl.window, wl.k_draft, wl.cached_lens, device=dev)
+    q0 = dev_t(x.q_bits)
+    k0 = dev_t(np.repeat(x.k_bits, G, axis=0))
+    v0 = dev_t(np.repeat(x.v_bits, G, axis=0))
+    n_tail = wl.window + wl.k_draft
+    n_sel = wl.budget_of_layer(0) - wl.window
+    S = max(1, args.sets) if wl.n_layers == 1 else 1
+    ws_score = torch.empty(dge.workspace_size(g1, dge.OP_SCORE), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(dge.workspace_size(g1, dge.OP_SELECT), dtype=torch.uint8, device=dev)
+    sets = []
+    for _ in range(S):
+        out = dict(raw=torch.empty(H, g1.total_rows, dtype=torch.float32, device=dev),
+                   idx=torch.empty(g1.batch, H, n_sel, dtype=torch.int32, device=dev),
+                   n_kept=torch.zeros(max(4, g1.batch), dtype=torch.int32, device=dev),
+                   k=torch.empty(g1.batch, H, n_sel + n_tail, wl.head_dim, dtype=k0.dtype, device=dev),
+                   v=torch.empty(g1.batch, H, n_sel + n_tail, wl.head_dim, dtype=k0.dtype, device=dev))
+        sets.append((q0.clone(), k0.clone(), v0.clone(), out))
+
+    def step(i):
+        q, k, v, out = sets[i % S]
+        dge.score(g1, dge.ROWS_WINDOW_DRAFT, q, k, raw=out["raw"], ws=ws_score)
+        dge.select_compact(g1, out["raw"], wl.pool, n_tail, n_sel, k, v, idx=out["idx"],
+                           n_kept=out["n_kept"], k_out=out["k"], v_out=out["v"], ws=ws_sel)
+
+    for i in range(max(args.warmup, S)):
+        step(i)
+    torch.cuda.synchronize()
+    gsteps = GRAPH_STEPS
+    stream = torch.cuda.Stream()
+    graphs = []
+    with torch.cuda.stream(stream):
+        for gi in range(max(1, S // gsteps)):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=stream):
+                for j in range(gsteps):
+                    step(gi * gsteps + j)
+            graphs.append(gr)
+    torch.cuda.synchronize()
+    n_rep = (args.steps + gsteps - 1) // gsteps
+    K = n_rep * gsteps
+    for r in range(min(n_rep, 2 * len(graphs))):
+        graphs[r % len(graphs)].replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for r in range(n_rep):
+        graphs[r % len(graphs)].replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / K
+    L = sum(wl.prompt_lens)
+    kv_native = 2 * wl.n_kv_heads * g1.total_rows * wl.head_dim * 2
+    print(json.dumps({
+        "metric": "prefix tokens x cache heads scored+compacted per second (repeated-KV layout)",
+        "value": round(L * H / (ms_per_step * 1e-3), 1), "unit": "token*head/s",
+        "ms_per_step": round(ms_per_step, 6), "steps": K, "warmup": args.warmup,
+        "workload": WORKLOAD_TEXT.get(wl.name, wl.name),
+        "layout": f"K/V repeated x{G} to {H} cache heads, per-query-head scores and top-(B-w)",
+        "kv_bytes_per_layer": {"repeated": kv_native * G, "native_gqa": kv_native}}), flush=True)
 
 
 def bench_compact_cmp(args, wl, x, dev):

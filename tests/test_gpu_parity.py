@@ -651,3 +651,42 @@ def test_compact_inplace_equals_compact(case):
             seg = got[:, offs[b]:offs[b] + N].view(bits)
             assert torch.equal(seg[:, :m], want[b, :, :m].view(bits)), (case, b, name)
             assert torch.equal(seg[:, m:], orig[:, offs[b] + m:offs[b] + N].view(bits)), (case, b, name)
+
+
+# ----------------------------------------------------------------------------------
+# Repeated-KV layout (every KV head copied to the G query heads of its group, scored and
+# selected per query head, no group mean): the geometry with G = 1 over the repeated cache
+# ----------------------------------------------------------------------------------
+def test_repeated_kv_layout_per_query_head():
+    wl = di.small_variant("c2", [700, 1300])
+    _log("repeated-KV layout: per-query-head scores and selection")
+    x = di.make_layer(wl, with_v=True)
+    G = wl.n_q_heads // wl.n_kv_heads
+    k_rep = np.repeat(x.k_bits, G, axis=0)
+    v_rep = np.repeat(x.v_bits, G, axis=0)
+    g1 = dge.Geometry(wl.n_q_heads, wl.n_q_heads, wl.head_dim, wl.window, wl.k_draft,
+                      wl.cached_lens, device=DEV)
+    kd, vd = to_dev(k_rep, "bf16"), to_dev(v_rep, "bf16")
+    raw = dge.score(g1, oracle.ROWS_WINDOW_DRAFT, to_dev(x.q_bits, "bf16"), kd)
+    torch.cuda.synchronize()
+    want = oracle.window_scores(x.q, np.repeat(x.k, G, axis=0), wl.kv_offsets, wl.n_q_heads,
+                                wl.n_q_heads, wl.window, wl.k_draft)
+    got = raw.cpu().numpy()
+    check_scores(got, want, "per-query-head scores")
+    # per-query-head top-B' and compaction on the repeated cache, bit-exact given the scores
+    n_tail = wl.window + wl.k_draft
+    n_sel = wl.budget - wl.window
+    idx, nk, k_out, v_out = dge.select_compact(g1, raw, wl.pool, n_tail, n_sel, kd, vd)
+    torch.cuda.synchronize()
+    idx = idx.cpu().numpy()
+    offs = wl.kv_offsets
+    for b, N in enumerate(wl.cached_lens):
+        C = N - n_tail
+        for h in range(wl.n_q_heads):
+            pooled = oracle.maxpool(got[h, offs[b]:offs[b + 1]].astype(np.float64), C, wl.pool)
+            sel = oracle.select_topb(pooled, n_sel)
+            assert np.array_equal(idx[b, h, :len(sel)], sel), (b, h)
+            rows = np.concatenate([sel, np.arange(C, N)])
+            ref_k = k_rep[h, offs[b] + rows]
+            assert np.array_equal(k_out[b, h, :len(rows)].view(torch.int16).cpu().numpy(),
+                                  ref_k.view(np.int16)), (b, h)

@@ -72,6 +72,26 @@ def test_score_mass_equals_rows(mode):
         assert np.allclose(tot, nr, rtol=1e-12, atol=0)
 
 
+def test_repeated_kv_scores_average_to_group_scores():
+    # App. "Complexity and overheads": the prototype repeats every KV head to the G query
+    # heads of its group and scores per query head; the native GQA score of a KV head is
+    # the mean of those G per-query-head scores (a dropped 1/G, a wrong head-to-group map
+    # or a transposed repeat fails here)
+    Hq, Hkv, d, w, kd = 12, 3, 16, 4, 2
+    G = Hq // Hkv
+    offs = [0, 37, 90]
+    nr = w + kd
+    q = _rand((Hq, 2 * nr, d), 5, 2.0)
+    k = _rand((Hkv, offs[-1], d), 6, 2.0)
+    per_head = oracle.window_scores(q, np.repeat(k, G, axis=0), offs, Hq, Hq, w, kd)
+    grouped = oracle.window_scores(q, k, offs, Hq, Hkv, w, kd)
+    assert per_head.shape == (Hq, offs[-1])
+    assert np.allclose(per_head.reshape(Hkv, G, -1).mean(axis=1), grouped, rtol=1e-12, atol=1e-300)
+    # and the per-query-head rows keep their own softmax mass (n_rows per head)
+    for b in range(2):
+        assert np.allclose(per_head[:, offs[b]:offs[b + 1]].sum(axis=1), nr, rtol=1e-12)
+
+
 def test_score_uniform_closed_form():
     # identical keys: a row at position p spreads 1/(p+1) over keys 0..p, so
     # raw[j] = sum_{p = max(j, p0)}^{N-1} 1/(p+1)  (the group mean of equal heads)
