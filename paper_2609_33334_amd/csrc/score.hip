@@ -759,8 +759,9 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
   }
   // Every workgroup loads its query fragments once and streams several 64-key tiles:
   // about one tile-walk per 256 tiles of the launch, at most 64 tiles (measured on
-  // MI355X: c2 with 3 tiles per workgroup 0.5 us faster than with 2; the layer-major
-  // c3 and c4 launches 3% and 7% faster walking 64 tiles than 16).
+  // MI355X: one 4096-token layer of 8 KV heads 0.5 us faster with 3 tiles per workgroup
+  // than with 2; 32 layers scored in one launch, at 16K tokens or at batch 8 of 16K-32K
+  // tokens, 3% and 7% faster walking 64 tiles than 16).
   const int64_t tiles_total = (int64_t)g.n_kv_heads * ((total_rows(g) + KT - 1) / KT);
   const int64_t nmax = max_seq_rows(g);
   int iters = (int)((tiles_total + 255) / 256);
