@@ -640,9 +640,28 @@ def cpu_baseline(wl, x, seconds):
             break
     rate = reps * L * wl.n_kv_heads / el
     log(f"[bench] cpu oracle: {reps} layers in {el:.1f}s -> {rate:.3g} token*kvhead/s")
+    # the same oracle on one core (BLAS limited to one thread), on a shorter sample
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            reps1 = 0
+            t0 = time.perf_counter()
+            while True:
+                oracle.evict_layer(x.q, x.k, x.v, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                   wl.window, wl.k_draft, budget, wl.pool)
+                reps1 += 1
+                el1 = time.perf_counter() - t0
+                if el1 >= seconds / 3:
+                    break
+        one = round(reps1 * L * wl.n_kv_heads / el1, 1)
+        log(f"[bench] cpu oracle, one core: {reps1} layers in {el1:.1f}s -> {one:.3g} token*kvhead/s")
+    except Exception:  # pragma: no cover
+        pass
     return {"value": round(rate, 1), "unit": "token*kvhead/s", "cores": cores, "kind": "oracle",
             "sample": f"{reps} repeats of one {wl.name} layer (score, pool, select, compact; "
-                      f"budget {budget}) in float64 numpy, {el:.1f} s"}
+                      f"budget {budget}) in float64 numpy, {el:.1f} s",
+            "value_one_core": one}
 
 
 if __name__ == "__main__":
