@@ -20,6 +20,7 @@
 //   lane and crosses lanes once, at the end of the segment.  A small reduction adds
 //   the segments' partial sums in a fixed order.
 // No atomics: every partial column sum is owned by exactly one wavefront.
+#include <type_traits>
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
 
@@ -262,33 +263,39 @@ __global__ __launch_bounds__(256) void h2o_colsum_kernel(H2oArgs a, float* part,
     }
     // rows that can be masked: below the key block, or past the segment / sequence
     const bool edge = (r0 < k0 + KB) || (r0 + RB > seg_hi);
+    // masking only in the (rare) edge blocks: the common body has no branch per logit
+    auto body = [&](auto edge_c) {
+      constexpr bool EDGE = decltype(edge_c)::value;
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
-      uint4 qf[NS];
+      for (int rt = 0; rt < 4; ++rt) {
+        uint4 qf[NS];
 #pragma unroll
-      for (int s = 0; s < NS; ++s) qf[s] = lds_frag(qlds[cur], rt * 16 + c16, s, g16);
-      f32x4_t acca = {0.f, 0.f, 0.f, 0.f}, accb = {0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < NS; ++s) qf[s] = lds_frag(qlds[cur], rt * 16 + c16, s, g16);
+        f32x4_t acca = {0.f, 0.f, 0.f, 0.f}, accb = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        acca = mma_step(bf16_t{}, qf[s], kfa[s], acca);
-        accb = mma_step(bf16_t{}, qf[s], kfb[s], accb);
-      }
-      // acc[i] = logit of row r0 + rt*16 + 4*g16 + i for key ja (jb)
-      const float4 l4 = *reinterpret_cast<const float4*>(&llds[cur][rt * 16 + 4 * g16]);
-      const float l2[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float pa = fast_exp2(fmaf(acca[i], a.scale_log2, -l2[i]));
-        float pb = fast_exp2(fmaf(accb[i], a.scale_log2, -l2[i]));
-        if (edge) {
-          const int p = r0 + rt * 16 + 4 * g16 + i;
-          pa = (p < seg_hi && ja <= p) ? pa : 0.0f;
-          pb = (p < seg_hi && jb <= p) ? pb : 0.0f;
+        for (int s = 0; s < NS; ++s) {
+          acca = mma_step(bf16_t{}, qf[s], kfa[s], acca);
+          accb = mma_step(bf16_t{}, qf[s], kfb[s], accb);
         }
-        cola += pa;
-        colb += pb;
+        // acc[i] = logit of row r0 + rt*16 + 4*g16 + i for key ja (jb)
+        const float4 l4 = *reinterpret_cast<const float4*>(&llds[cur][rt * 16 + 4 * g16]);
+        const float l2[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float pa = fast_exp2(fmaf(acca[i], a.scale_log2, -l2[i]));
+          float pb = fast_exp2(fmaf(accb[i], a.scale_log2, -l2[i]));
+          if constexpr (EDGE) {
+            const int p = r0 + rt * 16 + 4 * g16 + i;
+            pa = (p < seg_hi && ja <= p) ? pa : 0.0f;
+            pb = (p < seg_hi && jb <= p) ? pb : 0.0f;
+          }
+          cola += pa;
+          colb += pb;
+        }
       }
-    }
+    };
+    if (edge) body(std::true_type{});
+    else body(std::false_type{});
     __syncthreads();
   }
   cola += shfl_xor_f<16>(cola);
