@@ -97,9 +97,6 @@ def main():
         sys.exit(2)
     dev = "cuda:0"
     wl = di.WORKLOADS[args.workload]
-    if args.lse and wl.batch != 1:
-        print("bench.py: --lse is implemented for single-sequence workloads", file=sys.stderr)
-        sys.exit(2)
     log(f"[bench] workload {wl.name}: generating inputs")
     x = di.make_layer(wl, with_v=True)
     if args.compact_cmp:
@@ -170,16 +167,21 @@ def main():
     row_lse = None
     if args.lse:
         # natural-log softmax normaliser of each scoring row over keys j <= p (fp32, torch)
+        # (per sequence of the batch; rows in the order of q: [H_q][batch * n_rows])
         nr = wl.window + wl.k_draft
-        N = wl.cached_lens[0]
-        kk = k0.float()
-        qq = q0.float()
         G = wl.group
-        x = torch.einsum("hrd,hnd->hrn", qq, kk.repeat_interleave(G, dim=0)) / (wl.head_dim ** 0.5)
-        pos = torch.arange(N - nr, N, device=dev)
-        x = x.masked_fill(torch.arange(N, device=dev)[None, None, :] > pos[None, :, None], float("-inf"))
-        row_lse = torch.logsumexp(x, dim=2).repeat(L_layers, 1).contiguous()
-        del x, kk, qq
+        parts = []
+        for b, N in enumerate(wl.cached_lens):
+            off = int(wl.kv_offsets[b])
+            qq = q0[:, b * nr:(b + 1) * nr].float()
+            kk = k0[:, off:off + N].float().repeat_interleave(G, dim=0)
+            x = torch.einsum("hrd,hnd->hrn", qq, kk) / (wl.head_dim ** 0.5)
+            pos = torch.arange(N - nr, N, device=dev)
+            x = x.masked_fill(torch.arange(N, device=dev)[None, None, :] > pos[None, :, None],
+                              float("-inf"))
+            parts.append(torch.logsumexp(x, dim=2))
+            del x, kk, qq
+        row_lse = torch.cat(parts, dim=1).repeat(L_layers, 1).contiguous()
 
     def score_call(i):
         q_all, k_all, _, raw_all, _, _ = sets[i % S]
