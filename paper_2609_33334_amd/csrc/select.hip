@@ -581,10 +581,11 @@ SelectArgs make_args(const dge_geom_t& g, const float* scores, int pool_kernel, 
 }
 
 // Spread each head's row copies over enough replicas to occupy the chip while keeping
-// the repeated selection bounded: at most 32 replicas of at least 64 rows each.
+// the repeated selection bounded: at most 32 replicas of at least 32 rows each (at 8
+// heads of 514 output rows, 17 replicas run 0.25 us faster than 9 of 64 rows).
 void set_replicas(SelectArgs& a, int units, int n_out) {
   int reps = 256 / (units > 0 ? units : 1);
-  const int by_rows = (n_out + 63) / 64;
+  const int by_rows = (n_out + 31) / 32;
   reps = reps > by_rows ? by_rows : reps;
   reps = reps > 32 ? 32 : reps;
   reps = reps < 1 ? 1 : reps;
