@@ -8,6 +8,7 @@
 // a workgroup scan per 1024-key tile) then writes the kept positions in ascending
 // order.  Taking tied keys in index order gives the lower-position tie-break
 // directly, and the output needs no sort.
+#include <type_traits>
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
 
@@ -204,18 +205,24 @@ struct SegLds {
                           : (kStageWords > kHistWords ? kStageWords : kHistWords));
 };
 
-// Inclusive prefix sum over the 64 lanes of a wavefront: DPP row shifts by 1, 2, 4 and 8
-// within each row of 16 lanes, then the row broadcasts of lane 15 (into rows 1 and 3)
-// and lane 31 (into rows 2 and 3).  Lanes without a source add the zero `old` value.
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15
-  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+// Inclusive scan over the 64 lanes of a wavefront under an associative operation with
+// identity `id`: DPP row shifts by 1, 2, 4 and 8 within each row of 16 lanes, then the
+// row broadcasts of lane 15 (into rows 1 and 3) and lane 31 (into rows 2 and 3).  Lanes
+// without a source combine with the identity (the `old` operand).
+template <class Op>
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, uint32_t id, Op op) {
+  const int o = (int)id;
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(o, (int)v, 0x111, 0xf, 0xf, false));  // row_shr:1
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(o, (int)v, 0x112, 0xf, 0xf, false));  // row_shr:2
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(o, (int)v, 0x114, 0xf, 0xf, false));  // row_shr:4
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(o, (int)v, 0x118, 0xf, 0xf, false));  // row_shr:8
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(o, (int)v, 0x142, 0xa, 0xf, false));  // row_bcast:15
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(o, (int)v, 0x143, 0xc, 0xf, false));  // row_bcast:31
   return v;
 }
+struct OpAdd { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a + b; } };
+struct OpMin { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a < b ? a : b; } };
+struct OpMax { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a > b ? a : b; } };
 
 // Workgroup-wide exclusive prefix sum of one int per thread (one barrier).  Counts here
 // stay below 2^16 per half, so two counters can share one packed word.
@@ -223,13 +230,41 @@ template <int THREADS>
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* sh) {
   constexpr int WAVES = THREADS / kWave;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const uint32_t inc = wave_incl_scan(x);
+  const uint32_t inc = wave_incl_scan(x, 0u, OpAdd());
   if (lane == 63) sh[wv] = inc;
   __syncthreads();
   uint32_t before = 0;
 #pragma unroll
   for (int w = 0; w < WAVES; ++w)
     if (w < wv) before += sh[w];
+  return before + inc - x;
+}
+
+// block_excl_scan of x that also reduces lo (minimum) and hi (maximum) over the
+// workgroup in the same barrier; sh holds 3 * WAVES words.
+template <int THREADS>
+__device__ __forceinline__ uint32_t block_excl_scan_minmax(uint32_t x, uint32_t& lo, uint32_t& hi,
+                                                           uint32_t* sh) {
+  constexpr int WAVES = THREADS / kWave;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const uint32_t inc = wave_incl_scan(x, 0u, OpAdd());
+  const uint32_t wlo = wave_incl_scan(lo, 0xffffffffu, OpMin());
+  const uint32_t whi = wave_incl_scan(hi, 0u, OpMax());
+  if (lane == 63) {
+    sh[wv] = inc;
+    sh[WAVES + wv] = wlo;
+    sh[2 * WAVES + wv] = whi;
+  }
+  __syncthreads();
+  uint32_t before = 0;
+  lo = 0xffffffffu;
+  hi = 0u;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    if (w < wv) before += sh[w];
+    lo = min(lo, sh[WAVES + w]);
+    hi = max(hi, sh[2 * WAVES + w]);
+  }
   return before + inc - x;
 }
 
@@ -336,7 +371,7 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
   // the kept candidates in output order, written over the staging buffer (and the
   // histograms on top of it) once those are dead; nsel <= C <= THREADS * KPT words
   int32_t* const sel = reinterpret_cast<int32_t*>(stage);
-  __shared__ uint32_t scan_sh[WAVES];
+  __shared__ uint32_t scan_sh[3 * WAVES];
   __shared__ int sh_digit[3][4];
   const int r0 = rep * a.rows_per_rep;
   const int r1 = min(n_out, r0 + a.rows_per_rep);
@@ -437,30 +472,55 @@ __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) 
     // significant digit first, until the digit's bin holds exactly the keys still to take
     uint32_t prefix = 0, mask = 0x80000000u;
     int remaining = nsel;
-    const bool done = radix_pass<THREADS, KPT, Lds::kBits0, 31 - Lds::kBits0>(
+    bool exact = radix_pass<THREADS, KPT, Lds::kBits0, 31 - Lds::kBits0>(
         key, base, C, hist0, scan_sh, sh_digit[0], prefix, mask, remaining);
-    if (!done) {
-      const bool done1 = radix_pass<THREADS, KPT, Lds::kBits1, Lds::kBits2>(
+    if (!exact)
+      exact = radix_pass<THREADS, KPT, Lds::kBits1, Lds::kBits2>(
           key, base, C, hist1, scan_sh, sh_digit[1], prefix, mask, remaining);
-      if (!done1)
+
+    // (greater, tied) counts of this thread's segment under the current prefix, packed
+    // into one scanned word (C <= 32768, so neither half overflows 16 bits)
+    auto count_scan = [&](uint32_t& lo, uint32_t& hi, auto with_minmax) {
+      uint32_t packed = 0;
+      lo = 0xffffffffu;
+      hi = 0u;
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const bool valid = base + i < C;
+        const uint32_t km = key[i] & mask;
+        const bool eq = valid && km == prefix;
+        packed += (valid && km > prefix) ? 1u : 0u;
+        packed += eq ? (1u << 16) : 0u;
+        if constexpr (decltype(with_minmax)::value) {
+          lo = eq ? min(lo, key[i]) : lo;
+          hi = eq ? max(hi, key[i]) : hi;
+        }
+      }
+      if constexpr (decltype(with_minmax)::value)
+        return block_excl_scan_minmax<THREADS>(packed, lo, hi, scan_sh);
+      else
+        return block_excl_scan<THREADS>(packed, scan_sh);
+    };
+    uint32_t lo = 0, hi = 1, before;
+    if constexpr (THREADS * KPT <= 4096) {
+      // small candidate sets: the count scan also finds the smallest and largest key of
+      // the threshold's bin; equal keys (max-pool plateaus) are all the threshold and
+      // need no third pass (measured faster only at these sizes)
+      before = count_scan(lo, hi, std::true_type{});
+      if (!exact && lo != hi) {
         radix_pass<THREADS, KPT, Lds::kBits2, 0>(key, base, C, hist2, scan_sh, sh_digit[2],
                                                  prefix, mask, remaining);
+        before = count_scan(lo, hi, std::false_type{});
+      }
+    } else {
+      if (!exact)
+        radix_pass<THREADS, KPT, Lds::kBits2, 0>(key, base, C, hist2, scan_sh, sh_digit[2],
+                                                 prefix, mask, remaining);
+      before = count_scan(lo, hi, std::false_type{});
     }
     // kept: keys above the threshold prefix, and `need` of the keys on it (index order)
     const uint32_t thr = prefix;
     const int need = remaining;
-
-    // (greater, tied) counts of this thread's segment, packed into one scanned word
-    uint32_t packed = 0;
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const bool valid = base + i < C;
-      const uint32_t km = key[i] & mask;
-      packed += (valid && km > thr) ? 1u : 0u;
-      packed += (valid && km == thr) ? (1u << 16) : 0u;
-    }
-    // C <= 32768, so neither half of the packed prefix overflows 16 bits
-    const uint32_t before = block_excl_scan<THREADS>(packed, scan_sh);
     const int gt_before = (int)(before & 0xffffu), tie_before = (int)(before >> 16);
     // the kept candidates of the segment take consecutive output positions; ties are
     // kept in index order up to the quota.  The scan's barrier has retired every read of
