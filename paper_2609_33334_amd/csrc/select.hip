@@ -1,13 +1,18 @@
 // Retention rules R_E (Alg. 1 step B): SnapKV max-pool + per-head top-B, and
-// StreamingLLM sinks.  One workgroup per (sequence, KV head).
+// StreamingLLM sinks; optionally fused with the compaction (Alg. 1 step C).
 //
 // Top-B is an exact radix select on the float32 bit patterns of the pooled scores:
 // scores are non-negative, so their IEEE bits order exactly like the values as
-// unsigned integers.  Four 8-bit passes find the B'-th largest key T and how many
-// keys equal to T must be kept; an ordered stream compaction (wavefront ballots +
-// a workgroup scan per 1024-key tile) then writes the kept positions in ascending
-// order.  Taking tied keys in index order gives the lower-position tie-break
+// unsigned integers.  Radix passes find the B'-th largest key T and how many keys equal
+// to T must be kept; an ordered stream compaction then writes the kept positions in
+// ascending order.  Taking tied keys in index order gives the lower-position tie-break
 // directly, and the output needs no sort.
+//
+// Two kernels: select_topb_seg_kernel, the path for up to 32768 candidates per
+// sequence (keys in registers, up to three passes of 12-14/10/9-7 bits, one workgroup
+// per (replica, KV head, sequence, layer)); and select_topb_kernel, the fallback beyond
+// it (keys in a global workspace, four 8-bit passes, one workgroup per (KV head,
+// sequence), ordered compaction by wavefront ballots and a scan per 1024-key tile).
 #include <type_traits>
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
