@@ -92,6 +92,54 @@ def test_repeated_kv_scores_average_to_group_scores():
         assert np.allclose(per_head[:, offs[b]:offs[b + 1]].sum(axis=1), nr, rtol=1e-12)
 
 
+def _brute_scores(q, k, offs, Hq, Hkv, w, kd, h2o=False):
+    # the definitions written out as plain Python loops with math.exp: for each scoring
+    # row (or, for H2O, every cached row) a causal softmax over the sequence's keys,
+    # summed into the keys' columns and divided by the group size
+    G = Hq // Hkv
+    d = len(k[0][0])
+    T = offs[-1]
+    out = [[0.0] * T for _ in range(Hkv)]
+    for b in range(len(offs) - 1):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        if h2o:
+            rows = [(p, s0 + p) for p in range(N)]            # (position, row of q)
+        else:
+            nr = w + kd
+            rows = [(N - nr + r, b * nr + r) for r in range(nr)]
+        for hq in range(Hq):
+            h = hq // G
+            for p, qi in rows:
+                logits = [sum(q[hq][qi][e] * k[h][s0 + j][e] for e in range(d)) / math.sqrt(d)
+                          for j in range(p + 1)]
+                top = max(logits)
+                ex = [math.exp(x - top) for x in logits]
+                z = sum(ex)
+                for j in range(p + 1):
+                    out[h][s0 + j] += ex[j] / z / G
+    return np.array(out)
+
+
+def test_scores_match_plain_python_loops():
+    Hq, Hkv, d, w, kd = 4, 2, 5, 3, 2
+    offs = [0, 9, 23]
+    q = _rand((Hq, 2 * (w + kd), d), 11, 1.5)
+    k = _rand((Hkv, offs[-1], d), 12, 1.5)
+    want = _brute_scores(q.tolist(), k.tolist(), offs, Hq, Hkv, w, kd)
+    got = oracle.window_scores(q, k, offs, Hq, Hkv, w, kd)
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-15)
+
+
+def test_h2o_colsum_matches_plain_python_loops():
+    Hq, Hkv, d = 4, 2, 5
+    offs = [0, 11, 20]
+    q = _rand((Hq, offs[-1], d), 13, 1.5)
+    k = _rand((Hkv, offs[-1], d), 14, 1.5)
+    want = _brute_scores(q.tolist(), k.tolist(), offs, Hq, Hkv, 0, 0, h2o=True)
+    got = oracle.h2o_colsum(q, k, offs, Hq, Hkv)
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-15)
+
+
 def test_score_uniform_closed_form():
     # identical keys: a row at position p spreads 1/(p+1) over keys 0..p, so
     # raw[j] = sum_{p = max(j, p0)}^{N-1} 1/(p+1)  (the group mean of equal heads)
