@@ -33,6 +33,8 @@
  *   Element type of Q, K, V: bfloat16 (DGE_BF16) or float32 (DGE_F32).
  * - Thread safety: no global mutable state; concurrent calls on different
  *   streams with disjoint outputs and workspaces are safe.
+ * - Row counts are bounded by INT32_MAX / 2: a longer sequence is DGE_ERR_UNSUPPORTED,
+ *   a larger n_select DGE_ERR_INVALID (so that n_select + n_tail fits in int32).
  */
 #ifndef DGE_H_
 #define DGE_H_

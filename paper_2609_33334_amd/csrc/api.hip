@@ -11,6 +11,10 @@ using dge::ScorePlan;
 
 namespace {
 
+// bound on row counts (sequence lengths, n_select), so that n_select + n_tail and the
+// kernels' row indices stay within int32
+constexpr int32_t kMaxRows = INT32_MAX / 2;
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 dge_status_t check_geom(const dge_geom_t* g) {
@@ -125,7 +129,7 @@ dge_status_t dge_select_topb(const dge_geom_t* geom, const float* scores, int32_
   dge_status_t st = check_geom(geom);
   if (st != DGE_OK) return st;
   if (pool_kernel < 1 || (pool_kernel & 1) == 0) return DGE_ERR_INVALID;
-  if (n_select < 0) return DGE_ERR_INVALID;
+  if (n_select < 0 || n_select > kMaxRows) return DGE_ERR_INVALID;
   if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
   if (!scores || !n_kept || (n_select > 0 && !idx) || !aligned16(scores) || !aligned16(idx) ||
       !aligned16(n_kept))
@@ -143,7 +147,7 @@ dge_status_t dge_select_compact(const dge_geom_t* geom, const float* scores, int
   dge_status_t st = check_geom(geom);
   if (st != DGE_OK) return st;
   if (pool_kernel < 1 || (pool_kernel & 1) == 0) return DGE_ERR_INVALID;
-  if (n_select < 0) return DGE_ERR_INVALID;
+  if (n_select < 0 || n_select > kMaxRows) return DGE_ERR_INVALID;
   if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
   if (!scores || !n_kept || (n_select > 0 && !idx) || !aligned16(scores) || !aligned16(idx) ||
       !aligned16(n_kept))
@@ -168,7 +172,7 @@ dge_status_t dge_select_compact_layers(const dge_geom_t* geom, int32_t n_layers,
   if (pool_kernel < 1 || (pool_kernel & 1) == 0) return DGE_ERR_INVALID;
   bool any_sel = false;
   for (int l = 0; l < n_layers; ++l) {
-    if (n_select_host[l] < 0) return DGE_ERR_INVALID;
+    if (n_select_host[l] < 0 || n_select_host[l] > kMaxRows) return DGE_ERR_INVALID;
     any_sel = any_sel || n_select_host[l] > 0;
   }
   if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
@@ -201,7 +205,7 @@ dge_status_t dge_compact(const dge_geom_t* geom, const int32_t* idx, const int32
                          void* k_out, void* v_out, hipStream_t stream) {
   dge_status_t st = check_geom(geom);
   if (st != DGE_OK) return st;
-  if (n_select < 0) return DGE_ERR_INVALID;
+  if (n_select < 0 || n_select > kMaxRows) return DGE_ERR_INVALID;
   if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
   if (!n_kept || !k || !v || !k_out || !v_out || (n_select > 0 && !idx)) return DGE_ERR_INVALID;
   if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out) ||
@@ -216,7 +220,7 @@ dge_status_t dge_compact_inplace(const dge_geom_t* geom, const int32_t* idx,
                                  void* v, hipStream_t stream) {
   dge_status_t st = check_geom(geom);
   if (st != DGE_OK) return st;
-  if (n_select < 0) return DGE_ERR_INVALID;
+  if (n_select < 0 || n_select > kMaxRows) return DGE_ERR_INVALID;
   if ((st = check_tail(geom, n_tail)) != DGE_OK) return st;
   if (!n_kept || !k || !v || (n_select > 0 && !idx) || k == v) return DGE_ERR_INVALID;
   if (!aligned16(k) || !aligned16(v) || !aligned16(n_kept) || (idx && !aligned16(idx)))
@@ -230,7 +234,8 @@ dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t 
                                  float* out, float* lse, hipStream_t stream) {
   dge_status_t st = check_geom(geom);
   if (st != DGE_OK) return st;
-  if (n_q < 1 || n_select < 0 || n_tail < 0 || q_from_end > n_tail || n_select + n_tail < 1)
+  if (n_q < 1 || n_select < 0 || n_select > kMaxRows || n_tail < 0 || q_from_end > n_tail ||
+      n_select + n_tail < 1)
     return DGE_ERR_INVALID;
   if (!q || !k_c || !v_c || !n_kept || !out || !lse || !aligned16(q) || !aligned16(k_c) ||
       !aligned16(v_c) || !aligned16(out) || (reinterpret_cast<uintptr_t>(n_kept) & 3) ||
@@ -247,7 +252,8 @@ dge_status_t dge_retained_runs(const dge_geom_t* geom, const int32_t* idx, const
                                hipStream_t stream) {
   dge_status_t st = check_geom(geom);
   if (st != DGE_OK) return st;
-  if (n_select < 0 || !n_kept || !runs || !mean_len || (n_select > 0 && !idx)) return DGE_ERR_INVALID;
+  if (n_select < 0 || n_select > kMaxRows || !n_kept || !runs || !mean_len || (n_select > 0 && !idx))
+    return DGE_ERR_INVALID;
   if ((reinterpret_cast<uintptr_t>(idx) & 3) || (reinterpret_cast<uintptr_t>(n_kept) & 3) ||
       (reinterpret_cast<uintptr_t>(runs) & 3) || (reinterpret_cast<uintptr_t>(mean_len) & 3))
     return DGE_ERR_INVALID;

@@ -217,3 +217,15 @@ def test_compact_inplace_validation(L):
     assert call(nk=None) == _lib.DGE_ERR_INVALID
     assert call(idx=None) == _lib.DGE_ERR_INVALID
     assert call(k=FAKE + 8) == _lib.DGE_ERR_INVALID
+
+
+def test_row_counts_bounded(L):
+    # n_select + n_tail must stay a valid int32 row count
+    g = _G()
+    big = 2 ** 31 - 1
+    assert L.dge_select_topb(g.p, FAKE, 7, 10, big, FAKE, FAKE, FAKE, 1 << 40, None) == _lib.DGE_ERR_INVALID
+    assert L.dge_compact(g.p, FAKE, FAKE, big, 10, FAKE, FAKE, FAKE, FAKE, None) == _lib.DGE_ERR_INVALID
+    assert L.dge_compact_inplace(g.p, FAKE, FAKE, big, 10, FAKE, FAKE + 4096, None) == _lib.DGE_ERR_INVALID
+    ns = (ctypes.c_int32 * 2)(10, big)
+    assert L.dge_select_compact_layers(g.p, 2, FAKE, 7, 10, ns, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                       FAKE, 1 << 40, None) == _lib.DGE_ERR_INVALID
