@@ -162,8 +162,10 @@ dge_status_t dge_select_compact(const dge_geom_t *geom, const float *scores, int
                                 const void *k, const void *v, void *k_out, void *v_out, void *ws,
                                 size_t ws_bytes, hipStream_t stream);
 
-/* dge_select_compact for n_layers layers in one launch (Alg. 1 steps B-C run for every
- * layer at once after drafting), each layer with its own budget.  The caches are
+/* dge_select_compact for n_layers layers at once (Alg. 1 steps B-C run for every layer
+ * after drafting), each layer with its own budget: one launch per group of up to 64
+ * layers (one launch per layer when a sequence has more than 32768 candidates or the
+ * pool radius exceeds 8, as dge_select_compact does then).  The caches are
  * layer-major: layer l's scores are heads [l*H_kv, (l+1)*H_kv) of a [n_layers*H_kv][T]
  * array (one dge_score call over the layer-major geometry writes them), and its K and V
  * heads start at element l * H_kv * kv_head_stride of k and v.  geom describes one layer.
