@@ -66,6 +66,10 @@ def parse():
     p.add_argument("--repeat-kv", action="store_true",
                    help="the prototype's layout: every KV head repeated to the G query heads of its "
                         "group, scored and selected per query head (no group mean); one layer")
+    p.add_argument("--streams", type=int, default=1,
+                   help="single-layer workloads: run independent steps (different buffer sets, "
+                        "i.e. different requests' layers) on this many streams at once; reported "
+                        "on its own line, the default bench keeps one stream")
     p.add_argument("--compact-cmp", action="store_true",
                    help="only time dge_compact (out of place) against dge_compact_inplace on one "
                         "layer of the workload, the cache restored outside the timed events")
@@ -103,6 +107,8 @@ def main():
         return bench_compact_cmp(args, wl, x, dev)
     if args.repeat_kv:
         return bench_repeat_kv(args, wl, x, dev)
+    if args.streams > 1:
+        return bench_streams(args, wl, x, dev)
     if wl.h2o:
         return bench_h2o(args, wl, x, dev)
     is_bf16 = wl.dtype == "bf16"
@@ -396,6 +402,104 @@ def bench_repeat_kv(args, wl, x, dev):
         "workload": WORKLOAD_TEXT.get(wl.name, wl.name),
         "layout": f"K/V repeated x{G} to {H} cache heads, per-query-head scores and top-(B-w)",
         "kv_bytes_per_layer": {"repeated": kv_native * G, "native_gqa": kv_native}}), flush=True)
+
+
+def bench_streams(args, wl, x, dev):
+    """Throughput of independent eviction steps of a single-layer workload in flight together:
+    step j of a graph runs on stream j % n (its own workspaces), the streams forked from and
+    joined back to the timed stream, so the latency-bound launches of different steps
+    overlap.  Prints one JSON line (not the default bench line)."""
+    import torch
+    import paper_2609_33334_amd as dge
+
+    if wl.n_layers != 1 or wl.h2o:
+        print("bench.py: --streams is for the single-layer eviction workloads", file=sys.stderr)
+        sys.exit(2)
+    n = args.streams
+
+    def dev_t(bits):
+        t = torch.from_numpy(np.ascontiguousarray(bits))
+        if wl.dtype == "bf16":
+            t = t.view(torch.int16).view(torch.bfloat16)
+        return t.to(dev)
+
+    geom = dge.Geometry(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.window, wl.k_draft,
+                        wl.cached_lens, dtype=dge.DGE_BF16 if wl.dtype == "bf16" else dge.DGE_F32,
+                        device=dev)
+    q0, k0, v0 = dev_t(x.q_bits), dev_t(x.k_bits), dev_t(x.v_bits)
+    n_tail = wl.window + wl.k_draft
+    n_sel = wl.budget_of_layer(0) - wl.window
+    S = max(n, args.sets)
+    ws = [(torch.empty(dge.workspace_size(geom, dge.OP_SCORE), dtype=torch.uint8, device=dev),
+           torch.empty(dge.workspace_size(geom, dge.OP_SELECT), dtype=torch.uint8, device=dev))
+          for _ in range(n)]
+    sets = []
+    for _ in range(S):
+        out = dict(raw=torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=dev),
+                   idx=torch.empty(geom.batch, geom.n_kv_heads, n_sel, dtype=torch.int32, device=dev),
+                   n_kept=torch.zeros(max(4, geom.batch), dtype=torch.int32, device=dev),
+                   k=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
+                                 dtype=k0.dtype, device=dev),
+                   v=torch.empty(geom.batch, geom.n_kv_heads, n_sel + n_tail, wl.head_dim,
+                                 dtype=k0.dtype, device=dev))
+        sets.append((q0.clone(), k0.clone(), v0.clone(), out))
+
+    def step(i, c):
+        q, k, v, out = sets[i % S]
+        dge.score(geom, dge.ROWS_WINDOW_DRAFT, q, k, raw=out["raw"], ws=ws[c][0])
+        dge.select_compact(geom, out["raw"], wl.pool, n_tail, n_sel, k, v, idx=out["idx"],
+                           n_kept=out["n_kept"], k_out=out["k"], v_out=out["v"], ws=ws[c][1])
+
+    for i in range(max(args.warmup, S)):
+        step(i, 0)
+    torch.cuda.synchronize()
+    ref = {kk: vv.clone() for kk, vv in sets[n - 1][3].items()}
+    gsteps = GRAPH_STEPS * n
+    main_s = torch.cuda.Stream()
+    side = [torch.cuda.Stream() for _ in range(n - 1)]
+    graphs = []
+    with torch.cuda.stream(main_s):
+        for gi in range(max(1, S // gsteps)):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=main_s):
+                for sd in side:
+                    sd.wait_stream(main_s)
+                for j in range(gsteps):
+                    c = j % n
+                    with torch.cuda.stream(main_s if c == 0 else side[c - 1]):
+                        step(gi * gsteps + j, c)
+                for sd in side:
+                    main_s.wait_stream(sd)
+            graphs.append(gr)
+    torch.cuda.synchronize()
+    for kk in ref:
+        sets[n - 1][3][kk].zero_()
+    torch.cuda.synchronize()
+    graphs[0].replay()
+    torch.cuda.synchronize()
+    for kk in ref:
+        assert torch.equal(sets[n - 1][3][kk], ref[kk]), f"graph replay differs from eager ({kk})"
+    n_rep = max(1, (args.steps + gsteps - 1) // gsteps)
+    K = n_rep * gsteps
+    for r in range(min(n_rep, 2 * len(graphs))):
+        graphs[r % len(graphs)].replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(main_s):
+        e0.record()
+        for r in range(n_rep):
+            graphs[r % len(graphs)].replay()
+        e1.record()
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / K
+    L = sum(wl.prompt_lens)
+    print(json.dumps({
+        "metric": "prefix tokens x KV heads scored+compacted per second (DGE eviction step)",
+        "value": round(L * wl.n_kv_heads / (ms_per_step * 1e-3), 1), "unit": "token*kvhead/s",
+        "ms_per_step": round(ms_per_step, 6), "steps": K, "warmup": args.warmup,
+        "concurrent_steps": n, "workload": WORKLOAD_TEXT.get(wl.name, wl.name),
+        "step": "dge_score -> dge_select_compact; independent steps on separate streams"}),
+        flush=True)
 
 
 def bench_compact_cmp(args, wl, x, dev):
