@@ -348,7 +348,7 @@ template <int THREADS, int KPT, int PH>
 __global__ __launch_bounds__(THREADS) void select_topb_seg_kernel(SelectArgs a) {
   using Lds = SegLds<THREADS, KPT, PH>;
   constexpr int WAVES = THREADS / kWave;
-  static_assert(KPT <= 32, "kept-candidate bit mask is 32 bits");
+  static_assert(KPT <= 32, "a thread keeps at most 32 pooled keys in registers");
   extern __shared__ __attribute__((aligned(16))) float stage[];
   const int per_layer = a.replicas * a.n_kv_heads * a.batch;
   const int units = per_layer * a.n_layers;
