@@ -19,9 +19,12 @@ struct ScorePlan {
   int ft;              // row tiles each wavefront owns in a row group (all keys)
   int rt;              // shared row tiles, split across wavefronts by key subtile
   int groups;          // row groups of 4 * ft + rt tiles covering all tiles
-  int tiles_per_wave;  // 64-key iterations per workgroup
+  int tiles_per_wave;  // 64-key iterations per workgroup (stats pass)
   int chunk_keys;      // keys per workgroup (4 wavefronts)
   int n_chunks;        // workgroups per (sequence, KV head)
+  int c_tiles;         // the same three for the colsum pass, which only needs the merged
+  int c_chunk_keys;    // row normalisers and may split the keys differently
+  int c_n_chunks;
 };
 
 struct SeqOffsets;
