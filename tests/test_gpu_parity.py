@@ -129,6 +129,38 @@ def test_score_c3_layer():
     check_scores(got, want, "c3/l5")
 
 
+def test_score_and_select_c4_layer_sampled():
+    # the full ragged c4 layer (8 sequences of 16K-32K rows, 64-tile walks as in the
+    # 32-layer launch) on the GPU; the oracle scores two of its sequences, and the
+    # selection of those sequences must pass the end-to-end threshold rule
+    wl = di.WORKLOADS["c4"]
+    _log("score + select parity: c4 layer, sequences 0 and 7 sampled")
+    x = di.make_layer(wl, with_v=False)
+    g = geom_of(wl)
+    raw = dge.score(g, oracle.ROWS_WINDOW_DRAFT, to_dev(x.q_bits, "bf16"), to_dev(x.k_bits, "bf16"))
+    n_tail = wl.window + wl.k_draft
+    nsel = wl.budget - wl.window
+    idx, nk = dge.select_topb(g, raw, wl.pool, n_tail, nsel)
+    torch.cuda.synchronize()
+    raw, idx, nk = raw.cpu().numpy(), idx.cpu().numpy(), nk.cpu().numpy()
+    nr = n_tail
+    for b in (0, 7):
+        s0, s1 = int(wl.kv_offsets[b]), int(wl.kv_offsets[b + 1])
+        want = oracle.window_scores(x.q[:, b * nr:(b + 1) * nr], x.k[:, s0:s1], [0, s1 - s0],
+                                    wl.n_q_heads, wl.n_kv_heads, wl.window, wl.k_draft)
+        check_scores(raw[:, s0:s1], want, f"c4 sequence {b}")
+        C = s1 - s0 - n_tail
+        assert nk[b] == min(nsel, C)
+        for h in range(wl.n_kv_heads):
+            pooled = oracle.maxpool(want[h], C, wl.pool)
+            t = np.sort(pooled)[::-1][nsel - 1]
+            got = set(idx[b, h].tolist())
+            assert len(got) == nsel
+            must = set(np.nonzero(pooled > t * (1 + 1e-3))[0].tolist())
+            never = set(np.nonzero(pooled < t * (1 - 1e-3))[0].tolist())
+            assert must <= got and not (never & got), (b, h)
+
+
 def test_score_layer_major_long_walks():
     # eight copies of a c3 layer scored as one layer-major geometry (64 KV heads): every
     # workgroup walks the longest chunk (64 tiles of 64 keys); each copy must match the
