@@ -127,6 +127,23 @@ def test_score_c3_layer():
     x = di.make_layer(wl, layer=5, with_v=False)
     got, want = run_score(wl, x)
     check_scores(got, want, "c3/l5")
+    # selection of that layer under its own budget, end to end by the threshold rule
+    g = geom_of(wl)
+    n_tail = wl.window + wl.k_draft
+    nsel = wl.budget_of_layer(5) - wl.window
+    idx, nk = dge.select_topb(g, torch.from_numpy(np.ascontiguousarray(got)).to(DEV), wl.pool,
+                              n_tail, nsel)
+    torch.cuda.synchronize()
+    idx = idx.cpu().numpy()
+    C = wl.cached_lens[0] - n_tail
+    for h in range(wl.n_kv_heads):
+        pooled = oracle.maxpool(want[h], C, wl.pool)
+        t = np.sort(pooled)[::-1][nsel - 1]
+        sel = set(idx[0, h].tolist())
+        assert len(sel) == nsel
+        must = set(np.nonzero(pooled > t * (1 + 1e-3))[0].tolist())
+        never = set(np.nonzero(pooled < t * (1 - 1e-3))[0].tolist())
+        assert must <= sel and not (never & sel), h
 
 
 def test_score_and_select_c4_layer_sampled():
