@@ -344,3 +344,26 @@ def retained_runs(idx) -> tuple:
             runs += 1
     return runs, len(pos) / runs
 
+
+def rope(x, positions, theta: float = 500000.0) -> np.ndarray:
+    """Rotary position embedding of the query/key rows, the step that produces the
+    post-RoPE Q and K the scoring reads (App. "Draft-guided eviction implementation":
+    queries recomputed post-RoPE from each layer's input; App. on the compensation token:
+    rotate-half pairs (i, i + d/2); Table "Backbones": theta = 500,000).
+
+    x: [..., n_rows, d] (any leading dims), positions: [n_rows].  Pair i of a row at
+    position p, i < d/2, is rotated by the angle p * theta^(-2i/d):
+        x_i'       = x_i cos - x_{i+d/2} sin
+        x_{i+d/2}' = x_{i+d/2} cos + x_i sin
+    Returns float64.
+    """
+    x = as_f64(x)
+    d = x.shape[-1]
+    half = d // 2
+    pos = np.asarray(positions, np.float64)
+    inv = theta ** (-2.0 * np.arange(half, dtype=np.float64) / d)
+    ang = pos[:, None] * inv[None, :]                 # [n_rows, d/2]
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+

@@ -504,3 +504,33 @@ def test_maxpool_plateau_is_one_run():
         width = min(C - 1, j + kappa // 2) - max(0, j - kappa // 2) + 1
         idx = oracle.select_topb(pooled, width)
         assert oracle.retained_runs(idx) == (1, float(width))
+
+
+def test_rope_hand_example_pairs_and_frequencies():
+    # d = 4, theta = 10000, p = 1: pair (x0, x2) turns by 1 rad, pair (x1, x3) by
+    # 10000^(-2/4) = 0.01 rad (rotate-half pairing; the lowest index has the fastest turn)
+    got = oracle.rope(np.array([[1.0, 2.0, 3.0, 4.0]]), [1], theta=10000.0)[0]
+    c1, s1, c2, s2 = math.cos(1.0), math.sin(1.0), math.cos(0.01), math.sin(0.01)
+    want = [1 * c1 - 3 * s1, 2 * c2 - 4 * s2, 3 * c1 + 1 * s1, 4 * c2 + 2 * s2]
+    assert np.allclose(got, want, rtol=0, atol=1e-15)
+
+
+def test_rope_is_a_complex_phase_and_keeps_relative_positions():
+    rng = np.random.default_rng(21)
+    d, n = 128, 6
+    x = rng.standard_normal((3, n, d))
+    pos = np.array([0, 1, 7, 300, 4097, 32767])
+    got = oracle.rope(x, pos)
+    # as complex numbers z = x_i + i x_{i+d/2}, each pair is multiplied by exp(i p theta_i)
+    z = x[..., :d // 2] + 1j * x[..., d // 2:]
+    ph = np.exp(1j * pos[:, None] * 500000.0 ** (-np.arange(d // 2) * 2.0 / d))
+    w = z * ph
+    assert np.allclose(got, np.concatenate([w.real, w.imag], axis=-1), rtol=0, atol=1e-9)
+    assert np.array_equal(got[:, 0], x[:, 0])                      # position 0: identity
+    assert np.allclose(np.linalg.norm(got, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-12)
+    # the logit of a rotated query/key pair depends on the position difference only
+    q, k = rng.standard_normal(d), rng.standard_normal(d)
+    def logit(p, s):
+        return float(oracle.rope(q[None], [p])[0] @ oracle.rope(k[None], [s])[0])
+    assert math.isclose(logit(50, 20), logit(1050, 1020), rel_tol=1e-10)
+    assert math.isclose(logit(7, 7), float(q @ k), rel_tol=1e-10)
