@@ -70,6 +70,9 @@ def parse():
                    help="single-layer workloads: run independent steps (different buffer sets, "
                         "i.e. different requests' layers) on this many streams at once; reported "
                         "on its own line, the default bench keeps one stream")
+    p.add_argument("--rope", action="store_true",
+                   help="only time dge_rope on the workload's keys (every cached row of every KV "
+                        "head), HIP events per call; one JSON line with its HBM rate")
     p.add_argument("--compact-cmp", action="store_true",
                    help="only time dge_compact (out of place) against dge_compact_inplace on one "
                         "layer of the workload, the cache restored outside the timed events")
@@ -105,6 +108,8 @@ def main():
     x = di.make_layer(wl, with_v=True)
     if args.compact_cmp:
         return bench_compact_cmp(args, wl, x, dev)
+    if args.rope:
+        return bench_rope(args, wl, x, dev)
     if args.repeat_kv:
         return bench_repeat_kv(args, wl, x, dev)
     if args.streams > 1:
@@ -512,6 +517,37 @@ def bench_streams(args, wl, x, dev):
         "concurrent_steps": n, "workload": WORKLOAD_TEXT.get(wl.name, wl.name),
         "step": "dge_score -> dge_select_compact; independent steps on separate streams"}),
         flush=True)
+
+
+def bench_rope(args, wl, x, dev):
+    """dge_rope over every cached key row of one layer (the K the scoring reads), in place,
+    each call bracketed by HIP events (median of the repetitions).  Elementwise: the
+    roofline is one read and one write of K."""
+    import torch
+    import paper_2609_33334_amd as dge
+
+    k = torch.from_numpy(np.ascontiguousarray(x.k_bits)).view(torch.int16).view(torch.bfloat16).to(dev)
+    T = k.shape[1]
+    pos = torch.arange(T, dtype=torch.int32, device=dev)
+    for _ in range(3):
+        dge.rope(k, pos)
+    torch.cuda.synchronize()
+    reps = max(20, min(args.steps, 200))
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dge.rope(k, pos)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e3)
+    us = float(np.median(ts))
+    nbytes = 2 * k.numel() * 2
+    print(json.dumps({"kernel": "dge_rope (keys of one layer, in place)", "workload": wl.name,
+                      "rows": int(k.shape[0] * T), "bytes": nbytes, "us_per_call": round(us, 3),
+                      "GBps": round(nbytes / us / 1e3, 1),
+                      "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "reps": reps}),
+          flush=True)
 
 
 def bench_compact_cmp(args, wl, x, dev):

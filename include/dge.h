@@ -257,6 +257,24 @@ dge_status_t dge_cache_attention(const dge_geom_t *geom, const void *q, int32_t 
                                  int32_t n_select, int32_t n_tail, const int32_t *n_kept,
                                  float *out, float *lse, hipStream_t stream);
 
+/* Rotary position embedding of query or key rows, in place (the post-RoPE Q and K the
+ * scoring reads; App. "Draft-guided eviction implementation": queries recomputed post-RoPE
+ * from each layer's input; rotate-half pairs (i, i + d/2) as in the compensation-token
+ * appendix; theta = 500,000 for the Table "Backbones" models).  For head h, row r with
+ * position p = positions[r], and pair i < head_dim/2:
+ *   x_i       <- x_i cos(p w_i) - x_{i+d/2} sin(p w_i)
+ *   x_{i+d/2} <- x_{i+d/2} cos(p w_i) + x_i sin(p w_i),     w_i = theta^(-2i/head_dim)
+ * computed in double and rounded once to the stored type (bf16: round to nearest even).
+ *   x         : [n_heads][head_stride] elements, row r of head h at h*head_stride + r*head_dim
+ *               (the Q layout [H_q][rows][d] or the K layout [H_kv][T][d]); 16-byte aligned.
+ *   positions : [n_rows] int32 device array (the rows' absolute positions).
+ * Errors: DGE_ERR_INVALID for n_heads < 1, n_rows < 0, theta <= 1 or not finite,
+ * head_stride < n_rows * head_dim, a bad dtype or a NULL / misaligned pointer;
+ * DGE_ERR_UNSUPPORTED for an odd head_dim or one above 128. */
+dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t dtype,
+                      int64_t head_stride, const int32_t *positions, double theta, void *x,
+                      hipStream_t stream);
+
 /* Contiguity of the retained sets (Sec. 4, "Selection trades coverage for contiguity";
  * Table "Selection decomposition", column "run len."): for sequence b and KV head h,
  *   runs[b][h]     = number of maximal runs of consecutive positions among the first

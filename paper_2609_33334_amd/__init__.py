@@ -25,7 +25,7 @@ from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  
 __all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact",
            "select_compact_layers", "select_streaming", "compact", "compact_inplace",
            "cache_attention",
-           "retained_runs", "h2o_colsum",
+           "rope", "retained_runs", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
 
@@ -268,6 +268,18 @@ def cache_attention(geom: Geometry, q, n_q: int, q_from_end: int, k_c, v_c, n_se
                                               _ptr(n_kept), _ptr(out), _ptr(lse),
                                               _stream(stream)), "dge_cache_attention")
     return out, lse
+
+
+def rope(x, positions, theta: float = 500000.0, stream=None):
+    """dge_rope: rotary position embedding of the rows of x ([heads][rows][head_dim],
+    bf16 or float32, contiguous) at the given int32 positions, in place.  Returns x."""
+    torch = _torch()
+    assert x.dim() == 3 and x.is_contiguous()
+    dt = DGE_BF16 if x.dtype == torch.bfloat16 else DGE_F32
+    _lib.check(_lib.lib().dge_rope(x.shape[0], x.shape[1], x.shape[2], dt,
+                                   x.shape[1] * x.shape[2], _ptr(positions), float(theta),
+                                   _ptr(x), _stream(stream)), "dge_rope")
+    return x
 
 
 def retained_runs(geom: Geometry, idx, n_kept, runs=None, mean_len=None, stream=None):

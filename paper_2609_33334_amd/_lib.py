@@ -7,7 +7,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_int, c_int32, c_int64, c_size_t, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_int, c_int32, c_int64, c_size_t, c_void_p
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdge.so")
 
@@ -21,7 +21,7 @@ ABI_VERSION = 1
 EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_score", "dge_score_lse",
            "dge_select_topb", "dge_select_compact", "dge_select_compact_layers",
            "dge_select_streaming", "dge_compact", "dge_compact_inplace",
-           "dge_cache_attention", "dge_retained_runs", "dge_h2o_colsum",
+           "dge_cache_attention", "dge_rope", "dge_retained_runs", "dge_h2o_colsum",
            "dge_pyramid_budgets")
 
 
@@ -96,6 +96,9 @@ def lib() -> ctypes.CDLL:
                                       c_int32, c_void_p, c_void_p, c_void_p, c_void_p]
     L.dge_h2o_colsum.argtypes = [GP, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                  c_void_p]
+    L.dge_rope.restype = c_int
+    L.dge_rope.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int64, c_void_p, c_double,
+                           c_void_p, c_void_p]
     L.dge_retained_runs.restype = c_int
     L.dge_retained_runs.argtypes = [GP, c_void_p, c_void_p, c_int32, c_void_p, c_void_p, c_void_p]
     L.dge_pyramid_budgets.restype = c_int

@@ -228,6 +228,20 @@ dge_status_t dge_compact_inplace(const dge_geom_t* geom, const int32_t* idx,
   return hip_status(dge::launch_compact_inplace(*geom, idx, n_kept, n_select, n_tail, k, v, stream));
 }
 
+dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t dtype,
+                      int64_t head_stride, const int32_t* positions, double theta, void* x,
+                      hipStream_t stream) {
+  if (n_heads < 1 || n_rows < 0 || n_rows > kMaxRows) return DGE_ERR_INVALID;
+  if (head_dim < 2 || head_dim > 128 || (head_dim & 1)) return DGE_ERR_UNSUPPORTED;
+  if (dtype != DGE_BF16 && dtype != DGE_F32) return DGE_ERR_INVALID;
+  if (!(theta > 1.0) || !(theta < 1e300)) return DGE_ERR_INVALID;
+  if (head_stride < (int64_t)n_rows * head_dim) return DGE_ERR_INVALID;
+  if (n_rows > 0 && (!positions || !x)) return DGE_ERR_INVALID;
+  if ((reinterpret_cast<uintptr_t>(positions) & 3) || !aligned16(x)) return DGE_ERR_INVALID;
+  return hip_status(
+      dge::launch_rope(n_heads, n_rows, head_dim, dtype, head_stride, positions, theta, x, stream));
+}
+
 dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t n_q,
                                  int32_t q_from_end, const void* k_c, const void* v_c,
                                  int32_t n_select, int32_t n_tail, const int32_t* n_kept,

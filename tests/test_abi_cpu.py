@@ -229,3 +229,20 @@ def test_row_counts_bounded(L):
     ns = (ctypes.c_int32 * 2)(10, big)
     assert L.dge_select_compact_layers(g.p, 2, FAKE, 7, 10, ns, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                        FAKE, 1 << 40, None) == _lib.DGE_ERR_INVALID
+
+
+def test_rope_validation(L):
+    pos = FAKE
+    def call(h=4, n=10, d=128, dt=0, stride=1280, p=pos, theta=500000.0, x=FAKE):
+        return L.dge_rope(h, n, d, dt, stride, p, theta, x, None)
+    assert call(h=0) == _lib.DGE_ERR_INVALID
+    assert call(n=-1) == _lib.DGE_ERR_INVALID
+    assert call(d=127) == _lib.DGE_ERR_UNSUPPORTED
+    assert call(d=256, stride=2560) == _lib.DGE_ERR_UNSUPPORTED
+    assert call(dt=7) == _lib.DGE_ERR_INVALID
+    assert call(theta=1.0) == _lib.DGE_ERR_INVALID
+    assert call(theta=float("nan")) == _lib.DGE_ERR_INVALID
+    assert call(stride=1279) == _lib.DGE_ERR_INVALID
+    assert call(p=None) == _lib.DGE_ERR_INVALID
+    assert call(x=FAKE + 2) == _lib.DGE_ERR_INVALID
+    assert call(n=0, p=None, x=None) == _lib.DGE_OK            # nothing to rotate, nothing launched

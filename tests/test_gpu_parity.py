@@ -739,3 +739,40 @@ def test_repeated_kv_layout_per_query_head():
             ref_k = k_rep[h, offs[b] + rows]
             assert np.array_equal(k_out[b, h, :len(rows)].view(torch.int16).cpu().numpy(),
                                   ref_k.view(np.int16)), (b, h)
+
+
+# ----------------------------------------------------------------------------------
+# Rotary position embedding of the query/key rows (dge_rope) against the oracle
+# ----------------------------------------------------------------------------------
+@pytest.mark.parametrize("case", ["bf16_d128", "f32_d64", "bf16_long_positions"])
+def test_rope_parity(case):
+    _log(f"rope parity {case}")
+    rng = np.random.default_rng(np.random.SeedSequence([31, len(case)]))
+    H, n, d, dt = {"bf16_d128": (8, 300, 128, "bf16"), "f32_d64": (4, 257, 64, "f32"),
+                   "bf16_long_positions": (2, 130, 128, "bf16")}[case]
+    x = rng.standard_normal((H, n, d), dtype=np.float32) * 2.0
+    if case == "bf16_long_positions":
+        pos = np.sort(rng.integers(0, 1 << 20, size=n)).astype(np.int32)
+    else:
+        pos = np.arange(n, dtype=np.int32) + 17
+    if dt == "bf16":
+        xt = torch.from_numpy(x).to(torch.bfloat16)
+        x_in = xt.float().numpy().astype(np.float64)      # the stored bf16 values
+        xd = xt.to(DEV)
+    else:
+        x_in = x.astype(np.float64)
+        xd = torch.from_numpy(x).to(DEV)
+    dge.rope(xd, torch.from_numpy(pos).to(DEV))
+    torch.cuda.synchronize()
+    got = xd.float().cpu().numpy().astype(np.float64)
+    want = oracle.rope(x_in, pos)
+    # one rounding to the stored type: half an ulp, plus the double-to-float step for bf16
+    ulp = 2.0 ** -8 if dt == "bf16" else 2.0 ** -23
+    tol = ulp * np.maximum(np.abs(want), 2.0 ** -126)
+    bad = np.abs(got - want) > tol
+    assert not bad.any(), (case, int(bad.sum()), float(np.abs(got - want).max()))
+    # rotations keep every pair's length
+    half = d // 2
+    r_in = np.hypot(x_in[..., :half], x_in[..., half:])
+    r_out = np.hypot(got[..., :half], got[..., half:])
+    assert np.allclose(r_out, r_in, rtol=2 * ulp, atol=1e-6)
