@@ -269,8 +269,9 @@ dge_status_t dge_cache_attention(const dge_geom_t *geom, const void *q, int32_t 
  *               (the Q layout [H_q][rows][d] or the K layout [H_kv][T][d]); 16-byte aligned.
  *   positions : [n_rows] int32 device array (the rows' absolute positions).
  * Errors: DGE_ERR_INVALID for n_heads < 1, n_rows < 0, theta <= 1 or not finite,
- * head_stride < n_rows * head_dim, a bad dtype or a NULL / misaligned pointer;
- * DGE_ERR_UNSUPPORTED for an odd head_dim or one above 128. */
+ * head_stride < n_rows * head_dim or a head stride that is not a multiple of 8 bytes, a
+ * bad dtype or a NULL / misaligned pointer; DGE_ERR_UNSUPPORTED for a head_dim that is not
+ * a multiple of 4 or is above 128. */
 dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t dtype,
                       int64_t head_stride, const int32_t *positions, double theta, void *x,
                       hipStream_t stream);

@@ -232,10 +232,11 @@ dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t
                       int64_t head_stride, const int32_t* positions, double theta, void* x,
                       hipStream_t stream) {
   if (n_heads < 1 || n_rows < 0 || n_rows > kMaxRows) return DGE_ERR_INVALID;
-  if (head_dim < 2 || head_dim > 128 || (head_dim & 1)) return DGE_ERR_UNSUPPORTED;
+  if (head_dim < 4 || head_dim > 128 || (head_dim & 3)) return DGE_ERR_UNSUPPORTED;
   if (dtype != DGE_BF16 && dtype != DGE_F32) return DGE_ERR_INVALID;
   if (!(theta > 1.0) || !(theta < 1e300)) return DGE_ERR_INVALID;
   if (head_stride < (int64_t)n_rows * head_dim) return DGE_ERR_INVALID;
+  if ((head_stride * (dtype == DGE_BF16 ? 2 : 4)) % 8 != 0) return DGE_ERR_INVALID;  // 8-byte aligned heads
   if (n_rows > 0 && (!positions || !x)) return DGE_ERR_INVALID;
   if ((reinterpret_cast<uintptr_t>(positions) & 3) || !aligned16(x)) return DGE_ERR_INVALID;
   return hip_status(

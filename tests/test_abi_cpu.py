@@ -238,6 +238,8 @@ def test_rope_validation(L):
     assert call(h=0) == _lib.DGE_ERR_INVALID
     assert call(n=-1) == _lib.DGE_ERR_INVALID
     assert call(d=127) == _lib.DGE_ERR_UNSUPPORTED
+    assert call(d=66, stride=660) == _lib.DGE_ERR_UNSUPPORTED      # head_dim not a multiple of 4
+    assert call(stride=1281) == _lib.DGE_ERR_INVALID               # heads not 8-byte aligned
     assert call(d=256, stride=2560) == _lib.DGE_ERR_UNSUPPORTED
     assert call(dt=7) == _lib.DGE_ERR_INVALID
     assert call(theta=1.0) == _lib.DGE_ERR_INVALID
