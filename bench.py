@@ -48,12 +48,23 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def graph_steps(steps: int, sets: int) -> int:
+    """Steps per captured graph: the largest of GRAPH_STEPS, 4, 2, 1 that divides both the
+    requested step count (so exactly that many are timed) and the number of buffer sets."""
+    for g in (GRAPH_STEPS, 4, 2, 1):
+        if steps % g == 0 and sets % g == 0:
+            return g
+    return 1
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=4000)
-    p.add_argument("--warmup", type=int, default=64)
-    p.add_argument("--workload", default="c2")
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="c4",
+                   help="c1..c5 (default c4, the largest single-GPU configuration: 32 layers, "
+                        "a ragged batch of 8 sequences of 16K-32K tokens)")
     p.add_argument("--sets", type=int, default=48)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-cal", action="store_true",
@@ -145,10 +156,30 @@ def main():
     ws_score = torch.empty(dge.workspace_size(geom_all, dge.OP_SCORE), dtype=torch.uint8, device=dev)
     ws_sel = torch.empty(dge.workspace_size(geom, dge.OP_SELECT), dtype=torch.uint8, device=dev)
     sets = []     # sets[set] = (q_all, k_all, v_all, raw_all, per-layer [(q, k, v, out, budget)])
+    nr = wl.window + wl.k_draft
     for i in range(S):
-        q_all = q0.repeat(L_layers, 1, 1)
-        k_all = k0.repeat(L_layers, 1, 1)
-        v_all = v0.repeat(L_layers, 1, 1)
+        if L_layers == 1:
+            q_all, k_all, v_all = q0.clone(), k0.clone(), v0.clone()
+        else:
+            # every layer its own inputs: layer 0 is the seeded host layer the oracle checks,
+            # the others are drawn per layer (planted workloads on the host with their own
+            # seeds, unplanted ones on the device)
+            q_all = torch.empty(Hq * L_layers, geom.batch * nr, wl.head_dim, dtype=q0.dtype, device=dev)
+            k_all = torch.empty(Hkv * L_layers, geom.total_rows, wl.head_dim, dtype=k0.dtype, device=dev)
+            v_all = torch.empty_like(k_all)
+            for l in range(L_layers):
+                if l == 0:
+                    ql, kl, vl = q0, k0, v0
+                elif wl.plant == "none":
+                    ql, kl, vl = di.device_layer(wl, l, dev)
+                else:
+                    xl = di.make_layer(wl, layer=l)
+                    ql, kl, vl = dev_t(xl.q_bits), dev_t(xl.k_bits), dev_t(xl.v_bits)
+                q_all[l * Hq:(l + 1) * Hq] = ql
+                k_all[l * Hkv:(l + 1) * Hkv] = kl
+                v_all[l * Hkv:(l + 1) * Hkv] = vl
+                del ql, kl, vl
+            log(f"[bench] {L_layers} layers generated")
         raw_all = torch.empty(Hkv * L_layers, geom.total_rows, dtype=torch.float32, device=dev)
         # outputs packed layer after layer (the layout of dge_select_compact_layers)
         nb = geom.batch * Hkv
@@ -177,22 +208,22 @@ def main():
     torch.cuda.synchronize()
     row_lse = None
     if args.lse:
-        # natural-log softmax normaliser of each scoring row over keys j <= p (fp32, torch)
-        # (per sequence of the batch; rows in the order of q: [H_q][batch * n_rows])
-        nr = wl.window + wl.k_draft
+        # natural-log softmax normaliser of each scoring row over keys j <= p (fp32, torch),
+        # per layer and sequence; rows in the order of q: [layer * H_q][batch * n_rows]
         G = wl.group
-        parts = []
-        for b, N in enumerate(wl.cached_lens):
-            off = int(wl.kv_offsets[b])
-            qq = q0[:, b * nr:(b + 1) * nr].float()
-            kk = k0[:, off:off + N].float().repeat_interleave(G, dim=0)
-            x = torch.einsum("hrd,hnd->hrn", qq, kk) / (wl.head_dim ** 0.5)
-            pos = torch.arange(N - nr, N, device=dev)
-            x = x.masked_fill(torch.arange(N, device=dev)[None, None, :] > pos[None, :, None],
-                              float("-inf"))
-            parts.append(torch.logsumexp(x, dim=2))
-            del x, kk, qq
-        row_lse = torch.cat(parts, dim=1).repeat(L_layers, 1).contiguous()
+        q_all0, k_all0 = sets[0][0], sets[0][1]
+        row_lse = torch.empty(Hq * L_layers, geom.batch * nr, dtype=torch.float32, device=dev)
+        for l in range(L_layers):
+            for b, N in enumerate(wl.cached_lens):
+                off = int(wl.kv_offsets[b])
+                qq = q_all0[l * Hq:(l + 1) * Hq, b * nr:(b + 1) * nr].float()
+                kk = k_all0[l * Hkv:(l + 1) * Hkv, off:off + N].float().repeat_interleave(G, dim=0)
+                xx = torch.matmul(qq, kk.transpose(1, 2).contiguous()) / (wl.head_dim ** 0.5)
+                pos = torch.arange(N - nr, N, device=dev)
+                xx = xx.masked_fill(torch.arange(N, device=dev)[None, None, :] > pos[None, :, None],
+                                    float("-inf"))
+                row_lse[l * Hq:(l + 1) * Hq, b * nr:(b + 1) * nr] = torch.logsumexp(xx, dim=2)
+                del xx, kk, qq
 
     def score_call(i):
         q_all, k_all, _, raw_all, _, _ = sets[i % S]
@@ -226,8 +257,9 @@ def main():
     outs0 = dict(sets[0][5], raw=sets[0][3])
     ref = {kk: vv.clone() for kk, vv in outs0.items()}
 
-    # HIP graphs of GRAPH_STEPS consecutive steps, covering every buffer set
-    gsteps = GRAPH_STEPS if L_layers == 1 else 1
+    # HIP graphs of gsteps consecutive steps, covering every buffer set; gsteps divides
+    # --steps, so exactly the requested number of steps is timed
+    gsteps = graph_steps(args.steps, S) if L_layers == 1 else 1
     stream = torch.cuda.Stream()
     graphs, sgraphs = [], []
     n_graphs = max(1, S // gsteps)
@@ -254,8 +286,7 @@ def main():
         assert torch.equal(outs0[kk], ref[kk]), f"graph replay differs from eager ({kk})"
 
     K = args.steps
-    n_rep = (K + gsteps - 1) // gsteps
-    K = n_rep * gsteps
+    n_rep = K // gsteps
     for r in range(min(n_rep, 2 * n_graphs)):
         graphs[r % n_graphs].replay()
     torch.cuda.synchronize()
@@ -387,7 +418,7 @@ def bench_repeat_kv(args, wl, x, dev):
     for i in range(max(args.warmup, S)):
         step(i)
     torch.cuda.synchronize()
-    gsteps = GRAPH_STEPS
+    gsteps = graph_steps(args.steps, S)
     stream = torch.cuda.Stream()
     graphs = []
     with torch.cuda.stream(stream):
@@ -398,7 +429,7 @@ def bench_repeat_kv(args, wl, x, dev):
                     step(gi * gsteps + j)
             graphs.append(gr)
     torch.cuda.synchronize()
-    n_rep = (args.steps + gsteps - 1) // gsteps
+    n_rep = args.steps // gsteps
     K = n_rep * gsteps
     for r in range(min(n_rep, 2 * len(graphs))):
         graphs[r % len(graphs)].replay()
@@ -652,14 +683,15 @@ def bench_h2o(args, wl, x, dev):
     torch.cuda.synchronize()
     ref = {kk: vv.clone() for kk, vv in sets[0][3].items()}
     stream = torch.cuda.Stream()
+    gs = graph_steps(args.steps, S)      # steps per graph, dividing --steps
     with torch.cuda.stream(stream):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
-            for j in range(S):
+            for j in range(gs):
                 step(j)
         sg = torch.cuda.CUDAGraph()
         with torch.cuda.graph(sg, stream=stream):
-            for j in range(S):
+            for j in range(gs):
                 h2o_only(j)
     torch.cuda.synchronize()
     for kk in ref:
@@ -669,8 +701,8 @@ def bench_h2o(args, wl, x, dev):
     torch.cuda.synchronize()
     for kk in ref:
         assert torch.equal(sets[0][3][kk], ref[kk]), f"graph replay differs from eager ({kk})"
-    n_rep = max(1, (args.steps + S - 1) // S)
-    K = n_rep * S
+    n_rep = max(1, args.steps // gs)
+    K = n_rep * gs
     g.replay()
     torch.cuda.synchronize()
 
@@ -684,7 +716,7 @@ def bench_h2o(args, wl, x, dev):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / K
 
-    log(f"[bench] timing {K} H2O steps ({n_rep} replays of {S})")
+    log(f"[bench] timing {K} H2O steps ({n_rep} replays of {gs})")
     ms_per_step = timed(g)
     h2o_ms = timed(sg)
     N = wl.cached_lens[0]
@@ -720,17 +752,15 @@ def cpu_baseline_h2o(wl, x, seconds):
     """The float64 oracle's H2O colsum on a bounded sample: the query heads of the first
     KV head (one GQA group), scaled to all 8 KV heads."""
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        cores = 1
+    from threadpoolctl import threadpool_limits
+    cores = cpu_threads()
     G = wl.group
     q = x.q_all[:G]
     k = x.k[:1]
-    t0 = time.perf_counter()
-    oracle.h2o_colsum(q, k, wl.kv_offsets, G, 1)
-    el = time.perf_counter() - t0
+    with threadpool_limits(limits=cores):
+        t0 = time.perf_counter()
+        oracle.h2o_colsum(q, k, wl.kv_offsets, G, 1)
+        el = time.perf_counter() - t0
     N = wl.cached_lens[0]
     rate = N / el                      # one KV head of N tokens in el seconds
     log(f"[bench] cpu oracle: one GQA group of H2O colsum in {el:.1f}s -> {rate:.3g} token*kvhead/s")
@@ -773,49 +803,70 @@ def measured_traffic(workload: str, lse: bool, layers_per_call: int):
     return rec.get("hbm_bytes_per_call")
 
 
-def cpu_baseline(wl, x, seconds):
-    """The float64 oracle, untuned, on this host's cores: repeats of the same layer."""
-    import oracle
+def cpu_threads() -> int:
+    """Host threads the oracle may use: this process's CPU affinity, capped by
+    OMP_NUM_THREADS when that is set (the GPU host's share of cores)."""
+    n = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        cores = 1
-    L = sum(wl.prompt_lens)
-    budget = wl.budget_of_layer(0)
-    reps = 0
+        cap = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        cap = 0
+    return min(n, cap) if cap > 0 else n
+
+
+def _oracle_sample(wl, x):
+    """The bounded sample of a workload the CPU oracle is timed on, as a list of
+    (workload, layer inputs) and its description: whole layers for c1/c2, four distinct
+    layers for c3, sequence 0 of layers 0 and 1 for c4 (same seeds as in the full batch)."""
+    import dge_inputs as di
+    if wl.n_layers == 1:
+        return [(wl, x)], f"one {wl.name} layer"
+    if wl.batch == 1:
+        return ([(wl, x)] + [(wl, di.make_layer(wl, layer=l)) for l in (1, 2, 3)],
+                f"layers 0-3 of {wl.name}")
+    w1 = di.small_variant(wl.name, [wl.prompt_lens[0]], name=f"{wl.name}_seq0")
+    return ([(w1, di.make_layer(w1, layer=l)) for l in (0, 1)],
+            f"sequence 0 (L={wl.prompt_lens[0]}) of layers 0 and 1 of {wl.name}")
+
+
+def _time_oracle(sample, seconds):
+    import oracle
+    reps = units = 0
     t0 = time.perf_counter()
     while True:
-        oracle.evict_layer(x.q, x.k, x.v, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
-                           wl.k_draft, budget, wl.pool)
+        w, xl = sample[reps % len(sample)]
+        oracle.evict_layer(xl.q, xl.k, xl.v, w.kv_offsets, w.n_q_heads, w.n_kv_heads, w.window,
+                           w.k_draft, w.budget_of_layer(xl.layer), w.pool)
         reps += 1
+        units += sum(w.prompt_lens) * w.n_kv_heads
         el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    rate = reps * L * wl.n_kv_heads / el
-    log(f"[bench] cpu oracle: {reps} layers in {el:.1f}s -> {rate:.3g} token*kvhead/s")
-    # the same oracle on one core (BLAS limited to one thread), on a shorter sample
+        if el >= seconds and reps >= len(sample):
+            return reps, units, el
+
+
+def cpu_baseline(wl, x, seconds):
+    """The float64 oracle, untuned, on this host's cores, timed on a bounded sample of the
+    workload (score, pool, select, compact of each sampled layer); the rate is per prefix
+    token x KV head, and the whole step's time is extrapolated from it."""
+    from threadpoolctl import threadpool_limits
+    threads = cpu_threads()
+    sample, what = _oracle_sample(wl, x)
+    with threadpool_limits(limits=threads):
+        reps, units, el = _time_oracle(sample, seconds)
+    rate = units / el
+    step_units = sum(wl.prompt_lens) * wl.n_kv_heads * wl.n_layers
+    log(f"[bench] cpu oracle ({threads} threads): {reps} layer passes over {what} in {el:.1f}s "
+        f"-> {rate:.3g} token*kvhead/s")
     one = None
-    try:
-        from threadpoolctl import threadpool_limits
-        with threadpool_limits(limits=1):
-            reps1 = 0
-            t0 = time.perf_counter()
-            while True:
-                oracle.evict_layer(x.q, x.k, x.v, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
-                                   wl.window, wl.k_draft, budget, wl.pool)
-                reps1 += 1
-                el1 = time.perf_counter() - t0
-                if el1 >= seconds / 3:
-                    break
-        one = round(reps1 * L * wl.n_kv_heads / el1, 1)
-        log(f"[bench] cpu oracle, one core: {reps1} layers in {el1:.1f}s -> {one:.3g} token*kvhead/s")
-    except Exception:  # pragma: no cover
-        pass
-    return {"value": round(rate, 1), "unit": "token*kvhead/s", "cores": cores, "kind": "oracle",
-            "sample": f"{reps} repeats of one {wl.name} layer (score, pool, select, compact; "
-                      f"budget {budget}) in float64 numpy, {el:.1f} s",
-            "value_one_core": one}
+    with threadpool_limits(limits=1):
+        r1, u1, e1 = _time_oracle(sample, seconds / 3)
+    one = round(u1 / e1, 1)
+    log(f"[bench] cpu oracle, one thread: {r1} layer passes in {e1:.1f}s -> {one:.3g} token*kvhead/s")
+    return {"value": round(rate, 1), "unit": "token*kvhead/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} passes over {what} (score, pool, select, compact; float64 numpy), "
+                      f"{el:.1f} s; the full step's {step_units} token*kvheads would take "
+                      f"{step_units / rate:.0f} s (extrapolated)",
+            "affinity_cpus": len(os.sched_getaffinity(0)), "value_one_core": one}
 
 
 if __name__ == "__main__":

@@ -250,3 +250,23 @@ def random_scores(shape, seed: int, kind: str = "continuous") -> np.ndarray:
         off = rng.integers(0, 3000, size=shape).astype(np.uint32)
         return (np.uint32(0x3F800000) + off).view(np.float32)
     raise ValueError(kind)
+
+
+def device_layer(wl: Workload, layer: int, device: str):
+    """One layer of a workload without planted structure (c4), drawn on the GPU: the same
+    distribution as make_layer (standard normal float32, rounded to nearest even bf16),
+    from torch's Philox generator seeded by (cfg_id, layer).  For benchmark layers beyond
+    the one the oracle checks, where drawing tens of GB on the host would take minutes.
+    Returns device tensors (q [H_q][batch*(w+k)][d], k, v [H_kv][T][d])."""
+    import torch
+    if wl.plant != "none" or wl.h2o:
+        raise ValueError("device_layer draws unplanted layers only")
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    gen = torch.Generator(device=device)
+    out = []
+    for tensor, shape in ((T_Q, (wl.n_q_heads, wl.batch * wl.n_rows, wl.head_dim)),
+                          (T_K, (wl.n_kv_heads, wl.total_rows, wl.head_dim)),
+                          (T_V, (wl.n_kv_heads, wl.total_rows, wl.head_dim))):
+        gen.manual_seed(int(np.random.SeedSequence([wl.cfg_id, layer, tensor]).generate_state(1)[0]))
+        out.append(torch.randn(shape, generator=gen, device=device, dtype=torch.float32).to(dt))
+    return tuple(out)

@@ -85,7 +85,42 @@ class Geometry:
 
 
 def _ptr(t) -> Optional[int]:
-    return None if t is None else t.data_ptr()
+    """Device address of a tensor handed to the library (None for NULL); a host tensor
+    is refused, since every pointer argument of the C ABI is a device pointer."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"a {tuple(t.shape)} tensor on {t.device} passed where the library "
+                         "needs a GPU tensor")
+    return t.data_ptr()
+
+
+def _need(t, name: str, dtypes, min_numel: int = 0, optional: bool = False):
+    """Argument check before anything reaches the library: a contiguous tensor of one of
+    the given dtypes with at least min_numel elements (the C ABI sees raw pointers only, so
+    a wrong element type or a short buffer would be misread).  The device is checked when
+    the pointer is taken (_ptr)."""
+    torch = _torch()
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name}: a tensor is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {[str(d) for d in dtypes]}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if t.numel() < min_numel:
+        raise ValueError(f"{name}: {t.numel()} elements, at least {min_numel} needed")
+
+
+def _f32():
+    return (_torch().float32,)
+
+
+def _i32():
+    return (_torch().int32,)
 
 
 def _stream(stream) -> int:
@@ -111,8 +146,13 @@ def _workspace(geom: Geometry, op: int, ws):
 def score(geom: Geometry, rows: int, q, k, raw=None, ws=None, stream=None):
     """dge_score: raw[h][j] for every cached key.  Returns raw [H_kv][T] float32."""
     torch = _torch()
+    nr = n_scoring_rows(geom.window, geom.k_draft, rows)
+    _need(q, "q", (geom.elt_dtype,), geom.n_q_heads * geom.batch * nr * geom.head_dim)
+    _need(k, "k", (geom.elt_dtype,), (geom.n_kv_heads - 1) * geom.kv_head_stride
+          + geom.total_rows * geom.head_dim)
     if raw is None:
         raw = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=geom.device)
+    _need(raw, "raw", _f32(), geom.n_kv_heads * geom.total_rows)
     ws = _workspace(geom, OP_SCORE, ws)
     _lib.check(_lib.lib().dge_score(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k), _ptr(raw),
                                     _ptr(ws), ws.numel(), _stream(stream)), "dge_score")
@@ -123,8 +163,14 @@ def score_lse(geom: Geometry, rows: int, q, k, row_lse, raw=None, stream=None):
     """dge_score_lse: dge_score with caller-supplied scoring-row log-sum-exp (one pass
     over K).  row_lse is [H_q][batch * n_rows] float32.  Returns raw [H_kv][T]."""
     torch = _torch()
+    nr = n_scoring_rows(geom.window, geom.k_draft, rows)
+    _need(q, "q", (geom.elt_dtype,), geom.n_q_heads * geom.batch * nr * geom.head_dim)
+    _need(k, "k", (geom.elt_dtype,), (geom.n_kv_heads - 1) * geom.kv_head_stride
+          + geom.total_rows * geom.head_dim)
+    _need(row_lse, "row_lse", _f32(), geom.n_q_heads * geom.batch * nr)
     if raw is None:
         raw = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=geom.device)
+    _need(raw, "raw", _f32(), geom.n_kv_heads * geom.total_rows)
     _lib.check(_lib.lib().dge_score_lse(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k), _ptr(row_lse),
                                         _ptr(raw), _stream(stream)), "dge_score_lse")
     return raw
@@ -139,6 +185,9 @@ def select_topb(geom: Geometry, scores, pool_kernel: int, n_tail: int, n_select:
                           device=geom.device)
     if n_kept is None:
         n_kept = torch.empty(max(geom.batch, 4), dtype=torch.int32, device=geom.device)
+    _need(scores, "scores", _f32(), geom.n_kv_heads * geom.total_rows)
+    _need(idx, "idx", _i32(), geom.batch * geom.n_kv_heads * max(n_select, 0))
+    _need(n_kept, "n_kept", _i32(), geom.batch)
     ws = _workspace(geom, OP_SELECT, ws)
     _lib.check(_lib.lib().dge_select_topb(ctypes.byref(geom.c), _ptr(scores), pool_kernel, n_tail,
                                           n_select, _ptr(idx), _ptr(n_kept), _ptr(ws), ws.numel(),
@@ -161,6 +210,15 @@ def select_compact(geom: Geometry, scores, pool_kernel: int, n_tail: int, n_sele
         k_out = torch.empty(shape, dtype=k.dtype, device=geom.device)
     if v_out is None:
         v_out = torch.empty(shape, dtype=v.dtype, device=geom.device)
+    kv_min = (geom.n_kv_heads - 1) * geom.kv_head_stride + geom.total_rows * geom.head_dim
+    _need(scores, "scores", _f32(), geom.n_kv_heads * geom.total_rows)
+    _need(idx, "idx", _i32(), geom.batch * geom.n_kv_heads * max(n_select, 0))
+    _need(n_kept, "n_kept", _i32(), geom.batch)
+    _need(k, "k", (geom.elt_dtype,), kv_min)
+    _need(v, "v", (geom.elt_dtype,), kv_min)
+    _need(k_out, "k_out", (geom.elt_dtype,), k_out_numel := geom.batch * geom.n_kv_heads
+          * (n_select + n_tail) * geom.head_dim)
+    _need(v_out, "v_out", (geom.elt_dtype,), k_out_numel)
     ws = _workspace(geom, OP_SELECT, ws)
     _lib.check(_lib.lib().dge_select_compact(ctypes.byref(geom.c), _ptr(scores), pool_kernel,
                                              n_tail, n_select, _ptr(idx), _ptr(n_kept), _ptr(k),
@@ -191,6 +249,14 @@ def select_compact_layers(geom: Geometry, scores, pool_kernel: int, n_tail: int,
         k_out = torch.empty(tot_rows, geom.head_dim, dtype=k.dtype, device=geom.device)
     if v_out is None:
         v_out = torch.empty(tot_rows, geom.head_dim, dtype=v.dtype, device=geom.device)
+    kv_min = ((nl * geom.n_kv_heads - 1) * geom.kv_head_stride + geom.total_rows * geom.head_dim)
+    _need(scores, "scores", _f32(), nl * geom.n_kv_heads * geom.total_rows)
+    _need(idx, "idx", _i32(), tot_idx)
+    _need(n_kept, "n_kept", _i32(), nl * geom.batch)
+    _need(k, "k", (geom.elt_dtype,), kv_min)
+    _need(v, "v", (geom.elt_dtype,), kv_min)
+    _need(k_out, "k_out", (geom.elt_dtype,), tot_rows * geom.head_dim)
+    _need(v_out, "v_out", (geom.elt_dtype,), tot_rows * geom.head_dim)
     ws = _workspace(geom, OP_SELECT, ws)
     arr = (ctypes.c_int32 * nl)(*n_sel)
     _lib.check(_lib.lib().dge_select_compact_layers(
@@ -235,6 +301,14 @@ def compact(geom: Geometry, idx, n_kept, n_select: int, n_tail: int, k, v, k_out
         k_out = torch.empty(shape, dtype=k.dtype, device=geom.device)
     if v_out is None:
         v_out = torch.empty(shape, dtype=v.dtype, device=geom.device)
+    kv_min = (geom.n_kv_heads - 1) * geom.kv_head_stride + geom.total_rows * geom.head_dim
+    _need(idx, "idx", _i32(), geom.batch * geom.n_kv_heads * max(n_select, 0))
+    _need(n_kept, "n_kept", _i32(), geom.batch)
+    _need(k, "k", (geom.elt_dtype,), kv_min)
+    _need(v, "v", (geom.elt_dtype,), kv_min)
+    _need(k_out, "k_out", (geom.elt_dtype,), n_out := geom.batch * geom.n_kv_heads
+          * (n_select + n_tail) * geom.head_dim)
+    _need(v_out, "v_out", (geom.elt_dtype,), n_out)
     _lib.check(_lib.lib().dge_compact(ctypes.byref(geom.c), _ptr(idx), _ptr(n_kept), n_select,
                                       n_tail, _ptr(k), _ptr(v), _ptr(k_out), _ptr(v_out),
                                       _stream(stream)), "dge_compact")
@@ -245,6 +319,11 @@ def compact_inplace(geom: Geometry, idx, n_kept, n_select: int, n_tail: int, k, 
                     stream=None):
     """dge_compact_inplace: the compacted rows overwrite the first n_kept[b] + n_tail rows
     of each (sequence, KV head) segment of k and v.  Returns (k, v)."""
+    kv_min = (geom.n_kv_heads - 1) * geom.kv_head_stride + geom.total_rows * geom.head_dim
+    _need(idx, "idx", _i32(), geom.batch * geom.n_kv_heads * max(n_select, 0))
+    _need(n_kept, "n_kept", _i32(), geom.batch)
+    _need(k, "k", (geom.elt_dtype,), kv_min)
+    _need(v, "v", (geom.elt_dtype,), kv_min)
     _lib.check(_lib.lib().dge_compact_inplace(ctypes.byref(geom.c), _ptr(idx), _ptr(n_kept),
                                               n_select, n_tail, _ptr(k), _ptr(v),
                                               _stream(stream)), "dge_compact_inplace")
@@ -263,6 +342,13 @@ def cache_attention(geom: Geometry, q, n_q: int, q_from_end: int, k_c, v_c, n_se
                           device=geom.device)
     if lse is None:
         lse = torch.empty(geom.n_q_heads, rows, dtype=torch.float32, device=geom.device)
+    n_c = geom.batch * geom.n_kv_heads * (n_select + n_tail) * geom.head_dim
+    _need(q, "q", (geom.elt_dtype,), geom.n_q_heads * rows * geom.head_dim)
+    _need(k_c, "k_c", (geom.elt_dtype,), n_c)
+    _need(v_c, "v_c", (geom.elt_dtype,), n_c)
+    _need(n_kept, "n_kept", _i32(), geom.batch)
+    _need(out, "out", _f32(), geom.n_q_heads * rows * geom.head_dim)
+    _need(lse, "lse", _f32(), geom.n_q_heads * rows)
     _lib.check(_lib.lib().dge_cache_attention(ctypes.byref(geom.c), _ptr(q), n_q, q_from_end,
                                               _ptr(k_c), _ptr(v_c), n_select, n_tail,
                                               _ptr(n_kept), _ptr(out), _ptr(lse),
@@ -274,7 +360,16 @@ def rope(x, positions, theta: float = 500000.0, stream=None):
     """dge_rope: rotary position embedding of the rows of x ([heads][rows][head_dim],
     bf16 or float32, contiguous) at the given int32 positions, in place.  Returns x."""
     torch = _torch()
-    assert x.dim() == 3 and x.is_contiguous()
+    if not isinstance(x, torch.Tensor) or x.dim() != 3:
+        raise ValueError("x: expected a [heads][rows][head_dim] tensor")
+    # element types first (an fp16 x would be read as float32, int64 positions as pairs
+    # of int32), then sizes and devices
+    if x.dtype not in (torch.bfloat16, torch.float32):
+        raise TypeError(f"x: dtype {x.dtype}; rope takes bfloat16 or float32 rows")
+    if not isinstance(positions, torch.Tensor) or positions.dtype != torch.int32:
+        raise TypeError("positions: expected an int32 tensor")
+    _need(x, "x", (torch.bfloat16, torch.float32))
+    _need(positions, "positions", _i32(), x.shape[1])
     dt = DGE_BF16 if x.dtype == torch.bfloat16 else DGE_F32
     _lib.check(_lib.lib().dge_rope(x.shape[0], x.shape[1], x.shape[2], dt,
                                    x.shape[1] * x.shape[2], _ptr(positions), float(theta),
@@ -293,6 +388,8 @@ def retained_runs(geom: Geometry, idx, n_kept, runs=None, mean_len=None, stream=
     if mean_len is None:
         mean_len = torch.empty(geom.batch, geom.n_kv_heads, dtype=torch.float32,
                                device=geom.device)
+    _need(idx, "idx", _i32(), geom.batch * geom.n_kv_heads * n_select)
+    _need(n_kept, "n_kept", _i32(), geom.batch)
     _lib.check(_lib.lib().dge_retained_runs(ctypes.byref(geom.c), _ptr(idx), _ptr(n_kept),
                                             n_select, _ptr(runs), _ptr(mean_len),
                                             _stream(stream)), "dge_retained_runs")
@@ -305,6 +402,11 @@ def h2o_colsum(geom: Geometry, q_all, k, lse=None, colsum=None, ws=None, stream=
     if colsum is None:
         colsum = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32,
                              device=geom.device)
+    _need(q_all, "q_all", (geom.elt_dtype,), geom.n_q_heads * geom.total_rows * geom.head_dim)
+    _need(k, "k", (geom.elt_dtype,), (geom.n_kv_heads - 1) * geom.kv_head_stride
+          + geom.total_rows * geom.head_dim)
+    _need(lse, "lse", _f32(), geom.n_q_heads * geom.total_rows, optional=True)
+    _need(colsum, "colsum", _f32(), geom.n_kv_heads * geom.total_rows)
     ws = _workspace(geom, OP_H2O, ws)
     nbytes = ws.numel()
     _lib.check(_lib.lib().dge_h2o_colsum(ctypes.byref(geom.c), _ptr(q_all), _ptr(k), _ptr(lse),

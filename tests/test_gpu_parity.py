@@ -63,6 +63,60 @@ def check_scores(got, want, what):
     assert not bad.any(), f"{what}: {int(bad.sum())} scores out of tolerance (worst rel {worst:.3g})"
 
 
+def oracle_select_compact(scores, k_bits, v_bits, lens, H, pool, n_tail, n_sel):
+    """The oracle's pool -> top-B' -> compact for every (sequence, KV head) of one layer,
+    on the given fp32 scores [H][T] and stored K/V element bits [H][T][d]:
+    {(b, h): (idx, k rows, v rows)}."""
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    out = {}
+    for b, N in enumerate(lens):
+        C = N - n_tail
+        seg = slice(offs[b], offs[b + 1])
+        for h in range(H):
+            pooled = oracle.maxpool(np.asarray(scores[h, seg], np.float64), C, pool)
+            sel = oracle.select_topb(pooled, n_sel)
+            out[(b, h)] = (sel,) + oracle.compact(k_bits[h, seg], v_bits[h, seg], sel, C)
+    return out
+
+
+def check_select_compact(idx, n_kept, k_out, v_out, want, n_sel, n_tail, what):
+    """GPU idx [batch][H][n_sel], n_kept [batch], K/V [batch][H][n_sel + n_tail][d] against
+    oracle_select_compact: bit-exact indices (-1 padded), exact counts, byte-exact rows
+    followed by zero rows."""
+    idx = idx.cpu().numpy()
+    n_kept = n_kept.cpu().numpy()
+    iv = torch.int16 if k_out.dtype == torch.bfloat16 else torch.int32
+    kg = k_out.cpu().view(iv).numpy()
+    vg = v_out.cpu().view(iv).numpy()
+    assert kg.shape[2] == n_sel + n_tail, what
+    for (b, h), (sel, ko, vo) in want.items():
+        assert n_kept[b] == len(sel), (what, b)
+        assert np.array_equal(idx[b, h, :len(sel)], sel), (what, b, h)
+        assert (idx[b, h, len(sel):] == -1).all(), (what, b, h)
+        m = ko.shape[0]
+        assert np.array_equal(kg[b, h, :m], ko.view(kg.dtype)), (what, b, h, "k")
+        assert np.array_equal(vg[b, h, :m], vo.view(vg.dtype)), (what, b, h, "v")
+        assert (kg[b, h, m:] == 0).all() and (vg[b, h, m:] == 0).all(), (what, b, h)
+
+
+def check_threshold_rule(pooled, got_idx, n_sel, what):
+    """End-to-end selection rule: with t the oracle's B'-th largest pooled score, every
+    candidate above t by more than 1e-3 relative is kept, every one below by more than
+    1e-3 dropped, and the count is B' = min(n_sel, C)."""
+    C = pooled.shape[0]
+    n = min(n_sel, C)
+    got = set(int(i) for i in got_idx if i >= 0)
+    assert len(got) == n, (what, len(got), n)
+    if n == 0 or n == C:
+        assert got == set(range(n)), what
+        return
+    t = np.sort(pooled)[::-1][n - 1]
+    must = set(np.nonzero(pooled > t * (1 + 1e-3))[0].tolist())
+    never = set(np.nonzero(pooled < t * (1 - 1e-3))[0].tolist())
+    assert must <= got, (what, "missing", sorted(must - got)[:8])
+    assert not (never & got), (what, "extra", sorted(never & got)[:8])
+
+
 def run_score(wl, x, mode=oracle.ROWS_WINDOW_DRAFT):
     g = geom_of(wl)
     q, qb = mode_rows(x, wl, mode)
@@ -337,20 +391,24 @@ FUSED_CASES = {
 
 
 @pytest.mark.parametrize("case", list(FUSED_CASES))
-def test_select_compact_fused_equals_separate(case):
+def test_select_compact_fused_and_separate_vs_oracle(case):
+    """dge_select_compact (one launch) and dge_select_topb + dge_compact against the
+    oracle's pool -> top-B' -> compact on the GPU's own fp32 scores: indices bit-exact,
+    n_kept exact, compacted K/V byte-exact with zero padding (Alg. 1 steps B-C)."""
     wl, budget = FUSED_CASES[case]
     budget = wl.budget if budget is None else budget
-    _log(f"fused select+compact {case}")
+    _log(f"select+compact vs oracle {case}")
     x = di.make_layer(wl)
     g = geom_of(wl)
     q, k, v = to_dev(x.q_bits, wl.dtype), to_dev(x.k_bits, wl.dtype), to_dev(x.v_bits, wl.dtype)
-    a = dge.evict_layer(g, q, k, v, budget, wl.pool, fused=True)
-    b = dge.evict_layer(g, q, k, v, budget, wl.pool, fused=False)
-    torch.cuda.synchronize()
-    for key in ("raw", "idx", "n_kept"):
-        assert torch.equal(a[key], b[key]), key
-    iv = torch.int16 if wl.dtype == "bf16" else torch.int32
-    assert torch.equal(a["k"].view(iv), b["k"].view(iv)) and torch.equal(a["v"].view(iv), b["v"].view(iv))
+    n_tail, n_sel = wl.window + wl.k_draft, budget - wl.window
+    for fused in (True, False):
+        out = dge.evict_layer(g, q, k, v, budget, wl.pool, fused=fused)
+        torch.cuda.synchronize()
+        want = oracle_select_compact(out["raw"].cpu().numpy(), x.k_bits, x.v_bits,
+                                     wl.cached_lens, wl.n_kv_heads, wl.pool, n_tail, n_sel)
+        check_select_compact(out["idx"], out["n_kept"], out["k"], out["v"], want, n_sel,
+                             n_tail, f"{case} fused={fused}")
 
 
 def test_compact_keep_all_is_identity():
@@ -622,34 +680,72 @@ LAYER_CASES = {
 
 
 @pytest.mark.parametrize("case", list(LAYER_CASES))
-def test_select_compact_layers_equals_per_layer(case):
+def test_select_compact_layers_vs_oracle(case):
+    """dge_select_compact_layers (every layer's pool, top-B'_l and gather in one launch)
+    against the oracle layer by layer: indices bit-exact given the same fp32 scores,
+    n_kept exact, compacted K/V byte-exact (Alg. 1 steps B-C for all layers)."""
     lens, H, d, dtype, n_sel, pool, n_tail, kind = LAYER_CASES[case]
-    _log(f"select_compact_layers {case}: lens={lens} H={H} layers={len(n_sel)}")
+    _log(f"select_compact_layers vs oracle {case}: lens={lens} H={H} layers={len(n_sel)}")
     nl, T = len(n_sel), sum(lens)
     rng = np.random.default_rng(np.random.SeedSequence([7, len(case)]))
-    scores = torch.from_numpy(di.random_scores((nl * H, T), seed=len(case), kind=kind)).to(DEV)
+    scores_h = di.random_scores((nl * H, T), seed=len(case), kind=kind)
     if dtype == "bf16":
-        k = to_dev(rng.integers(0, 1 << 16, size=(nl * H, T, d), dtype=np.uint16), "bf16")
-        v = to_dev(rng.integers(0, 1 << 16, size=(nl * H, T, d), dtype=np.uint16), "bf16")
+        kb = rng.integers(0, 1 << 16, size=(nl * H, T, d), dtype=np.uint16)
+        vb = rng.integers(0, 1 << 16, size=(nl * H, T, d), dtype=np.uint16)
     else:
-        k = torch.from_numpy(rng.standard_normal((nl * H, T, d), dtype=np.float32)).to(DEV)
-        v = torch.from_numpy(rng.standard_normal((nl * H, T, d), dtype=np.float32)).to(DEV)
+        kb = rng.standard_normal((nl * H, T, d), dtype=np.float32)
+        vb = rng.standard_normal((nl * H, T, d), dtype=np.float32)
     g = dge.Geometry(2 * H, H, d, 0, 0, lens, dtype=dge.DGE_BF16 if dtype == "bf16" else dge.DGE_F32,
                      device=DEV)
-    idx_l, nk, k_l, v_l = dge.select_compact_layers(g, scores, pool, n_tail, n_sel, k, v)
+    idx_l, nk, k_l, v_l = dge.select_compact_layers(g, torch.from_numpy(scores_h).to(DEV), pool,
+                                                    n_tail, n_sel, to_dev(kb, dtype),
+                                                    to_dev(vb, dtype))
     torch.cuda.synchronize()
     for l in range(nl):
         sl = slice(l * H, (l + 1) * H)
-        # fresh (aligned) copies of the layer's slices for the one-layer call
-        ri, rn, rk, rv = dge.select_compact(g, scores[sl].clone(), pool, n_tail, n_sel[l],
-                                            k[sl].clone(), v[sl].clone())
-        torch.cuda.synchronize()
-        assert torch.equal(nk[l], rn), (case, l)
-        assert torch.equal(idx_l[l], ri), (case, l)
-        assert torch.equal(k_l[l].view(torch.int16 if dtype == "bf16" else torch.int32),
-                           rk.view(torch.int16 if dtype == "bf16" else torch.int32)), (case, l)
-        assert torch.equal(v_l[l].view(torch.int16 if dtype == "bf16" else torch.int32),
-                           rv.view(torch.int16 if dtype == "bf16" else torch.int32)), (case, l)
+        want = oracle_select_compact(scores_h[sl], kb[sl], vb[sl], lens, H, pool, n_tail, n_sel[l])
+        check_select_compact(idx_l[l], nk[l], k_l[l], v_l[l], want, n_sel[l], n_tail,
+                             f"{case} layer {l}")
+
+
+def test_c3_layers_score_select_compact_vs_oracle():
+    """Four c3-shaped layers (32q/8kv, d 128, L 16384, each generated with its own seeds
+    and planted spans) scored by one dge_score call over the layer-major cache and
+    evicted by one dge_select_compact_layers launch with distinct budgets: the PyramidKV
+    maximum (2048), the window only (B' = 0), keep-all, and an interior value.  Scores
+    within 1e-3 of the oracle; selection by the threshold rule against the oracle's own
+    scores and bit-exact given the GPU's scores; K/V byte-exact."""
+    wl = di.WORKLOADS["c3"]
+    budgets = [wl.budget_of_layer(0), wl.window, 20000, wl.budget_of_layer(20)]
+    nl, Hq, H = len(budgets), wl.n_q_heads, wl.n_kv_heads
+    _log(f"c3 layers vs oracle: budgets {budgets}")
+    xs = [di.make_layer(wl, layer=l) for l in range(nl)]
+    g1 = geom_of(wl)
+    ga = dge.Geometry(Hq * nl, H * nl, wl.head_dim, wl.window, wl.k_draft, wl.cached_lens,
+                      device=DEV)
+    q = to_dev(np.concatenate([x.q_bits for x in xs]), "bf16")
+    k = to_dev(np.concatenate([x.k_bits for x in xs]), "bf16")
+    v = to_dev(np.concatenate([x.v_bits for x in xs]), "bf16")
+    raw = dge.score(ga, dge.ROWS_WINDOW_DRAFT, q, k)
+    n_tail = wl.window + wl.k_draft
+    n_sel = [B - wl.window for B in budgets]
+    idx_l, nk, k_l, v_l = dge.select_compact_layers(g1, raw, wl.pool, n_tail, n_sel, k, v)
+    torch.cuda.synchronize()
+    raw_h = raw.cpu().numpy()
+    N = wl.cached_lens[0]
+    C = N - n_tail
+    for l, x in enumerate(xs):
+        sl = slice(l * H, (l + 1) * H)
+        want_raw = oracle.window_scores(x.q, x.k, wl.kv_offsets, Hq, H, wl.window, wl.k_draft)
+        check_scores(raw_h[sl], want_raw, f"c3 layer {l} scores")
+        want = oracle_select_compact(raw_h[sl], x.k_bits, x.v_bits, wl.cached_lens, H, wl.pool,
+                                     n_tail, n_sel[l])
+        check_select_compact(idx_l[l], nk[l], k_l[l], v_l[l], want, n_sel[l], n_tail,
+                             f"c3 layer {l}")
+        gi = idx_l[l].cpu().numpy()
+        for h in range(H):
+            pooled = oracle.maxpool(want_raw[h], C, wl.pool)
+            check_threshold_rule(pooled, gi[0, h], n_sel[l], f"c3 layer {l} head {h}")
 
 
 # ----------------------------------------------------------------------------------
@@ -668,38 +764,131 @@ INPLACE_CASES = {
 
 
 @pytest.mark.parametrize("case", list(INPLACE_CASES))
-def test_compact_inplace_equals_compact(case):
+def test_compact_inplace_vs_oracle(case):
+    """dge_compact_inplace (Alg. 1 step C as one in-place edit, temporal order kept)
+    against the oracle: the selection bit-exact to the oracle's rule on the same scores
+    (or the StreamingLLM closed form), the first n_kept + n_tail rows of every segment
+    byte-equal to oracle.compact, the rest of the segment untouched."""
     lens, H, d, dtype, n_select, n_tail, pool, selector = INPLACE_CASES[case]
-    _log(f"compact_inplace {case}: lens={lens} H={H} sel={n_select} tail={n_tail}")
+    _log(f"compact_inplace vs oracle {case}: lens={lens} H={H} sel={n_select} tail={n_tail}")
     T = sum(lens)
     rng = np.random.default_rng(np.random.SeedSequence([11, len(case)]))
     g = dge.Geometry(2 * H, H, d, 0, 0, lens, dtype=dge.DGE_BF16 if dtype == "bf16" else dge.DGE_F32,
                      device=DEV)
     if dtype == "bf16":
-        k = to_dev(rng.integers(0, 1 << 16, size=(H, T, d), dtype=np.uint16), "bf16")
-        v = to_dev(rng.integers(0, 1 << 16, size=(H, T, d), dtype=np.uint16), "bf16")
-        bits = torch.int16
+        kb = rng.integers(0, 1 << 16, size=(H, T, d), dtype=np.uint16)
+        vb = rng.integers(0, 1 << 16, size=(H, T, d), dtype=np.uint16)
+        bits = np.int16
     else:
-        k = torch.from_numpy(rng.standard_normal((H, T, d), dtype=np.float32)).to(DEV)
-        v = torch.from_numpy(rng.standard_normal((H, T, d), dtype=np.float32)).to(DEV)
-        bits = torch.int32
+        kb = rng.standard_normal((H, T, d), dtype=np.float32)
+        vb = rng.standard_normal((H, T, d), dtype=np.float32)
+        bits = np.int32
+    k, v = to_dev(kb, dtype), to_dev(vb, dtype)
+    offs = np.concatenate([[0], np.cumsum(lens)])
     if selector == "topb":
-        scores = torch.from_numpy(di.random_scores((H, T), seed=len(case), kind="plateau")).to(DEV)
-        idx, nk = dge.select_topb(g, scores, pool, n_tail, n_select)
+        scores_h = di.random_scores((H, T), seed=len(case), kind="plateau")
+        idx, nk = dge.select_topb(g, torch.from_numpy(scores_h).to(DEV), pool, n_tail, n_select)
+        want = oracle_select_compact(scores_h, kb, vb, lens, H, pool, n_tail, n_select)
     else:
         idx, nk = dge.select_streaming(g, n_select, n_tail)
-    k_out, v_out = dge.compact(g, idx, nk, n_select, n_tail, k, v)
-    k0, v0 = k.clone(), v.clone()
+        want = {}
+        for b, N in enumerate(lens):
+            sel = oracle.streaming_select(N, n_select, n_tail)
+            for h in range(H):
+                seg = slice(offs[b], offs[b + 1])
+                want[(b, h)] = (sel,) + oracle.compact(kb[h, seg], vb[h, seg], sel, N - n_tail)
     dge.compact_inplace(g, idx, nk, n_select, n_tail, k, v)
     torch.cuda.synchronize()
-    nk = nk.cpu().numpy()
-    offs = np.concatenate([[0], np.cumsum(lens)])
+    idx, nk = idx.cpu().numpy(), nk.cpu().numpy()
+    kg = k.cpu().view(torch.int16 if dtype == "bf16" else torch.int32).numpy()
+    vg = v.cpu().view(torch.int16 if dtype == "bf16" else torch.int32).numpy()
     for b, N in enumerate(lens):
-        m = int(nk[b]) + n_tail
-        for name, got, want, orig in (("k", k, k_out, k0), ("v", v, v_out, v0)):
-            seg = got[:, offs[b]:offs[b] + N].view(bits)
-            assert torch.equal(seg[:, :m], want[b, :, :m].view(bits)), (case, b, name)
-            assert torch.equal(seg[:, m:], orig[:, offs[b] + m:offs[b] + N].view(bits)), (case, b, name)
+        for h in range(H):
+            sel, ko, vo = want[(b, h)]
+            assert nk[b] == len(sel), (case, b)
+            assert np.array_equal(idx[b, h, :len(sel)], sel), (case, b, h)
+            m = len(sel) + n_tail
+            s0 = offs[b]
+            assert np.array_equal(kg[h, s0:s0 + m], ko.view(bits)), (case, b, h, "k")
+            assert np.array_equal(vg[h, s0:s0 + m], vo.view(bits)), (case, b, h, "v")
+            assert np.array_equal(kg[h, s0 + m:s0 + N], kb[h, s0 + m:s0 + N].view(bits)), (case, b, h)
+            assert np.array_equal(vg[h, s0 + m:s0 + N], vb[h, s0 + m:s0 + N].view(bits)), (case, b, h)
+
+
+# ----------------------------------------------------------------------------------
+# More sequences than travel inline in the kernel arguments (16): every kernel reads the
+# device offsets array
+# ----------------------------------------------------------------------------------
+BIG_BATCH = tuple(int(n) for n in np.random.default_rng(np.random.SeedSequence([18, 0])).integers(40, 700, size=18))
+
+
+def test_batch_of_18_sequences_vs_oracle():
+    """18 ragged sequences through every entry point that takes the sequence offsets:
+    dge_score, dge_select_compact, dge_select_topb + dge_compact, dge_compact_inplace,
+    dge_select_streaming, dge_retained_runs, dge_cache_attention and dge_h2o_colsum,
+    each against the oracle."""
+    wl = di.small_variant("c2", BIG_BATCH)
+    _log(f"batch of {wl.batch} sequences, lens {BIG_BATCH}")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    q, k, v = to_dev(x.q_bits, "bf16"), to_dev(x.k_bits, "bf16"), to_dev(x.v_bits, "bf16")
+    n_tail, n_sel = wl.window + wl.k_draft, 100
+    raw = dge.score(g, dge.ROWS_WINDOW_DRAFT, q, k)
+    torch.cuda.synchronize()
+    raw_h = raw.cpu().numpy()
+    want_raw = oracle.window_scores(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                    wl.window, wl.k_draft)
+    check_scores(raw_h, want_raw, "batch 18 scores")
+    want = oracle_select_compact(raw_h, x.k_bits, x.v_bits, wl.cached_lens, wl.n_kv_heads,
+                                 wl.pool, n_tail, n_sel)
+    idx, nk, kc, vc = dge.select_compact(g, raw, wl.pool, n_tail, n_sel, k, v)
+    torch.cuda.synchronize()
+    check_select_compact(idx, nk, kc, vc, want, n_sel, n_tail, "batch 18 fused")
+    gi = idx.cpu().numpy()
+    offs = wl.kv_offsets
+    for b, N in enumerate(wl.cached_lens):
+        for h in range(wl.n_kv_heads):
+            pooled = oracle.maxpool(want_raw[h, offs[b]:offs[b + 1]], N - n_tail, wl.pool)
+            check_threshold_rule(pooled, gi[b, h], n_sel, f"batch 18 seq {b} head {h}")
+    idx2, nk2 = dge.select_topb(g, raw, wl.pool, n_tail, n_sel)
+    kc2, vc2 = dge.compact(g, idx2, nk2, n_sel, n_tail, k, v)
+    torch.cuda.synchronize()
+    check_select_compact(idx2, nk2, kc2, vc2, want, n_sel, n_tail, "batch 18 separate")
+    # in place, on copies of the cache
+    kw, vw = k.clone(), v.clone()
+    dge.compact_inplace(g, idx2, nk2, n_sel, n_tail, kw, vw)
+    torch.cuda.synchronize()
+    kg = kw.cpu().view(torch.int16).numpy()
+    vg = vw.cpu().view(torch.int16).numpy()
+    for (b, h), (sel, ko, vo) in want.items():
+        m = len(sel) + n_tail
+        assert np.array_equal(kg[h, offs[b]:offs[b] + m], ko.view(np.int16)), (b, h)
+        assert np.array_equal(vg[h, offs[b]:offs[b] + m], vo.view(np.int16)), (b, h)
+    # StreamingLLM and the run-length diagnostic
+    sidx, snk = dge.select_streaming(g, 4, 40)
+    torch.cuda.synchronize()
+    for b, N in enumerate(wl.cached_lens):
+        s_want = oracle.streaming_select(N, 4, 40)
+        assert snk[b].item() == len(s_want)
+        for h in range(wl.n_kv_heads):
+            assert sidx[b, h, :len(s_want)].cpu().numpy().tolist() == s_want.tolist()
+    _runs_check(g, gi.astype(np.int32), nk.cpu().numpy().astype(np.int32)[:wl.batch], "batch 18")
+    # attention over the compacted caches: decode queries and the scoring rows
+    kc64, vc64 = _host_f64(kc, "bf16"), _host_f64(vc, "bf16")
+    n_kept = nk.cpu().numpy()[:wl.batch]
+    out, lse = dge.cache_attention(g, q, n_tail, n_tail, kc, vc, n_sel, n_tail, nk)
+    torch.cuda.synchronize()
+    wo, wlse = oracle.cache_attention(x.q, kc64, vc64, n_kept, n_tail, n_tail, wl.n_q_heads,
+                                      wl.n_kv_heads)
+    _check_att(out, lse, wo, wlse, "batch 18 scoring rows")
+    # H2O accumulated attention over every cached row of the 18 sequences
+    wh = di.small_variant("c5", BIG_BATCH)
+    xh = di.make_layer(wh, with_v=False)
+    gh = geom_of(wh)
+    col = dge.h2o_colsum(gh, to_dev(xh.q_all_bits, "bf16"), to_dev(xh.k_bits, "bf16"))
+    torch.cuda.synchronize()
+    want_col = oracle.h2o_colsum(xh.q_all, xh.k, wh.kv_offsets, wh.n_q_heads, wh.n_kv_heads)
+    check_scores(col.cpu().numpy(), want_col, "batch 18 h2o colsum")
 
 
 # ----------------------------------------------------------------------------------
