@@ -31,8 +31,9 @@
  *                 h*kv_head_stride + r*head_dim; head_dim elements contiguous.
  *     scores    : [H_kv][T] float32, T = kv_offsets[batch] (total cached rows).
  *   Element type of Q, K, V: bfloat16 (DGE_BF16) or float32 (DGE_F32).
- * - Thread safety: no global mutable state; concurrent calls on different
- *   streams with disjoint outputs and workspaces are safe.
+ * - Thread safety: no global mutable state except the per-GPU scratch of
+ *   dge_score_noalloc; concurrent calls on different streams with disjoint outputs and
+ *   workspaces are safe (dge_score_noalloc calls on one GPU excepted).
  * - Row counts are bounded by INT32_MAX / 2: a longer sequence is DGE_ERR_UNSUPPORTED,
  *   a larger n_select DGE_ERR_INVALID (so that n_select + n_tail fits in int32).
  */
@@ -117,6 +118,26 @@ dge_status_t dge_workspace_size(const dge_geom_t *geom, int32_t op, size_t *byte
  * DGE_ERR_UNSUPPORTED for head_dim outside {64, 128}. */
 dge_status_t dge_score(const dge_geom_t *geom, int32_t rows, const void *q, const void *k,
                        float *raw, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* dge_score for callers that cannot allocate device memory or pass a workspace (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * kernels and results as dge_score (bit-identical), with the softmax partials kept in a
+ * fixed scratch array that the library holds in every GPU's memory until the process
+ * ends.  No allocation of any kind is made by this call.
+ *   Limit: the call needs dge_workspace_size(geom, DGE_OP_SCORE)-style scratch for its
+ *   rows mode of at most DGE_NOALLOC_SCRATCH_BYTES (16 MiB: e.g. 32 layers x 8 KV heads x
+ *   8 sequences of up to 32K rows, 34 scoring rows, G = 4); larger geometries return
+ *   DGE_ERR_WORKSPACE before anything is launched.
+ *   Every call on one GPU shares that GPU's scratch, and calls keep no state in it between
+ *   them (each value read was written earlier in the same call): calls whose executions
+ *   overlap on one GPU (different streams or threads) RACE and must be serialised by the
+ *   caller.  The stream must belong to the current device; the scratch address is
+ *   resolved on the first call on each device (hipGetSymbolAddress, no allocation).
+ * Arguments and other errors are those of dge_score; DGE_ERR_HIP if the scratch address
+ * cannot be resolved. */
+#define DGE_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+dge_status_t dge_score_noalloc(const dge_geom_t *geom, int32_t rows, const void *q,
+                               const void *k, float *raw, hipStream_t stream);
 
 /* dge_score with the scoring rows' softmax normalisers supplied by the caller, e.g. the
  * log-sum-exp an attention forward already produced for the window and draft rows.

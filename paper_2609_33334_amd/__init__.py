@@ -22,7 +22,7 @@ from . import _lib
 from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  # noqa: F401
                    ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
 
-__all__ = ["Geometry", "score", "score_lse", "select_topb", "select_compact",
+__all__ = ["Geometry", "score", "score_noalloc", "score_lse", "select_topb", "select_compact",
            "select_compact_layers", "select_streaming", "compact", "compact_inplace",
            "cache_attention",
            "rope", "retained_runs", "h2o_colsum",
@@ -156,6 +156,23 @@ def score(geom: Geometry, rows: int, q, k, raw=None, ws=None, stream=None):
     ws = _workspace(geom, OP_SCORE, ws)
     _lib.check(_lib.lib().dge_score(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k), _ptr(raw),
                                     _ptr(ws), ws.numel(), _stream(stream)), "dge_score")
+    return raw
+
+
+def score_noalloc(geom: Geometry, rows: int, q, k, raw=None, stream=None):
+    """dge_score_noalloc: dge_score with the library's fixed per-GPU scratch instead of a
+    workspace (no device allocation inside the call; calls on one GPU must not overlap).
+    Returns raw [H_kv][T] float32."""
+    torch = _torch()
+    nr = n_scoring_rows(geom.window, geom.k_draft, rows)
+    _need(q, "q", (geom.elt_dtype,), geom.n_q_heads * geom.batch * nr * geom.head_dim)
+    _need(k, "k", (geom.elt_dtype,), (geom.n_kv_heads - 1) * geom.kv_head_stride
+          + geom.total_rows * geom.head_dim)
+    if raw is None:
+        raw = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=geom.device)
+    _need(raw, "raw", _f32(), geom.n_kv_heads * geom.total_rows)
+    _lib.check(_lib.lib().dge_score_noalloc(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k),
+                                            _ptr(raw), _stream(stream)), "dge_score_noalloc")
     return raw
 
 

@@ -3,6 +3,7 @@
 // check fails.  See include/dge.h for the contract of every entry point.
 #include <cstddef>
 #include <cstdint>
+#include <mutex>
 
 #include "dge.h"
 #include "dge_internal.hpp"
@@ -51,6 +52,42 @@ dge_status_t check_tail(const dge_geom_t* g, int32_t n_tail) {
 
 dge_status_t hip_status(hipError_t e) { return e == hipSuccess ? DGE_OK : DGE_ERR_HIP; }
 
+// Scratch of dge_score_noalloc: one fixed array per GPU, held until the process ends.  In
+// host code `scratch` names a host-side stand-in, never the device memory; the device
+// address is resolved once per device with that device current and kept in scratch_ptr.
+static __device__ __align__(256) unsigned char scratch[DGE_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices];
+
+dge_status_t scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return DGE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return DGE_ERR_HIP;
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return DGE_OK;
+}
+
+// Checks shared by dge_score and dge_score_noalloc (everything but the workspace).
+dge_status_t check_score(const dge_geom_t* geom, int32_t rows, const void* q, const void* k,
+                         const float* raw) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (rows < DGE_ROWS_WINDOW_DRAFT || rows > DGE_ROWS_WINDOW) return DGE_ERR_INVALID;
+  if (!q || !k || !raw || !aligned16(q) || !aligned16(k) || !aligned16(raw)) return DGE_ERR_INVALID;
+  for (int b = 0; b < geom->batch; ++b)
+    if (seq_rows(geom, b) < (int64_t)geom->window + geom->k_draft || seq_rows(geom, b) < 1)
+      return DGE_ERR_INVALID;
+  if (dge::plan_score(*geom, rows).n_rows <= 0) return DGE_ERR_INVALID;
+  return DGE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -92,17 +129,22 @@ dge_status_t dge_workspace_size(const dge_geom_t* geom, int32_t op, size_t* byte
 
 dge_status_t dge_score(const dge_geom_t* geom, int32_t rows, const void* q, const void* k,
                        float* raw, void* ws, size_t ws_bytes, hipStream_t stream) {
-  dge_status_t st = check_geom(geom);
+  dge_status_t st = check_score(geom, rows, q, k, raw);
   if (st != DGE_OK) return st;
-  if (rows < DGE_ROWS_WINDOW_DRAFT || rows > DGE_ROWS_WINDOW) return DGE_ERR_INVALID;
-  if (!q || !k || !raw || !aligned16(q) || !aligned16(k) || !aligned16(raw)) return DGE_ERR_INVALID;
-  for (int b = 0; b < geom->batch; ++b)
-    if (seq_rows(geom, b) < (int64_t)geom->window + geom->k_draft || seq_rows(geom, b) < 1)
-      return DGE_ERR_INVALID;
   const ScorePlan p = dge::plan_score(*geom, rows);
-  if (p.n_rows <= 0) return DGE_ERR_INVALID;
   if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::score_workspace_bytes(*geom, p))
     return DGE_ERR_WORKSPACE;
+  return hip_status(dge::launch_score(*geom, p, q, k, nullptr, raw, ws, stream));
+}
+
+dge_status_t dge_score_noalloc(const dge_geom_t* geom, int32_t rows, const void* q,
+                               const void* k, float* raw, hipStream_t stream) {
+  dge_status_t st = check_score(geom, rows, q, k, raw);
+  if (st != DGE_OK) return st;
+  const ScorePlan p = dge::plan_score(*geom, rows);
+  if (dge::score_workspace_bytes(*geom, p) > DGE_NOALLOC_SCRATCH_BYTES) return DGE_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if ((st = scratch_of_current_device(&ws)) != DGE_OK) return st;
   return hip_status(dge::launch_score(*geom, p, q, k, nullptr, raw, ws, stream));
 }
 

@@ -123,6 +123,26 @@ def test_score_validation(L):
     assert L.dge_score_lse(_G(lens=(100, 9)).p, 0, FAKE, FAKE, FAKE, FAKE, None) == _lib.DGE_ERR_INVALID
 
 
+def test_score_noalloc_validation(L):
+    """dge_score_noalloc: dge_score's checks, and a geometry whose partials exceed the fixed
+    scratch is refused (DGE_ERR_WORKSPACE) before the scratch address is even looked up."""
+    def call(G, rows=0, q=FAKE, k=FAKE, raw=FAKE):
+        return L.dge_score_noalloc(G.p, rows, q, k, raw, None)
+    assert call(_G(hq=6, hkv=4)) == _lib.DGE_ERR_INVALID
+    assert call(_G(d=96)) == _lib.DGE_ERR_UNSUPPORTED
+    assert call(_G(lens=(100, 9))) == _lib.DGE_ERR_INVALID
+    assert call(_G(w=0, k=0)) == _lib.DGE_ERR_INVALID
+    assert call(_G(), raw=None) == _lib.DGE_ERR_INVALID
+    assert call(_G(), k=FAKE + 8) == _lib.DGE_ERR_INVALID
+    # 8 sequences of 32K rows over 512 KV heads, 136 query rows per head: ~18.9 MB of partials
+    big = _G(lens=(32768,) * 8, hq=2048, hkv=512, w=32, k=2)
+    n = ctypes.c_size_t(0)
+    assert L.dge_workspace_size(big.p, 0, ctypes.byref(n)) == 0
+    assert n.value > _lib.NOALLOC_SCRATCH_BYTES
+    assert call(big) == _lib.DGE_ERR_WORKSPACE
+    assert L.dge_score_noalloc(None, 0, FAKE, FAKE, FAKE, None) == _lib.DGE_ERR_INVALID
+
+
 def test_workspace_size(L):
     g = _G()
     n = ctypes.c_size_t(0)
