@@ -119,6 +119,19 @@ dge_status_t dge_workspace_size(const dge_geom_t *geom, int32_t op, size_t *byte
 dge_status_t dge_score(const dge_geom_t *geom, int32_t rows, const void *q, const void *k,
                        float *raw, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* dge_score that also returns the softmax normaliser of every scoring row, which the
+ * scoring computes anyway (the full-cache log-partition log Z(q) of the attention-matching
+ * loss, App. "Attention-matching loss"; with dge_evicted_mass it gives the rows' evicted
+ * mass without a second pass over the full cache):
+ *   row_lse : [H_q][batch * n_rows] float32 output, natural log:
+ *             row_lse[hq][b * n_rows + r] = log sum_{j <= p_r} exp(q_{hq,r} . k_j / sqrt(d)),
+ *             rows in the order of q.
+ * Other arguments, the raw output and errors are those of dge_score (DGE_ERR_INVALID for a
+ * NULL or misaligned row_lse). */
+dge_status_t dge_score_with_lse(const dge_geom_t *geom, int32_t rows, const void *q,
+                                const void *k, float *raw, float *row_lse, void *ws,
+                                size_t ws_bytes, hipStream_t stream);
+
 /* dge_score for callers that cannot allocate device memory or pass a workspace (code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
  * kernels and results as dge_score (bit-identical), with the softmax partials kept in a
@@ -277,6 +290,35 @@ dge_status_t dge_cache_attention(const dge_geom_t *geom, const void *q, int32_t 
                                  int32_t q_from_end, const void *k_c, const void *v_c,
                                  int32_t n_select, int32_t n_tail, const int32_t *n_kept,
                                  float *out, float *lse, hipStream_t stream);
+
+/* Evicted attention mass of the observation rows and the attention-matching loss of a
+ * selection (App. "Attention-matching loss", Eq. match; Sec. 3 Eq. 1, where beta is the
+ * missed mass; App. "Why deferral can recover FullKV", the eviction-mass equation), from
+ * the compacted cache and the full-cache normalisers dge_score_with_lse returns, with no
+ * second pass over the full cache.  For sequence b, query head hq and observation row r
+ * (position N_b - q_from_end + r, inside the tail, so every candidate precedes it):
+ *   lse_R          = log sum over the retained rows k_c[b][h][0 .. n_kept[b]) and the tail
+ *                    rows at positions <= its own of exp(q . k_j / sqrt(d))   (float32)
+ *   rho[hq][b*n_q + r] = 1 - exp(lse_R - lse_full[hq][b*n_q + r]), the softmax mass the row
+ *                    places on the evicted keys (computed as -expm1 of the clamped deficit)
+ *   beta[b][h]     = mean of rho over the G query heads of KV head h and the n_q rows
+ *   l_match[b][h]  = mean of -log(1 - rho) over the same rows (= mean |log Z - log Z_R|)
+ *   q        : [H_q][batch * n_q][d] observation rows (dge_score's q for the window + draft
+ *              rows: n_q = q_from_end = w + k); element type of the cache.
+ *   k_c      : [batch][H_kv][n_select + n_tail][d], the dge_compact layout (V is not read).
+ *   n_kept   : [batch] int32 (clamped to [0, n_select]).
+ *   lse_full : [H_q][batch * n_q] float32, natural-log partition of each row over the full
+ *              cache (dge_score_with_lse's row_lse for the same rows).
+ *   rho      : [H_q][batch * n_q] float32 output; beta, l_match : [batch][H_kv] float32 outputs.
+ * Accuracy: rho is the difference of two float32 log-partitions, so its absolute error is
+ * about their rounding (~1e-6 for rows of 32K keys), not relative to rho.
+ * No workspace.  Errors: DGE_ERR_INVALID for n_q < 1, n_select < 0, n_tail < 1,
+ * q_from_end > n_tail or < n_q, or a NULL / misaligned pointer; DGE_ERR_UNSUPPORTED for more
+ * than 8 query heads per KV head. */
+dge_status_t dge_evicted_mass(const dge_geom_t *geom, const void *q, int32_t n_q,
+                              int32_t q_from_end, const void *k_c, int32_t n_select,
+                              int32_t n_tail, const int32_t *n_kept, const float *lse_full,
+                              float *rho, float *beta, float *l_match, hipStream_t stream);
 
 /* Rotary position embedding of query or key rows, in place (the post-RoPE Q and K the
  * scoring reads; App. "Draft-guided eviction implementation": queries recomputed post-RoPE

@@ -287,6 +287,58 @@ def log_partition(qrow: np.ndarray, keys: np.ndarray) -> float:
     return float(m + np.log(np.exp(x - m).sum()))
 
 
+def eviction_diagnostics(q, k, kv_offsets, n_q_heads: int, n_kv_heads: int, kept, n_tail: int,
+                         q_from_end: int):
+    """Evicted mass of the observation rows and the attention-matching loss of a selection.
+
+    App. "Attention-matching loss", Eq. match: for an observation query q,
+    rho_q = sum_{j in E} e^{q.k_j/sqrt d} / sum_{j in R u E} e^{q.k_j/sqrt d}, and the loss
+    is E_q[-log(1 - rho_q)] = E_q |log Z - log Z_R|.  Sec. 3 Eq. 1 calls the same quantity
+    for a query the missed mass beta.  Here, for sequence b and KV head h, the rows are
+    q[hq][b * n_q + r] at positions p = N_b - q_from_end + r (inside the tail, so every
+    candidate precedes them), each attending keys j <= p of the full cache; R is the kept
+    past keys kept[(b, h)] plus the tail [N_b - n_tail, N_b), E the other candidates.
+
+    Returns rho [H_q][batch * n_q], beta [batch][H_kv] (mean rho over the group's G heads
+    and n_q rows) and l_match [batch][H_kv] (mean of -log(1 - rho) over the same rows).
+    rho is computed directly as the softmax mass on E; l_match from the two log-partitions.
+    """
+    q = as_f64(q)
+    k = as_f64(k)
+    G = n_q_heads // n_kv_heads
+    offs = [int(o) for o in kv_offsets]
+    batch = len(offs) - 1
+    n_q = q.shape[1] // batch
+    d = k.shape[2]
+    rho = np.zeros((n_q_heads, batch * n_q), np.float64)
+    beta = np.zeros((batch, n_kv_heads), np.float64)
+    l_match = np.zeros((batch, n_kv_heads), np.float64)
+    for b in range(batch):
+        s0, N = offs[b], offs[b + 1] - offs[b]
+        C = N - n_tail
+        for h in range(n_kv_heads):
+            keep = np.zeros(N, bool)
+            keep[np.asarray(kept[(b, h)], np.int64)] = True
+            keep[C:] = True
+            losses = []
+            for g in range(G):
+                hq = h * G + g
+                for r in range(n_q):
+                    p = N - q_from_end + r
+                    x = k[h, s0:s0 + p + 1] @ q[hq, b * n_q + r] / math.sqrt(d)
+                    m = x.max()
+                    e = np.exp(x - m)
+                    kp = keep[:p + 1]
+                    rho[hq, b * n_q + r] = e[~kp].sum() / e.sum()
+                    log_z = m + np.log(e.sum())
+                    log_zr = m + np.log(e[kp].sum())
+                    losses.append(log_z - log_zr)
+            rows = [rho[h * G + g, b * n_q + r] for g in range(G) for r in range(n_q)]
+            beta[b, h] = np.mean(rows)
+            l_match[b, h] = np.mean(losses)
+    return rho, beta, l_match
+
+
 def cache_attention(q, k_c, v_c, n_kept, n_tail: int, q_from_end: int, n_q_heads: int,
                     n_kv_heads: int):
     """Attention of query rows over compacted caches: the check of a continuation on the

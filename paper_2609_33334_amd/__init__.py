@@ -22,7 +22,7 @@ from . import _lib
 from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  # noqa: F401
                    ROWS_WINDOW, ROWS_WINDOW_DRAFT, DGEError, Geom)
 
-__all__ = ["Geometry", "score", "score_noalloc", "score_lse", "select_topb", "select_compact",
+__all__ = ["Geometry", "score", "score_noalloc", "score_with_lse", "score_lse", "evicted_mass", "select_topb", "select_compact",
            "select_compact_layers", "select_streaming", "compact", "compact_inplace",
            "cache_attention",
            "rope", "retained_runs", "h2o_colsum",
@@ -157,6 +157,56 @@ def score(geom: Geometry, rows: int, q, k, raw=None, ws=None, stream=None):
     _lib.check(_lib.lib().dge_score(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k), _ptr(raw),
                                     _ptr(ws), ws.numel(), _stream(stream)), "dge_score")
     return raw
+
+
+def score_with_lse(geom: Geometry, rows: int, q, k, raw=None, row_lse=None, ws=None,
+                   stream=None):
+    """dge_score_with_lse: raw scores and the scoring rows' full-cache log-partitions.
+    Returns (raw [H_kv][T], row_lse [H_q][batch * n_rows] natural log)."""
+    torch = _torch()
+    nr = n_scoring_rows(geom.window, geom.k_draft, rows)
+    _need(q, "q", (geom.elt_dtype,), geom.n_q_heads * geom.batch * nr * geom.head_dim)
+    _need(k, "k", (geom.elt_dtype,), (geom.n_kv_heads - 1) * geom.kv_head_stride
+          + geom.total_rows * geom.head_dim)
+    if raw is None:
+        raw = torch.empty(geom.n_kv_heads, geom.total_rows, dtype=torch.float32, device=geom.device)
+    if row_lse is None:
+        row_lse = torch.empty(geom.n_q_heads, geom.batch * nr, dtype=torch.float32,
+                              device=geom.device)
+    _need(raw, "raw", _f32(), geom.n_kv_heads * geom.total_rows)
+    _need(row_lse, "row_lse", _f32(), geom.n_q_heads * geom.batch * nr)
+    ws = _workspace(geom, OP_SCORE, ws)
+    _lib.check(_lib.lib().dge_score_with_lse(ctypes.byref(geom.c), rows, _ptr(q), _ptr(k),
+                                             _ptr(raw), _ptr(row_lse), _ptr(ws), ws.numel(),
+                                             _stream(stream)), "dge_score_with_lse")
+    return raw, row_lse
+
+
+def evicted_mass(geom: Geometry, q, n_q: int, q_from_end: int, k_c, n_select: int, n_tail: int,
+                 n_kept, lse_full, rho=None, beta=None, l_match=None, stream=None):
+    """dge_evicted_mass: per-row evicted mass rho [H_q][batch*n_q], and per (sequence, KV
+    head) its mean beta and the attention-matching loss l_match ([batch][H_kv] each)."""
+    torch = _torch()
+    rows = geom.batch * n_q
+    _need(q, "q", (geom.elt_dtype,), geom.n_q_heads * rows * geom.head_dim)
+    _need(k_c, "k_c", (geom.elt_dtype,),
+          geom.batch * geom.n_kv_heads * (n_select + n_tail) * geom.head_dim)
+    _need(n_kept, "n_kept", _i32(), geom.batch)
+    _need(lse_full, "lse_full", _f32(), geom.n_q_heads * rows)
+    if rho is None:
+        rho = torch.empty(geom.n_q_heads, rows, dtype=torch.float32, device=geom.device)
+    if beta is None:
+        beta = torch.empty(geom.batch, geom.n_kv_heads, dtype=torch.float32, device=geom.device)
+    if l_match is None:
+        l_match = torch.empty(geom.batch, geom.n_kv_heads, dtype=torch.float32, device=geom.device)
+    _need(rho, "rho", _f32(), geom.n_q_heads * rows)
+    _need(beta, "beta", _f32(), geom.batch * geom.n_kv_heads)
+    _need(l_match, "l_match", _f32(), geom.batch * geom.n_kv_heads)
+    _lib.check(_lib.lib().dge_evicted_mass(ctypes.byref(geom.c), _ptr(q), n_q, q_from_end,
+                                           _ptr(k_c), n_select, n_tail, _ptr(n_kept),
+                                           _ptr(lse_full), _ptr(rho), _ptr(beta), _ptr(l_match),
+                                           _stream(stream)), "dge_evicted_mass")
+    return rho, beta, l_match
 
 
 def score_noalloc(geom: Geometry, rows: int, q, k, raw=None, stream=None):

@@ -20,7 +20,7 @@ NOALLOC_SCRATCH_BYTES = 16 << 20   # DGE_NOALLOC_SCRATCH_BYTES
 
 # every entry point declared in include/dge.h
 EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_score",
-           "dge_score_noalloc", "dge_score_lse",
+           "dge_score_noalloc", "dge_score_with_lse", "dge_score_lse", "dge_evicted_mass",
            "dge_select_topb", "dge_select_compact", "dge_select_compact_layers",
            "dge_select_streaming", "dge_compact", "dge_compact_inplace",
            "dge_cache_attention", "dge_rope", "dge_retained_runs", "dge_h2o_colsum",
@@ -72,6 +72,12 @@ def lib() -> ctypes.CDLL:
     L.dge_score.argtypes = [GP, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
     L.dge_score_noalloc.restype = c_int
     L.dge_score_noalloc.argtypes = [GP, c_int32, c_void_p, c_void_p, c_void_p, c_void_p]
+    L.dge_score_with_lse.restype = c_int
+    L.dge_score_with_lse.argtypes = [GP, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p, c_size_t, c_void_p]
+    L.dge_evicted_mass.restype = c_int
+    L.dge_evicted_mass.argtypes = [GP, c_void_p, c_int32, c_int32, c_void_p, c_int32, c_int32,
+                                   c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
     L.dge_score_lse.restype = c_int
     L.dge_score_lse.argtypes = [GP, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]
     L.dge_select_topb.restype = c_int

@@ -137,6 +137,18 @@ dge_status_t dge_score(const dge_geom_t* geom, int32_t rows, const void* q, cons
   return hip_status(dge::launch_score(*geom, p, q, k, nullptr, raw, ws, stream));
 }
 
+dge_status_t dge_score_with_lse(const dge_geom_t* geom, int32_t rows, const void* q,
+                                const void* k, float* raw, float* row_lse, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  dge_status_t st = check_score(geom, rows, q, k, raw);
+  if (st != DGE_OK) return st;
+  if (row_lse == nullptr || !aligned16(row_lse)) return DGE_ERR_INVALID;
+  const ScorePlan p = dge::plan_score(*geom, rows);
+  if (ws == nullptr || !aligned16(ws) || ws_bytes < dge::score_workspace_bytes(*geom, p))
+    return DGE_ERR_WORKSPACE;
+  return hip_status(dge::launch_score(*geom, p, q, k, nullptr, raw, ws, stream, row_lse));
+}
+
 dge_status_t dge_score_noalloc(const dge_geom_t* geom, int32_t rows, const void* q,
                                const void* k, float* raw, hipStream_t stream) {
   dge_status_t st = check_score(geom, rows, q, k, raw);
@@ -302,6 +314,26 @@ dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t 
     return DGE_ERR_UNSUPPORTED;
   return hip_status(dge::launch_cache_attention(*geom, q, n_q, q_from_end, k_c, v_c, n_select,
                                                 n_tail, n_kept, out, lse, stream));
+}
+
+dge_status_t dge_evicted_mass(const dge_geom_t* geom, const void* q, int32_t n_q,
+                              int32_t q_from_end, const void* k_c, int32_t n_select,
+                              int32_t n_tail, const int32_t* n_kept, const float* lse_full,
+                              float* rho, float* beta, float* l_match, hipStream_t stream) {
+  dge_status_t st = check_geom(geom);
+  if (st != DGE_OK) return st;
+  if (n_q < 1 || n_select < 0 || n_select > kMaxRows || n_tail < 1 || q_from_end > n_tail ||
+      q_from_end < n_q)
+    return DGE_ERR_INVALID;
+  if (!q || !k_c || !n_kept || !lse_full || !rho || !beta || !l_match || !aligned16(q) ||
+      !aligned16(k_c) || (reinterpret_cast<uintptr_t>(n_kept) & 3) ||
+      (reinterpret_cast<uintptr_t>(lse_full) & 3) || (reinterpret_cast<uintptr_t>(rho) & 3) ||
+      (reinterpret_cast<uintptr_t>(beta) & 3) || (reinterpret_cast<uintptr_t>(l_match) & 3))
+    return DGE_ERR_INVALID;
+  if (geom->n_q_heads / geom->n_kv_heads > dge::cache_attention_max_group())
+    return DGE_ERR_UNSUPPORTED;
+  return hip_status(dge::launch_evicted_mass(*geom, q, n_q, q_from_end, k_c, n_select, n_tail,
+                                             n_kept, lse_full, rho, beta, l_match, stream));
 }
 
 dge_status_t dge_retained_runs(const dge_geom_t* geom, const int32_t* idx, const int32_t* n_kept,

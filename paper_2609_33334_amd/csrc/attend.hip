@@ -13,6 +13,11 @@
 //     reads one V row with consecutive lanes on consecutive elements.
 // This is a check kernel: it reads the compacted K/V once per query row and is bound by
 // that traffic and by latency, not by arithmetic.
+//
+// The MASS variant reads only K: from the log-partition over the retained rows and the
+// caller's full-cache log-partition it writes each observation row's evicted mass
+// rho = 1 - Z_R / Z = -expm1(-(lse_full - lse_R)); a second launch averages rho and the
+// deficit -log(1 - rho) over each (sequence, KV head)'s rows in a fixed order.
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
 
@@ -30,6 +35,10 @@ struct AttArgs {
   const int32_t* n_kept;
   float* out;
   float* lse;
+  const float* lse_full;              // MASS: [H_q][batch * n_q] natural log, full cache
+  float* rho;                         // MASS: [H_q][batch * n_q] evicted mass per row
+  float* beta;                        // MASS: [batch][H_kv] mean rho
+  float* l_match;                     // MASS: [batch][H_kv] mean -log(1 - rho)
   int batch, n_kv_heads, G, n_q, q_from_end, n_select, n_tail, n_out;
   float scale_log2;                   // log2(e) / sqrt(d)
 };
@@ -55,7 +64,7 @@ __device__ __forceinline__ void row_chunk(const float* row, int e0, float (&x)[8
   x[2] = __uint_as_float(u.z); x[3] = __uint_as_float(u.w);
 }
 
-template <typename E, int D>
+template <typename E, int D, bool MASS>
 __global__ __launch_bounds__(kAttThreads) void cache_attention_kernel(AttArgs a) {
   constexpr int kPer16 = 16 / (int)sizeof(E);                 // elements per 16 bytes
   constexpr int kOwn = (kMaxAttG * D + kAttThreads - 1) / kAttThreads;
@@ -142,6 +151,10 @@ __global__ __launch_bounds__(kAttThreads) void cache_attention_kernel(AttArgs a)
       if (g >= G) break;
       sum[g] = sum[g] * alpha[g] + ((reds[g][0] + reds[g][1]) + (reds[g][2] + reds[g][3]));
     }
+    if constexpr (MASS) {
+      __syncthreads();                                        // redm, reds free
+      continue;
+    }
     // output: o[head][dim] = o * alpha + sum_t p[head][t] * V[c0 + t][dim]
     const int n_here = min(kChunk, n_vis - c0);
 #pragma unroll
@@ -162,6 +175,18 @@ __global__ __launch_bounds__(kAttThreads) void cache_attention_kernel(AttArgs a)
     __syncthreads();                                          // ps, redm, reds free
   }
 
+  if constexpr (MASS) {
+    if (tid < G) {
+      const int g = tid;
+      const int64_t ri = (int64_t)(h * G + g) * q_rows + row;
+      const float lse_r = n_vis > 0 ? (m2[g] + __log2f(sum[g])) * 0.6931471805599453f : -INFINITY;
+      // deficit log Z - log Z_R >= 0 (rounding can leave it a hair below 0 when nothing of
+      // the row's attention is evicted)
+      const float dlt = fmaxf(a.lse_full[ri] - lse_r, 0.0f);
+      a.rho[ri] = -expm1f(-dlt);
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < kOwn; ++i) {
     const int e = tid + kAttThreads * i;
@@ -178,11 +203,45 @@ __global__ __launch_bounds__(kAttThreads) void cache_attention_kernel(AttArgs a)
   }
 }
 
-template <typename E, int D>
+// beta[b][h] and l_match[b][h]: means of rho and -log(1 - rho) over the G * n_q rows of
+// (sequence b, KV head h), one wavefront each, summed in a fixed order.
+__global__ __launch_bounds__(64) void mass_reduce_kernel(AttArgs a) {
+  const int b = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int n = a.G * a.n_q;
+  const int64_t q_rows = (int64_t)a.batch * a.n_q;
+  float s_rho = 0.0f, s_def = 0.0f;
+  for (int i = lane; i < n; i += 64) {
+    const int g = i / a.n_q, r = i - g * a.n_q;
+    const float rho = a.rho[(int64_t)(h * a.G + g) * q_rows + b * a.n_q + r];
+    s_rho += rho;
+    s_def += -log1pf(-rho);
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    s_rho += __shfl_xor(s_rho, off, 64);
+    s_def += __shfl_xor(s_def, off, 64);
+  }
+  if (lane == 0) {
+    a.beta[b * a.n_kv_heads + h] = s_rho / (float)n;
+    a.l_match[b * a.n_kv_heads + h] = s_def / (float)n;
+  }
+}
+
+template <typename E, int D, bool MASS>
 hipError_t launch_att(const AttArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((cache_attention_kernel<E, D>), dim3(a.batch * a.n_q, a.n_kv_heads),
+  hipLaunchKernelGGL((cache_attention_kernel<E, D, MASS>), dim3(a.batch * a.n_q, a.n_kv_heads),
                      dim3(kAttThreads), 0, st, a);
+  if constexpr (MASS)
+    hipLaunchKernelGGL(mass_reduce_kernel, dim3(a.batch, a.n_kv_heads), dim3(64), 0, st, a);
   return hipGetLastError();
+}
+
+template <bool MASS>
+hipError_t launch_att_typed(const dge_geom_t& g, const AttArgs& a, hipStream_t st) {
+  if (g.dtype == DGE_BF16)
+    return g.head_dim == 128 ? launch_att<uint16_t, 128, MASS>(a, st)
+                             : launch_att<uint16_t, 64, MASS>(a, st);
+  return g.head_dim == 128 ? launch_att<float, 128, MASS>(a, st) : launch_att<float, 64, MASS>(a, st);
 }
 
 }  // namespace
@@ -209,9 +268,31 @@ hipError_t launch_cache_attention(const dge_geom_t& g, const void* q, int n_q, i
   a.n_tail = n_tail;
   a.n_out = n_select + n_tail;
   a.scale_log2 = kLog2e / sqrtf((float)g.head_dim);
-  if (g.dtype == DGE_BF16)
-    return g.head_dim == 128 ? launch_att<uint16_t, 128>(a, st) : launch_att<uint16_t, 64>(a, st);
-  return g.head_dim == 128 ? launch_att<float, 128>(a, st) : launch_att<float, 64>(a, st);
+  return launch_att_typed<false>(g, a, st);
+}
+
+hipError_t launch_evicted_mass(const dge_geom_t& g, const void* q, int n_q, int q_from_end,
+                               const void* k_c, int n_select, int n_tail, const int32_t* n_kept,
+                               const float* lse_full, float* rho, float* beta, float* l_match,
+                               hipStream_t st) {
+  AttArgs a{};
+  a.q = q;
+  a.k = k_c;
+  a.n_kept = n_kept;
+  a.lse_full = lse_full;
+  a.rho = rho;
+  a.beta = beta;
+  a.l_match = l_match;
+  a.batch = g.batch;
+  a.n_kv_heads = g.n_kv_heads;
+  a.G = g.n_q_heads / g.n_kv_heads;
+  a.n_q = n_q;
+  a.q_from_end = q_from_end;
+  a.n_select = n_select;
+  a.n_tail = n_tail;
+  a.n_out = n_select + n_tail;
+  a.scale_log2 = kLog2e / sqrtf((float)g.head_dim);
+  return launch_att_typed<true>(g, a, st);
 }
 
 }  // namespace dge

@@ -35,7 +35,8 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode);
 size_t score_workspace_bytes(const dge_geom_t& g, const ScorePlan& p);
 
 hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, const void* k,
-                        const float* row_lse, float* raw, void* ws, hipStream_t stream);
+                        const float* row_lse, float* raw, void* ws, hipStream_t stream,
+                        float* lse_out = nullptr);
 
 size_t select_workspace_bytes(const dge_geom_t& g);
 hipError_t launch_select_topb(const dge_geom_t& g, const float* scores, int pool_kernel,
@@ -66,6 +67,11 @@ hipError_t launch_cache_attention(const dge_geom_t& g, const void* q, int n_q, i
                                   const void* k_c, const void* v_c, int n_select, int n_tail,
                                   const int32_t* n_kept, float* out, float* lse,
                                   hipStream_t stream);
+
+hipError_t launch_evicted_mass(const dge_geom_t& g, const void* q, int n_q, int q_from_end,
+                               const void* k_c, int n_select, int n_tail, const int32_t* n_kept,
+                               const float* lse_full, float* rho, float* beta, float* l_match,
+                               hipStream_t stream);
 
 hipError_t launch_retained_runs(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,
                                 int n_select, int32_t* runs, float* mean_len, hipStream_t stream);

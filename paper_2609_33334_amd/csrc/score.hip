@@ -62,6 +62,7 @@ struct ScoreArgs {
   float* partial;    // [batch][H_kv][n_chunks][M_pad] log2-sum-exp of each row per chunk
   float* rowc;       // [batch][H_kv][M_pad]  log2 of each row's softmax normaliser
   const float* lse_in;      // optional [H_q][batch * n_rows] natural-log row LSE
+  float* lse_out;           // optional output: the merged row LSE, natural log, same layout
   SeqOffsets offs;
   int64_t kv_head_stride;   // elements
   int64_t q_head_stride;    // elements between query heads = batch * n_rows * D
@@ -593,7 +594,15 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
   ss *= rescale(mm, mx);
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) ss += __shfl_xor(ss, o, 64);
-  if (lane == 0) a.rowc[base * a.M_pad + m] = mx + __log2f(ss);
+  if (lane == 0) {
+    const float c = mx + __log2f(ss);
+    a.rowc[base * a.M_pad + m] = c;
+    if (a.lse_out != nullptr) {          // query head h * G + g, row b * n_rows + r
+      const int g = m / a.n_rows, r = m - g * a.n_rows;
+      a.lse_out[(int64_t)(h * a.G + g) * a.batch * a.n_rows + b * a.n_rows + r] =
+          c * 0.6931471805599453f;
+    }
+  }
 }
 
 template <typename T, int D, int FT, int RT>
@@ -795,9 +804,11 @@ size_t score_workspace_bytes(const dge_geom_t& g, const ScorePlan& p) {
 }
 
 hipError_t launch_score(const dge_geom_t& g, const ScorePlan& p, const void* q, const void* k,
-                        const float* row_lse, float* raw, void* ws, hipStream_t st) {
+                        const float* row_lse, float* raw, void* ws, hipStream_t st,
+                        float* lse_out) {
   ScoreArgs a{};
   a.lse_in = row_lse;
+  a.lse_out = lse_out;
   a.q = q;
   a.k = k;
   a.raw = raw;

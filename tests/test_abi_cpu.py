@@ -143,6 +143,28 @@ def test_score_noalloc_validation(L):
     assert L.dge_score_noalloc(None, 0, FAKE, FAKE, FAKE, None) == _lib.DGE_ERR_INVALID
 
 
+def test_score_with_lse_and_evicted_mass_validation(L):
+    G = _G()
+    def sl(g=G, lse=FAKE, ws=FAKE, nbytes=1 << 40):
+        return L.dge_score_with_lse(g.p, 0, FAKE, FAKE, FAKE, lse, ws, nbytes, None)
+    assert sl(lse=None) == _lib.DGE_ERR_INVALID
+    assert sl(lse=FAKE + 4) == _lib.DGE_ERR_INVALID
+    assert sl(ws=None) == _lib.DGE_ERR_WORKSPACE
+    assert sl(g=_G(d=96)) == _lib.DGE_ERR_UNSUPPORTED
+
+    def em(g=G, n_q=10, q_from_end=10, n_select=20, n_tail=10, rho=FAKE, lse=FAKE):
+        return L.dge_evicted_mass(g.p, FAKE, n_q, q_from_end, FAKE, n_select, n_tail, FAKE, lse,
+                                  rho, FAKE, FAKE, None)
+    assert em(n_q=0) == _lib.DGE_ERR_INVALID
+    assert em(q_from_end=11) == _lib.DGE_ERR_INVALID         # rows beyond the tail
+    assert em(n_q=11, q_from_end=10, n_tail=12) == _lib.DGE_ERR_INVALID   # rows past the cache end
+    assert em(n_tail=0, q_from_end=0) == _lib.DGE_ERR_INVALID
+    assert em(n_select=-1) == _lib.DGE_ERR_INVALID
+    assert em(rho=None) == _lib.DGE_ERR_INVALID
+    assert em(lse=FAKE + 2) == _lib.DGE_ERR_INVALID
+    assert em(g=_G(hq=18, hkv=1)) == _lib.DGE_ERR_UNSUPPORTED    # more than 8 heads per group
+
+
 def test_workspace_size(L):
     g = _G()
     n = ctypes.c_size_t(0)

@@ -611,6 +611,57 @@ def test_cache_attention_eq1_and_evicted_mass():
     assert err < 2e-4
 
 
+MASS_CASES = {
+    "c2_two_seqs": (di.small_variant("c2", [900, 1400]), None),
+    "c1_f32_d64": (di.WORKLOADS["c1"], None),
+    "c4_length": (di.small_variant("c4", [32768 - 2]), None),
+    "keep_all": (di.small_variant("c2", [300, 500]), 2000),
+}
+
+
+@pytest.mark.parametrize("case", list(MASS_CASES))
+def test_score_with_lse_and_evicted_mass_vs_oracle(case):
+    """dge_score_with_lse's row normalisers against the oracle's log-partitions, its raw
+    scores bit-identical to dge_score's; dge_evicted_mass on the GPU's own compaction
+    against the oracle's rho_q, beta and attention-matching loss (Eq. match) computed
+    directly from the evicted keys of the full cache."""
+    wl, budget = MASS_CASES[case]
+    budget = wl.budget if budget is None else budget
+    _log(f"score_with_lse + evicted_mass {case}: lens={wl.prompt_lens} B={budget}")
+    x = di.make_layer(wl)
+    g = geom_of(wl)
+    q, k, v = to_dev(x.q_bits, wl.dtype), to_dev(x.k_bits, wl.dtype), to_dev(x.v_bits, wl.dtype)
+    n_tail, n_sel = wl.window + wl.k_draft, budget - wl.window
+    raw, row_lse = dge.score_with_lse(g, dge.ROWS_WINDOW_DRAFT, q, k)
+    raw_ref = dge.score(g, dge.ROWS_WINDOW_DRAFT, q, k)
+    idx, nk, kc, vc = dge.select_compact(g, raw, wl.pool, n_tail, n_sel, k, v)
+    rho, beta, lm = dge.evicted_mass(g, q, n_tail, n_tail, kc, n_sel, n_tail, nk, row_lse)
+    torch.cuda.synchronize()
+    assert torch.equal(raw.view(torch.int32), raw_ref.view(torch.int32))
+    want_lse = oracle.scoring_row_lse(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                      wl.window, wl.k_draft)
+    lerr = float(np.abs(row_lse.cpu().numpy().astype(np.float64) - want_lse).max())
+    _log(f"  row log-partitions: max |err| {lerr:.2e}")
+    assert lerr <= 1e-4
+    idx_h, nk_h = idx.cpu().numpy(), nk.cpu().numpy()
+    kept = {(b, h): idx_h[b, h, :nk_h[b]] for b in range(wl.batch) for h in range(wl.n_kv_heads)}
+    w_rho, w_beta, w_lm = oracle.eviction_diagnostics(x.q, x.k, wl.kv_offsets, wl.n_q_heads,
+                                                      wl.n_kv_heads, kept, n_tail, n_tail)
+    g_rho = rho.cpu().numpy().astype(np.float64)
+    g_beta, g_lm = beta.cpu().numpy().astype(np.float64), lm.cpu().numpy().astype(np.float64)
+    e_rho = float(np.abs(g_rho - w_rho).max())
+    e_beta = float(np.abs(g_beta - w_beta).max())
+    e_lm = float(np.abs(g_lm - w_lm).max())
+    _log(f"  rho max |err| {e_rho:.2e}, beta {e_beta:.2e}, L_match {e_lm:.2e}; "
+         f"beta in [{w_beta.min():.3g}, {w_beta.max():.3g}], L_match mean {w_lm.mean():.4f}")
+    # rho is a difference of two float32 log-partitions: absolute bound, plus 1e-3 relative
+    # on the loss (which grows as rho approaches 1)
+    assert e_rho <= 1e-4 and e_beta <= 1e-4
+    assert (np.abs(g_lm - w_lm) <= 1e-4 + 1e-3 * np.abs(w_lm)).all()
+    if case == "keep_all":
+        assert w_rho.max() == 0 and g_rho.max() <= 1e-5
+
+
 # ----------------------------------------------------------------------------------
 # Retained-set contiguity (dge_retained_runs) against the oracle: exact counts, and the
 # float32 mean n_kept / runs

@@ -303,6 +303,78 @@ def test_compaction_attention_identities():
 
 
 # ----------------------------------------------------------------------------------
+# Evicted mass of the observation rows and the attention-matching loss (Eq. match)
+# ----------------------------------------------------------------------------------
+def _diag_case(seed, lens=(40, 57), Hq=4, Hkv=2, d=16, n_tail=6):
+    q = _rand((Hq, len(lens) * n_tail, d), seed, 1.5)
+    k = _rand((Hkv, sum(lens), d), seed + 1, 1.5)
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    return q, k, offs, Hq, Hkv, n_tail, lens
+
+
+def test_eviction_diagnostics_against_torch_softmax():
+    """rho_q against torch's float64 softmax mass on the evicted keys, and the loss against
+    torch's logsumexp over the full and the retained keys (the two sides of Eq. match)."""
+    q, k, offs, Hq, Hkv, n_tail, lens = _diag_case(41)
+    rng = np.random.default_rng(5)
+    kept = {(b, h): np.sort(rng.choice(N - n_tail, size=(N - n_tail) // 3, replace=False))
+            for b, N in enumerate(lens) for h in range(Hkv)}
+    rho, beta, lm = oracle.eviction_diagnostics(q, k, offs, Hq, Hkv, kept, n_tail, n_tail)
+    G = Hq // Hkv
+    for b, N in enumerate(lens):
+        C = N - n_tail
+        for h in range(Hkv):
+            keep = torch.zeros(N, dtype=torch.bool)
+            keep[torch.from_numpy(kept[(b, h)])] = True
+            keep[C:] = True
+            rows, losses = [], []
+            for g in range(G):
+                for r in range(n_tail):
+                    p = C + r
+                    x = torch.from_numpy(k[h, offs[b]:offs[b] + p + 1]) @ torch.from_numpy(q[h * G + g, b * n_tail + r])
+                    x = x / math.sqrt(k.shape[2])
+                    a = torch.softmax(x, dim=0)
+                    want = float(a[~keep[:p + 1]].sum())
+                    assert abs(rho[h * G + g, b * n_tail + r] - want) < 1e-13
+                    rows.append(want)
+                    losses.append(float(torch.logsumexp(x, 0) - torch.logsumexp(x[keep[:p + 1]], 0)))
+            assert abs(beta[b, h] - np.mean(rows)) < 1e-13
+            assert abs(lm[b, h] - np.mean(losses)) < 1e-12
+
+
+def test_eviction_diagnostics_match_loss_identity_and_special_cases():
+    q, k, offs, Hq, Hkv, n_tail, lens = _diag_case(43)
+    G = Hq // Hkv
+    rng = np.random.default_rng(6)
+    kept = {(b, h): np.sort(rng.choice(N - n_tail, size=5, replace=False))
+            for b, N in enumerate(lens) for h in range(Hkv)}
+    rho, beta, lm = oracle.eviction_diagnostics(q, k, offs, Hq, Hkv, kept, n_tail, n_tail)
+    # Eq. match: E_q[-log(1 - rho_q)] equals the mean log-partition deficit
+    for b in range(len(lens)):
+        for h in range(Hkv):
+            r = rho[h * G:(h + 1) * G, b * n_tail:(b + 1) * n_tail]
+            assert abs(lm[b, h] - np.mean(-np.log1p(-r))) < 1e-12
+            assert 0 < beta[b, h] < 1
+    # keep-all: nothing evicted
+    all_kept = {(b, h): np.arange(N - n_tail) for b, N in enumerate(lens) for h in range(Hkv)}
+    rho0, beta0, lm0 = oracle.eviction_diagnostics(q, k, offs, Hq, Hkv, all_kept, n_tail, n_tail)
+    assert (rho0 == 0).all() and (beta0 == 0).all() and np.abs(lm0).max() < 1e-12
+    # uniform attention (q = 0), nothing kept but the tail: a row at position p spreads
+    # 1/(p+1) over its keys, so rho = C/(p+1) and the loss is log((p+1)/(p+1-C))
+    none = {(b, h): np.zeros(0, np.int64) for b in range(len(lens)) for h in range(Hkv)}
+    rho1, beta1, lm1 = oracle.eviction_diagnostics(np.zeros_like(q), k, offs, Hq, Hkv, none,
+                                                   n_tail, n_tail)
+    for b, N in enumerate(lens):
+        C = N - n_tail
+        want = np.array([C / (C + r + 1) for r in range(n_tail)])
+        for hq in range(Hq):
+            assert np.allclose(rho1[hq, b * n_tail:(b + 1) * n_tail], want, rtol=1e-14)
+        for h in range(Hkv):
+            assert abs(beta1[b, h] - want.mean()) < 1e-14
+            assert abs(lm1[b, h] - np.mean([math.log((C + r + 1) / (r + 1)) for r in range(n_tail)])) < 1e-12
+
+
+# ----------------------------------------------------------------------------------
 # Attention over a compacted cache (continuation check)
 # ----------------------------------------------------------------------------------
 def _compacted(k, v, idx_per_seq, n_tail, offs, n_out):
