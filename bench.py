@@ -84,6 +84,10 @@ def parse():
     p.add_argument("--rope", action="store_true",
                    help="only time dge_rope on the workload's keys (every cached row of every KV "
                         "head), HIP events per call; one JSON line with its HBM rate")
+    p.add_argument("--project", action="store_true",
+                   help="only time dge_project_rope (query/key capture from the layer input) at "
+                        "Llama-3-8B shapes: the scoring rows' q and k projections (HBM-bound on the "
+                        "weights) and every row of an 8194-row layer (matrix cores); one JSON line")
     p.add_argument("--compact-cmp", action="store_true",
                    help="only time dge_compact (out of place) against dge_compact_inplace on one "
                         "layer of the workload, the cache restored outside the timed events")
@@ -114,6 +118,8 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     dev = "cuda:0"
+    if args.project:
+        return bench_project(args, dev)
     wl = di.WORKLOADS[args.workload]
     log(f"[bench] workload {wl.name}: generating inputs")
     x = di.make_layer(wl, with_v=True)
@@ -360,7 +366,9 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6),
         "ms_per_step_median": round(ms_median, 6), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if is_bf16 else "f32",
-        "data": "synthetic (seeded Gaussian Q/K/V with planted spans; no model weights)",
+        "data": ("synthetic (seeded Gaussian Q/K/V"
+                 + {"spans": " with planted spans", "scale_rows": " with planted x4 keys"}.get(wl.plant, "")
+                 + (", every layer its own draw" if L_layers > 1 else "") + "; no model weights)"),
         "config": {"workload": WORKLOAD_TEXT.get(wl.name, wl.name),
                    "global_batch": wl.batch, "seq_len": L, "layers": L_layers,
                    "parallelism": "single GPU",
@@ -579,6 +587,65 @@ def bench_rope(args, wl, x, dev):
                       "GBps": round(nbytes / us / 1e3, 1),
                       "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "reps": reps}),
           flush=True)
+
+
+def bench_project(args, dev):
+    """dge_project_rope at Llama-3-8B shapes (hidden 4096, 32 query / 8 KV heads of 128): the
+    34 scoring rows (window 32 + k 2) through W_q and W_k, bound by streaming the weights
+    from HBM, and all 8194 rows of a layer through W_q (H2O's prompt queries), bound by the
+    matrix cores.  Synthetic bf16 inputs (x ~ N(0,1), W ~ N(0, 1/hidden)), weights rotated
+    over enough copies that no call finds them in the Infinity Cache; HIP events around
+    back-to-back calls on the launching stream (median of five groups).  Prints one JSON
+    line."""
+    import torch
+    import paper_2609_33334_amd as dge
+    hidden, d = 4096, 128
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2609)
+    reps = max(20, min(args.steps, 200))
+    res = {}
+    for name, rows, heads, n_sets in (("q_scoring_rows", 34, 32, 16), ("k_scoring_rows", 34, 8, 48),
+                                      ("fused_qk_scoring_rows", 34, 40, 16),
+                                      ("q_all_rows_8194", 8194, 32, 4)):
+        x = torch.randn(rows, hidden, generator=gen, device=dev).to(torch.bfloat16)
+        ws = [(torch.randn(heads * d, hidden, generator=gen, device=dev) / hidden ** 0.5).to(torch.bfloat16)
+              for _ in range(n_sets)]
+        pos = torch.arange(26507, 26507 + rows, dtype=torch.int32, device=dev)
+        out = torch.empty(heads, rows, d, dtype=torch.bfloat16, device=dev)
+        for i in range(2 * n_sets):
+            dge.project_rope(x, ws[i % n_sets], pos, heads, d, out=out)
+        torch.cuda.synchronize()
+        # back-to-back calls between two HIP events on the launching stream: the average
+        # launch duration (a lone event pair would add the launch latency to every call)
+        stream = torch.cuda.current_stream()
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for i in range(reps):
+                dge.project_rope(x, ws[i % n_sets], pos, heads, d, out=out)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3 / reps)
+        us = float(np.median(ts))
+        nbytes = heads * d * hidden * 2 + rows * hidden * 2 + heads * rows * d * 2 + rows * 4
+        flops = 2 * rows * heads * d * hidden
+        gbs = nbytes / us / 1e3
+        tfs = flops / us / 1e6
+        entry = {"rows": rows, "heads": heads, "us_per_call": round(us, 3), "bytes": nbytes,
+                 "flops": flops, "GBps": round(gbs, 1), "TFLOPs": round(tfs, 1)}
+        if rows < 1000:
+            entry["roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                                 "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        else:
+            entry["roofline"] = {"bound": "mfma", "achieved": round(tfs, 1),
+                                 "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                                 "frac": round(tfs / MFMA_BF16_PEAK_TFS, 4)}
+        res[name] = entry
+        log(f"[bench] project_rope {name}: {us:.2f} us, {gbs:.0f} GB/s, {tfs:.0f} TFLOP/s")
+        del ws, x, out
+    print(json.dumps({"kernel": "dge_project_rope (RoPE(x W^T), hidden 4096, head_dim 128, bf16)",
+                      "reps": reps, "cases": res}), flush=True)
 
 
 def bench_compact_cmp(args, wl, x, dev):

@@ -339,6 +339,27 @@ dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t
                       int64_t head_stride, const int32_t *positions, double theta, void *x,
                       hipStream_t stream);
 
+/* Query/key capture from a layer's input (App. "Draft-guided eviction implementation": the
+ * post-RoPE queries are recomputed from each layer's input by forward pre-hooks): the
+ * projection by a Linear weight and the rotary embedding of dge_rope in one launch,
+ *   out[h][r][:] = RoPE_{positions[r]}( (x W^T)[r][h*head_dim .. (h+1)*head_dim) ),
+ * products on the matrix cores (bf16 in, float32 accumulate), each rotate-half pair
+ * (i, i + head_dim/2) turned by positions[r] * theta^(-2i/head_dim) (the angle formed and
+ * reduced modulo 2 pi in double, the rotation applied in float to the float32 sums), rounded
+ * once to bf16 (round to nearest even).
+ *   x         : [n_rows][hidden] bf16, the layer input rows (e.g. the window and draft rows).
+ *   w         : [n_heads * head_dim][hidden] bf16, the Linear weight (W_q, or W_k for keys),
+ *               rows = output features, as torch.nn.Linear stores it.
+ *   positions : [n_rows] int32 absolute positions.
+ *   out       : [n_heads][n_rows][head_dim] bf16 output, the Q layout dge_score reads.
+ * No workspace; n_rows == 0 does nothing.  Errors: DGE_ERR_INVALID for n_rows < 0,
+ * n_heads < 1, hidden < 1, theta <= 1 or not finite, a NULL / misaligned pointer (16 bytes;
+ * positions 4); DGE_ERR_UNSUPPORTED for head_dim outside {64, 128}, hidden not a multiple of
+ * 128 or more than 4,194,240 rows. */
+dge_status_t dge_project_rope(int32_t n_rows, int32_t hidden, const void *x, int32_t n_heads,
+                              int32_t head_dim, const void *w, const int32_t *positions,
+                              double theta, void *out, hipStream_t stream);
+
 /* Contiguity of the retained sets (Sec. 4, "Selection trades coverage for contiguity";
  * Table "Selection decomposition", column "run len."): for sequence b and KV head h,
  *   runs[b][h]     = number of maximal runs of consecutive positions among the first

@@ -419,3 +419,16 @@ def rope(x, positions, theta: float = 500000.0) -> np.ndarray:
     a, b = x[..., :half], x[..., half:]
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
 
+
+
+def project_rope(x, w, positions, n_heads: int, head_dim: int, theta: float = 500000.0) -> np.ndarray:
+    """Query/key capture from a layer's input: the Linear projection x W^T split into heads,
+    then the rotary embedding of each row at its position (App. "Draft-guided eviction
+    implementation": post-RoPE queries recomputed from the layer input).
+
+    x [n_rows][hidden], w [n_heads * head_dim][hidden] (rows = output features) ->
+    [n_heads][n_rows][head_dim], float64.
+    """
+    y = as_f64(x) @ as_f64(w).T
+    y = y.reshape(y.shape[0], n_heads, head_dim).transpose(1, 0, 2)
+    return rope(y, positions, theta)

@@ -25,7 +25,7 @@ from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  
 __all__ = ["Geometry", "score", "score_noalloc", "score_with_lse", "score_lse", "evicted_mass", "select_topb", "select_compact",
            "select_compact_layers", "select_streaming", "compact", "compact_inplace",
            "cache_attention",
-           "rope", "retained_runs", "h2o_colsum",
+           "rope", "project_rope", "retained_runs", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
 
@@ -442,6 +442,31 @@ def rope(x, positions, theta: float = 500000.0, stream=None):
                                    x.shape[1] * x.shape[2], _ptr(positions), float(theta),
                                    _ptr(x), _stream(stream)), "dge_rope")
     return x
+
+
+def project_rope(x, w, positions, n_heads: int, head_dim: int, theta: float = 500000.0,
+                 out=None, stream=None):
+    """dge_project_rope: out = RoPE(x W^T) per head, x [n_rows][hidden] bf16, w
+    [n_heads*head_dim][hidden] bf16 (a Linear weight), int32 positions [n_rows].  Returns
+    out [n_heads][n_rows][head_dim] bf16."""
+    torch = _torch()
+    if not isinstance(x, torch.Tensor) or x.dim() != 2 or not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise ValueError("x: [n_rows][hidden] and w: [n_heads * head_dim][hidden] expected")
+    n_rows, hidden = x.shape
+    if w.shape[0] != n_heads * head_dim or w.shape[1] != hidden:
+        raise ValueError(f"w: shape {tuple(w.shape)}, expected ({n_heads * head_dim}, {hidden})")
+    _need(x, "x", (torch.bfloat16,))
+    _need(w, "w", (torch.bfloat16,))
+    if not isinstance(positions, torch.Tensor) or positions.dtype != torch.int32:
+        raise TypeError("positions: expected an int32 tensor")
+    _need(positions, "positions", _i32(), n_rows)
+    if out is None:
+        out = torch.empty(n_heads, n_rows, head_dim, dtype=torch.bfloat16, device=x.device)
+    _need(out, "out", (torch.bfloat16,), n_heads * n_rows * head_dim)
+    _lib.check(_lib.lib().dge_project_rope(n_rows, hidden, _ptr(x), n_heads, head_dim, _ptr(w),
+                                           _ptr(positions), float(theta), _ptr(out),
+                                           _stream(stream)), "dge_project_rope")
+    return out
 
 
 def retained_runs(geom: Geometry, idx, n_kept, runs=None, mean_len=None, stream=None):

@@ -297,6 +297,22 @@ dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t
       dge::launch_rope(n_heads, n_rows, head_dim, dtype, head_stride, positions, theta, x, stream));
 }
 
+dge_status_t dge_project_rope(int32_t n_rows, int32_t hidden, const void* x, int32_t n_heads,
+                              int32_t head_dim, const void* w, const int32_t* positions,
+                              double theta, void* out, hipStream_t stream) {
+  if (n_rows < 0 || n_heads < 1 || hidden < 1) return DGE_ERR_INVALID;
+  if (head_dim != 64 && head_dim != 128) return DGE_ERR_UNSUPPORTED;
+  if (hidden % 128 != 0) return DGE_ERR_UNSUPPORTED;
+  if (n_rows > 64 * 65535 || (int64_t)n_heads * (head_dim / 16) > INT32_MAX) return DGE_ERR_UNSUPPORTED;
+  if (!(theta > 1.0) || !(theta < 1e300)) return DGE_ERR_INVALID;
+  if (n_rows == 0) return DGE_OK;
+  if (!x || !w || !positions || !out || !aligned16(x) || !aligned16(w) || !aligned16(out) ||
+      (reinterpret_cast<uintptr_t>(positions) & 3))
+    return DGE_ERR_INVALID;
+  return hip_status(dge::launch_project_rope(n_rows, hidden, x, n_heads, head_dim, w, positions,
+                                             theta, out, stream));
+}
+
 dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t n_q,
                                  int32_t q_from_end, const void* k_c, const void* v_c,
                                  int32_t n_select, int32_t n_tail, const int32_t* n_kept,

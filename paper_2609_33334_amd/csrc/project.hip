@@ -1,0 +1,175 @@
+// Query/key capture from a layer's input: out = RoPE(x W^T), the post-RoPE rows the scoring
+// reads (App. "Draft-guided eviction implementation": queries recomputed post-RoPE from each
+// layer's input by forward pre-hooks; rotate-half pairs (i, i + d/2) as in the
+// compensation-token appendix; theta = 500,000 for the Table "Backbones" models).
+//
+// A bf16 matrix-core product with the rotation in its epilogue.  W is a Linear weight
+// [n_heads * d][hidden] (rows = output features, K contiguous), x is [n_rows][hidden], so
+// both operands stream along K with 16-byte loads, like Q and K in the scoring.
+//
+// Work split.  A workgroup owns 16 output columns that hold 8 complete rotation pairs,
+// columns {8q .. 8q+7} and {d/2 + 8q .. d/2 + 8q+7} of one head, and a block of up to 64
+// rows (as many 16-row tiles as the rows need); its eight wavefronts take an eighth of the
+// hidden dimension each, with eight K steps of loads in flight, and their partial products
+// are summed in LDS in a fixed order.  For the scoring rows (tens of rows) the product is
+// bound by streaming W once (HBM); a Llama-3-8B query projection gives 4096 / 16 = 256
+// workgroups, and a fused [W_q; W_k] weight (40 heads) 320 in one launch.  In a 16x16
+// accumulator tile lane l holds column l % 16, so the partner of a low column sits eight
+// lanes away and one shuffle pairs them.  The angle is formed and reduced modulo 2 pi in
+// double (positions reach 32K and beyond), its sine and cosine and the rotation of the
+// float32 sums in float, and the result is rounded once to bf16.
+#include "dge_device.hpp"
+#include "dge_internal.hpp"
+
+namespace dge {
+namespace {
+
+constexpr int kProjUnroll = 8;               // K steps of 32 whose loads are issued together
+constexpr int kMaxHalfProj = 64;
+
+struct ProjArgs {
+  const uint16_t* x;        // [n_rows][hidden] bf16
+  const uint16_t* w;        // [n_heads * d][hidden] bf16
+  const int32_t* pos;       // [n_rows]
+  uint16_t* out;            // [n_heads][n_rows][d] bf16
+  int n_rows, hidden, n_heads, d, half;
+  double inv_freq[kMaxHalfProj];
+};
+
+__device__ __forceinline__ uint16_t to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// MT row tiles per workgroup, WAVES wavefronts splitting the hidden dimension.
+template <int MT, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void project_rope_kernel(ProjArgs a) {
+  const int groups = a.half / 8;                     // 8-pair column groups per head
+  const int head = blockIdx.x / groups, grp = blockIdx.x % groups;
+  const int row0 = blockIdx.y * (16 * MT);
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c16 = lane & 15, g16 = lane >> 4;
+  // this lane's output column (low half for c16 < 8, its partner d/2 columns higher)
+  const int pair = 8 * grp + (c16 & 7);
+  const int col = head * a.d + (c16 < 8 ? pair : a.half + pair);
+  const int kq = a.hidden / WAVES;                   // K range of this wavefront
+  const int k_begin = wv * kq;
+  const uint16_t* wrow = a.w + (int64_t)col * a.hidden + k_begin + 8 * g16;
+  const uint16_t* xrow[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int r = min(row0 + 16 * i + c16, a.n_rows - 1);   // rows past the end repeat the last
+    xrow[i] = a.x + (int64_t)r * a.hidden + k_begin + 8 * g16;
+  }
+  f32x4_t acc[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int steps = kq / 32;
+  int s = 0;
+  for (; s + kProjUnroll <= steps; s += kProjUnroll) {
+    // every load of the unrolled steps in flight at once (asm loads: the compiler would
+    // otherwise issue them one step at a time to save registers), one wait, then the
+    // products
+    u32x4_t bw[kProjUnroll], ax[kProjUnroll][MT];
+#pragma unroll
+    for (int u = 0; u < kProjUnroll; ++u) {
+      bw[u] = async_load16(wrow + 32 * (s + u));
+#pragma unroll
+      for (int i = 0; i < MT; ++i) ax[u][i] = async_load16(xrow[i] + 32 * (s + u));
+    }
+    asm_wait_vmcnt<0>();
+#pragma unroll
+    for (int u = 0; u < kProjUnroll; ++u) {
+      reg_fence(bw[u]);
+#pragma unroll
+      for (int i = 0; i < MT; ++i) reg_fence(ax[u][i]);
+    }
+#pragma unroll
+    for (int u = 0; u < kProjUnroll; ++u)
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+        acc[i] = mma_step(bf16_t{}, as_uint4(ax[u][i]), as_uint4(bw[u]), acc[i]);
+  }
+  for (; s < steps; ++s) {
+    const uint4 bw = load16(wrow + 32 * s);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) acc[i] = mma_step(bf16_t{}, load16(xrow[i] + 32 * s), bw, acc[i]);
+  }
+  // sum of the wavefronts' partial products in a fixed order, wavefront i finishing row
+  // tile i
+  __shared__ float part[WAVES][MT][4][64];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) part[wv][i][t][lane] = acc[i][t];
+  __syncthreads();
+  if (wv >= MT) return;
+  const int i = wv;
+  float v[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    float sum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) sum += part[w][i][t][lane];
+    v[t] = sum;
+  }
+  // rotation: lane c16 < 8 holds x_pair, lane c16 + 8 holds x_{pair + d/2}, same rows
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int r = row0 + 16 * i + 4 * g16 + t;
+    const float other = __shfl_xor(v[t], 8, 64);
+    if (r < a.n_rows) {
+      // the angle in double, reduced to [-pi, pi] with a two-part 2 pi, then sine and cosine
+      // in float: ~3e-7 of error, far below the bf16 rounding of the result
+      const double ang = (double)a.pos[r] * a.inv_freq[pair];
+      const double k = rint(ang * 0.15915494309189535);
+      const double red = fma(-k, 2.4492935982947064e-16, fma(-k, 6.283185307179586, ang));
+      float sn, cs;
+      sincosf((float)red, &sn, &cs);
+      const float lo = c16 < 8 ? v[t] : other;
+      const float hi = c16 < 8 ? other : v[t];
+      const float res = c16 < 8 ? fmaf(lo, cs, -hi * sn) : fmaf(hi, cs, lo * sn);
+      const int dcol = c16 < 8 ? pair : a.half + pair;
+      a.out[((int64_t)head * a.n_rows + r) * a.d + dcol] = to_bf16_rne(res);
+    }
+  }
+}
+
+template <int WAVES>
+hipError_t launch_proj_waves(const ProjArgs& a, hipStream_t st) {
+  // row tiles per workgroup: just enough for a short row set (the scoring rows), else 4
+  const int mt = a.n_rows >= 64 ? 4 : (a.n_rows + 15) / 16;
+  const dim3 grid(a.n_heads * (a.half / 8), (a.n_rows + 16 * mt - 1) / (16 * mt));
+  const dim3 block(64 * WAVES);
+  switch (mt) {
+    case 1: hipLaunchKernelGGL((project_rope_kernel<1, WAVES>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((project_rope_kernel<2, WAVES>), grid, block, 0, st, a); break;
+    case 3: hipLaunchKernelGGL((project_rope_kernel<3, WAVES>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((project_rope_kernel<4, WAVES>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_heads, int head_dim,
+                               const void* w, const int32_t* positions, double theta, void* out,
+                               hipStream_t st) {
+  ProjArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.w = static_cast<const uint16_t*>(w);
+  a.pos = positions;
+  a.out = static_cast<uint16_t*>(out);
+  a.n_rows = n_rows;
+  a.hidden = hidden;
+  a.n_heads = n_heads;
+  a.d = head_dim;
+  a.half = head_dim / 2;
+  for (int i = 0; i < a.half; ++i) a.inv_freq[i] = pow(theta, -2.0 * i / head_dim);
+  // eight wavefronts split the hidden dimension (each keeps 8 K steps of loads in flight),
+  // four when it is not a multiple of 256
+  return hidden % 256 == 0 ? launch_proj_waves<8>(a, st) : launch_proj_waves<4>(a, st);
+}
+
+}  // namespace dge

@@ -10,6 +10,7 @@ Tolerances (written here, derived in the design notes):
   1e-3 is dropped, and the counts agree;
 * compaction: byte-exact given the GPU's own indices.
 """
+import math
 import sys
 
 import numpy as np
@@ -1016,3 +1017,47 @@ def test_rope_parity(case):
     r_in = np.hypot(x_in[..., :half], x_in[..., half:])
     r_out = np.hypot(got[..., :half], got[..., half:])
     assert np.allclose(r_out, r_in, rtol=2 * ulp, atol=1e-6)
+
+
+# ----------------------------------------------------------------------------------
+# Query/key capture from the layer input: RoPE(x W^T) (dge_project_rope)
+# ----------------------------------------------------------------------------------
+PROJ_CASES = {
+    # name: (n_rows, hidden, n_heads, head_dim, first position, rows checked)
+    "llama_q_scoring_rows": (34, 4096, 32, 128, 26507, None),
+    "llama_k_scoring_rows": (34, 4096, 8, 128, 26507, None),
+    "fused_qk_weight": (34, 4096, 40, 128, 26507, None),
+    "hidden_384_rows_70": (70, 384, 6, 128, 100, None),
+    "d64_ragged_rows": (130, 1024, 4, 64, 0, None),
+    "one_row": (1, 128, 1, 64, 7, None),
+    "h2o_all_rows_sampled": (8194, 4096, 32, 128, 0, 48),
+}
+
+
+@pytest.mark.parametrize("case", list(PROJ_CASES))
+def test_project_rope_vs_oracle(case):
+    """dge_project_rope against the float64 composition RoPE(x W^T): each output within half
+    a bf16 ulp of the exact value plus the float32 accumulation bound (2^-8 |o| +
+    8e-5 * sum_k |x_k| (|w_lo,k| + |w_hi,k|), the rotation mixing the two columns of a pair);
+    on the 8194-row case sampled rows only."""
+    n, hidden, H, d, p0, n_check = PROJ_CASES[case]
+    _log(f"project_rope {case}: rows={n} hidden={hidden} heads={H} d={d}")
+    rng = np.random.default_rng(np.random.SeedSequence([61, n, hidden, H]))
+    xb = di.f32_to_bf16_bits(rng.standard_normal((n, hidden), dtype=np.float32))
+    wb = di.f32_to_bf16_bits((rng.standard_normal((H * d, hidden)) / math.sqrt(hidden)).astype(np.float32))
+    pos = (p0 + np.arange(n)).astype(np.int32)
+    if case == "d64_ragged_rows":
+        pos = np.sort(rng.integers(0, 1 << 17, size=n)).astype(np.int32)
+    out = dge.project_rope(to_dev(xb, "bf16"), to_dev(wb, "bf16"), torch.from_numpy(pos).to(DEV), H, d)
+    torch.cuda.synchronize()
+    got = di.bf16_bits_to_f32(out.cpu().view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
+    rows = np.arange(n) if n_check is None else np.sort(rng.choice(n, size=n_check, replace=False))
+    x64 = di.bf16_bits_to_f32(xb).astype(np.float64)[rows]
+    w64 = di.bf16_bits_to_f32(wb).astype(np.float64)
+    want = oracle.project_rope(x64, w64, pos[rows], H, d)
+    s = (np.abs(x64) @ np.abs(w64).T).reshape(len(rows), H, d).transpose(1, 0, 2)
+    s_pair = np.concatenate([s[..., :d // 2] + s[..., d // 2:]] * 2, axis=-1)
+    err = np.abs(got[:, rows] - want)
+    tol = 2.0 ** -8 * np.abs(want) + 8e-5 * s_pair
+    _log(f"  max |err| {err.max():.3e}, max err/tol {float((err / tol).max()):.3f}")
+    assert (err <= tol).all(), (case, int((err > tol).sum()))

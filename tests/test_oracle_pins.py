@@ -606,3 +606,38 @@ def test_rope_is_a_complex_phase_and_keeps_relative_positions():
         return float(oracle.rope(q[None], [p])[0] @ oracle.rope(k[None], [s])[0])
     assert math.isclose(logit(50, 20), logit(1050, 1020), rel_tol=1e-10)
     assert math.isclose(logit(7, 7), float(q @ k), rel_tol=1e-10)
+
+
+# ----------------------------------------------------------------------------------
+# Query/key capture: RoPE(x W^T) per head
+# ----------------------------------------------------------------------------------
+def test_project_rope_against_torch_linear_and_complex_phase():
+    """The composition against torch's float64 Linear (head split [n][H*d] -> [H][n][d])
+    and the rotation written as a complex phase (an implementation independent of
+    oracle.rope); at position 0 the output is the plain projection."""
+    rng = np.random.default_rng(23)
+    n, hidden, H, d = 7, 48, 3, 16
+    x = rng.standard_normal((n, hidden))
+    w = rng.standard_normal((H * d, hidden)) / math.sqrt(hidden)
+    pos = np.array([0, 3, 17, 255, 4096, 30000, 2])
+    got = oracle.project_rope(x, w, pos, H, d)
+    y = torch.nn.functional.linear(torch.from_numpy(x), torch.from_numpy(w))
+    y = y.view(n, H, d).permute(1, 0, 2).numpy()
+    z = y[..., :d // 2] + 1j * y[..., d // 2:]
+    z = z * np.exp(1j * pos[:, None] * 500000.0 ** (-np.arange(d // 2) * 2.0 / d))
+    assert np.allclose(got, np.concatenate([z.real, z.imag], axis=-1), rtol=0, atol=1e-12)
+    assert np.allclose(got[:, 0], y[:, 0], rtol=0, atol=1e-13)      # position 0: identity
+    assert got.shape == (H, n, d)
+
+
+def test_project_rope_logits_depend_on_position_difference():
+    rng = np.random.default_rng(29)
+    hidden, d = 32, 8
+    xq, xk = rng.standard_normal((1, hidden)), rng.standard_normal((1, hidden))
+    wq, wk = rng.standard_normal((d, hidden)), rng.standard_normal((d, hidden))
+    def logit(p, s):
+        q = oracle.project_rope(xq, wq, [p], 1, d)[0, 0]
+        k = oracle.project_rope(xk, wk, [s], 1, d)[0, 0]
+        return float(q @ k)
+    assert math.isclose(logit(40, 10), logit(1040, 1010), rel_tol=1e-10)
+    assert math.isclose(logit(9, 9), float((xq @ wq.T)[0] @ (xk @ wk.T)[0]), rel_tol=1e-10)
