@@ -257,7 +257,10 @@ dge_status_t dge_compact(const dge_geom_t *geom, const int32_t *idx, const int32
  *                 idx[b][h][r] >= r (an entry below r is raised to r, one past C_b - 1
  *                 lowered to C_b - 1; rows are never moved upwards).
  *   k, v        : the cache, layout above; distinct buffers.
- * No workspace; one workgroup per (KV head, sequence) copies its rows in order.
+ * No workspace.  Two launches: the rows whose source lies below n_kept[b] + n_tail (a short
+ * prefix, typically) are moved in order by one workgroup per (KV head, sequence); every
+ * other row's source is never overwritten, and those rows are copied by many workgroups
+ * at once.
  * Errors: DGE_ERR_INVALID for n_select < 0, n_tail outside [0, N_b], k == v or a NULL /
  * misaligned pointer. */
 dge_status_t dge_compact_inplace(const dge_geom_t *geom, const int32_t *idx,

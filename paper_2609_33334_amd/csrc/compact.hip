@@ -63,20 +63,35 @@ hipError_t launch_rb(const CompactArgs& a, const dge_geom_t& g, hipStream_t st) 
   return hipGetLastError();
 }
 
-// In-place compaction: the compacted rows of (b, h) overwrite the first n_kept + n_tail
-// rows of that head's own segment of the cache.  Every retained row moves down or stays
-// (idx is ascending, so idx[r] >= r; tail row t moves from C + t to n_kept + t).  One
-// workgroup per (KV head, sequence) walks the output rows in chunks: it reads every
-// source row of a chunk, meets a barrier, then writes the chunk.  The rows a chunk
-// writes lie below every source of the later chunks (a source is never below its own
-// output row), and the sources of this and the earlier chunks were read before the
-// barrier, so no row is overwritten before it has been read.
+// In-place compaction: the compacted rows of (b, h) overwrite the first n_out = n_kept +
+// n_tail rows of that head's own segment of the cache.  Output row r takes source row
+// src(r) = idx[r] (r < n_kept) or C + (r - n_kept) (the tail); sources ascend with r and
+// src(r) >= r, so rows only move down.  Only rows [0, n_out) are written, so a source at or
+// above n_out is never overwritten: the rows whose source lies there ("far" rows) can be
+// copied in any order by any number of workgroups.  The others ("near" rows, src(r) <
+// n_out) form a prefix of the output rows, and their sources may be the destinations of
+// other rows.  Two launches:
+//   1. near rows, one workgroup per (KV head, sequence), in order: it reads every source
+//      of a chunk of rows, meets a barrier, then writes the chunk (a chunk's rows lie below
+//      every source of the later chunks, and the sources of this and the earlier chunks
+//      were read before the barrier); it stops at the first chunk without near rows.
+//      Typically the near prefix is short (the kept keys that already sit below n_out).
+//   2. far rows, many workgroups per head, each thread loading the 16-byte pieces of
+//      several rows before storing them.  Their sources (>= n_out) are never written,
+//      their destinations [r*, n_out) are not read by this launch, and launch 1 read the
+//      near rows' sources before any of them is overwritten.
 constexpr int kInplaceThreads = 1024;
 constexpr int kInplaceUnroll = 8;
 
+__device__ __forceinline__ int inplace_src(const int32_t* ix, int r, int nk, int C, int n_out) {
+  if (r < nk) return max(r, min(ix[r], C - 1));   // a malformed index never moves a row up
+  if (r < n_out) return C + (r - nk);
+  return -1;
+}
+
 template <int RB>
-__global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(CompactArgs a,
-                                                                         char* k, char* v) {
+__global__ __launch_bounds__(kInplaceThreads) void compact_inplace_near_kernel(CompactArgs a,
+                                                                              char* k, char* v) {
   constexpr int TPR = RB / 16;                    // threads per row
   constexpr int RPP = kInplaceThreads / TPR;      // rows per pass
   constexpr int CHUNK = RPP * kInplaceUnroll;     // rows read before each barrier
@@ -92,21 +107,22 @@ __global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(Compac
   for (int c0 = 0; c0 < n_out; c0 += CHUNK) {
     uint4 kv[kInplaceUnroll], vv[kInplaceUnroll];
     int src[kInplaceUnroll];
+    bool near = false;
 #pragma unroll
     for (int u = 0; u < kInplaceUnroll; ++u) {
       const int r = c0 + u * RPP + sub;
-      int s = -1;
-      if (r < nk)
-        s = max(r, min(ix[r], C - 1));   // a malformed index never moves a row upwards
-      else if (r < n_out)
-        s = C + (r - nk);
-      src[u] = s == r ? -1 : s;          // a row already in place is not copied
+      const int s = inplace_src(ix, r, nk, C, n_out);
+      // far rows and rows already in place are left to launch 2 / not copied
+      src[u] = (s >= 0 && s < n_out && s != r) ? s : -1;
+      near |= s >= 0 && s < n_out;
       if (src[u] >= 0) {
         kv[u] = load16(k + base + (int64_t)src[u] * RB);
         vv[u] = load16(v + base + (int64_t)src[u] * RB);
       }
     }
-    __syncthreads();   // every source row of this chunk has been read
+    // every source row of this chunk has been read; a chunk with no near row ends the
+    // prefix (sources ascend, so no later row is near)
+    if (!__syncthreads_or(near)) break;
 #pragma unroll
     for (int u = 0; u < kInplaceUnroll; ++u) {
       if (src[u] >= 0) {
@@ -116,6 +132,57 @@ __global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(Compac
       }
     }
   }
+}
+
+constexpr int kFarRows = 4;     // rows per thread in launch 2
+
+template <int RB>
+__global__ __launch_bounds__(256) void compact_inplace_far_kernel(CompactArgs a, char* k, char* v) {
+  constexpr int TPR = RB / 16;
+  constexpr int RPB = 256 / TPR;                  // rows per pass of the workgroup
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int sub = threadIdx.x / TPR, part = threadIdx.x % TPR;
+  const int64_t s0 = a.offs[b];
+  const int N = (int)(a.offs[b + 1] - s0);
+  const int C = N - a.n_tail;
+  const int nk = max(0, min(a.n_kept[b], min(a.n_select, C)));
+  const int n_out = nk + a.n_tail;
+  const int r0 = blockIdx.x * (RPB * kFarRows);
+  if (r0 >= n_out) return;
+  const int32_t* ix = a.idx + ((int64_t)b * a.n_kv_heads + h) * a.n_select;
+  const int64_t base = h * a.head_stride_bytes + s0 * RB + part * 16;
+  int src[kFarRows];
+  uint4 kv[kFarRows], vv[kFarRows];
+#pragma unroll
+  for (int u = 0; u < kFarRows; ++u) {
+    const int r = r0 + u * RPB + sub;
+    const int s = inplace_src(ix, r, nk, C, n_out);
+    src[u] = s >= n_out ? s : -1;                 // far rows only
+  }
+#pragma unroll
+  for (int u = 0; u < kFarRows; ++u)
+    if (src[u] >= 0) {
+      kv[u] = load16(k + base + (int64_t)src[u] * RB);
+      vv[u] = load16(v + base + (int64_t)src[u] * RB);
+    }
+#pragma unroll
+  for (int u = 0; u < kFarRows; ++u)
+    if (src[u] >= 0) {
+      const int r = r0 + u * RPB + sub;
+      *reinterpret_cast<uint4*>(k + base + (int64_t)r * RB) = kv[u];
+      *reinterpret_cast<uint4*>(v + base + (int64_t)r * RB) = vv[u];
+    }
+}
+
+template <int RB>
+hipError_t launch_inplace_rb(const CompactArgs& a, const dge_geom_t& g, char* k, char* v,
+                             hipStream_t st) {
+  constexpr int RPB = 256 / (RB / 16);
+  hipLaunchKernelGGL((compact_inplace_near_kernel<RB>), dim3(g.n_kv_heads, g.batch),
+                     dim3(kInplaceThreads), 0, st, a, k, v);
+  const dim3 grid((a.n_out + RPB * kFarRows - 1) / (RPB * kFarRows), g.n_kv_heads, g.batch);
+  hipLaunchKernelGGL((compact_inplace_far_kernel<RB>), grid, dim3(256), 0, st, a, k, v);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -135,14 +202,13 @@ hipError_t launch_compact_inplace(const dge_geom_t& g, const int32_t* idx, const
   a.n_out = n_select + n_tail;
   char* kc = static_cast<char*>(k);
   char* vc = static_cast<char*>(v);
-  const dim3 grid(g.n_kv_heads, g.batch);
+  if (a.n_out == 0) return hipSuccess;
   switch (rb) {
-    case 128: hipLaunchKernelGGL((compact_inplace_kernel<128>), grid, dim3(kInplaceThreads), 0, st, a, kc, vc); break;
-    case 256: hipLaunchKernelGGL((compact_inplace_kernel<256>), grid, dim3(kInplaceThreads), 0, st, a, kc, vc); break;
-    case 512: hipLaunchKernelGGL((compact_inplace_kernel<512>), grid, dim3(kInplaceThreads), 0, st, a, kc, vc); break;
+    case 128: return launch_inplace_rb<128>(a, g, kc, vc, st);
+    case 256: return launch_inplace_rb<256>(a, g, kc, vc, st);
+    case 512: return launch_inplace_rb<512>(a, g, kc, vc, st);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_compact(const dge_geom_t& g, const int32_t* idx, const int32_t* n_kept,

@@ -812,6 +812,11 @@ INPLACE_CASES = {
     "f32_d64": ((2500, 333), 2, 64, "f32", 300, 8, 5, "topb"),
     "streaming": ((4098, 2000), 8, 128, "bf16", 4, 1020, 1, "streaming"),
     "c4_length": ((32802,), 1, 128, "bf16", 2016, 34, 7, "topb"),
+    # kept keys packed at the front: long chains of rows whose sources are other rows'
+    # destinations (every second candidate from 100 on, or the first ones shifted by one)
+    "near_every_second": ((9000, 5000), 2, 128, "bf16", 2016, 34, 1, "front2"),
+    "near_shift_one": ((6000,), 2, 128, "bf16", 3000, 34, 1, "shift1"),
+    "near_f32_d64": ((7000, 300), 2, 64, "f32", 1500, 8, 1, "front2"),
 }
 
 
@@ -837,8 +842,14 @@ def test_compact_inplace_vs_oracle(case):
         bits = np.int32
     k, v = to_dev(kb, dtype), to_dev(vb, dtype)
     offs = np.concatenate([[0], np.cumsum(lens)])
-    if selector == "topb":
+    if selector in ("topb", "front2", "shift1"):
         scores_h = di.random_scores((H, T), seed=len(case), kind="plateau")
+        for b, N in enumerate(lens):
+            seg = scores_h[:, offs[b]:offs[b + 1]]
+            if selector == "front2":      # the kept keys: 100, 102, 104, ...
+                seg[:, 100:100 + 2 * n_select:2] += 10.0
+            elif selector == "shift1":    # the kept keys: 1 .. n_select
+                seg[:, 1:1 + n_select] += 10.0
         idx, nk = dge.select_topb(g, torch.from_numpy(scores_h).to(DEV), pool, n_tail, n_select)
         want = oracle_select_compact(scores_h, kb, vb, lens, H, pool, n_tail, n_select)
     else:
