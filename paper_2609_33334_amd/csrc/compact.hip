@@ -74,7 +74,8 @@ hipError_t launch_rb(const CompactArgs& a, const dge_geom_t& g, hipStream_t st) 
 //   1. near rows, one workgroup per (KV head, sequence), in order: it reads every source
 //      of a chunk of rows, meets a barrier, then writes the chunk (a chunk's rows lie below
 //      every source of the later chunks, and the sources of this and the earlier chunks
-//      were read before the barrier); it stops at the first chunk without near rows.
+//      were read before the barrier); it stops after the chunk whose successor starts with
+//      a far row.
 //      Typically the near prefix is short (the kept keys that already sit below n_out).
 //   2. far rows, many workgroups per head, each thread loading the 16-byte pieces of
 //      several rows before storing them.  Their sources (>= n_out) are never written,
@@ -83,6 +84,7 @@ hipError_t launch_rb(const CompactArgs& a, const dge_geom_t& g, hipStream_t st) 
 constexpr int kInplaceThreads = 1024;
 constexpr int kInplaceUnroll = 8;
 
+// (launch 2) source of output row r, -1 past the compacted rows
 __device__ __forceinline__ int inplace_src(const int32_t* ix, int r, int nk, int C, int n_out) {
   if (r < nk) return max(r, min(ix[r], C - 1));   // a malformed index never moves a row up
   if (r < n_out) return C + (r - nk);
@@ -100,29 +102,38 @@ __global__ __launch_bounds__(kInplaceThreads) void compact_inplace_near_kernel(C
   const int64_t s0 = a.offs[b];
   const int N = (int)(a.offs[b + 1] - s0);
   const int C = N - a.n_tail;
-  const int nk = max(0, min(a.n_kept[b], min(a.n_select, C)));
-  const int n_out = nk + a.n_tail;
   const int32_t* ix = a.idx + ((int64_t)b * a.n_kv_heads + h) * a.n_select;
   const int64_t base = h * a.head_stride_bytes + s0 * RB + part * 16;
-  for (int c0 = 0; c0 < n_out; c0 += CHUNK) {
+  // the indices are loaded for every r < n_select without waiting for n_kept (a chain
+  // of dependent round trips is what this launch costs); n_kept then picks index or tail
+  auto index_at = [&](int r) { return r < a.n_select ? ix[r] : 0; };
+  const int nk_raw = a.n_kept[b];
+  for (int c0 = 0;; c0 += CHUNK) {
+    int iv[kInplaceUnroll];
+#pragma unroll
+    for (int u = 0; u < kInplaceUnroll; ++u) iv[u] = index_at(c0 + u * RPP + sub);
+    const int iv_next = index_at(c0 + CHUNK);     // first row of the next chunk
+    const int nk = max(0, min(nk_raw, min(a.n_select, C)));
+    const int n_out = nk + a.n_tail;
+    auto src_of = [&](int r, int i) {
+      if (r < nk) return max(r, min(i, C - 1));   // a malformed index never moves a row up
+      if (r < n_out) return C + (r - nk);
+      return -1;
+    };
     uint4 kv[kInplaceUnroll], vv[kInplaceUnroll];
     int src[kInplaceUnroll];
-    bool near = false;
 #pragma unroll
     for (int u = 0; u < kInplaceUnroll; ++u) {
       const int r = c0 + u * RPP + sub;
-      const int s = inplace_src(ix, r, nk, C, n_out);
-      // far rows and rows already in place are left to launch 2 / not copied
-      src[u] = (s >= 0 && s < n_out && s != r) ? s : -1;
-      near |= s >= 0 && s < n_out;
+      const int sr = src_of(r, iv[u]);
+      // far rows are left to launch 2, rows already in place are not copied
+      src[u] = (sr >= 0 && sr < n_out && sr != r) ? sr : -1;
       if (src[u] >= 0) {
         kv[u] = load16(k + base + (int64_t)src[u] * RB);
         vv[u] = load16(v + base + (int64_t)src[u] * RB);
       }
     }
-    // every source row of this chunk has been read; a chunk with no near row ends the
-    // prefix (sources ascend, so no later row is near)
-    if (!__syncthreads_or(near)) break;
+    __syncthreads();   // every source row of this chunk has been read
 #pragma unroll
     for (int u = 0; u < kInplaceUnroll; ++u) {
       if (src[u] >= 0) {
@@ -131,6 +142,10 @@ __global__ __launch_bounds__(kInplaceThreads) void compact_inplace_near_kernel(C
         *reinterpret_cast<uint4*>(v + base + (int64_t)r * RB) = vv[u];
       }
     }
+    // sources ascend, so once the next chunk's first row is not near, no later row is;
+    // the decision is the same in every thread
+    const int s_next = src_of(c0 + CHUNK, iv_next);
+    if (c0 + CHUNK >= n_out || s_next < 0 || s_next >= n_out) break;
   }
 }
 
