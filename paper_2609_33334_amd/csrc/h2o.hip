@@ -207,6 +207,7 @@ __global__ __launch_bounds__(256, 3) void h2o_lse_kernel(H2oArgs a) {
 // to part[s][h][j]; h2o_reduce_kernel adds the segments in a fixed order.
 // ------------------------------------------------------------------------------------
 constexpr int SEG = 512;
+constexpr int NKT = KB / 64;     // 16-key tiles of K per wavefront (4 wavefronts per key block)
 
 __global__ __launch_bounds__(256) void h2o_colsum_kernel(H2oArgs a, float* part, int nkb_max,
                                                          int nseg_max) {
@@ -226,20 +227,22 @@ __global__ __launch_bounds__(256) void h2o_colsum_kernel(H2oArgs a, float* part,
   __shared__ __attribute__((aligned(16))) char qlds[2][RB * RowBytes];
   __shared__ __attribute__((aligned(16))) float llds[2][RB];
 
-  // this wavefront's two 16-key tiles of K (B operand: lane supplies key c16)
-  const int ja = k0 + wv * 32 + c16, jb = ja + 16;
-  uint4 kfa[NS], kfb[NS];
+  // this wavefront's NKT 16-key tiles of K (B operand: lane supplies key c16)
+  int jk[NKT];
+  uint4 kf[NKT][NS];
   {
     const bf16_t* kh = a.k + (int64_t)h * a.kv_head_stride + s0 * D;
-    const char* ra = reinterpret_cast<const char*>(kh + (int64_t)min(ja, N - 1) * D);
-    const char* rbp = reinterpret_cast<const char*>(kh + (int64_t)min(jb, N - 1) * D);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      kfa[s] = load16(ra + (s * 4 + g16) * 16);
-      kfb[s] = load16(rbp + (s * 4 + g16) * 16);
+    for (int t = 0; t < NKT; ++t) {
+      jk[t] = k0 + wv * (16 * NKT) + 16 * t + c16;
+      const char* rk = reinterpret_cast<const char*>(kh + (int64_t)min(jk[t], N - 1) * D);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) kf[t][s] = load16(rk + (s * 4 + g16) * 16);
     }
   }
-  float cola = 0.0f, colb = 0.0f;
+  float col[NKT];
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) col[t] = 0.0f;
   const int rlo = max(seg_lo, k0 / RB * RB);   // first 64-row block with rows >= k0
   const int per = (seg_hi - rlo + RB - 1) / RB;
   const int nblk = per * a.G;                  // (head, row block) iterations
@@ -271,41 +274,43 @@ __global__ __launch_bounds__(256) void h2o_colsum_kernel(H2oArgs a, float* part,
         uint4 qf[NS];
 #pragma unroll
         for (int s = 0; s < NS; ++s) qf[s] = lds_frag(qlds[cur], rt * 16 + c16, s, g16);
-        f32x4_t acca = {0.f, 0.f, 0.f, 0.f}, accb = {0.f, 0.f, 0.f, 0.f};
+        f32x4_t acc[NKT];
 #pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          acca = mma_step(bf16_t{}, qf[s], kfa[s], acca);
-          accb = mma_step(bf16_t{}, qf[s], kfb[s], accb);
-        }
-        // acc[i] = logit of row r0 + rt*16 + 4*g16 + i for key ja (jb)
+        for (int t = 0; t < NKT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+          for (int t = 0; t < NKT; ++t) acc[t] = mma_step(bf16_t{}, qf[s], kf[t][s], acc[t]);
+        // acc[t][i] = logit of row r0 + rt*16 + 4*g16 + i for key jk[t]
         const float4 l4 = *reinterpret_cast<const float4*>(&llds[cur][rt * 16 + 4 * g16]);
         const float l2[4] = {l4.x, l4.y, l4.z, l4.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float pa = fast_exp2(fmaf(acca[i], a.scale_log2, -l2[i]));
-          float pb = fast_exp2(fmaf(accb[i], a.scale_log2, -l2[i]));
-          if constexpr (EDGE) {
-            const int p = r0 + rt * 16 + 4 * g16 + i;
-            pa = (p < seg_hi && ja <= p) ? pa : 0.0f;
-            pb = (p < seg_hi && jb <= p) ? pb : 0.0f;
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int t = 0; t < NKT; ++t) {
+            float pv = fast_exp2(fmaf(acc[t][i], a.scale_log2, -l2[i]));
+            if constexpr (EDGE) {
+              const int p = r0 + rt * 16 + 4 * g16 + i;
+              pv = (p < seg_hi && jk[t] <= p) ? pv : 0.0f;
+            }
+            col[t] += pv;
           }
-          cola += pa;
-          colb += pb;
-        }
       }
     };
     if (edge) body(std::true_type{});
     else body(std::false_type{});
     __syncthreads();
   }
-  cola += shfl_xor_f<16>(cola);
-  colb += shfl_xor_f<16>(colb);
-  cola += shfl_xor_f<32>(cola);
-  colb += shfl_xor_f<32>(colb);
+#pragma unroll
+  for (int t = 0; t < NKT; ++t) {
+    col[t] += shfl_xor_f<16>(col[t]);
+    col[t] += shfl_xor_f<32>(col[t]);
+  }
   if (g16 == 0) {
     float* out = part + ((int64_t)seg * a.n_kv_heads + h) * a.total_rows + s0;
-    if (ja < N) out[ja] = cola;
-    if (jb < N) out[jb] = colb;
+#pragma unroll
+    for (int t = 0; t < NKT; ++t)
+      if (jk[t] < N) out[jk[t]] = col[t];
   }
 }
 
