@@ -612,8 +612,10 @@ def bench_project(args, dev):
               for _ in range(n_sets)]
         pos = torch.arange(26507, 26507 + rows, dtype=torch.int32, device=dev)
         out = torch.empty(heads, rows, d, dtype=torch.bfloat16, device=dev)
+        need = dge.project_rope_workspace(rows, hidden, heads, d)
+        wsp = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
         for i in range(2 * n_sets):
-            dge.project_rope(x, ws[i % n_sets], pos, heads, d, out=out)
+            dge.project_rope(x, ws[i % n_sets], pos, heads, d, out=out, ws=wsp)
         torch.cuda.synchronize()
         # back-to-back calls between two HIP events on the launching stream: the average
         # launch duration (a lone event pair would add the launch latency to every call)
@@ -623,7 +625,7 @@ def bench_project(args, dev):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             for i in range(reps):
-                dge.project_rope(x, ws[i % n_sets], pos, heads, d, out=out)
+                dge.project_rope(x, ws[i % n_sets], pos, heads, d, out=out, ws=wsp)
             e1.record(stream)
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1) * 1e3 / reps)

@@ -344,24 +344,35 @@ dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t
 
 /* Query/key capture from a layer's input (App. "Draft-guided eviction implementation": the
  * post-RoPE queries are recomputed from each layer's input by forward pre-hooks): the
- * projection by a Linear weight and the rotary embedding of dge_rope in one launch,
+ * projection by a Linear weight and the rotary embedding of dge_rope in one call,
  *   out[h][r][:] = RoPE_{positions[r]}( (x W^T)[r][h*head_dim .. (h+1)*head_dim) ),
  * products on the matrix cores (bf16 in, float32 accumulate), each rotate-half pair
  * (i, i + head_dim/2) turned by positions[r] * theta^(-2i/head_dim) (the angle formed and
  * reduced modulo 2 pi in double, the rotation applied in float to the float32 sums), rounded
- * once to bf16 (round to nearest even).
+ * once to bf16 (round to nearest even).  For up to 64 rows (the window and draft rows) the
+ * hidden dimension is split over several workgroups whose float32 partial sums go to the
+ * workspace and are added in a fixed order by a second launch, so results are deterministic.
  *   x         : [n_rows][hidden] bf16, the layer input rows (e.g. the window and draft rows).
- *   w         : [n_heads * head_dim][hidden] bf16, the Linear weight (W_q, or W_k for keys),
- *               rows = output features, as torch.nn.Linear stores it.
+ *   w         : [n_heads * head_dim][hidden] bf16, the Linear weight (W_q, W_k, or a fused
+ *               [W_q; W_k] whose heads come out in that order), rows = output features, as
+ *               torch.nn.Linear stores it.
  *   positions : [n_rows] int32 absolute positions.
  *   out       : [n_heads][n_rows][head_dim] bf16 output, the Q layout dge_score reads.
- * No workspace; n_rows == 0 does nothing.  Errors: DGE_ERR_INVALID for n_rows < 0,
- * n_heads < 1, hidden < 1, theta <= 1 or not finite, a NULL / misaligned pointer (16 bytes;
- * positions 4); DGE_ERR_UNSUPPORTED for head_dim outside {64, 128}, hidden not a multiple of
- * 128 or more than 4,194,240 rows. */
+ *   ws        : at least dge_project_rope_workspace(...) bytes (may be NULL when that is 0).
+ * n_rows == 0 does nothing.  Errors: DGE_ERR_INVALID for n_rows < 0, n_heads < 1, hidden < 1,
+ * theta <= 1 or not finite, a NULL / misaligned pointer (16 bytes; positions 4);
+ * DGE_ERR_WORKSPACE for a missing or short workspace; DGE_ERR_UNSUPPORTED for head_dim
+ * outside {64, 128}, hidden not a multiple of 128 or more than 4,194,240 rows. */
 dge_status_t dge_project_rope(int32_t n_rows, int32_t hidden, const void *x, int32_t n_heads,
                               int32_t head_dim, const void *w, const int32_t *positions,
-                              double theta, void *out, hipStream_t stream);
+                              double theta, void *out, void *ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/* Bytes of workspace dge_project_rope needs for these sizes (0 when it needs none); writes
+ * *bytes (host pointer).  Errors: those of dge_project_rope's size checks, DGE_ERR_INVALID
+ * for a NULL bytes pointer. */
+dge_status_t dge_project_rope_workspace(int32_t n_rows, int32_t hidden, int32_t n_heads,
+                                        int32_t head_dim, size_t *bytes);
 
 /* Contiguity of the retained sets (Sec. 4, "Selection trades coverage for contiguity";
  * Table "Selection decomposition", column "run len."): for sequence b and KV head h,

@@ -25,7 +25,7 @@ from ._lib import (DGE_BF16, DGE_F32, OP_H2O, OP_SCORE, OP_SELECT, ROWS_DRAFT,  
 __all__ = ["Geometry", "score", "score_noalloc", "score_with_lse", "score_lse", "evicted_mass", "select_topb", "select_compact",
            "select_compact_layers", "select_streaming", "compact", "compact_inplace",
            "cache_attention",
-           "rope", "project_rope", "retained_runs", "h2o_colsum",
+           "rope", "project_rope", "project_rope_workspace", "retained_runs", "h2o_colsum",
            "pyramid_budgets", "workspace_size", "evict_layer", "DGEError", "ROWS_WINDOW_DRAFT",
            "ROWS_DRAFT", "ROWS_WINDOW", "n_scoring_rows"]
 
@@ -444,8 +444,16 @@ def rope(x, positions, theta: float = 500000.0, stream=None):
     return x
 
 
+def project_rope_workspace(n_rows: int, hidden: int, n_heads: int, head_dim: int) -> int:
+    """dge_project_rope_workspace: bytes of workspace dge_project_rope needs (0 for none)."""
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.lib().dge_project_rope_workspace(n_rows, hidden, n_heads, head_dim,
+                                                     ctypes.byref(n)), "dge_project_rope_workspace")
+    return int(n.value)
+
+
 def project_rope(x, w, positions, n_heads: int, head_dim: int, theta: float = 500000.0,
-                 out=None, stream=None):
+                 out=None, ws=None, stream=None):
     """dge_project_rope: out = RoPE(x W^T) per head, x [n_rows][hidden] bf16, w
     [n_heads*head_dim][hidden] bf16 (a Linear weight), int32 positions [n_rows].  Returns
     out [n_heads][n_rows][head_dim] bf16."""
@@ -463,8 +471,12 @@ def project_rope(x, w, positions, n_heads: int, head_dim: int, theta: float = 50
     if out is None:
         out = torch.empty(n_heads, n_rows, head_dim, dtype=torch.bfloat16, device=x.device)
     _need(out, "out", (torch.bfloat16,), n_heads * n_rows * head_dim)
+    need = project_rope_workspace(n_rows, hidden, n_heads, head_dim)
+    if ws is None and need > 0:
+        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
     _lib.check(_lib.lib().dge_project_rope(n_rows, hidden, _ptr(x), n_heads, head_dim, _ptr(w),
-                                           _ptr(positions), float(theta), _ptr(out),
+                                           _ptr(positions), float(theta), _ptr(out), _ptr(ws),
+                                           0 if ws is None else ws.numel() * ws.element_size(),
                                            _stream(stream)), "dge_project_rope")
     return out
 

@@ -23,7 +23,7 @@ EXPORTS = ("dge_abi_version", "dge_status_string", "dge_workspace_size", "dge_sc
            "dge_score_noalloc", "dge_score_with_lse", "dge_score_lse", "dge_evicted_mass",
            "dge_select_topb", "dge_select_compact", "dge_select_compact_layers",
            "dge_select_streaming", "dge_compact", "dge_compact_inplace",
-           "dge_cache_attention", "dge_rope", "dge_project_rope", "dge_retained_runs", "dge_h2o_colsum",
+           "dge_cache_attention", "dge_rope", "dge_project_rope", "dge_project_rope_workspace", "dge_retained_runs", "dge_h2o_colsum",
            "dge_pyramid_budgets")
 
 
@@ -111,7 +111,9 @@ def lib() -> ctypes.CDLL:
                            c_void_p, c_void_p]
     L.dge_project_rope.restype = c_int
     L.dge_project_rope.argtypes = [c_int32, c_int32, c_void_p, c_int32, c_int32, c_void_p, c_void_p,
-                                   c_double, c_void_p, c_void_p]
+                                   c_double, c_void_p, c_void_p, c_size_t, c_void_p]
+    L.dge_project_rope_workspace.restype = c_int
+    L.dge_project_rope_workspace.argtypes = [c_int32, c_int32, c_int32, c_int32, POINTER(c_size_t)]
     L.dge_retained_runs.restype = c_int
     L.dge_retained_runs.argtypes = [GP, c_void_p, c_void_p, c_int32, c_void_p, c_void_p, c_void_p]
     L.dge_pyramid_budgets.restype = c_int

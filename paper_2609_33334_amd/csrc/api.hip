@@ -297,20 +297,39 @@ dge_status_t dge_rope(int32_t n_heads, int32_t n_rows, int32_t head_dim, int32_t
       dge::launch_rope(n_heads, n_rows, head_dim, dtype, head_stride, positions, theta, x, stream));
 }
 
-dge_status_t dge_project_rope(int32_t n_rows, int32_t hidden, const void* x, int32_t n_heads,
-                              int32_t head_dim, const void* w, const int32_t* positions,
-                              double theta, void* out, hipStream_t stream) {
+static dge_status_t check_project(int32_t n_rows, int32_t hidden, int32_t n_heads,
+                                  int32_t head_dim) {
   if (n_rows < 0 || n_heads < 1 || hidden < 1) return DGE_ERR_INVALID;
   if (head_dim != 64 && head_dim != 128) return DGE_ERR_UNSUPPORTED;
   if (hidden % 128 != 0) return DGE_ERR_UNSUPPORTED;
-  if (n_rows > 64 * 65535 || (int64_t)n_heads * (head_dim / 16) > INT32_MAX) return DGE_ERR_UNSUPPORTED;
+  if (n_rows > 64 * 65535 || (int64_t)n_heads * (head_dim / 16) > INT32_MAX / 16) return DGE_ERR_UNSUPPORTED;
+  return DGE_OK;
+}
+
+dge_status_t dge_project_rope_workspace(int32_t n_rows, int32_t hidden, int32_t n_heads,
+                                        int32_t head_dim, size_t* bytes) {
+  if (bytes == nullptr) return DGE_ERR_INVALID;
+  const dge_status_t st = check_project(n_rows, hidden, n_heads, head_dim);
+  if (st != DGE_OK) return st;
+  *bytes = dge::project_workspace_bytes(n_rows, hidden, n_heads, head_dim);
+  return DGE_OK;
+}
+
+dge_status_t dge_project_rope(int32_t n_rows, int32_t hidden, const void* x, int32_t n_heads,
+                              int32_t head_dim, const void* w, const int32_t* positions,
+                              double theta, void* out, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  dge_status_t st = check_project(n_rows, hidden, n_heads, head_dim);
+  if (st != DGE_OK) return st;
   if (!(theta > 1.0) || !(theta < 1e300)) return DGE_ERR_INVALID;
   if (n_rows == 0) return DGE_OK;
   if (!x || !w || !positions || !out || !aligned16(x) || !aligned16(w) || !aligned16(out) ||
       (reinterpret_cast<uintptr_t>(positions) & 3))
     return DGE_ERR_INVALID;
+  const size_t need = dge::project_workspace_bytes(n_rows, hidden, n_heads, head_dim);
+  if (need > 0 && (ws == nullptr || !aligned16(ws) || ws_bytes < need)) return DGE_ERR_WORKSPACE;
   return hip_status(dge::launch_project_rope(n_rows, hidden, x, n_heads, head_dim, w, positions,
-                                             theta, out, stream));
+                                             theta, out, ws, stream));
 }
 
 dge_status_t dge_cache_attention(const dge_geom_t* geom, const void* q, int32_t n_q,

@@ -62,9 +62,10 @@ hipError_t launch_compact_inplace(const dge_geom_t& g, const int32_t* idx, const
 hipError_t launch_rope(int n_heads, int n_rows, int head_dim, int dtype, int64_t head_stride,
                        const int32_t* positions, double theta, void* x, hipStream_t stream);
 
+size_t project_workspace_bytes(int n_rows, int hidden, int n_heads, int head_dim);
 hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_heads, int head_dim,
                                const void* w, const int32_t* positions, double theta, void* out,
-                               hipStream_t stream);
+                               void* ws, hipStream_t stream);
 
 int cache_attention_max_group();
 hipError_t launch_cache_attention(const dge_geom_t& g, const void* q, int n_q, int q_from_end,

@@ -136,6 +136,111 @@ __global__ __launch_bounds__(64 * WAVES) void project_rope_kernel(ProjArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Short row sets (the scoring rows): the hidden dimension split over KS workgroups.
+// The whole x is smaller than nothing here -- 34 rows x 8 KB is ~2x a compute unit's share
+// of W_q -- so every workgroup that covers all of K for 16 columns (above) reads ~3x more
+// x than W through its compute unit's ~30 GB/s load path.  Here a workgroup covers 64
+// columns (4 pair groups, one per wavefront) for 1/KS of K: it stages that K slice of x
+// in LDS once (16-byte units XOR-swizzled by row, so the 16 rows of a fragment read hit
+// different banks) and streams its W slice; float32 partial sums go to the workspace,
+// [KS][n_rows][n_heads * d], and a second launch adds the KS slices in a fixed order,
+// rotates and rounds.
+// ---------------------------------------------------------------------------------------
+constexpr int kSplitCols = 64;
+
+// STEPS = kr / 32 K steps per wavefront (8 or 16): every W load of the slice and the x
+// staging loads are issued before the first wait, so the workgroup pays one memory round
+// trip (a chain of round trips is what a short workgroup costs).
+template <int MT, int STEPS>
+__global__ __launch_bounds__(256) void project_split_kernel(ProjArgs a, float* part) {
+  constexpr int kr = 32 * STEPS;
+  constexpr int units = kr / 8;                       // 16-byte units per staged row
+  const int groups = a.half / 8;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c16 = lane & 15, g16 = lane >> 4;
+  const int ks = blockIdx.y;                          // K slice
+  const int k_lo = ks * kr;
+  const int pg = blockIdx.x * 4 + wv;                 // this wavefront's pair group
+  const int head = pg / groups, grp = pg % groups;
+  const int pair = 8 * grp + (c16 & 7);
+  const int col = head * a.d + (c16 < 8 ? pair : a.half + pair);
+  const int ncols = a.n_heads * a.d;
+  __shared__ __attribute__((aligned(16))) char xs[16 * MT * kr * 2];   // [rows][kr] bf16, swizzled
+  const uint16_t* wrow = a.w + (int64_t)col * a.hidden + k_lo + 8 * g16;
+  u32x4_t bw[STEPS];
+#pragma unroll
+  for (int u = 0; u < STEPS; ++u) bw[u] = async_load16(wrow + 32 * u);
+  // stage x[rows][k_lo, k_lo + kr) (rows past the end repeat the last row); the compiler's
+  // wait before the LDS stores also covers the W loads issued above
+  constexpr int kPer = (16 * MT * units + 255) / 256;
+  uint4 xv[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int e = tid + 256 * i;
+    const int r = min(e / units, 16 * MT - 1), u = e % units;
+    xv[i] = load16(a.x + (int64_t)min(r, a.n_rows - 1) * a.hidden + k_lo + 8 * u);
+  }
+  asm_wait_vmcnt<0>();
+#pragma unroll
+  for (int u = 0; u < STEPS; ++u) reg_fence(bw[u]);
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int e = tid + 256 * i;
+    if (e < 16 * MT * units) {
+      const int r = e / units, u = e % units;
+      *reinterpret_cast<uint4*>(xs + ((r * units) + (u ^ (r & 15))) * 16) = xv[i];
+    }
+  }
+  __syncthreads();
+  f32x4_t acc[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < STEPS; ++u)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int r = 16 * i + c16, unit = 4 * u + g16;
+      const uint4 ax = *reinterpret_cast<const uint4*>(xs + ((r * units) + (unit ^ (r & 15))) * 16);
+      acc[i] = mma_step(bf16_t{}, ax, as_uint4(bw[u]), acc[i]);
+    }
+  // lane holds rows 16 i + 4 g16 + t of column col
+  float* pk = part + (int64_t)ks * a.n_rows * ncols;
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int r = 16 * i + 4 * g16 + t;
+      if (r < a.n_rows) pk[(int64_t)r * ncols + col] = acc[i][t];
+    }
+}
+
+// sum of the KS slices (fixed order), rotation, bf16: one thread per (row, head, pair)
+__global__ __launch_bounds__(256) void project_finish_kernel(ProjArgs a, const float* part, int n_split) {
+  const int half = a.half;
+  const int64_t total = (int64_t)a.n_rows * a.n_heads * half;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= total) return;
+  const int pair = (int)(t % half);
+  const int head = (int)((t / half) % a.n_heads);
+  const int r = (int)(t / ((int64_t)half * a.n_heads));
+  const int ncols = a.n_heads * a.d;
+  const int64_t o = (int64_t)r * ncols + head * a.d + pair;
+  float lo = 0.0f, hi = 0.0f;
+  for (int k = 0; k < n_split; ++k) {
+    lo += part[(int64_t)k * a.n_rows * ncols + o];
+    hi += part[(int64_t)k * a.n_rows * ncols + o + half];
+  }
+  const double ang = (double)a.pos[r] * a.inv_freq[pair];
+  const double kk = rint(ang * 0.15915494309189535);
+  const double red = fma(-kk, 2.4492935982947064e-16, fma(-kk, 6.283185307179586, ang));
+  float sn, cs;
+  sincosf((float)red, &sn, &cs);
+  uint16_t* orow = a.out + ((int64_t)head * a.n_rows + r) * a.d;
+  orow[pair] = to_bf16_rne(fmaf(lo, cs, -hi * sn));
+  orow[half + pair] = to_bf16_rne(fmaf(hi, cs, lo * sn));
+}
+
 template <int WAVES>
 hipError_t launch_proj_waves(const ProjArgs& a, hipStream_t st) {
   // row tiles per workgroup: just enough for a short row set (the scoring rows), else 4
@@ -153,9 +258,27 @@ hipError_t launch_proj_waves(const ProjArgs& a, hipStream_t st) {
 
 }  // namespace
 
+// Hidden-dimension split of the short-row path: about 512 workgroups of 64 columns, K
+// slices of 256 or 512 (8 or 16 K steps per wavefront, all in flight at once; the staged x
+// slice, 16 MT x kr bf16, stays within 64 KB of LDS).  1 = no split.
+int project_split(int n_rows, int hidden, int n_heads, int head_dim) {
+  if (n_rows > 64 || hidden % 256 != 0) return 1;
+  const int colblocks = n_heads * head_dim / kSplitCols;
+  if (colblocks < 1 || (n_heads * head_dim) % kSplitCols != 0) return 1;
+  int ks = 1;
+  while (ks * 2 * colblocks <= 768 && hidden / (ks * 2) >= 256 && hidden % (ks * 2 * 256) == 0) ks *= 2;
+  while (hidden / ks > 512 && hidden % (ks * 2 * 256) == 0) ks *= 2;
+  return hidden / ks > 512 ? 1 : ks;
+}
+
+size_t project_workspace_bytes(int n_rows, int hidden, int n_heads, int head_dim) {
+  const int ks = project_split(n_rows, hidden, n_heads, head_dim);
+  return ks == 1 ? 0 : (size_t)ks * n_rows * n_heads * head_dim * sizeof(float);
+}
+
 hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_heads, int head_dim,
                                const void* w, const int32_t* positions, double theta, void* out,
-                               hipStream_t st) {
+                               void* ws, hipStream_t st) {
   ProjArgs a{};
   a.x = static_cast<const uint16_t*>(x);
   a.w = static_cast<const uint16_t*>(w);
@@ -167,6 +290,35 @@ hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_head
   a.d = head_dim;
   a.half = head_dim / 2;
   for (int i = 0; i < a.half; ++i) a.inv_freq[i] = pow(theta, -2.0 * i / head_dim);
+  const int ks = project_split(n_rows, hidden, n_heads, head_dim);
+  if (ks > 1) {
+    float* part = static_cast<float*>(ws);
+    const int kr = hidden / ks;
+    const int mt = (n_rows + 15) / 16;
+    const dim3 grid(n_heads * head_dim / kSplitCols, ks);
+#define DGE_SPLIT_LAUNCH(MT, STEPS) \
+    hipLaunchKernelGGL((project_split_kernel<MT, STEPS>), grid, dim3(256), 0, st, a, part)
+    if (kr == 256) {
+      switch (mt) {
+        case 1: DGE_SPLIT_LAUNCH(1, 8); break;
+        case 2: DGE_SPLIT_LAUNCH(2, 8); break;
+        case 3: DGE_SPLIT_LAUNCH(3, 8); break;
+        default: DGE_SPLIT_LAUNCH(4, 8); break;
+      }
+    } else {
+      switch (mt) {
+        case 1: DGE_SPLIT_LAUNCH(1, 16); break;
+        case 2: DGE_SPLIT_LAUNCH(2, 16); break;
+        case 3: DGE_SPLIT_LAUNCH(3, 16); break;
+        default: DGE_SPLIT_LAUNCH(4, 16); break;
+      }
+    }
+#undef DGE_SPLIT_LAUNCH
+    const int64_t total = (int64_t)n_rows * n_heads * a.half;
+    hipLaunchKernelGGL(project_finish_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
+                       a, part, ks);
+    return hipGetLastError();
+  }
   // eight wavefronts split the hidden dimension (each keeps 8 K steps of loads in flight),
   // four when it is not a multiple of 256
   return hidden % 256 == 0 ? launch_proj_waves<8>(a, st) : launch_proj_waves<4>(a, st);

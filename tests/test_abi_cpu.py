@@ -165,6 +165,25 @@ def test_score_with_lse_and_evicted_mass_validation(L):
     assert em(g=_G(hq=18, hkv=1)) == _lib.DGE_ERR_UNSUPPORTED    # more than 8 heads per group
 
 
+def test_project_rope_validation(L):
+    n = ctypes.c_size_t(0)
+    assert L.dge_project_rope_workspace(34, 4096, 32, 128, ctypes.byref(n)) == 0 and n.value > 0
+    need = n.value
+    assert L.dge_project_rope_workspace(8194, 4096, 32, 128, ctypes.byref(n)) == 0 and n.value == 0
+    assert L.dge_project_rope_workspace(34, 4096, 32, 96, ctypes.byref(n)) == _lib.DGE_ERR_UNSUPPORTED
+    assert L.dge_project_rope_workspace(34, 4000, 32, 128, ctypes.byref(n)) == _lib.DGE_ERR_UNSUPPORTED
+    assert L.dge_project_rope_workspace(34, 4096, 32, 128, None) == _lib.DGE_ERR_INVALID
+    def call(rows=34, hidden=4096, heads=32, d=128, theta=5e5, ws=FAKE, nbytes=1 << 40, x=FAKE):
+        return L.dge_project_rope(rows, hidden, x, heads, d, FAKE, FAKE, theta, FAKE, ws, nbytes, None)
+    assert call(ws=None) == _lib.DGE_ERR_WORKSPACE
+    assert call(nbytes=need - 1) == _lib.DGE_ERR_WORKSPACE
+    assert call(theta=1.0) == _lib.DGE_ERR_INVALID
+    assert call(rows=-1) == _lib.DGE_ERR_INVALID
+    assert call(x=FAKE + 2) == _lib.DGE_ERR_INVALID
+    assert call(d=96) == _lib.DGE_ERR_UNSUPPORTED
+    assert call(rows=0, ws=None) == _lib.DGE_OK            # nothing to do, nothing launched
+
+
 def test_workspace_size(L):
     g = _G()
     n = ctypes.c_size_t(0)

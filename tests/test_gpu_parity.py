@@ -1039,6 +1039,8 @@ PROJ_CASES = {
     "llama_k_scoring_rows": (34, 4096, 8, 128, 26507, None),
     "fused_qk_weight": (34, 4096, 40, 128, 26507, None),
     "hidden_384_rows_70": (70, 384, 6, 128, 100, None),
+    "split_d64_rows_10": (10, 2048, 6, 64, 3, None),
+    "split_rows_64": (64, 4096, 4, 128, 1000, None),
     "d64_ragged_rows": (130, 1024, 4, 64, 0, None),
     "one_row": (1, 128, 1, 64, 7, None),
     "h2o_all_rows_sampled": (8194, 4096, 32, 128, 0, 48),
