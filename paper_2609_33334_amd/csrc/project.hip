@@ -258,6 +258,136 @@ hipError_t launch_proj_waves(const ProjArgs& a, hipStream_t st) {
 
 }  // namespace
 
+// ---------------------------------------------------------------------------------------
+// Many rows (every prompt row of a layer, e.g. H2O's queries): a 128 x 128 output tile per
+// workgroup over all of K.  x rows (A) and W rows (B, the output columns) stream through a
+// 4-stage LDS ring of 32-wide K slices (8 KB + 8 KB per stage, 3 stages in flight) with
+// global->LDS copies, as the scoring streams K.  Within a 64-byte row slice the 16-byte unit
+// u of row r sits at u ^ ((r >> 1) & 3), so the 8 rows a fragment read serves together hit
+// 8 different 16-byte bank groups.  Wavefront w computes rows 64 (w & 1) .. +64 and four
+// 16-column tiles: two low tiles of rotation pairs and their partners d/2 columns higher,
+// so each lane holds both halves of its pairs and the epilogue rotates in registers.
+// ---------------------------------------------------------------------------------------
+constexpr int kGT = 128;                       // rows and columns per workgroup
+constexpr int kGBK = 32;                       // K per stage
+constexpr int kGStages = 4;
+constexpr int kGHalfBytes = kGT * kGBK * 2;    // A or B part of a stage: 8 KB
+constexpr int kGStageBytes = 2 * kGHalfBytes;  // 16 KB
+constexpr int kGCopies = kGStageBytes / (256 * 16);   // global->LDS copies per thread per stage
+
+// Tile order: each XCD takes a contiguous range of tiles (xcd_unit), walked in groups of
+// 8 row blocks across all column blocks, so the workgroups resident on one XCD share both
+// x row blocks and W column blocks in its L2.
+constexpr int kGGroup = 8;
+
+__global__ __launch_bounds__(256, 2) void project_tile_kernel(ProjArgs a, int nrb, int ncb) {
+  const int units = nrb * ncb;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int group = unit / (kGGroup * ncb), in_group = unit % (kGGroup * ncb);
+  const int first = group * kGGroup, rows_g = min(nrb - first, kGGroup);
+  const int rb = first + in_group % rows_g, cb = in_group / rows_g;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c16 = lane & 15, g16 = lane >> 4;
+  const int row0 = rb * kGT, col0 = cb * kGT;
+  __shared__ __attribute__((aligned(16))) char ring[kGStages][kGStageBytes];
+  // this thread's copies: wavefront wv's instruction i fills bytes [(4 wv + i) KB, +1 KB) of a
+  // stage, lane l the 16 bytes at 16 l of that kilobyte; it fetches the unit that belongs there
+  uint32_t goff[kGCopies];
+  const int wvu = __builtin_amdgcn_readfirstlane(wv);        // wave-uniform copy of wv
+  bool is_b[kGCopies];                                       // B part (W rows): wave-uniform
+#pragma unroll
+  for (int i = 0; i < kGCopies; ++i) {
+    const int o = ((wv * kGCopies + i) * 64 + lane) * 16;    // byte offset in the stage
+    is_b[i] = (wvu * kGCopies + i) * 1024 >= kGHalfBytes;
+    const int ob = is_b[i] ? o - kGHalfBytes : o;
+    const int r = ob / 64, pu = (ob % 64) / 16;               // row, physical unit
+    const int u = pu ^ ((r >> 1) & 3);                        // logical unit (K offset 8u)
+    const int grow = is_b[i] ? col0 + r : min(row0 + r, a.n_rows - 1);
+    goff[i] = (uint32_t)(((int64_t)grow * a.hidden + 8 * u) * 2);
+  }
+  const uint32_t lds_wave = (uint32_t)(wvu * kGCopies * 1024);
+  const int nk = a.hidden / kGBK;
+  auto issue = [&](int t) {                    // copies of stage t (t >= nk: stage 0 again)
+    const int te = t < nk ? t : 0;
+    char* buf = ring[t % kGStages];
+    const uint32_t lds = (uint32_t)(uintptr_t)(lds_ptr_t)buf + lds_wave;
+    const char* xa = reinterpret_cast<const char*>(a.x) + (int64_t)te * kGBK * 2;
+    const char* wb = reinterpret_cast<const char*>(a.w) + (int64_t)te * kGBK * 2;
+#pragma unroll
+    for (int i = 0; i < kGCopies; ++i) dma16_sbase(is_b[i] ? wb : xa, goff[i], lds + i * 1024);
+  };
+  // the wavefront's tiles: row half rh, low column tiles lt[e] and partners lt[e] + P
+  const int rh = wv & 1, j = wv >> 1;
+  const int lpt = a.d / 32;                    // low 16-column tiles per head
+  int ct[4];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int L = 2 * j + e;
+    const int lo = (L / lpt) * (a.d / 16) + L % lpt;
+    ct[e] = lo;
+    ct[e + 2] = lo + lpt;
+  }
+  f32x4_t acc[4][4];                           // [row tile][column tile]
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[i][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < kGStages - 1; ++t) issue(t);
+  for (int t = 0; t < nk; ++t) {
+    asm_wait_vmcnt<(kGStages - 2) * kGCopies>();   // stage t has landed (this thread's part)
+    lds_barrier();                                 // ... everyone's; slot (t - 1) % S is free
+    issue(t + kGStages - 1);
+    const char* st = ring[t % kGStages];
+    uint4 af[4], bf[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = rh * 64 + i * 16 + c16;
+      af[i] = *reinterpret_cast<const uint4*>(st + r * 64 + ((g16 ^ ((r >> 1) & 3)) * 16));
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = ct[e] * 16 + c16;
+      bf[e] = *reinterpret_cast<const uint4*>(st + kGHalfBytes + r * 64 + ((g16 ^ ((r >> 1) & 3)) * 16));
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[i][e] = mma_step(bf16_t{}, af[i], bf[e], acc[i][e]);
+  }
+  asm_wait_vmcnt<0>();                         // no copy still writes into the ring
+  // epilogue: lane holds rows 4 g16 + k of each row tile, column c16 of each column tile
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int colg = col0 + ct[e] * 16 + c16;  // global low column
+    const int head = colg / a.d, pair = colg % a.d;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int r = row0 + rh * 64 + i * 16 + 4 * g16 + k;
+        if (r < a.n_rows) {
+          const double ang = (double)a.pos[r] * a.inv_freq[pair];
+          const double kk = rint(ang * 0.15915494309189535);
+          const double red = fma(-kk, 2.4492935982947064e-16, fma(-kk, 6.283185307179586, ang));
+          float sn, cs;
+          sincosf((float)red, &sn, &cs);
+          const float lo = acc[i][e][k], hi = acc[i][e + 2][k];
+          uint16_t* orow = a.out + ((int64_t)head * a.n_rows + r) * a.d;
+          orow[pair] = to_bf16_rne(fmaf(lo, cs, -hi * sn));
+          orow[a.half + pair] = to_bf16_rne(fmaf(hi, cs, lo * sn));
+        }
+      }
+  }
+}
+
+bool project_tiled(int n_rows, int hidden, int n_heads, int head_dim) {
+  const int64_t ncols = (int64_t)n_heads * head_dim;
+  return n_rows > 64 && ncols % kGT == 0 && hidden % kGBK == 0 &&
+         (int64_t)n_rows * hidden * 2 < ((int64_t)1 << 32) && ncols * hidden * 2 < ((int64_t)1 << 32);
+}
+
 // Hidden-dimension split of the short-row path: about 512 workgroups of 64 columns, K
 // slices of 256 or 512 (8 or 16 K steps per wavefront, all in flight at once; the staged x
 // slice, 16 MT x kr bf16, stays within 64 KB of LDS).  1 = no split.
@@ -317,6 +447,11 @@ hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_head
     const int64_t total = (int64_t)n_rows * n_heads * a.half;
     hipLaunchKernelGGL(project_finish_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
                        a, part, ks);
+    return hipGetLastError();
+  }
+  if (project_tiled(n_rows, hidden, n_heads, head_dim)) {
+    const int nrb = (n_rows + kGT - 1) / kGT, ncb = (int)((int64_t)n_heads * head_dim / kGT);
+    hipLaunchKernelGGL(project_tile_kernel, dim3(xcd_grid(nrb * ncb)), dim3(256), 0, st, a, nrb, ncb);
     return hipGetLastError();
   }
   // eight wavefronts split the hidden dimension (each keeps 8 K steps of loads in flight),
