@@ -94,46 +94,52 @@ __device__ __forceinline__ float rescale(float m, float mx) {
   return m == mx ? 1.0f : fast_exp2(m - mx);
 }
 
-// Online sum of 2^x over a stream of logits, kept relative to a reference mref (log2
-// domain) that moves only when a logit exceeds it by more than 2^kLazyBound: the
-// common update is fma + exp2 + add per logit, with no rescale.  mref starts finite and
-// very negative (kLazyRefInit) so that fully masked groups (-inf) add exactly 0; the
-// result (mref, srow) merges with others like any (max, sum) pair.  x are unscaled
-// logits, scale = log2(e)/sqrt(d).  The rescale branch is wave-uniform.
+// Online sums of 2^(x*scale - m) (log2 domain) for R rows, NV logits of each per call,
+// x unscaled logits and scale = log2(e)/sqrt(d).  The common path is fma + exp2 + add per
+// logit against the current reference m, with no maximum: a row's sum leaves the finite
+// range only when one of its logits exceeds m by about 2^7 (or very many exceed it by
+// less), and then, in one wave-uniform branch, that row's reference moves up to its
+// batch maximum (and at least kLazyBound above the old reference) and the batch is
+// summed again onto the rescaled old sum.  m starts finite and very negative
+// (kLazyRefInit): the first live batch of a row takes the branch, masked logits (-inf)
+// add exactly 0, and the result merges with others like any (max, sum) pair.
 constexpr float kLazyBound = 64.0f;
 constexpr float kLazyRefInit = -1.0e30f;
-__device__ __forceinline__ void lazy_lse_update4(const float (&x)[4], float scale, float& mref,
-                                                 float& srow) {
-  const float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])) * scale;
-  if (__any(mx > mref + kLazyBound)) {
-    const float nr = fmaxf(mref, mx);
-    srow *= fast_exp2(mref - nr);
-    mref = nr;
+template <int R, int NV>
+__device__ __forceinline__ void rebase_lse_update(const float (&x)[R][NV], float scale, float* m,
+                                                  float* s) {
+  auto batch = [&](int r, float ref) {
+    float e[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) e[i] = fast_exp2(fmaf(x[r][i], scale, -ref));
+#pragma unroll
+    for (int w = 1; w < NV; w *= 2)
+#pragma unroll
+      for (int i = 0; i + w < NV; i += 2 * w) e[i] += e[i + w];
+    return e[0];
+  };
+  float ns[R];
+  bool out = false;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    ns[r] = s[r] + batch(r, m[r]);
+    out = out || !(ns[r] < INFINITY);
   }
-  srow += (fast_exp2(fmaf(x[0], scale, -mref)) + fast_exp2(fmaf(x[1], scale, -mref))) +
-          (fast_exp2(fmaf(x[2], scale, -mref)) + fast_exp2(fmaf(x[3], scale, -mref)));
-}
-
-// Online (max, sum) update with NV logits of one row at once, branch-free: the
-// reference becomes the running maximum, the old sum is rescaled once (one exp2 per NV
-// logits) and every logit adds 2^(x*scale - m).  m starts finite (kLazyRefInit), so
-// masked logits (-inf) add exactly 0 and a fully masked batch leaves (m, s) unchanged.
-template <int NV>
-__device__ __forceinline__ void online_lse_update(const float (&x)[NV], float scale, float& m,
-                                                  float& s) {
-  float mx = x[0];
+  if (__any(out)) {
 #pragma unroll
-  for (int i = 1; i < NV; ++i) mx = fmaxf(mx, x[i]);
-  const float nm = fmaxf(m, mx * scale);
-  float e[NV];
+    for (int r = 0; r < R; ++r) {
+      if (!(ns[r] < INFINITY)) {
+        float mx = x[r][0];
 #pragma unroll
-  for (int i = 0; i < NV; ++i) e[i] = fast_exp2(fmaf(x[i], scale, -nm));
+        for (int i = 1; i < NV; ++i) mx = fmaxf(mx, x[r][i]);
+        const float nr = fmaxf(mx * scale, m[r] + kLazyBound);
+        ns[r] = fmaf(s[r], fast_exp2(m[r] - nr), batch(r, nr));
+        m[r] = nr;
+      }
+    }
+  }
 #pragma unroll
-  for (int w = 1; w < NV; w *= 2)
-#pragma unroll
-    for (int i = 0; i + w < NV; i += 2 * w) e[i] += e[i + w];
-  s = fmaf(s, fast_exp2(m - nm), e[0]);
-  m = nm;
+  for (int r = 0; r < R; ++r) s[r] = ns[r];
 }
 
 // Sum of v over the four lane groups (lanes l, l^16, l^32, l^48), returned in every

@@ -10,7 +10,7 @@
 //   of one KV head; wavefront g is query head g of the group and keeps its 4 row tiles
 //   of Q in registers.  64-key tiles of K are staged once in XOR-swizzled LDS and read
 //   by all G wavefronts.  The product is taken transposed (A = keys, B = query rows) so
-//   a lane holds 4 keys of one row and keeps that row's (max, sum) in registers.
+//   a lane holds 4 keys of one row and keeps that row's (reference, sum) in registers.
 //
 // colsum: a workgroup owns a 128-key block and a 512-row segment of one KV head; each
 //   wavefront keeps two 16-key tiles of K in registers.  For every query head of the
@@ -79,9 +79,9 @@ __device__ __forceinline__ void block_store(char* lds, int tid, const uint4 (&st
 // Row log-sum-exp: one (row-block pair, KV head, sequence) per workgroup.
 // ------------------------------------------------------------------------------------
 // One 64-key tile for the wavefront's four 16-row tiles (rows r0 + rt*16 + c16): the
-// transposed product (A = keys) puts 4 keys of one row in each lane.  The four rows'
-// sums are kept relative to lazy references (as lazy_lse_update4); one wave-uniform
-// check per 16-key subtile moves them, so the common path has no branch per row.
+// transposed product (A = keys) puts 4 keys of one row in each lane, and each 16-key
+// subtile's four logits per row go through rebase_lse_update (no maximum in the common
+// path, one wave-uniform overflow check per subtile).
 template <bool MASK>
 __device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N, int c16,
                                          int g16, const uint4 (&qf)[4][NS], float scale,
@@ -99,10 +99,9 @@ __device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N,
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) acc[rt] = mma_step(bf16_t{}, kf[s], qf[rt][s], acc[rt]);
     // acc[rt][i] = logit of key j0 + sub*16 + 4*g16 + i for row r0 + rt*16 + c16
-    float x[4][4], mx[4];
-    bool up = false;
+    float x[4][4];
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+    for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         x[rt][i] = acc[rt][i];
@@ -111,21 +110,7 @@ __device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N,
           x[rt][i] = (j <= p && j < N) ? x[rt][i] : -INFINITY;
         }
       }
-      mx[rt] = fmaxf(fmaxf(x[rt][0], x[rt][1]), fmaxf(x[rt][2], x[rt][3])) * scale;
-      up = up || mx[rt] > m[rt] + kLazyBound;
-    }
-    if (__any(up)) {
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        const float nr = fmaxf(m[rt], mx[rt]);
-        sm[rt] *= fast_exp2(m[rt] - nr);
-        m[rt] = nr;
-      }
-    }
-#pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
-      sm[rt] += (fast_exp2(fmaf(x[rt][0], scale, -m[rt])) + fast_exp2(fmaf(x[rt][1], scale, -m[rt]))) +
-                (fast_exp2(fmaf(x[rt][2], scale, -m[rt])) + fast_exp2(fmaf(x[rt][3], scale, -m[rt])));
+    rebase_lse_update<4, 4>(x, scale, m, sm);
   }
 }
 
@@ -143,8 +128,9 @@ __global__ __launch_bounds__(256, 3) void h2o_lse_kernel(H2oArgs a) {
   if (pair >= (nrb + 1) / 2) return;        // a shorter sequence of a ragged batch
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int g16 = lane >> 4, c16 = lane & 15;
-  const bool active = wv < a.G;             // wavefront wv = query head h*G + wv
-  const int hq = h * a.G + (active ? wv : 0);
+  const int wvu = __builtin_amdgcn_readfirstlane(wv);   // wave-uniform: scalar addresses
+  const bool active = wvu < a.G;            // wavefront wv = query head h*G + wv
+  const int hq = h * a.G + (active ? wvu : 0);
   const char* kb = reinterpret_cast<const char*>(a.k + (int64_t)h * a.kv_head_stride + s0 * D);
   const char* qb = reinterpret_cast<const char*>(a.q + (int64_t)hq * a.total_rows * D + s0 * D);
   __shared__ __attribute__((aligned(16))) char lds[2][KTL * RowBytes];
@@ -162,7 +148,7 @@ __global__ __launch_bounds__(256, 3) void h2o_lse_kernel(H2oArgs a) {
 #pragma unroll
       for (int s = 0; s < NS; ++s) qf[rt][s] = load16(row + (s * 4 + g16) * 16);
     }
-    float m[4], sm[4];                      // lazy reference and sum (lazy_lse_update4)
+    float m[4], sm[4];                      // reference and sum (rebase_lse_update)
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) { m[rt] = kLazyRefInit; sm[rt] = 0.0f; }
     const int last = min(r0 + RB, N);       // keys [0, last) can be seen by this block

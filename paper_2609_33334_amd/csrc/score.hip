@@ -257,8 +257,8 @@ __device__ __forceinline__ void ktile_stream(const char* kb, int c0, int ntiles,
 }
 
 // Subtiles of a 64-key tile whose products the stats pass issues together before their
-// results are used (16 registers per own tile per subtile); the running maxima are
-// updated once per group (one rescale per 4 * group logits of a row).  The products of
+// results are used (16 registers per own tile per subtile); the row sums take each
+// group's logits in one rebase_lse_update (one overflow check per group).  The products of
 // one group are independent of the exp2 work of the previous one, so the matrix cores
 // and the vector ALUs overlap.
 template <int FT>
@@ -278,7 +278,7 @@ constexpr int score_waves() {
 // Per-wavefront row state of the stats pass: lane (c16, g16) holds row c16 of each
 // slot's tile and keys 4*g16..4*g16+3 of every 16-key subtile; (mref, srow) is the
 // running (max, sum of 2^(x - max)) of those logits in the log2 domain, mref starting
-// finite (see online_lse_update).
+// finite (see rebase_lse_update).
 template <int NQ>
 struct StatsRows {
   int pos[NQ];
@@ -341,34 +341,32 @@ __device__ __forceinline__ void stats_tile_body(const ScoreArgs& a, const char* 
 #pragma unroll
           for (int i = 0; i < FT; ++i) acc[u][i] = mma_step(T{}, kf[s], as_uint4(qf[i][s]), acc[u][i]);
       }
+      float x[FT][4 * SG];
 #pragma unroll
-      for (int i = 0; i < FT; ++i) {
-        float x[4 * SG];
+      for (int i = 0; i < FT; ++i)
 #pragma unroll
         for (int u = 0; u < SG; ++u)
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            x[4 * u + t] = acc[u][i][t];
+            x[i][4 * u + t] = acc[u][i][t];
             if constexpr (MASK)
-              x[4 * u + t] = stats_mask(x[4 * u + t], j0 + (sg + u) * 16 + 4 * g16 + t,
-                                        st.live[i], st.pos[i], N);
+              x[i][4 * u + t] = stats_mask(x[i][4 * u + t], j0 + (sg + u) * 16 + 4 * g16 + t,
+                                           st.live[i], st.pos[i], N);
           }
-        online_lse_update<4 * SG>(x, a.scale_log2, st.mref[i], st.srow[i]);
-      }
+      rebase_lse_update<FT, 4 * SG>(x, a.scale_log2, st.mref, st.srow);
     }
   }
   if constexpr (RT > 0) {
+    float x[RT][4];
 #pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      float x[4];
+    for (int r = 0; r < RT; ++r)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        x[t] = accr[r][t];
+        x[r][t] = accr[r][t];
         if constexpr (MASK)
-          x[t] = stats_mask(x[t], j0 + wv * 16 + 4 * g16 + t, st.live[FT + r], st.pos[FT + r], N);
+          x[r][t] = stats_mask(x[r][t], j0 + wv * 16 + 4 * g16 + t, st.live[FT + r], st.pos[FT + r], N);
       }
-      online_lse_update<4>(x, a.scale_log2, st.mref[FT + r], st.srow[FT + r]);
-    }
+    rebase_lse_update<RT, 4>(x, a.scale_log2, st.mref + FT, st.srow + FT);
   }
 }
 
