@@ -96,15 +96,17 @@ __device__ __forceinline__ float rescale(float m, float mx) {
 
 // Online sums of 2^(x*scale - m) (log2 domain) for R rows, NV logits of each per call,
 // x unscaled logits and scale = log2(e)/sqrt(d).  The common path is fma + exp2 + add per
-// logit against the current reference m, with no maximum: a row's sum leaves the finite
-// range only when one of its logits exceeds m by about 2^7 (or very many exceed it by
-// less), and then, in one wave-uniform branch, that row's reference moves up to its
-// batch maximum (and at least kLazyBound above the old reference) and the batch is
-// summed again onto the rescaled old sum.  m starts finite and very negative
+// logit against the current reference m, with no maximum: only when a row's sum reaches
+// kSumLimit = 2^100 (a logit about 2^7 above m, or very many somewhat above it) does
+// that row, in one wave-uniform branch, move its reference up to its batch maximum (and
+// at least kLazyBound above the old one) and sum the batch again onto the rescaled old
+// sum, which then stays below 2^37.  Accepted sums stay below 2^100, so merging a few
+// of them (lane groups, wavefronts) cannot overflow.  m starts finite and very negative
 // (kLazyRefInit): the first live batch of a row takes the branch, masked logits (-inf)
 // add exactly 0, and the result merges with others like any (max, sum) pair.
 constexpr float kLazyBound = 64.0f;
 constexpr float kLazyRefInit = -1.0e30f;
+constexpr float kSumLimit = 0x1p100f;
 template <int R, int NV>
 __device__ __forceinline__ void rebase_lse_update(const float (&x)[R][NV], float scale, float* m,
                                                   float* s) {
@@ -123,12 +125,12 @@ __device__ __forceinline__ void rebase_lse_update(const float (&x)[R][NV], float
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     ns[r] = s[r] + batch(r, m[r]);
-    out = out || !(ns[r] < INFINITY);
+    out = out || !(ns[r] < kSumLimit);
   }
   if (__any(out)) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      if (!(ns[r] < INFINITY)) {
+      if (!(ns[r] < kSumLimit)) {
         float mx = x[r][0];
 #pragma unroll
         for (int i = 1; i < NV; ++i) mx = fmaxf(mx, x[r][i]);

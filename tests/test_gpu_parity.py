@@ -463,6 +463,56 @@ def test_h2o_parity_small(supply_lse, lens):
         assert np.allclose(got[:, s0:s1].sum(1), s1 - s0, rtol=1e-4)
 
 
+def _wide_logit_layer(kind, lens):
+    """A small H2O-shaped layer (every row has a query) whose logits span hundreds of
+    log2 units along the keys, so that the row sums' reference must move mid-stream:
+    every query is a * (1, ..., 1) plus noise and key j is r_j * (1, ..., 1) plus noise,
+    giving logits of about a * r_j * sqrt(d).  "ramp": r_j grows linearly to 8.8 (a
+    single new key exceeds the running reference by far more than 2^7); "step": r_j = 0
+    for the first 64 keys of a sequence and 1.9 after them (every later term is ~2^124
+    times the first tile's, so the sums overflow by accumulation)."""
+    wl = di.small_variant("c5", list(lens))
+    x = di.make_layer(wl, with_v=False)
+    d = wl.head_dim
+    k = 0.1 * x.k.astype(np.float32)
+    q = 0.1 * x.q_all.astype(np.float32) + np.float32(4.0)
+    for b in range(wl.batch):
+        s0, N = int(wl.kv_offsets[b]), wl.cached_lens[b]
+        j = np.arange(N, dtype=np.float32)
+        r = 8.8 * j / max(N - 1, 1) if kind == "ramp" else np.where(j < 64, 0.0, 1.9)
+        k[:, s0:s0 + N] += r.astype(np.float32)[None, :, None]
+    kb = di.f32_to_bf16_bits(k)
+    qab = di.f32_to_bf16_bits(q)
+    x.k, x.k_bits = di.bf16_bits_to_f32(kb).reshape(k.shape), kb.reshape(k.shape)
+    x.q_all, x.q_all_bits = di.bf16_bits_to_f32(qab).reshape(q.shape), qab.reshape(q.shape)
+    nr = wl.n_rows
+    qs = np.empty((wl.n_q_heads, wl.batch * nr, d), np.float32)
+    qsb = np.empty(qs.shape, np.uint16)
+    for b in range(wl.batch):
+        s0, N = int(wl.kv_offsets[b]), wl.cached_lens[b]
+        qs[:, b * nr:(b + 1) * nr] = x.q_all[:, s0 + N - nr:s0 + N]
+        qsb[:, b * nr:(b + 1) * nr] = x.q_all_bits[:, s0 + N - nr:s0 + N]
+    x.q, x.q_bits = qs, qsb
+    return wl, x
+
+
+@pytest.mark.parametrize("kind", ["ramp", "step"])
+def test_wide_logit_range_scores_and_h2o_vs_oracle(kind):
+    wl, x = _wide_logit_layer(kind, (700, 130))
+    _log(f"wide logit range {kind}: lens={wl.cached_lens}")
+    got, want = run_score(wl, x)
+    check_scores(got, want, f"scores {kind}")
+    g = geom_of(wl)
+    col = dge.h2o_colsum(g, to_dev(x.q_all_bits, "bf16"), to_dev(x.k_bits, "bf16"))
+    torch.cuda.synchronize()
+    want_h = oracle.h2o_colsum(x.q_all, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads)
+    got_h = col.cpu().numpy()
+    check_scores(got_h, want_h, f"h2o {kind}")
+    for b in range(wl.batch):
+        s0, s1 = wl.kv_offsets[b], wl.kv_offsets[b + 1]
+        assert np.allclose(got_h[:, s0:s1].sum(1), s1 - s0, rtol=1e-4)
+
+
 def test_h2o_c5_two_heads_and_select():
     wl = di.WORKLOADS["c5"]
     _log("h2o c5 full size, oracle on KV heads 0 and 5")
