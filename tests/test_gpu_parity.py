@@ -503,6 +503,16 @@ def test_wide_logit_range_scores_and_h2o_vs_oracle(kind):
     got, want = run_score(wl, x)
     check_scores(got, want, f"scores {kind}")
     g = geom_of(wl)
+    # the merged row normalisers: logits of a few hundred carry fp32 accumulation error
+    # proportional to their size, hence the relative term
+    _, row_lse = dge.score_with_lse(g, dge.ROWS_WINDOW_DRAFT, to_dev(x.q_bits, "bf16"),
+                                    to_dev(x.k_bits, "bf16"))
+    torch.cuda.synchronize()
+    want_lse = oracle.scoring_row_lse(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                      wl.window, wl.k_draft)
+    lerr = np.abs(row_lse.cpu().numpy().astype(np.float64) - want_lse)
+    _log(f"  row log-partitions in [{want_lse.min():.1f}, {want_lse.max():.1f}]: max |err| {lerr.max():.2e}")
+    assert (lerr <= 1e-4 + 1e-6 * np.abs(want_lse)).all()
     col = dge.h2o_colsum(g, to_dev(x.q_all_bits, "bf16"), to_dev(x.k_bits, "bf16"))
     torch.cuda.synchronize()
     want_h = oracle.h2o_colsum(x.q_all, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads)
