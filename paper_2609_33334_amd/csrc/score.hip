@@ -8,8 +8,9 @@
 //   1. stats : each workgroup streams its chunk of K and keeps, per query row, the
 //              running (max, sum of 2^(x - max)) of its logits (log2 domain), stored
 //              as one log2-sum-exp per row and chunk;
-//   2. reduce: one wavefront per (row, sequence, KV head) merges the chunk partials
-//              into c_r = log2 Z_r;
+//   2. reduce: the chunk partials of every (row, sequence, KV head) merge into
+//              c_r = log2 Z_r (a lane per row when there are few chunks, else a
+//              wavefront per row);
 //   3. colsum: each workgroup streams its chunk again, P = 2^(x - c_r), sums over all
 //              rows of the group and writes raw[] (the K slab of one layer, 8-34 MB at
 //              Llama-3-8B geometry, is still in the 256 MB Infinity Cache).
@@ -565,9 +566,53 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
   }
 }
 
-// One wavefront per query row: merge that row's chunk partials (log2-sum-exps, -inf
-// for a chunk whose keys are all masked for the row) into log2 of its normaliser.
-__global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
+// Merging each query row's chunk partials (log2-sum-exps, -inf for a chunk whose keys
+// are all masked for the row) into log2 of its normaliser, in one of two layouts:
+// - score_reduce_rows_kernel, for at most kReduceBatch chunks (long chunks: the
+//   layer-major c3/c4 launches): a lane per row, 64 consecutive rows of one (KV head,
+//   sequence) per wavefront, every chunk's partials of those rows one coalesced
+//   256-byte read, all in flight at once, merged in chunk order;
+// - score_reduce_chunks_kernel, for more chunks (short launches of one layer): a
+//   wavefront per row, a lane per chunk, merged by shuffles.
+// Both write rowc and, when asked, the row's natural-log LSE.
+constexpr int kReduceBatch = 8;
+
+__device__ __forceinline__ void reduce_store(const ScoreArgs& a, int64_t base, int h, int b,
+                                             int m, float c) {
+  a.rowc[base * a.M_pad + m] = c;
+  if (a.lse_out != nullptr) {          // query head h * G + g, row b * n_rows + r
+    const int g = m / a.n_rows, r = m - g * a.n_rows;
+    a.lse_out[(int64_t)(h * a.G + g) * a.batch * a.n_rows + b * a.n_rows + r] =
+        c * 0.6931471805599453f;
+  }
+}
+
+__global__ __launch_bounds__(64) void score_reduce_rows_kernel(ScoreArgs a) {
+  const int m = blockIdx.x * 64 + (int)threadIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  if (m >= a.M_pad) return;
+  const int64_t base = (int64_t)(b * a.n_kv_heads + h);
+  if (m >= a.M) {   // padding rows: 2^(x - inf) = 0
+    a.rowc[base * a.M_pad + m] = INFINITY;
+    return;
+  }
+  const int N = (int)(a.offs[b + 1] - a.offs[b]);
+  const int nch = (N + a.chunk_keys - 1) / a.chunk_keys;   // <= kReduceBatch
+  const float* src = a.partial + base * a.n_chunks * a.M_pad + m;
+  float p[kReduceBatch];
+#pragma unroll
+  for (int u = 0; u < kReduceBatch; ++u) p[u] = u < nch ? src[(int64_t)u * a.M_pad] : -INFINITY;
+  float mm = -INFINITY, ss = 0.0f;
+#pragma unroll
+  for (int u = 0; u < kReduceBatch; ++u) {
+    const float mx = fmaxf(mm, p[u]);
+    ss = ss * rescale(mm, mx) + (p[u] > -INFINITY ? fast_exp2(p[u] - mx) : 0.0f);
+    mm = mx;
+  }
+  reduce_store(a, base, h, b, m, mm + __log2f(ss));
+}
+
+__global__ __launch_bounds__(256) void score_reduce_chunks_kernel(ScoreArgs a) {
   const int lane = threadIdx.x & 63;
   const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int h = blockIdx.y, b = blockIdx.z;
@@ -592,15 +637,7 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(ScoreArgs a) {
   ss *= rescale(mm, mx);
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) ss += __shfl_xor(ss, o, 64);
-  if (lane == 0) {
-    const float c = mx + __log2f(ss);
-    a.rowc[base * a.M_pad + m] = c;
-    if (a.lse_out != nullptr) {          // query head h * G + g, row b * n_rows + r
-      const int g = m / a.n_rows, r = m - g * a.n_rows;
-      a.lse_out[(int64_t)(h * a.G + g) * a.batch * a.n_rows + b * a.n_rows + r] =
-          c * 0.6931471805599453f;
-    }
-  }
+  if (lane == 0) reduce_store(a, base, h, b, m, mx + __log2f(ss));
 }
 
 template <typename T, int D, int FT, int RT>
@@ -685,8 +722,12 @@ hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st)
   const dim3 grid(xcd_grid(a.n_chunks * g.n_kv_heads * g.batch));
   if (a.lse_in == nullptr) {   // normalisers computed here: stats and reduce first
     hipLaunchKernelGGL((score_stats_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
-    hipLaunchKernelGGL(score_reduce_kernel, dim3(a.M_pad / 4, g.n_kv_heads, g.batch), dim3(256),
-                       0, st, a);
+    if (a.n_chunks <= kReduceBatch)
+      hipLaunchKernelGGL(score_reduce_rows_kernel, dim3((a.M_pad + 63) / 64, g.n_kv_heads, g.batch),
+                         dim3(64), 0, st, a);
+    else
+      hipLaunchKernelGGL(score_reduce_chunks_kernel, dim3(a.M_pad / 4, g.n_kv_heads, g.batch),
+                         dim3(256), 0, st, a);
   }
   // the colsum pass with its own split of the keys (it reads only the merged normalisers)
   ScoreArgs ac = a;
