@@ -88,6 +88,10 @@ def parse():
                    help="only time dge_project_rope (query/key capture from the layer input) at "
                         "Llama-3-8B shapes: the scoring rows' q and k projections (HBM-bound on the "
                         "weights) and every row of an 8194-row layer (matrix cores); one JSON line")
+    p.add_argument("--attend", action="store_true",
+                   help="the checks after the path on one layer of the workload: attention of the "
+                        "scoring rows over the compacted cache (dge_cache_attention) and the "
+                        "evicted mass / matching loss (dge_evicted_mass)")
     p.add_argument("--compact-cmp", action="store_true",
                    help="only time dge_compact (out of place) against dge_compact_inplace on one "
                         "layer of the workload, the cache restored outside the timed events")
@@ -127,6 +131,8 @@ def main():
         return bench_compact_cmp(args, wl, x, dev)
     if args.rope:
         return bench_rope(args, wl, x, dev)
+    if args.attend:
+        return bench_attend(args, wl, x, dev)
     if args.repeat_kv:
         return bench_repeat_kv(args, wl, x, dev)
     if args.streams > 1:
@@ -587,6 +593,73 @@ def bench_rope(args, wl, x, dev):
                       "GBps": round(nbytes / us / 1e3, 1),
                       "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "reps": reps}),
           flush=True)
+
+
+def bench_attend(args, wl, x, dev):
+    """The two checks that follow the path, on one layer of the workload, after its scoring
+    (dge_score_with_lse) and selection + compaction (dge_select_compact): attention of the
+    window and draft rows over the compacted cache (dge_cache_attention: output and
+    log-partition, the continuation check of Eq. 1) and their evicted mass, missed mass and
+    matching loss (dge_evicted_mass, K only).  Back-to-back calls between HIP events on the
+    launching stream (median of five groups).  Algorithmic bytes: the compacted K (and V for
+    the attention) once, the query rows, the outputs.  Prints one JSON line."""
+    import torch
+    import paper_2609_33334_amd as dge
+    is_bf16 = wl.dtype == "bf16"
+    elt = 2 if is_bf16 else 4
+
+    def dev_t(bits):
+        t = torch.from_numpy(np.ascontiguousarray(bits))
+        if is_bf16:
+            t = t.view(torch.int16).view(torch.bfloat16)
+        return t.to(dev)
+
+    g = dge.Geometry(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.window, wl.k_draft,
+                     wl.cached_lens, dtype=dge.DGE_BF16 if is_bf16 else dge.DGE_F32, device=dev)
+    q, k, v = dev_t(x.q_bits), dev_t(x.k_bits), dev_t(x.v_bits)
+    n_tail = wl.window + wl.k_draft
+    n_sel = wl.budget_of_layer(0) - wl.window
+    raw, row_lse = dge.score_with_lse(g, dge.ROWS_WINDOW_DRAFT, q, k)
+    idx, nk, kc, vc = dge.select_compact(g, raw, wl.pool, n_tail, n_sel, k, v)
+    out, lse = dge.cache_attention(g, q, n_tail, n_tail, kc, vc, n_sel, n_tail, nk)
+    rho, beta, lm = dge.evicted_mass(g, q, n_tail, n_tail, kc, n_sel, n_tail, nk, row_lse)
+    torch.cuda.synchronize()
+    reps = max(20, min(args.steps, 200))
+    stream = torch.cuda.current_stream()
+    rows = wl.batch * n_tail
+    kc_bytes = wl.batch * wl.n_kv_heads * (n_sel + n_tail) * wl.head_dim * elt
+    q_bytes = wl.n_q_heads * rows * wl.head_dim * elt
+    cases = {
+        "cache_attention": (lambda: dge.cache_attention(g, q, n_tail, n_tail, kc, vc, n_sel, n_tail, nk,
+                                                        out=out, lse=lse),
+                            2 * kc_bytes + q_bytes + wl.n_q_heads * rows * (wl.head_dim + 1) * 4),
+        "evicted_mass": (lambda: dge.evicted_mass(g, q, n_tail, n_tail, kc, n_sel, n_tail, nk, row_lse,
+                                                  rho=rho, beta=beta, l_match=lm),
+                         kc_bytes + q_bytes + 2 * wl.n_q_heads * rows * 4 + 2 * wl.batch * wl.n_kv_heads * 4),
+    }
+    res = {}
+    for name, (call, nbytes) in cases.items():
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3 / reps)
+        us = float(np.median(ts))
+        gbs = nbytes / us / 1e3
+        res[name] = {"us_per_call": round(us, 3), "bytes": int(nbytes),
+                     "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                                  "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)}}
+        log(f"[bench] {name} {wl.name}: {us:.2f} us, {gbs:.0f} GB/s")
+    print(json.dumps({"kernel": "dge_cache_attention / dge_evicted_mass over one compacted layer",
+                      "workload": wl.name, "query_rows": rows, "retained_rows_per_head": n_sel + n_tail,
+                      "reps": reps, "cases": res}), flush=True)
 
 
 def bench_project(args, dev):
