@@ -204,27 +204,28 @@ __global__ __launch_bounds__(kAttThreads) void cache_attention_kernel(AttArgs a)
 }
 
 // ---------------------------------------------------------------------------------------
-// Matrix-core path (bf16; d = 128, or d = 64 for the evicted mass; G <= 4; n_q <= 64).
-// One workgroup of 8 wavefronts per (KV head, sequence): wavefront w is query head
-// h*G + (w % 4) and takes row tiles 2 (w / 4) and 2 (w / 4) + 1 of that head's n_q rows,
-// so every cache row is read once for the whole group.  64-key tiles of the compacted K
-// (and V) are staged through registers into double-buffered LDS: K rows XOR-swizzled by
-// row as in the scoring, V transposed to [dim][key] (four keys of one dimension per 8-byte
-// unit, units swizzled by dimension) so that a lane reads the 8 keys of an MFMA operand
-// with two 8-byte loads.
+// Matrix-core path (bf16; d = 128, or d = 64 for the evicted mass; n_q <= 64).  One
+// workgroup of 4 wavefronts per (query head, sequence), wavefront w taking row tile w of
+// the head's n_q rows; the G workgroups of a KV head are consecutive units of the
+// XCD-aware order, so they share one L2 and each compacted row leaves HBM once.  64-key
+// tiles of the compacted K (and V) are loaded from asm into a ring of register slots
+// (tiles in flight while one is computed; past the end the loads re-read the last row
+// and those tiles are fully masked, so every wait has a fixed count) and stored into
+// double-buffered LDS: K rows XOR-swizzled by row as in the scoring, V transposed to
+// [dim][key] (four keys of one dimension per 8-byte unit, units swizzled by dimension) so
+// that a lane reads the 8 keys of an MFMA operand with two 8-byte loads.
 //   logits:  S^T = K Q^T per 16-key subtile (A = keys, B = query rows): a lane holds 4 keys
-//            of one row;
+//            of one row; tiles below every row's first invisible key skip the mask;
 //   softmax: per row a reference m, the same in the row's four lane groups, and a sum per
 //            lane; m moves only when a sum reaches kSumLimit (then to the row's batch
 //            maximum, the sums and outputs rescaled), so the common path is fma, exp2, add;
-//   output:  O^T += V^T P^T per 32 keys (A = V^T from LDS, B = the lane's own 8 values of
-//            P from two subtiles), P split into bf16 high and low parts (two products) so
-//            the weights keep ~16 bits; a lane then holds 4 dimensions of its row, so the
-//            rescale of a row is local to the lane.
+//   output:  O^T += V^T P^T per 32 keys (A = V^T from LDS, B = the lane's own 8 weights
+//            from two subtiles), P split into a truncated bf16 high part and the bf16 of
+//            the remainder (two products, ~15 bits of weight); a lane holds 4 dimensions of
+//            its own row, so the rescale of a row is local to the lane.
 // The evicted-mass variant stops after the sums.
 constexpr int kAttKT = 64;                 // keys per tile
-constexpr int kAttWaves = 8;
-constexpr int kAttMfmaThreads = kAttWaves * kWave;
+constexpr int kAttMfmaThreads = 256;
 
 template <int D>
 struct AttMfma {
@@ -233,260 +234,256 @@ struct AttMfma {
   static constexpr int kKBytes = kAttKT * kRowBytes;       // one K tile
   static constexpr int kKLoads = kAttKT * kUnits / kAttMfmaThreads;   // per thread
   static constexpr int kVBytes = D * kAttKT * 2;           // one transposed V tile
+  static constexpr int kVQuads = kAttKT / 4;               // 4-key units per V^T dimension row
+  static constexpr int kVPer = kVQuads * 16 / kAttMfmaThreads;   // (quad, octet) pairs per thread
   static constexpr int kNS = D / 32;                       // MFMA steps over d
   static constexpr int kDT = D / 16;                       // 16-dimension output tiles
 };
-
-__device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-
-// hi = bf16(p), lo = bf16(p - hi): p ~ hi + lo to about 16 bits
-__device__ __forceinline__ void split_bf16(float p, uint32_t& hi, uint32_t& lo) {
-  hi = bf16_bits_rne(p);
-  lo = bf16_bits_rne(p - __uint_as_float(hi << 16));
-}
 
 template <int D, bool MASS>
 __global__ __launch_bounds__(kAttMfmaThreads) void cache_attention_mfma_kernel(AttArgs a) {
   using AT = AttMfma<D>;
   constexpr int NS = AT::kNS;
   static_assert(MASS || D == 128, "the V transpose covers 128 dimensions (16 x 8)");
-  const int h = blockIdx.x, b = blockIdx.y;
+  const int units = a.batch * a.n_kv_heads * a.G;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int hq = unit % (a.n_kv_heads * a.G), b = unit / (a.n_kv_heads * a.G);
+  const int h = hq / a.G;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wvu = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int gq = wvu & 3, half = wvu >> 2;
   const int g16 = lane >> 4, c16 = lane & 15;
-  const int G = a.G;
-  const bool active = gq < G;                                  // wave-uniform
-  const int hq = h * G + (active ? gq : 0);
+  const bool own = wvu * 16 < a.n_q;                           // wave-uniform: row tile wvu
   const int64_t q_rows = (int64_t)a.batch * a.n_q;
-  const int n_rt = (a.n_q + 15) / 16;                          // row tiles of a head
   const int nk = max(0, min(a.n_kept[b], a.n_select));
   const int n_vis_max = nk + max(0, min(a.n_tail, a.n_tail - a.q_from_end + a.n_q));
+  const int n_vis_min = nk + max(0, min(a.n_tail, a.n_tail - a.q_from_end + 1));
   const int64_t row0 = ((int64_t)b * a.n_kv_heads + h) * a.n_out;
   const char* kc = reinterpret_cast<const char*>(a.k) + row0 * AT::kRowBytes;
   const char* vc = MASS ? nullptr : reinterpret_cast<const char*>(a.v) + row0 * AT::kRowBytes;
   __shared__ __attribute__((aligned(16))) char klds[2][AT::kKBytes];
   __shared__ __attribute__((aligned(16))) char vlds[MASS ? 1 : 2][MASS ? 16 : AT::kVBytes];
 
-  // this wavefront's row tiles (up to two) and, per lane, the last visible key of its row
-  const uint16_t* qb = reinterpret_cast<const uint16_t*>(a.q);
-  uint4 qf[2][NS];
-  int lim[2];
-  bool own[2];
+  // this wavefront's row tile and, per lane, the first key its row does not see
+  const int r = wvu * 16 + c16;
+  if (n_vis_max == 0) {                                        // nothing visible: no loads
+    if (own && r < a.n_q) {
+      const int64_t ri = (int64_t)hq * q_rows + (int64_t)b * a.n_q + r;
+      if constexpr (MASS) {
+        if (g16 == 0) a.rho[ri] = 1.0f;
+      } else {
+        if (g16 == 0) a.lse[ri] = -INFINITY;
+        for (int e = 4 * g16; e < D; e += 16)
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int rt = 2 * half + i;
-    own[i] = active && rt < n_rt;                              // wave-uniform
-    const int r = rt * 16 + c16;
-    const int rc = min(r, a.n_q - 1);
-    const uint16_t* qrow = qb + ((int64_t)hq * q_rows + (int64_t)b * a.n_q + rc) * D;
-#pragma unroll
-    for (int st = 0; st < NS; ++st) qf[i][st] = load16(reinterpret_cast<const char*>(qrow) + (st * 4 + g16) * 16);
-    lim[i] = r < a.n_q ? nk + max(0, min(a.n_tail, a.n_tail - a.q_from_end + r + 1)) : 0;
+          for (int q = 0; q < 4; ++q) a.out[ri * D + e + q] = 0.0f;
+      }
+    }
+    return;
   }
-  float m[2], ssum[2];
-  f32x4_t o[2][AT::kDT];
+  const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
+                         ((int64_t)hq * q_rows + (int64_t)b * a.n_q + min(r, a.n_q - 1)) * D;
+  u32x4_t qf[NS];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    m[i] = kLazyRefInit;
-    ssum[i] = 0.0f;
+  for (int st = 0; st < NS; ++st) qf[st] = async_load16(reinterpret_cast<const char*>(qrow) + (st * 4 + g16) * 16);
+  const int lim = r < a.n_q ? nk + max(0, min(a.n_tail, a.n_tail - a.q_from_end + r + 1)) : 0;
+  float m = kLazyRefInit, ssum = 0.0f;
+  f32x4_t o[AT::kDT];
 #pragma unroll
-    for (int dt = 0; dt < AT::kDT; ++dt) o[i][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int dt = 0; dt < AT::kDT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // staging of tile t: K units (this thread's kKLoads) and, for the attention, the V quad
-  // of keys 4 (tid / 16) .. +3 at dimensions 8 (tid % 16) .. +7 (d = 128: one per thread)
-  uint4 kst[AT::kKLoads], vst[4];
-  const int vq = tid >> 4, vo = tid & 15;
-  auto stage_load = [&](int t) {
+  // tile staging: K units (kKLoads per thread) and, for the attention, the V quad of keys
+  // 4 (tid / 16) .. +3 at dimensions 8 (tid % 16) .. +7
+  constexpr int PF = MASS ? 4 : 3;                             // tiles in flight
+  constexpr int NV = 4 * AT::kVPer;                             // V loads per thread
+  constexpr int LPT = AT::kKLoads + (MASS ? 0 : NV);          // loads per tile per thread
+  u32x4_t kst[PF][AT::kKLoads], vst[PF][NV];
+  const int vo = tid & 15;
+  auto stage_load = [&](int t, u32x4_t (&ks)[AT::kKLoads], u32x4_t (&vs)[NV]) {
     const int j0 = t * kAttKT;
 #pragma unroll
     for (int i = 0; i < AT::kKLoads; ++i) {
       const int e = tid + kAttMfmaThreads * i;
-      const int r = e / AT::kUnits, u = e % AT::kUnits;
-      kst[i] = load16(kc + (int64_t)min(j0 + r, n_vis_max - 1) * AT::kRowBytes + u * 16);
+      const int rr = e / AT::kUnits, u = e % AT::kUnits;
+      ks[i] = async_load16(kc + (int64_t)max(0, min(j0 + rr, n_vis_max - 1)) * AT::kRowBytes + u * 16);
     }
     if constexpr (!MASS) {
-      if (tid < 256) {
+#pragma unroll
+      for (int n = 0; n < AT::kVPer; ++n) {
+        const int vq = (tid >> 4) + 16 * n;                     // key quad of this thread
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-          vst[k] = load16(vc + (int64_t)min(j0 + 4 * vq + k, n_vis_max - 1) * AT::kRowBytes + vo * 16);
+          vs[4 * n + k] = async_load16(vc + (int64_t)max(0, min(j0 + 4 * vq + k, n_vis_max - 1)) * AT::kRowBytes + vo * 16);
       }
     }
   };
-  auto stage_store = [&](int buf) {
+  auto stage_store = [&](int buf, u32x4_t (&ks)[AT::kKLoads], u32x4_t (&vs)[NV]) {
 #pragma unroll
     for (int i = 0; i < AT::kKLoads; ++i) {
+      reg_fence(ks[i]);
       const int e = tid + kAttMfmaThreads * i;
-      const int r = e / AT::kUnits, u = e % AT::kUnits;
-      *reinterpret_cast<uint4*>(klds[buf] + r * AT::kRowBytes + ((u ^ (r % AT::kUnits)) * 16)) = kst[i];
+      const int rr = e / AT::kUnits, u = e % AT::kUnits;
+      *reinterpret_cast<uint4*>(klds[buf] + rr * AT::kRowBytes + ((u ^ (rr % AT::kUnits)) * 16)) = as_uint4(ks[i]);
     }
     if constexpr (!MASS) {
-      if (tid < 256) {
-        const uint32_t w[4][4] = {{vst[0].x, vst[0].y, vst[0].z, vst[0].w},
-                                  {vst[1].x, vst[1].y, vst[1].z, vst[1].w},
-                                  {vst[2].x, vst[2].y, vst[2].z, vst[2].w},
-                                  {vst[3].x, vst[3].y, vst[3].z, vst[3].w}};
+#pragma unroll
+      for (int k = 0; k < NV; ++k) reg_fence(vs[k]);
+#pragma unroll
+      for (int n = 0; n < AT::kVPer; ++n) {
+        const int vq = (tid >> 4) + 16 * n;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
+          const uint32_t w0 = vs[4 * n][i], w1 = vs[4 * n + 1][i], w2 = vs[4 * n + 2][i], w3 = vs[4 * n + 3][i];
 #pragma unroll
           for (int odd = 0; odd < 2; ++odd) {
             const uint32_t sel = odd ? 0x07060302u : 0x05040100u;
-            const uint32_t lo = __builtin_amdgcn_perm(w[1][i], w[0][i], sel);
-            const uint32_t hi = __builtin_amdgcn_perm(w[3][i], w[2][i], sel);
             const int d = 8 * vo + 2 * i + odd;
             *reinterpret_cast<uint2*>(vlds[buf] + d * (kAttKT * 2) + ((vq ^ (d & 15)) * 8)) =
-                make_uint2(lo, hi);
+                make_uint2(__builtin_amdgcn_perm(w1, w0, sel), __builtin_amdgcn_perm(w3, w2, sel));
           }
         }
       }
     }
   };
 
-  const int nt = (n_vis_max + kAttKT - 1) / kAttKT;
-  if (nt > 0) stage_load(0);
-  for (int t = 0; t < nt; ++t) {
-    const int cur = t & 1;
-    stage_store(cur);
-    __syncthreads();
-    if (t + 1 < nt) stage_load(t + 1);
+  auto compute = [&](int t, int cur) {
+    if (!own) return;
     const int j0 = t * kAttKT;
-    if (active) {
+    const bool masked = j0 + kAttKT > n_vis_min;                // uniform: some key may be hidden
 #pragma unroll
-      for (int pr = 0; pr < 2; ++pr) {                         // subtiles 2 pr, 2 pr + 1
-        f32x4_t acc[2][2];
+    for (int pr = 0; pr < kAttKT / 32; ++pr) {                 // subtiles 2 pr, 2 pr + 1
+      float x[8];
 #pragma unroll
-        for (int su = 0; su < 2; ++su) {
-          const int kr = (2 * pr + su) * 16 + c16;
-          uint4 kf[NS];
+      for (int su = 0; su < 2; ++su) {
+        const int kr = (2 * pr + su) * 16 + c16;
+        uint4 kf[NS];
 #pragma unroll
-          for (int st = 0; st < NS; ++st)
-            kf[st] = *reinterpret_cast<const uint4*>(
-                klds[cur] + kr * AT::kRowBytes + (((st * 4 + g16) ^ (kr % AT::kUnits)) * 16));
+        for (int st = 0; st < NS; ++st)
+          kf[st] = *reinterpret_cast<const uint4*>(
+              klds[cur] + kr * AT::kRowBytes + (((st * 4 + g16) ^ (kr % AT::kUnits)) * 16));
+        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            acc[i][su] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            if (own[i])
+        for (int st = 0; st < NS; ++st) acc = mma_step(bf16_t{}, kf[st], as_uint4(qf[st]), acc);
+        // acc[q] = logit of key j0 + (2 pr + su) 16 + 4 g16 + q for this lane's row
 #pragma unroll
-              for (int st = 0; st < NS; ++st) acc[i][su] = mma_step(bf16_t{}, kf[st], qf[i][st], acc[i][su]);
-          }
+        for (int q = 0; q < 4; ++q) {
+          const int j = j0 + (2 * pr + su) * 16 + 4 * g16 + q;
+          x[4 * su + q] = (!masked || j < lim) ? acc[q] : -INFINITY;
         }
-        // acc[i][su][q] = logit of key j0 + (2 pr + su) 16 + 4 g16 + q for row (2 half + i) 16 + c16
-        float pv[2][8];
+      }
+      float pv[8], ps = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          float x[8];
+      for (int q = 0; q < 8; ++q) {
+        pv[q] = fast_exp2(fmaf(x[q], a.scale_log2, -m));
+        ps += pv[q];
+      }
+      float ns = ssum + ps;
+      // a row whose sum (in any of its lane groups) reaches kSumLimit moves its reference,
+      // the same in all four lane groups
+      int ov = !(ns < kSumLimit) ? 1 : 0;
+      if (__any(ov)) {
+        ov |= __shfl_xor(ov, 16, 64);
+        ov |= __shfl_xor(ov, 32, 64);
+        float mx = x[0];
 #pragma unroll
-          for (int su = 0; su < 2; ++su)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int j = j0 + (2 * pr + su) * 16 + 4 * g16 + q;
-              x[4 * su + q] = j < lim[i] ? acc[i][su][q] : -INFINITY;
-            }
-          float ps = 0.0f;
+        for (int q = 1; q < 8; ++q) mx = fmaxf(mx, x[q]);
+        mx *= a.scale_log2;
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        if (ov) {
+          const float nr = fmaxf(mx, m + kLazyBound);
+          const float f = fast_exp2(m - nr);
+          ps = 0.0f;
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
-            pv[i][q] = fast_exp2(fmaf(x[q], a.scale_log2, -m[i]));
-            ps += pv[i][q];
+            pv[q] = fast_exp2(fmaf(x[q], a.scale_log2, -nr));
+            ps += pv[q];
           }
-          float ns = ssum[i] + ps;
-          // a row whose sum (in any of its lane groups) reaches kSumLimit moves its
-          // reference, the same in all four lane groups
-          int ov = !(ns < kSumLimit) ? 1 : 0;
-          if (__any(ov)) {
-            ov |= __shfl_xor(ov, 16, 64);
-            ov |= __shfl_xor(ov, 32, 64);
-            float mx = x[0];
+          ns = ssum * f + ps;
+          if constexpr (!MASS) {
 #pragma unroll
-            for (int q = 1; q < 8; ++q) mx = fmaxf(mx, x[q]);
-            mx *= a.scale_log2;
-            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            if (ov) {
-              const float nr = fmaxf(mx, m[i] + kLazyBound);
-              const float f = fast_exp2(m[i] - nr);
-              ps = 0.0f;
+            for (int dt = 0; dt < AT::kDT; ++dt)
 #pragma unroll
-              for (int q = 0; q < 8; ++q) {
-                pv[i][q] = fast_exp2(fmaf(x[q], a.scale_log2, -nr));
-                ps += pv[i][q];
-              }
-              ns = ssum[i] * f + ps;
-              if constexpr (!MASS) {
-#pragma unroll
-                for (int dt = 0; dt < AT::kDT; ++dt)
-#pragma unroll
-                  for (int q = 0; q < 4; ++q) o[i][dt][q] *= f;
-              }
-              m[i] = nr;
-            }
+              for (int q = 0; q < 4; ++q) o[dt][q] *= f;
           }
-          ssum[i] = ns;
+          m = nr;
         }
-        if constexpr (!MASS) {
-          uint4 ph[2], pl[2];
+      }
+      ssum = ns;
+      if constexpr (!MASS) {
+        // P ~ hi + lo: hi = the upper half of each float (a bf16 truncation), lo = the
+        // remainder, also truncated; packed two weights per register
+        uint32_t hb[4], lb[4];
 #pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            uint32_t hb[8], lb[8];
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t u0 = __float_as_uint(pv[2 * q]), u1 = __float_as_uint(pv[2 * q + 1]);
+          const float l0 = pv[2 * q] - __uint_as_float(u0 & 0xffff0000u);
+          const float l1 = pv[2 * q + 1] - __uint_as_float(u1 & 0xffff0000u);
+          hb[q] = __builtin_amdgcn_perm(u1, u0, 0x07060302u);
+          lb[q] = __builtin_amdgcn_perm(__float_as_uint(l1), __float_as_uint(l0), 0x07060302u);
+        }
+        const uint4 ph = make_uint4(hb[0], hb[1], hb[2], hb[3]);
+        const uint4 pl = make_uint4(lb[0], lb[1], lb[2], lb[3]);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) split_bf16(pv[i][q], hb[q], lb[q]);
-            ph[i] = make_uint4(hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16), hb[4] | (hb[5] << 16), hb[6] | (hb[7] << 16));
-            pl[i] = make_uint4(lb[0] | (lb[1] << 16), lb[2] | (lb[3] << 16), lb[4] | (lb[5] << 16), lb[6] | (lb[7] << 16));
-          }
-#pragma unroll
-          for (int dt = 0; dt < AT::kDT; ++dt) {
-            const int d = dt * 16 + c16;
-            const char* vrow = vlds[cur] + d * (kAttKT * 2);
-            const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + (((8 * pr + g16) ^ (d & 15)) * 8));
-            const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + (((8 * pr + 4 + g16) ^ (d & 15)) * 8));
-            const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-              if (own[i]) {
-                o[i][dt] = mma_step(bf16_t{}, vf, ph[i], o[i][dt]);
-                o[i][dt] = mma_step(bf16_t{}, vf, pl[i], o[i][dt]);
-              }
-            }
-          }
+        for (int dt = 0; dt < AT::kDT; ++dt) {
+          const int d = dt * 16 + c16;
+          const char* vrow = vlds[cur] + d * (kAttKT * 2);
+          const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + (((8 * pr + g16) ^ (d & 15)) * 8));
+          const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + (((8 * pr + 4 + g16) ^ (d & 15)) * 8));
+          const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
+          o[dt] = mma_step(bf16_t{}, vf, ph, o[dt]);
+          o[dt] = mma_step(bf16_t{}, vf, pl, o[dt]);
         }
       }
     }
-    __syncthreads();
+  };
+
+  // Whole rounds of PF tiles: the loads of tile t + PF are issued while tile t is computed,
+  // so the PF - 1 younger tiles' loads are always in flight when tile t's are awaited and
+  // every wait has a fixed count; the first wait also covers the query fragments.
+  const int nt = (n_vis_max + kAttKT - 1) / kAttKT;
+  const int rounds = (nt + PF - 1) / PF;
+#pragma unroll
+  for (int p = 0; p < PF; ++p) stage_load(p, kst[p], vst[p]);
+  asm_wait_vmcnt<(PF - 1) * LPT>();
+#pragma unroll
+  for (int st = 0; st < NS; ++st) reg_fence(qf[st]);
+  for (int rd = 0; rd < rounds; ++rd) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      const int t = rd * PF + p;
+      if (p > 0) asm_wait_vmcnt<(PF - 1) * LPT>();        // tile t's loads have landed
+      stage_store(t & 1, kst[p], vst[p]);
+      __syncthreads();
+      stage_load(t + PF, kst[p], vst[p]);
+      compute(t, t & 1);
+      __syncthreads();
+    }
+    asm_wait_vmcnt<(PF - 1) * LPT>();                    // the next round's first tile
   }
+  asm_wait_vmcnt<0>();                                   // no load still writes a register
 
   // per row: the four lane groups share the reference; their sums add
-  if (active) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      if (!own[i]) continue;
-      float st = ssum[i];
-      st += __shfl_xor(st, 16, 64);
-      st += __shfl_xor(st, 32, 64);
-      const int r = (2 * half + i) * 16 + c16;
-      const bool seen = nt > 0 && st > 0.0f;
-      const float lse_r = seen ? (m[i] + __log2f(st)) * 0.6931471805599453f : -INFINITY;
-      if (r < a.n_q) {
-        const int64_t ri = (int64_t)hq * q_rows + (int64_t)b * a.n_q + r;
-        if constexpr (MASS) {
-          if (g16 == 0) {
-            const float dlt = fmaxf(a.lse_full[ri] - lse_r, 0.0f);
-            a.rho[ri] = -expm1f(-dlt);
-          }
-        } else {
-          if (g16 == 0) a.lse[ri] = lse_r;
-          const float inv = seen ? 1.0f / st : 0.0f;
-#pragma unroll
-          for (int dt = 0; dt < AT::kDT; ++dt)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              a.out[ri * D + dt * 16 + 4 * g16 + q] = o[i][dt][q] * inv;
-        }
-      }
+  if (!own) return;
+  float st = ssum;
+  st += __shfl_xor(st, 16, 64);
+  st += __shfl_xor(st, 32, 64);
+  const bool seen = nt > 0 && st > 0.0f;
+  const float lse_r = seen ? (m + __log2f(st)) * 0.6931471805599453f : -INFINITY;
+  if (r >= a.n_q) return;
+  const int64_t ri = (int64_t)hq * q_rows + (int64_t)b * a.n_q + r;
+  if constexpr (MASS) {
+    if (g16 == 0) {
+      // deficit log Z - log Z_R >= 0 (rounding can leave it a hair below 0)
+      const float dlt = fmaxf(a.lse_full[ri] - lse_r, 0.0f);
+      a.rho[ri] = -expm1f(-dlt);
     }
+  } else {
+    if (g16 == 0) a.lse[ri] = lse_r;
+    const float inv = seen ? 1.0f / st : 0.0f;
+#pragma unroll
+    for (int dt = 0; dt < AT::kDT; ++dt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) a.out[ri * D + dt * 16 + 4 * g16 + q] = o[dt][q] * inv;
   }
 }
 
@@ -525,8 +522,8 @@ hipError_t launch_att(const AttArgs& a, hipStream_t st) {
 
 template <int D, bool MASS>
 hipError_t launch_att_mfma(const AttArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((cache_attention_mfma_kernel<D, MASS>), dim3(a.n_kv_heads, a.batch),
-                     dim3(kAttMfmaThreads), 0, st, a);
+  hipLaunchKernelGGL((cache_attention_mfma_kernel<D, MASS>),
+                     dim3(xcd_grid(a.batch * a.n_kv_heads * a.G)), dim3(kAttMfmaThreads), 0, st, a);
   if constexpr (MASS)
     hipLaunchKernelGGL(mass_reduce_kernel, dim3(a.batch, a.n_kv_heads), dim3(64), 0, st, a);
   return hipGetLastError();
@@ -534,9 +531,9 @@ hipError_t launch_att_mfma(const AttArgs& a, hipStream_t st) {
 
 template <bool MASS>
 hipError_t launch_att_typed(const dge_geom_t& g, const AttArgs& a, hipStream_t st) {
-  // the matrix-core path: bf16, G <= 4 query heads per KV head, at most 64 query rows
-  // (two row tiles per wavefront), d = 128 (or 64 for the evicted mass)
-  if (g.dtype == DGE_BF16 && a.G <= 4 && a.n_q >= 1 && a.n_q <= 64) {
+  // the matrix-core path: bf16, at most 64 query rows (a row tile per wavefront), d = 128
+  // (or 64 for the evicted mass)
+  if (g.dtype == DGE_BF16 && a.n_q >= 1 && a.n_q <= 64) {
     if (g.head_dim == 128) return launch_att_mfma<128, MASS>(a, st);
     if constexpr (MASS) {
       if (g.head_dim == 64) return launch_att_mfma<64, true>(a, st);
