@@ -205,15 +205,18 @@ __global__ __launch_bounds__(kAttThreads) void cache_attention_kernel(AttArgs a)
 
 // ---------------------------------------------------------------------------------------
 // Matrix-core path (bf16; d = 128, or d = 64 for the evicted mass; n_q <= 64).  One
-// workgroup of 4 wavefronts per (query head, sequence), wavefront w taking row tile w of
-// the head's n_q rows; the G workgroups of a KV head are consecutive units of the
-// XCD-aware order, so they share one L2 and each compacted row leaves HBM once.  64-key
-// tiles of the compacted K (and V) are loaded from asm into a ring of register slots
-// (tiles in flight while one is computed; past the end the loads re-read the last row
-// and those tiles are fully masked, so every wait has a fixed count) and stored into
-// double-buffered LDS: K rows XOR-swizzled by row as in the scoring, V transposed to
-// [dim][key] (four keys of one dimension per 8-byte unit, units swizzled by dimension) so
-// that a lane reads the 8 keys of an MFMA operand with two 8-byte loads.
+// workgroup per (query head, sequence): wavefront w takes row tile w % 4 of the head's n_q
+// rows and key pair w / 4 (keys 32 (w / 4) .. +31) of every tile (64 keys and 8 wavefronts
+// for the attention, 128 keys and 16 for the mass), so several wavefronts per SIMD hide
+// each other's latencies; at the end the key pairs of a row tile are merged in LDS in a
+// fixed order.  The G workgroups of a KV head are
+// consecutive units of the XCD-aware order, so they share one L2 and each compacted row
+// leaves HBM once.  Tiles of the compacted K (and V) are loaded from asm into a ring of
+// register slots (tiles in flight while one is computed; past the end the loads re-read
+// the last row and those tiles are fully masked, so every wait has a fixed count) and
+// stored into double-buffered LDS: K rows XOR-swizzled by row as in the scoring, V
+// transposed to [dim][key] (four keys of one dimension per 8-byte unit, units swizzled by
+// dimension) so that a lane reads the 8 keys of an MFMA operand with two 8-byte loads.
 //   logits:  S^T = K Q^T per 16-key subtile (A = keys, B = query rows): a lane holds 4 keys
 //            of one row; tiles below every row's first invisible key skip the mask;
 //   softmax: per row a reference m, the same in the row's four lane groups, and a sum per
@@ -224,27 +227,31 @@ __global__ __launch_bounds__(kAttThreads) void cache_attention_kernel(AttArgs a)
 //            the remainder (two products, ~15 bits of weight); a lane holds 4 dimensions of
 //            its own row, so the rescale of a row is local to the lane.
 // The evicted-mass variant stops after the sums.
-constexpr int kAttKT = 64;                 // keys per tile
-constexpr int kAttMfmaThreads = 256;
-
-template <int D>
+// Tiles of 64 keys and 8 wavefronts (two key pairs) for the attention, whose output
+// accumulators need the registers of two wavefronts per SIMD; 128 keys and 16 wavefronts
+// (four key pairs) for the evicted mass.
+template <int D, bool MASS>
 struct AttMfma {
+  static constexpr int kKT = MASS ? 128 : 64;              // keys per tile
+  static constexpr int kSplit = kKT / 32;                  // key pairs: wavefronts per row tile
+  static constexpr int kThreads = 4 * kSplit * kWave;
   static constexpr int kRowBytes = D * 2;
   static constexpr int kUnits = kRowBytes / 16;            // 16-byte units per K row
-  static constexpr int kKBytes = kAttKT * kRowBytes;       // one K tile
-  static constexpr int kKLoads = kAttKT * kUnits / kAttMfmaThreads;   // per thread
-  static constexpr int kVBytes = D * kAttKT * 2;           // one transposed V tile
-  static constexpr int kVQuads = kAttKT / 4;               // 4-key units per V^T dimension row
-  static constexpr int kVPer = kVQuads * 16 / kAttMfmaThreads;   // (quad, octet) pairs per thread
+  static constexpr int kKBytes = kKT * kRowBytes;          // one K tile
+  static constexpr int kKLoads = kKT * kUnits / kThreads;  // per thread
+  static constexpr int kVBytes = D * kKT * 2;              // one transposed V tile
   static constexpr int kNS = D / 32;                       // MFMA steps over d
   static constexpr int kDT = D / 16;                       // 16-dimension output tiles
 };
 
 template <int D, bool MASS>
-__global__ __launch_bounds__(kAttMfmaThreads) void cache_attention_mfma_kernel(AttArgs a) {
-  using AT = AttMfma<D>;
+__global__ __launch_bounds__((AttMfma<D, MASS>::kThreads)) void cache_attention_mfma_kernel(AttArgs a) {
+  using AT = AttMfma<D, MASS>;
+  constexpr int kAttKT = AT::kKT, kAttSplit = AT::kSplit, kAttMfmaThreads = AT::kThreads;
   constexpr int NS = AT::kNS;
-  static_assert(MASS || D == 128, "the V transpose covers 128 dimensions (16 x 8)");
+  static_assert(MASS || (D == 128 && kAttKT * 16 == 2 * kAttMfmaThreads),
+                "the V transpose: 128 dimensions (16 x 8), a key pair per thread");
+  static_assert(AT::kKLoads >= 1 && AT::kKLoads * kAttMfmaThreads == kAttKT * AT::kUnits, "K staging");
   const int units = a.batch * a.n_kv_heads * a.G;
   const int unit = xcd_unit(units);
   if (unit >= units) return;
@@ -252,8 +259,9 @@ __global__ __launch_bounds__(kAttMfmaThreads) void cache_attention_mfma_kernel(A
   const int h = hq / a.G;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wvu = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rt = wvu & 3, ks = wvu >> 2;                       // row tile, key pair
   const int g16 = lane >> 4, c16 = lane & 15;
-  const bool own = wvu * 16 < a.n_q;                           // wave-uniform: row tile wvu
+  const bool own = rt * 16 < a.n_q;                            // wave-uniform
   const int64_t q_rows = (int64_t)a.batch * a.n_q;
   const int nk = max(0, min(a.n_kept[b], a.n_select));
   const int n_vis_max = nk + max(0, min(a.n_tail, a.n_tail - a.q_from_end + a.n_q));
@@ -261,13 +269,13 @@ __global__ __launch_bounds__(kAttMfmaThreads) void cache_attention_mfma_kernel(A
   const int64_t row0 = ((int64_t)b * a.n_kv_heads + h) * a.n_out;
   const char* kc = reinterpret_cast<const char*>(a.k) + row0 * AT::kRowBytes;
   const char* vc = MASS ? nullptr : reinterpret_cast<const char*>(a.v) + row0 * AT::kRowBytes;
-  __shared__ __attribute__((aligned(16))) char klds[2][AT::kKBytes];
-  __shared__ __attribute__((aligned(16))) char vlds[MASS ? 1 : 2][MASS ? 16 : AT::kVBytes];
+  constexpr int kStageBytes = AT::kKBytes + (MASS ? 0 : AT::kVBytes);
+  __shared__ __attribute__((aligned(16))) char lds[2 * kStageBytes];
+  __shared__ float mfin[kAttSplit][4][16], sfin[kAttSplit][4][16];
 
-  // this wavefront's row tile and, per lane, the first key its row does not see
-  const int r = wvu * 16 + c16;
+  const int r = rt * 16 + c16;                                 // this lane's row
   if (n_vis_max == 0) {                                        // nothing visible: no loads
-    if (own && r < a.n_q) {
+    if (ks == 0 && own && r < a.n_q) {
       const int64_t ri = (int64_t)hq * q_rows + (int64_t)b * a.n_q + r;
       if constexpr (MASS) {
         if (g16 == 0) a.rho[ri] = 1.0f;
@@ -287,152 +295,143 @@ __global__ __launch_bounds__(kAttMfmaThreads) void cache_attention_mfma_kernel(A
   for (int st = 0; st < NS; ++st) qf[st] = async_load16(reinterpret_cast<const char*>(qrow) + (st * 4 + g16) * 16);
   const int lim = r < a.n_q ? nk + max(0, min(a.n_tail, a.n_tail - a.q_from_end + r + 1)) : 0;
   float m = kLazyRefInit, ssum = 0.0f;
-  f32x4_t o[AT::kDT];
+  f32x4_t o[MASS ? 1 : AT::kDT];
 #pragma unroll
-  for (int dt = 0; dt < AT::kDT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int dt = 0; dt < (MASS ? 1 : AT::kDT); ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // tile staging: K units (kKLoads per thread) and, for the attention, the V quad of keys
-  // 4 (tid / 16) .. +3 at dimensions 8 (tid % 16) .. +7
+  // tile staging: K units (kKLoads per thread) and, for the attention, keys 2 (tid / 16),
+  // +1 of V at dimensions 8 (tid % 16) .. +7, stored as the 4-byte halves of V^T units
   constexpr int PF = MASS ? 4 : 3;                             // tiles in flight
-  constexpr int NV = 4 * AT::kVPer;                             // V loads per thread
-  constexpr int LPT = AT::kKLoads + (MASS ? 0 : NV);          // loads per tile per thread
-  u32x4_t kst[PF][AT::kKLoads], vst[PF][NV];
-  const int vo = tid & 15;
-  auto stage_load = [&](int t, u32x4_t (&ks)[AT::kKLoads], u32x4_t (&vs)[NV]) {
+  constexpr int NV = MASS ? 0 : 2;
+  constexpr int LPT = AT::kKLoads + NV;                        // loads per tile per thread
+  u32x4_t kst[PF][AT::kKLoads], vst[PF][MASS ? 1 : NV];
+  const int vp = tid >> 4, vo = tid & 15;
+  auto stage_load = [&](int t, u32x4_t (&kr)[AT::kKLoads], u32x4_t (&vr)[MASS ? 1 : NV]) {
     const int j0 = t * kAttKT;
 #pragma unroll
     for (int i = 0; i < AT::kKLoads; ++i) {
       const int e = tid + kAttMfmaThreads * i;
       const int rr = e / AT::kUnits, u = e % AT::kUnits;
-      ks[i] = async_load16(kc + (int64_t)max(0, min(j0 + rr, n_vis_max - 1)) * AT::kRowBytes + u * 16);
+      kr[i] = async_load16(kc + (int64_t)max(0, min(j0 + rr, n_vis_max - 1)) * AT::kRowBytes + u * 16);
     }
     if constexpr (!MASS) {
 #pragma unroll
-      for (int n = 0; n < AT::kVPer; ++n) {
-        const int vq = (tid >> 4) + 16 * n;                     // key quad of this thread
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          vs[4 * n + k] = async_load16(vc + (int64_t)max(0, min(j0 + 4 * vq + k, n_vis_max - 1)) * AT::kRowBytes + vo * 16);
-      }
+      for (int k = 0; k < 2; ++k)
+        vr[k] = async_load16(vc + (int64_t)max(0, min(j0 + 2 * vp + k, n_vis_max - 1)) * AT::kRowBytes + vo * 16);
     }
   };
-  auto stage_store = [&](int buf, u32x4_t (&ks)[AT::kKLoads], u32x4_t (&vs)[NV]) {
+  auto stage_store = [&](int buf, u32x4_t (&kr)[AT::kKLoads], u32x4_t (&vr)[MASS ? 1 : NV]) {
+    char* kl = lds + buf * kStageBytes;
 #pragma unroll
     for (int i = 0; i < AT::kKLoads; ++i) {
-      reg_fence(ks[i]);
+      reg_fence(kr[i]);
       const int e = tid + kAttMfmaThreads * i;
       const int rr = e / AT::kUnits, u = e % AT::kUnits;
-      *reinterpret_cast<uint4*>(klds[buf] + rr * AT::kRowBytes + ((u ^ (rr % AT::kUnits)) * 16)) = as_uint4(ks[i]);
+      *reinterpret_cast<uint4*>(kl + rr * AT::kRowBytes + ((u ^ (rr % AT::kUnits)) * 16)) = as_uint4(kr[i]);
     }
     if constexpr (!MASS) {
+      char* vl = kl + AT::kKBytes;
+      reg_fence(vr[0]);
+      reg_fence(vr[1]);
+      const int quad = vp >> 1, hpos = (vp & 1) * 4;
 #pragma unroll
-      for (int k = 0; k < NV; ++k) reg_fence(vs[k]);
+      for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int n = 0; n < AT::kVPer; ++n) {
-        const int vq = (tid >> 4) + 16 * n;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const uint32_t w0 = vs[4 * n][i], w1 = vs[4 * n + 1][i], w2 = vs[4 * n + 2][i], w3 = vs[4 * n + 3][i];
-#pragma unroll
-          for (int odd = 0; odd < 2; ++odd) {
-            const uint32_t sel = odd ? 0x07060302u : 0x05040100u;
-            const int d = 8 * vo + 2 * i + odd;
-            *reinterpret_cast<uint2*>(vlds[buf] + d * (kAttKT * 2) + ((vq ^ (d & 15)) * 8)) =
-                make_uint2(__builtin_amdgcn_perm(w1, w0, sel), __builtin_amdgcn_perm(w3, w2, sel));
-          }
+        for (int odd = 0; odd < 2; ++odd) {
+          const int d = 8 * vo + 2 * i + odd;
+          *reinterpret_cast<uint32_t*>(vl + d * (kAttKT * 2) + ((quad ^ (d & 15)) * 8) + hpos) =
+              __builtin_amdgcn_perm(vr[1][i], vr[0][i], odd ? 0x07060302u : 0x05040100u);
         }
       }
     }
   };
 
-  auto compute = [&](int t, int cur) {
+  auto compute = [&](int t, int buf) {
     if (!own) return;
-    const int j0 = t * kAttKT;
-    const bool masked = j0 + kAttKT > n_vis_min;                // uniform: some key may be hidden
+    const char* kl = lds + buf * kStageBytes;
+    const int j0 = t * kAttKT + 32 * ks;                       // this wavefront's 32 keys
+    const bool masked = j0 + 32 > n_vis_min;                    // uniform: some key may be hidden
+    float x[8];
 #pragma unroll
-    for (int pr = 0; pr < kAttKT / 32; ++pr) {                 // subtiles 2 pr, 2 pr + 1
-      float x[8];
+    for (int su = 0; su < 2; ++su) {
+      const int kr = 32 * ks + 16 * su + c16;
+      uint4 kf[NS];
 #pragma unroll
-      for (int su = 0; su < 2; ++su) {
-        const int kr = (2 * pr + su) * 16 + c16;
-        uint4 kf[NS];
+      for (int st = 0; st < NS; ++st)
+        kf[st] = *reinterpret_cast<const uint4*>(kl + kr * AT::kRowBytes + (((st * 4 + g16) ^ (kr % AT::kUnits)) * 16));
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int st = 0; st < NS; ++st)
-          kf[st] = *reinterpret_cast<const uint4*>(
-              klds[cur] + kr * AT::kRowBytes + (((st * 4 + g16) ^ (kr % AT::kUnits)) * 16));
-        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int st = 0; st < NS; ++st) acc = mma_step(bf16_t{}, kf[st], as_uint4(qf[st]), acc);
+      // acc[q] = logit of key j0 + 16 su + 4 g16 + q for this lane's row
 #pragma unroll
-        for (int st = 0; st < NS; ++st) acc = mma_step(bf16_t{}, kf[st], as_uint4(qf[st]), acc);
-        // acc[q] = logit of key j0 + (2 pr + su) 16 + 4 g16 + q for this lane's row
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int j = j0 + (2 * pr + su) * 16 + 4 * g16 + q;
-          x[4 * su + q] = (!masked || j < lim) ? acc[q] : -INFINITY;
-        }
+      for (int q = 0; q < 4; ++q) {
+        const int j = j0 + 16 * su + 4 * g16 + q;
+        x[4 * su + q] = (!masked || j < lim) ? acc[q] : -INFINITY;
       }
-      float pv[8], ps = 0.0f;
+    }
+    float pv[8], ps = 0.0f;
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        pv[q] = fast_exp2(fmaf(x[q], a.scale_log2, -m));
-        ps += pv[q];
+    for (int q = 0; q < 8; ++q) {
+      pv[q] = fast_exp2(fmaf(x[q], a.scale_log2, -m));
+      ps += pv[q];
+    }
+    float ns = ssum + ps;
+    // a row whose sum (in any of its lane groups) reaches kSumLimit moves its reference,
+    // the same in all four lane groups
+    int ov = !(ns < kSumLimit) ? 1 : 0;
+    if (__any(ov)) {
+      ov |= __shfl_xor(ov, 16, 64);
+      ov |= __shfl_xor(ov, 32, 64);
+      float mx = x[0];
+#pragma unroll
+      for (int q = 1; q < 8; ++q) mx = fmaxf(mx, x[q]);
+      mx *= a.scale_log2;
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      if (ov) {
+        const float nr = fmaxf(mx, m + kLazyBound);
+        const float f = fast_exp2(m - nr);
+        ps = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          pv[q] = fast_exp2(fmaf(x[q], a.scale_log2, -nr));
+          ps += pv[q];
+        }
+        ns = ssum * f + ps;
+        if constexpr (!MASS) {
+#pragma unroll
+          for (int dt = 0; dt < AT::kDT; ++dt)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) o[dt][q] *= f;
+        }
+        m = nr;
       }
-      float ns = ssum + ps;
-      // a row whose sum (in any of its lane groups) reaches kSumLimit moves its reference,
-      // the same in all four lane groups
-      int ov = !(ns < kSumLimit) ? 1 : 0;
-      if (__any(ov)) {
-        ov |= __shfl_xor(ov, 16, 64);
-        ov |= __shfl_xor(ov, 32, 64);
-        float mx = x[0];
+    }
+    ssum = ns;
+    if constexpr (!MASS) {
+      // P ~ hi + lo: hi = the upper half of each float (a bf16 truncation), lo = the
+      // remainder, also truncated; packed two weights per register
+      uint32_t hb[4], lb[4];
 #pragma unroll
-        for (int q = 1; q < 8; ++q) mx = fmaxf(mx, x[q]);
-        mx *= a.scale_log2;
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        if (ov) {
-          const float nr = fmaxf(mx, m + kLazyBound);
-          const float f = fast_exp2(m - nr);
-          ps = 0.0f;
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            pv[q] = fast_exp2(fmaf(x[q], a.scale_log2, -nr));
-            ps += pv[q];
-          }
-          ns = ssum * f + ps;
-          if constexpr (!MASS) {
-#pragma unroll
-            for (int dt = 0; dt < AT::kDT; ++dt)
-#pragma unroll
-              for (int q = 0; q < 4; ++q) o[dt][q] *= f;
-          }
-          m = nr;
-        }
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t u0 = __float_as_uint(pv[2 * q]), u1 = __float_as_uint(pv[2 * q + 1]);
+        const float l0 = pv[2 * q] - __uint_as_float(u0 & 0xffff0000u);
+        const float l1 = pv[2 * q + 1] - __uint_as_float(u1 & 0xffff0000u);
+        hb[q] = __builtin_amdgcn_perm(u1, u0, 0x07060302u);
+        lb[q] = __builtin_amdgcn_perm(__float_as_uint(l1), __float_as_uint(l0), 0x07060302u);
       }
-      ssum = ns;
-      if constexpr (!MASS) {
-        // P ~ hi + lo: hi = the upper half of each float (a bf16 truncation), lo = the
-        // remainder, also truncated; packed two weights per register
-        uint32_t hb[4], lb[4];
+      const uint4 ph = make_uint4(hb[0], hb[1], hb[2], hb[3]);
+      const uint4 pl = make_uint4(lb[0], lb[1], lb[2], lb[3]);
+      const char* vl = kl + AT::kKBytes;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t u0 = __float_as_uint(pv[2 * q]), u1 = __float_as_uint(pv[2 * q + 1]);
-          const float l0 = pv[2 * q] - __uint_as_float(u0 & 0xffff0000u);
-          const float l1 = pv[2 * q + 1] - __uint_as_float(u1 & 0xffff0000u);
-          hb[q] = __builtin_amdgcn_perm(u1, u0, 0x07060302u);
-          lb[q] = __builtin_amdgcn_perm(__float_as_uint(l1), __float_as_uint(l0), 0x07060302u);
-        }
-        const uint4 ph = make_uint4(hb[0], hb[1], hb[2], hb[3]);
-        const uint4 pl = make_uint4(lb[0], lb[1], lb[2], lb[3]);
-#pragma unroll
-        for (int dt = 0; dt < AT::kDT; ++dt) {
-          const int d = dt * 16 + c16;
-          const char* vrow = vlds[cur] + d * (kAttKT * 2);
-          const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + (((8 * pr + g16) ^ (d & 15)) * 8));
-          const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + (((8 * pr + 4 + g16) ^ (d & 15)) * 8));
-          const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
-          o[dt] = mma_step(bf16_t{}, vf, ph, o[dt]);
-          o[dt] = mma_step(bf16_t{}, vf, pl, o[dt]);
-        }
+      for (int dt = 0; dt < AT::kDT; ++dt) {
+        const int d = dt * 16 + c16;
+        const char* vrow = vl + d * (kAttKT * 2);
+        const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + (((8 * ks + g16) ^ (d & 15)) * 8));
+        const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + (((8 * ks + 4 + g16) ^ (d & 15)) * 8));
+        const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
+        o[dt] = mma_step(bf16_t{}, vf, ph, o[dt]);
+        o[dt] = mma_step(bf16_t{}, vf, pl, o[dt]);
       }
     }
   };
@@ -462,14 +461,39 @@ __global__ __launch_bounds__(kAttMfmaThreads) void cache_attention_mfma_kernel(A
   }
   asm_wait_vmcnt<0>();                                   // no load still writes a register
 
-  // per row: the four lane groups share the reference; their sums add
-  if (!own) return;
+  // merge the four key pairs of each row: references and sums first, then the outputs
+  // (through the staging buffers, which are free after the loop's last barrier)
   float st = ssum;
   st += __shfl_xor(st, 16, 64);
   st += __shfl_xor(st, 32, 64);
-  const bool seen = nt > 0 && st > 0.0f;
-  const float lse_r = seen ? (m + __log2f(st)) * 0.6931471805599453f : -INFINITY;
-  if (r >= a.n_q) return;
+  if (own && g16 == 0) {
+    mfin[ks][rt][c16] = m;
+    sfin[ks][rt][c16] = st;
+  }
+  float* ofin = reinterpret_cast<float*>(lds);                 // [ks][rt][16 rows][D]
+  static_assert(MASS || kAttSplit * 4 * 16 * D * 4 <= 2 * kStageBytes, "output merge area");
+  if constexpr (!MASS) {
+    if (own) {
+#pragma unroll
+      for (int dt = 0; dt < AT::kDT; ++dt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          ofin[((ks * 4 + rt) * 16 + c16) * D + dt * 16 + 4 * g16 + q] = o[dt][q];
+    }
+  }
+  __syncthreads();
+  if (ks != 0 || !own || r >= a.n_q) return;
+  float mf = mfin[0][rt][c16];
+#pragma unroll
+  for (int k = 1; k < kAttSplit; ++k) mf = fmaxf(mf, mfin[k][rt][c16]);
+  float w[kAttSplit], sf = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kAttSplit; ++k) {
+    w[k] = rescale(mfin[k][rt][c16], mf);
+    sf += sfin[k][rt][c16] * w[k];
+  }
+  const bool seen = sf > 0.0f;
+  const float lse_r = seen ? (mf + __log2f(sf)) * 0.6931471805599453f : -INFINITY;
   const int64_t ri = (int64_t)hq * q_rows + (int64_t)b * a.n_q + r;
   if constexpr (MASS) {
     if (g16 == 0) {
@@ -479,11 +503,17 @@ __global__ __launch_bounds__(kAttMfmaThreads) void cache_attention_mfma_kernel(A
     }
   } else {
     if (g16 == 0) a.lse[ri] = lse_r;
-    const float inv = seen ? 1.0f / st : 0.0f;
+    const float inv = seen ? 1.0f / sf : 0.0f;
 #pragma unroll
     for (int dt = 0; dt < AT::kDT; ++dt)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) a.out[ri * D + dt * 16 + 4 * g16 + q] = o[dt][q] * inv;
+      for (int q = 0; q < 4; ++q) {
+        const int e = dt * 16 + 4 * g16 + q;
+        float acc = 0.0f;
+#pragma unroll
+        for (int k = 0; k < kAttSplit; ++k) acc += ofin[((k * 4 + rt) * 16 + c16) * D + e] * w[k];
+        a.out[ri * D + e] = acc * inv;
+      }
   }
 }
 
@@ -523,7 +553,8 @@ hipError_t launch_att(const AttArgs& a, hipStream_t st) {
 template <int D, bool MASS>
 hipError_t launch_att_mfma(const AttArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((cache_attention_mfma_kernel<D, MASS>),
-                     dim3(xcd_grid(a.batch * a.n_kv_heads * a.G)), dim3(kAttMfmaThreads), 0, st, a);
+                     dim3(xcd_grid(a.batch * a.n_kv_heads * a.G)), dim3(AttMfma<D, MASS>::kThreads), 0,
+                     st, a);
   if constexpr (MASS)
     hipLaunchKernelGGL(mass_reduce_kernel, dim3(a.batch, a.n_kv_heads), dim3(64), 0, st, a);
   return hipGetLastError();
