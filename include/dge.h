@@ -275,7 +275,9 @@ dge_status_t dge_compact_inplace(const dge_geom_t *geom, const int32_t *idx,
  *   the retained past rows  k_c[b][h][0 .. n_kept[b])      (all precede the tail), and
  *   the tail rows           k_c[b][h][n_kept[b] + t], t <= n_tail - q_from_end + r
  *                           (tail row t sits at position N_b - n_tail + t),
- * with weights softmax_j(q . k_j / sqrt(d)) in float32:
+ * with weights softmax_j(q . k_j / sqrt(d)) (float32 logits, normalisers and sums; for
+ * bf16 caches each weight enters the product with V as a high and a low bf16 part, which
+ * keep about 16 of its significant bits):
  *   out[hq][b * n_q + r][:] = sum_j a_j v_j,
  *   lse[hq][b * n_q + r]    = log sum_j exp(q . k_j / sqrt(d))  (natural log; -inf and a
  *                             zero output when the row attends nothing).
