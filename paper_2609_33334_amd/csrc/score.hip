@@ -29,13 +29,14 @@
 //   for every key and takes the T%4 leftover tiles only for its own 16-key subtile of
 //   each K tile (see slot_tile), so the four wavefronts do equal work and none computes
 //   a padding tile.  Query fragments stay in registers for the whole chunk (48 VGPRs at
-//   Llama-3-8B geometry), so two workgroups fit on a compute unit.
+//   Llama-3-8B geometry), so two stats workgroups (three colsum ones) fit on a compute
+//   unit.
 // - Each 64-key tile of K is copied from HBM straight into LDS (global_load_lds, 16
 //   bytes per lane, a row per 16 lanes) with the 16-byte units of row r XOR-swizzled
 //   by r, so the 16 lanes that read one fragment column hit 16 different bank groups.
-//   Three tiles are always in flight (a 4-stage ring of 16 KB buffers; dummy copies
-//   past the end of a chunk keep every wait count fixed) while one is on the matrix
-//   cores; the loop's barriers wait on LDS traffic only, so the copies are never
+//   Three tiles are always in flight (a 4-stage ring of 16 KB buffers; two with three
+//   workgroups per compute unit; dummy copies past the end of a chunk keep every wait
+//   count fixed) while one is on the matrix cores; the loop's barriers wait on LDS traffic only, so the copies are never
 //   drained early.
 // - Tile bodies are branch-free: all products of a tile (or of a group of subtiles)
 //   are issued before their results are used, so the exp2 work overlaps the matrix
@@ -47,6 +48,8 @@
 // - colsum uses A = query rows, B = keys: a lane holds 4 rows of ONE key, the sum
 //   over rows is in-lane, then across the 4 lane groups (permlane swaps) and the 4
 //   wavefronts (LDS, double-buffered, flushed after the next tile's barrier).
+#include <type_traits>
+
 #include "dge_device.hpp"
 #include "dge_internal.hpp"
 
@@ -81,8 +84,6 @@ struct KTile {
   static constexpr int kUnits = kRowBytes / 16;                // 16-byte units per row
   static constexpr int kInstr = KT * kUnits / kThreads;        // copy instructions per wave
   static constexpr int kBytes = KT * kRowBytes;
-  // pipeline depth: up to 64 KB of LDS per workgroup, at most 4 tiles (3 in flight)
-  static constexpr int kStages = kBytes <= 16384 ? 4 : 2;
 };
 
 // Global->LDS copy of one 64-key tile, issued by all 4 wavefronts: wavefront w's
@@ -127,12 +128,12 @@ __device__ __forceinline__ void ktile_dma(const char* kb, int j0, int N, char* t
     dma16_sbase(base, min(cp.row[i], lim) * KTl::kRowBytes + cp.col[i], lds + i * kWave * 16);
 }
 
-// With S - 1 tiles always in flight, tile t has landed once at most S - 2 younger
-// tiles (and whatever was issued after them) are outstanding; loads issued before it
-// are complete too.
-template <typename T, int D>
+// With S - 1 tiles always in flight (an S-stage ring), tile t has landed once at most
+// S - 2 younger tiles (and whatever was issued after them) are outstanding; loads issued
+// before it are complete too.
+template <typename T, int D, int S>
 __device__ __forceinline__ void ktile_wait() {
-  asm_wait_vmcnt<(KTile<T, D>::kStages - 2) * KTile<T, D>::kInstr>();
+  asm_wait_vmcnt<(S - 2) * KTile<T, D>::kInstr>();
 }
 
 // Fragment of key row r (0..63 within the tile) for chunk step s and lane group g16.
@@ -217,23 +218,22 @@ __device__ __forceinline__ void cr_fence(float (&cr)[NQ][4]) {
 }
 
 // Copies of tiles 0..S-2 of a chunk (dummies past its end).
-template <typename T, int D>
+template <typename T, int D, int S>
 __device__ __forceinline__ void ktile_issue(const char* kb, int c0, int ntiles, int N,
                                             char (*buf)[KTile<T, D>::kBytes],
                                             const KCopy<T, D>& cp) {
-  constexpr int S = KTile<T, D>::kStages;
 #pragma unroll
   for (int t = 0; t < S - 1; ++t) ktile_dma<T, D>(kb, c0 + t * KT, N, buf[t], cp, t < ntiles);
 }
 
 // The copies, then the wait for tile 0: every load issued before the copies (query
 // fragments) has landed too.
-template <typename T, int D>
+template <typename T, int D, int S>
 __device__ __forceinline__ void ktile_prologue(const char* kb, int c0, int ntiles, int N,
                                                char (*buf)[KTile<T, D>::kBytes],
                                                const KCopy<T, D>& cp) {
-  ktile_issue<T, D>(kb, c0, ntiles, N, buf, cp);
-  ktile_wait<T, D>();
+  ktile_issue<T, D, S>(kb, c0, ntiles, N, buf, cp);
+  ktile_wait<T, D, S>();
 }
 
 // consume(tile, j0, t) for the tiles t of [c0, c0 + ntiles * KT), ntiles >= 1, after
@@ -241,14 +241,13 @@ __device__ __forceinline__ void ktile_prologue(const char* kb, int c0, int ntile
 // past the chunk's end) and all of them have landed when this returns.  The barrier
 // at the top of each iteration also waits for the wavefront's own LDS traffic, so
 // whatever consume(t - 1) wrote to LDS is visible to every wavefront in consume(t).
-template <typename T, int D, typename F>
+template <typename T, int D, int S, typename F>
 __device__ __forceinline__ void ktile_stream(const char* kb, int c0, int ntiles, int N,
                                              char (*buf)[KTile<T, D>::kBytes],
                                              const KCopy<T, D>& cp, F&& consume) {
-  constexpr int S = KTile<T, D>::kStages;
   int t = 0;
   do {
-    if (t > 0) ktile_wait<T, D>();
+    if (t > 0) ktile_wait<T, D, S>();
     lds_barrier();           // tile t landed everywhere; buffer (t - 1) % S free
     const int tn = t + S - 1;
     ktile_dma<T, D>(kb, c0 + tn * KT, N, buf[tn % S], cp, tn < ntiles);
@@ -275,11 +274,29 @@ constexpr int score_waves() {
   constexpr int NS = RowChunks<T, D>::kSteps;
   return (FT + RT) * NS <= 12 && FT < 3 && RT < 3 && NS <= 4 ? 2 : 1;
 }
+template <typename T, int D, int FT, int RT>
+constexpr int stats_waves() { return score_waves<T, D, FT, RT>(); }
+// The colsum pass at Llama-3-8B-like row counts (bf16, d = 128, at most two own and one
+// shared tile per wavefront) fits three wavefronts per SIMD (<= 168 registers) with a
+// 3-stage ring: measured 2.5% faster than two wavefronts and a 4-stage ring on 32 layers
+// of a batch of 8 sequences of 16K-32K tokens, unchanged on one layer or one sequence.
+// (The stats pass at three spills.)
+template <typename T, int D, int FT, int RT>
+constexpr int colsum_waves() {
+  return std::is_same<T, bf16_t>::value && D == 128 && FT <= 2 && RT <= 1
+             ? 3 : score_waves<T, D, FT, RT>();
+}
+
+// Depth of the K ring of a kernel compiled for W wavefronts per SIMD (W workgroups per
+// compute unit share its 160 KB of LDS): 4 stages of 16 KB (3 tiles in flight) for up
+// to two workgroups, 3 for three; tiles over 16 KB (fp32 rows of 128) get 2.
+template <typename T, int D, int W>
+constexpr int ring_stages() { return KTile<T, D>::kBytes > 16384 ? 2 : (W >= 3 ? 3 : 4); }
 
 // Per-wavefront row state of the stats pass: lane (c16, g16) holds row c16 of each
 // slot's tile and keys 4*g16..4*g16+3 of every 16-key subtile; (mref, srow) is the
-// running (max, sum of 2^(x - max)) of those logits in the log2 domain, mref starting
-// finite (see rebase_lse_update).
+// running (reference, sum of 2^(x - reference)) of those logits in the log2 domain, mref
+// starting finite (see rebase_lse_update).
 template <int NQ>
 struct StatsRows {
   int pos[NQ];
@@ -405,17 +422,26 @@ __device__ __forceinline__ void stats_rows_merge(StatsRows<NQ>& st) {
 // subtiles are independent straight-line code, so the products of one overlap the exp2
 // work of the previous one.  Ends with lane group g16 of every wavefront writing the
 // wavefront's sums of subtile g16 to redw[g16 * 16 + c16].  MASK: the tile reaches past
-// the first scoring position; pos(i, t) is then the position of row (slot i, 4*g16 + t).
+// the first scoring position; row (slot i, 4*g16 + t) then sits at position
+// p0 + ((rb[i] + t) mod n_rows), rb[i] being the row index of (slot i, 4*g16) mod n_rows.
 template <typename T, int D, int FT, int RT, bool MASK>
 __device__ __forceinline__ void colsum_tile_body(const ScoreArgs& a, const char* lds, int j0,
-                                                 int N, int p0, int tile0, int wv, int c16,
-                                                 int g16,
+                                                 int N, int p0, int wv, int c16, int g16,
                                                  const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
-                                                 const float (&cr)[FT + RT][4], float* redw) {
+                                                 const float (&cr)[FT + RT][4],
+                                                 const int (&rb)[FT + RT], float* redw) {
   constexpr int NS = RowChunks<T, D>::kSteps;
-  auto pos = [&](int i, int t) {
-    const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
-    return p0 + min(m, a.M - 1) % a.n_rows;
+  // key j visible to row (slot i, 4*g16 + t).  The row's position is derived here, in
+  // the rare masked body (the empty asm keeps the compiler from hoisting the 4 (FT + RT)
+  // positions out of the loop, where they would hold registers across every tile);
+  // padding rows (cr = +inf) contribute 0 whatever this says.
+  auto visible = [&](int i, int t, int j) {
+    int r = rb[i];
+    asm volatile("" : "+v"(r));
+    r += t;
+#pragma unroll
+    for (int w = 0; w < 3; ++w) r -= r >= a.n_rows ? a.n_rows : 0;   // t <= 3 < 4 n_rows
+    return j < N && j <= p0 + r;
   };
   float colp[4] = {0.f, 0.f, 0.f, 0.f};
   if constexpr (FT > 0) {
@@ -438,7 +464,7 @@ __device__ __forceinline__ void colsum_tile_body(const ScoreArgs& a, const char*
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           e[t] = fast_exp2(fmaf(acc[i][t], a.scale_log2, -cr[i][t]));
-          if constexpr (MASK) e[t] = (j < N && j <= pos(i, t)) ? e[t] : 0.0f;
+          if constexpr (MASK) e[t] = visible(i, t, j) ? e[t] : 0.0f;
         }
         colp[u] += (e[0] + e[1]) + (e[2] + e[3]);
       }
@@ -463,7 +489,7 @@ __device__ __forceinline__ void colsum_tile_body(const ScoreArgs& a, const char*
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         e[t] = fast_exp2(fmaf(accr[r][t], a.scale_log2, -cr[FT + r][t]));
-        if constexpr (MASK) e[t] = (j < N && j <= pos(FT + r, t)) ? e[t] : 0.0f;
+        if constexpr (MASK) e[t] = visible(FT + r, t, j) ? e[t] : 0.0f;
       }
       cp += (e[0] + e[1]) + (e[2] + e[3]);
     }
@@ -488,18 +514,20 @@ __device__ __forceinline__ void colsum_flush(const ScoreArgs& a, const float (*r
 
 template <typename T, int D, int FT, int RT>
 __device__ __forceinline__ void colsum_tile(const ScoreArgs& a, const char* lds, int j0, int N,
-                                            int p0, int tile0, int wv, int c16, int g16,
+                                            int p0, int wv, int c16, int g16,
                                             const u32x4_t (&qf)[FT + RT][RowChunks<T, D>::kSteps],
-                                            const float (&cr)[FT + RT][4], float* redw) {
+                                            const float (&cr)[FT + RT][4],
+                                            const int (&rb)[FT + RT], float* redw) {
   if (j0 + KT - 1 > p0)
-    colsum_tile_body<T, D, FT, RT, true>(a, lds, j0, N, p0, tile0, wv, c16, g16, qf, cr, redw);
+    colsum_tile_body<T, D, FT, RT, true>(a, lds, j0, N, p0, wv, c16, g16, qf, cr, rb, redw);
   else
-    colsum_tile_body<T, D, FT, RT, false>(a, lds, j0, N, p0, tile0, wv, c16, g16, qf, cr, redw);
+    colsum_tile_body<T, D, FT, RT, false>(a, lds, j0, N, p0, wv, c16, g16, qf, cr, rb, redw);
 }
 
 template <typename T, int D, int FT, int RT>
-__global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score_stats_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kThreads, (stats_waves<T, D, FT, RT>())) void score_stats_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
+  constexpr int S = ring_stages<T, D, stats_waves<T, D, FT, RT>()>();
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int NQ = FT + RT;
   prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
@@ -522,7 +550,7 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
   const char* kb = reinterpret_cast<const char*>(a.k) +
                    ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
   float* part = a.partial + ((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad;
-  __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
+  __shared__ __attribute__((aligned(16))) char ldsbuf[S][KTl::kBytes];
   __shared__ float2 xch[4][(RT > 0 ? RT : 1) * 16];   // shared-tile partials per wavefront
   const KCopy<T, D> kcp(wv, lane);
 
@@ -533,11 +561,11 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
     lds_barrier();                         // previous row group done with the buffers
     u32x4_t qf[NQ][NS];
     load_q_frags<T, D, FT, NQ>(a, h, b, tile0, wv, c16, g16, qf);
-    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, kcp);
+    ktile_prologue<T, D, S>(kb, c0, ntiles, N, ldsbuf, kcp);
     q_fence(qf);                           // landed with the first tile
     StatsRows<NQ> st;
     stats_rows_init<FT, NQ>(a, tile0, wv, c16, p0, st);
-    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, kcp,
+    ktile_stream<T, D, S>(kb, c0, ntiles, N, ldsbuf, kcp,
                        [&](const char* lds, int j0, int) {
                          stats_tile<T, D, FT, RT>(a, lds, j0, N, p0, wv, c16, g16, qf, st);
                        });
@@ -641,8 +669,9 @@ __global__ __launch_bounds__(256) void score_reduce_chunks_kernel(ScoreArgs a) {
 }
 
 template <typename T, int D, int FT, int RT>
-__global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score_colsum_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kThreads, (colsum_waves<T, D, FT, RT>())) void score_colsum_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
+  constexpr int S = ring_stages<T, D, colsum_waves<T, D, FT, RT>()>();
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int NQ = FT + RT;
   prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
@@ -669,7 +698,7 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
   const float* lse_in = a.lse_in;
   const float cr_scale = lse_in != nullptr ? kLog2e : 1.0f;
   float* out = a.raw + (int64_t)h * a.total_rows + s0;
-  __shared__ __attribute__((aligned(16))) char ldsbuf[KTl::kStages][KTl::kBytes];
+  __shared__ __attribute__((aligned(16))) char ldsbuf[S][KTl::kBytes];
   __shared__ float red[2][4][KT];          // per-wavefront column partials, double-buffered
   const KCopy<T, D> kcp(wv, lane);
 
@@ -693,7 +722,7 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
                                : rowc + m;
         cr[i][t] = slot_load4<NQ>(src);
       }
-    ktile_prologue<T, D>(kb, c0, ntiles, N, ldsbuf, kcp);
+    ktile_prologue<T, D, S>(kb, c0, ntiles, N, ldsbuf, kcp);
     q_fence(qf);                           // landed with the first tile
     cr_fence<NQ>(cr);
 #pragma unroll
@@ -703,13 +732,16 @@ __global__ __launch_bounds__(kThreads, (score_waves<T, D, FT, RT>())) void score
         const int m = slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16 + t;
         cr[i][t] = m < a.M ? cr[i][t] * cr_scale : INFINITY;   // padding rows add 0
       }
+    int rb[NQ];
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) rb[i] = min(slot_tile<FT>(tile0, wv, i) * 16 + 4 * g16, a.M - 1) % a.n_rows;
     int prev_j0 = c0;
-    ktile_stream<T, D>(kb, c0, ntiles, N, ldsbuf, kcp,
+    ktile_stream<T, D, S>(kb, c0, ntiles, N, ldsbuf, kcp,
                        [&](const char* lds, int j0, int t) {
                          // the previous tile's partials are visible after the stream's barrier
                          if (t > 0) colsum_flush(a, red[(t - 1) & 1], prev_j0, c1, wv, lane, out, grp > 0);
-                         colsum_tile<T, D, FT, RT>(a, lds, j0, N, p0, tile0, wv, c16, g16, qf,
-                                                   cr, red[t & 1][wv]);
+                         colsum_tile<T, D, FT, RT>(a, lds, j0, N, p0, wv, c16, g16, qf, cr, rb,
+                                                   red[t & 1][wv]);
                          prev_j0 = j0;
                        });
     lds_barrier();
