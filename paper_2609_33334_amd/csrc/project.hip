@@ -31,7 +31,8 @@ struct ProjArgs {
   const uint16_t* x;        // [n_rows][hidden] bf16
   const uint16_t* w;        // [n_heads * d][hidden] bf16
   const int32_t* pos;       // [n_rows]
-  uint16_t* out;            // [n_heads][n_rows][d] bf16
+  uint16_t* out;            // [n_heads][.. n_rows ..][d] bf16
+  int64_t out_head_stride;  // elements between heads of out (n_rows * d, or more for a row range)
   int n_rows, hidden, n_heads, d, half;
   double inv_freq[kMaxHalfProj];
 };
@@ -131,7 +132,7 @@ __global__ __launch_bounds__(64 * WAVES) void project_rope_kernel(ProjArgs a) {
       const float hi = c16 < 8 ? other : v[t];
       const float res = c16 < 8 ? fmaf(lo, cs, -hi * sn) : fmaf(hi, cs, lo * sn);
       const int dcol = c16 < 8 ? pair : a.half + pair;
-      a.out[((int64_t)head * a.n_rows + r) * a.d + dcol] = to_bf16_rne(res);
+      a.out[(int64_t)head * a.out_head_stride + (int64_t)r * a.d + dcol] = to_bf16_rne(res);
     }
   }
 }
@@ -215,7 +216,11 @@ __global__ __launch_bounds__(256) void project_split_kernel(ProjArgs a, float* p
     }
 }
 
-// sum of the KS slices (fixed order), rotation, bf16: one thread per (row, head, pair)
+// sum of the KS slices (fixed order), rotation, bf16: one thread per (row, head, pair).
+// The slices' loads are issued kFinishBatch at a time before they are added (a loop that
+// waits for each load before the next is a chain of KS memory round trips).
+constexpr int kFinishBatch = 16;
+
 __global__ __launch_bounds__(256) void project_finish_kernel(ProjArgs a, const float* part, int n_split) {
   const int half = a.half;
   const int64_t total = (int64_t)a.n_rows * a.n_heads * half;
@@ -226,17 +231,30 @@ __global__ __launch_bounds__(256) void project_finish_kernel(ProjArgs a, const f
   const int r = (int)(t / ((int64_t)half * a.n_heads));
   const int ncols = a.n_heads * a.d;
   const int64_t o = (int64_t)r * ncols + head * a.d + pair;
+  const int64_t slice = (int64_t)a.n_rows * ncols;
   float lo = 0.0f, hi = 0.0f;
-  for (int k = 0; k < n_split; ++k) {
-    lo += part[(int64_t)k * a.n_rows * ncols + o];
-    hi += part[(int64_t)k * a.n_rows * ncols + o + half];
+  for (int k0 = 0; k0 < n_split; k0 += kFinishBatch) {
+    float pl[kFinishBatch], ph[kFinishBatch];
+#pragma unroll
+    for (int k = 0; k < kFinishBatch; ++k) {
+      const bool in = k0 + k < n_split;
+      pl[k] = in ? part[(k0 + k) * slice + o] : 0.0f;
+      ph[k] = in ? part[(k0 + k) * slice + o + half] : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < kFinishBatch; ++k) {
+      if (k0 + k < n_split) {
+        lo += pl[k];
+        hi += ph[k];
+      }
+    }
   }
   const double ang = (double)a.pos[r] * a.inv_freq[pair];
   const double kk = rint(ang * 0.15915494309189535);
   const double red = fma(-kk, 2.4492935982947064e-16, fma(-kk, 6.283185307179586, ang));
   float sn, cs;
   sincosf((float)red, &sn, &cs);
-  uint16_t* orow = a.out + ((int64_t)head * a.n_rows + r) * a.d;
+  uint16_t* orow = a.out + (int64_t)head * a.out_head_stride + (int64_t)r * a.d;
   orow[pair] = to_bf16_rne(fmaf(lo, cs, -hi * sn));
   orow[half + pair] = to_bf16_rne(fmaf(hi, cs, lo * sn));
 }
@@ -333,14 +351,9 @@ __global__ __launch_bounds__(256, 2) void project_tile_kernel(ProjArgs a, int nr
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[i][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int t = 0; t < kGStages - 1; ++t) issue(t);
-  for (int t = 0; t < nk; ++t) {
-    asm_wait_vmcnt<(kGStages - 2) * kGCopies>();   // stage t has landed (this thread's part)
-    lds_barrier();                                 // ... everyone's; slot (t - 1) % S is free
-    issue(t + kGStages - 1);
+  // fragment reads of stage t (LDS -> registers)
+  auto frags = [&](int t, uint4 (&af)[4], uint4 (&bf)[4]) {
     const char* st = ring[t % kGStages];
-    uint4 af[4], bf[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = rh * 64 + i * 16 + c16;
@@ -351,10 +364,38 @@ __global__ __launch_bounds__(256, 2) void project_tile_kernel(ProjArgs a, int nr
       const int r = ct[e] * 16 + c16;
       bf[e] = *reinterpret_cast<const uint4*>(st + kGHalfBytes + r * 64 + ((g16 ^ ((r >> 1) & 3)) * 16));
     }
+  };
+  // Software-pipelined: the fragments of stage t + 1 are read while the products of stage
+  // t run.  Stage t + 1 has landed for everyone after the wait and barrier at the top of
+  // iteration t; the same barrier tells that every wavefront's reads of stage t (issued in
+  // iteration t - 1) have completed, so its slot may take the copies of stage t + S.
+#pragma unroll
+  for (int t = 0; t < kGStages - 1; ++t) issue(t);
+  asm_wait_vmcnt<(kGStages - 2) * kGCopies>();     // stage 0 has landed (this thread's part)
+  lds_barrier();                                   // ... everyone's
+  issue(kGStages - 1);
+  // stage t: the next stage's fragments into (an, bn), then the products of (af, bf).  No
+  // branch: the last stage reads a slot of dummy copies it never uses, so the products
+  // wait only for their own fragments (a join of paths would make the compiler wait for
+  // all LDS reads in flight).
+  auto step = [&](int t, const uint4 (&af)[4], const uint4 (&bf)[4], uint4 (&an)[4], uint4 (&bn)[4]) {
+    asm_wait_vmcnt<(kGStages - 2) * kGCopies>();   // stage t + 1 has landed (this thread's part)
+    lds_barrier();                                 // ... everyone's; stage t's slot is free
+    issue(t + kGStages);
+    frags(t + 1, an, bn);
+    // keep the reads above the products (the scheduler would otherwise sink them below,
+    // serialising LDS latency and matrix cores again)
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc[i][e] = mma_step(bf16_t{}, af[i], bf[e], acc[i][e]);
+  };
+  uint4 a0[4], b0[4], a1[4], b1[4];              // two fragment sets, used in turn
+  frags(0, a0, b0);
+  for (int t = 0; t < nk; t += 2) {
+    step(t, a0, b0, a1, b1);
+    if (t + 1 < nk) step(t + 1, a1, b1, a0, b0);
   }
   asm_wait_vmcnt<0>();                         // no copy still writes into the ring
   // epilogue: lane holds rows 4 g16 + k of each row tile, column c16 of each column tile
@@ -374,7 +415,7 @@ __global__ __launch_bounds__(256, 2) void project_tile_kernel(ProjArgs a, int nr
           float sn, cs;
           sincosf((float)red, &sn, &cs);
           const float lo = acc[i][e][k], hi = acc[i][e + 2][k];
-          uint16_t* orow = a.out + ((int64_t)head * a.n_rows + r) * a.d;
+          uint16_t* orow = a.out + (int64_t)head * a.out_head_stride + (int64_t)r * a.d;
           orow[pair] = to_bf16_rne(fmaf(lo, cs, -hi * sn));
           orow[a.half + pair] = to_bf16_rne(fmaf(hi, cs, lo * sn));
         }
@@ -384,7 +425,7 @@ __global__ __launch_bounds__(256, 2) void project_tile_kernel(ProjArgs a, int nr
 
 bool project_tiled(int n_rows, int hidden, int n_heads, int head_dim) {
   const int64_t ncols = (int64_t)n_heads * head_dim;
-  return n_rows > 64 && ncols % kGT == 0 && hidden % kGBK == 0 &&
+  return n_rows >= kGT && ncols % kGT == 0 && hidden % kGBK == 0 &&
          (int64_t)n_rows * hidden * 2 < ((int64_t)1 << 32) && ncols * hidden * 2 < ((int64_t)1 << 32);
 }
 
@@ -414,6 +455,7 @@ hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_head
   a.w = static_cast<const uint16_t*>(w);
   a.pos = positions;
   a.out = static_cast<uint16_t*>(out);
+  a.out_head_stride = (int64_t)n_rows * head_dim;
   a.n_rows = n_rows;
   a.hidden = hidden;
   a.n_heads = n_heads;
@@ -450,9 +492,21 @@ hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_head
     return hipGetLastError();
   }
   if (project_tiled(n_rows, hidden, n_heads, head_dim)) {
-    const int nrb = (n_rows + kGT - 1) / kGT, ncb = (int)((int64_t)n_heads * head_dim / kGT);
-    hipLaunchKernelGGL(project_tile_kernel, dim3(xcd_grid(nrb * ncb)), dim3(256), 0, st, a, nrb, ncb);
-    return hipGetLastError();
+    // whole 128-row blocks on the tiles; the rows past the last whole block (a partial
+    // block would cost as much as a full one, in a round of its own at the end of the
+    // launch) through the small-row kernel, as a row range of the same output
+    const int nrb = n_rows / kGT, ncb = (int)((int64_t)n_heads * head_dim / kGT);
+    const int rest = n_rows - nrb * kGT;
+    ProjArgs am = a;
+    am.n_rows = nrb * kGT;
+    hipLaunchKernelGGL(project_tile_kernel, dim3(xcd_grid(nrb * ncb)), dim3(256), 0, st, am, nrb, ncb);
+    if (rest == 0) return hipGetLastError();
+    ProjArgs ar = a;
+    ar.x = a.x + (int64_t)nrb * kGT * hidden;
+    ar.pos = a.pos + nrb * kGT;
+    ar.out = a.out + (int64_t)nrb * kGT * head_dim;
+    ar.n_rows = rest;
+    return hidden % 256 == 0 ? launch_proj_waves<8>(ar, st) : launch_proj_waves<4>(ar, st);
   }
   // eight wavefronts split the hidden dimension (each keeps 8 K steps of loads in flight),
   // four when it is not a multiple of 256

@@ -277,15 +277,18 @@ constexpr int score_waves() {
 template <typename T, int D, int FT, int RT>
 constexpr int stats_waves() { return score_waves<T, D, FT, RT>(); }
 // The colsum pass at Llama-3-8B-like row counts (bf16, d = 128, at most two own and one
-// shared tile per wavefront) fits three wavefronts per SIMD (<= 168 registers) with a
-// 3-stage ring: measured 2.5% faster than two wavefronts and a 4-stage ring on 32 layers
-// of a batch of 8 sequences of 16K-32K tokens, unchanged on one layer or one sequence.
-// (The stats pass at three spills.)
+// shared tile per wavefront) also fits three wavefronts per SIMD (<= 168 registers) with a
+// 3-stage ring; the stats pass at three spills.  Three are faster on launches of many
+// rounds of workgroups (32 layers of a batch of 8 sequences of 16K-32K tokens: colsum
+// 3.2 -> 2.9 ms) and slower on launches of one or two rounds (32 layers of one 16K
+// sequence, 1280 workgroups: 2-4%, the last round then leaving compute units idle), so
+// the launch picks the instance by its workgroup count (kColsumThreeWaveUnits).
 template <typename T, int D, int FT, int RT>
-constexpr int colsum_waves() {
+constexpr int colsum_max_waves() {
   return std::is_same<T, bf16_t>::value && D == 128 && FT <= 2 && RT <= 1
              ? 3 : score_waves<T, D, FT, RT>();
 }
+constexpr int kColsumThreeWaveUnits = 4096;
 
 // Depth of the K ring of a kernel compiled for W wavefronts per SIMD (W workgroups per
 // compute unit share its 160 KB of LDS): 4 stages of 16 KB (3 tiles in flight) for up
@@ -668,10 +671,10 @@ __global__ __launch_bounds__(256) void score_reduce_chunks_kernel(ScoreArgs a) {
   if (lane == 0) reduce_store(a, base, h, b, m, mx + __log2f(ss));
 }
 
-template <typename T, int D, int FT, int RT>
-__global__ __launch_bounds__(kThreads, (colsum_waves<T, D, FT, RT>())) void score_colsum_kernel(ScoreArgs a) {
+template <typename T, int D, int FT, int RT, int W>
+__global__ __launch_bounds__(kThreads, W) void score_colsum_kernel(ScoreArgs a) {
   using KTl = KTile<T, D>;
-  constexpr int S = ring_stages<T, D, colsum_waves<T, D, FT, RT>()>();
+  constexpr int S = ring_stages<T, D, W>();
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int NQ = FT + RT;
   prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
@@ -766,8 +769,13 @@ hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st)
   ac.iters = a.c_iters;
   ac.chunk_keys = a.c_chunk_keys;
   ac.n_chunks = a.c_n_chunks;
-  const dim3 gridc(xcd_grid(ac.n_chunks * g.n_kv_heads * g.batch));
-  hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT>), gridc, dim3(kThreads), 0, st, ac);
+  const int cunits = ac.n_chunks * g.n_kv_heads * g.batch;
+  const dim3 gridc(xcd_grid(cunits));
+  constexpr int W2 = score_waves<T, D, FT, RT>(), W3 = colsum_max_waves<T, D, FT, RT>();
+  if (W3 != W2 && cunits >= kColsumThreeWaveUnits)
+    hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT, W3>), gridc, dim3(kThreads), 0, st, ac);
+  else
+    hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT, W2>), gridc, dim3(kThreads), 0, st, ac);
   return hipGetLastError();
 }
 

@@ -1014,6 +1014,39 @@ def test_batch_of_18_sequences_vs_oracle():
     check_scores(col.cpu().numpy(), want_col, "batch 18 h2o colsum")
 
 
+MANY_SEQS = tuple(int(n) for n in np.random.default_rng(np.random.SeedSequence([520, 0])).integers(100, 300, size=520))
+
+
+def test_score_launch_of_many_workgroups_vs_oracle():
+    """A launch with more than 4096 colsum workgroups (520 ragged sequences x 8 KV heads,
+    one chunk each), which takes the colsum instance compiled for three wavefronts per
+    SIMD: dge_score, dge_score_with_lse and dge_score_lse (the oracle's row LSEs) against
+    the oracle on every sequence."""
+    wl = di.small_variant("c2", MANY_SEQS)
+    _log(f"score launch of {wl.batch} sequences x {wl.n_kv_heads} heads, lens {min(MANY_SEQS)}..{max(MANY_SEQS)}")
+    x = di.make_layer(wl, with_v=False)
+    g = geom_of(wl)
+    q, k = to_dev(x.q_bits, "bf16"), to_dev(x.k_bits, "bf16")
+    want_raw = oracle.window_scores(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                    wl.window, wl.k_draft)
+    want_lse = oracle.scoring_row_lse(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads,
+                                      wl.window, wl.k_draft)
+    raw = dge.score(g, dge.ROWS_WINDOW_DRAFT, q, k)
+    torch.cuda.synchronize()
+    check_scores(raw.cpu().numpy(), want_raw, "many workgroups, score")
+    raw2, lse = dge.score_with_lse(g, dge.ROWS_WINDOW_DRAFT, q, k)
+    torch.cuda.synchronize()
+    check_scores(raw2.cpu().numpy(), want_raw, "many workgroups, score_with_lse")
+    lse_h = lse.cpu().numpy().astype(np.float64)
+    lerr = np.abs(lse_h - want_lse)
+    _log(f"  row lse: max abs err {lerr.max():.2e}")
+    assert (lerr <= 1e-4 + 1e-6 * np.abs(want_lse)).all()
+    raw3 = dge.score_lse(g, dge.ROWS_WINDOW_DRAFT, q, k,
+                         torch.from_numpy(want_lse.astype(np.float32)).to(DEV))
+    torch.cuda.synchronize()
+    check_scores(raw3.cpu().numpy(), want_raw, "many workgroups, score_lse")
+
+
 # ----------------------------------------------------------------------------------
 # Repeated-KV layout (every KV head copied to the G query heads of its group, scored and
 # selected per query head, no group mean): the geometry with G = 1 over the repeated cache
@@ -1102,6 +1135,7 @@ PROJ_CASES = {
     "split_d64_rows_10": (10, 2048, 6, 64, 3, None),
     "split_rows_64": (64, 4096, 4, 128, 1000, None),
     "d64_ragged_rows": (130, 1024, 4, 64, 0, None),
+    "tiles_and_122_rows": (250, 1024, 4, 128, 5, None),
     "one_row": (1, 128, 1, 64, 7, None),
     "h2o_all_rows_sampled": (8194, 4096, 32, 128, 0, 48),
 }
@@ -1124,7 +1158,10 @@ def test_project_rope_vs_oracle(case):
     out = dge.project_rope(to_dev(xb, "bf16"), to_dev(wb, "bf16"), torch.from_numpy(pos).to(DEV), H, d)
     torch.cuda.synchronize()
     got = di.bf16_bits_to_f32(out.cpu().view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
-    rows = np.arange(n) if n_check is None else np.sort(rng.choice(n, size=n_check, replace=False))
+    # sampled rows: a random set plus the edges of the 128-row tiles and the last rows (the
+    # rows past the last whole tile take another kernel)
+    rows = np.arange(n) if n_check is None else np.unique(np.concatenate(
+        [rng.choice(n, size=n_check, replace=False), [0, 127, 128, n - 131, n - 130, n - 3, n - 2, n - 1]]))
     x64 = di.bf16_bits_to_f32(xb).astype(np.float64)[rows]
     w64 = di.bf16_bits_to_f32(wb).astype(np.float64)
     want = oracle.project_rope(x64, w64, pos[rows], H, d)
