@@ -57,13 +57,19 @@ __device__ __forceinline__ uint4 lds_frag(const char* lds, int r, int s, int g16
   return *reinterpret_cast<const uint4*>(lds + swz(r, s * 4 + g16));
 }
 
-// Global loads of a 64-row block (rows clamped to the sequence); 4 units per thread.
+// Global loads of a 64-row block (rows clamped to the sequence); 4 units per thread.  The
+// address is a wave-uniform base at row min(r0, N - 1) plus a 32-bit lane offset below 16
+// KB, which the compiler turns into scalar-base loads (one vector add, min, subtract and
+// shift per load instead of a 64-bit multiply-add chain).
 __device__ __forceinline__ void block_load(const char* base, int r0, int N, int tid, uint4 (&st)[4]) {
+  const int rb = min(r0, N - 1);
+  const char* b0 = base + (int64_t)rb * RowBytes;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int e = tid + 256 * i;
     const int r = e >> 4, u = e & 15;
-    st[i] = load16(base + (int64_t)min(r0 + r, N - 1) * RowBytes + u * 16);
+    const uint32_t off = (uint32_t)((min(r0 + r, N - 1) - rb) * RowBytes + u * 16);
+    st[i] = load16(b0 + off);
   }
 }
 
