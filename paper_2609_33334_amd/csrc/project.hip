@@ -423,6 +423,118 @@ __global__ __launch_bounds__(256, 2) void project_tile_kernel(ProjArgs a, int nr
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Large tiles for many rows: 256 x 256 per workgroup, eight wavefronts, each computing 128
+// rows x 64 columns (eight row tiles; two low 16-column tiles and their partners, as
+// above).  Per 32-wide K slice a workgroup copies 32 KB into LDS for 512 products, half
+// the L2-to-LDS bytes per product of the 128 x 128 tiles; 3 stages (96 KB) leave one
+// workgroup per compute unit.  Same LDS row format and swizzle as the 128 x 128 kernel.
+// ---------------------------------------------------------------------------------------
+constexpr int kHT = 256;                        // rows and columns per workgroup
+constexpr int kHWaves = 8;
+constexpr int kHStages = 3;
+constexpr int kHHalfBytes = kHT * kGBK * 2;     // A or B part of a stage: 16 KB
+constexpr int kHStageBytes = 2 * kHHalfBytes;   // 32 KB
+constexpr int kHCopies = kHStageBytes / (64 * kHWaves * 16);   // copies per thread per stage
+
+__global__ __launch_bounds__(64 * kHWaves, 1) void project_tile256_kernel(ProjArgs a, int nrb, int ncb) {
+  const int units = nrb * ncb;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int group = unit / (kGGroup * ncb), in_group = unit % (kGGroup * ncb);
+  const int first = group * kGGroup, rows_g = min(nrb - first, kGGroup);
+  const int rb = first + in_group % rows_g, cb = in_group / rows_g;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c16 = lane & 15, g16 = lane >> 4;
+  const int row0 = rb * kHT, col0 = cb * kHT;
+  __shared__ __attribute__((aligned(16))) char ring[kHStages][kHStageBytes];
+  // wavefront wv's copy i fills bytes [(kHCopies wv + i) KB, +1 KB) of a stage: the A part
+  // (x rows) for wavefronts 0-3, the B part (W rows) for 4-7
+  const int wvu = __builtin_amdgcn_readfirstlane(wv);
+  const bool is_b = wvu * kHCopies * 1024 >= kHHalfBytes;
+  uint32_t goff[kHCopies];
+#pragma unroll
+  for (int i = 0; i < kHCopies; ++i) {
+    const int o = ((wv * kHCopies + i) * 64 + lane) * 16 - (is_b ? kHHalfBytes : 0);
+    const int r = o / 64, pu = (o % 64) / 16;
+    const int u = pu ^ ((r >> 1) & 3);
+    const int grow = is_b ? col0 + r : min(row0 + r, a.n_rows - 1);
+    goff[i] = (uint32_t)(((int64_t)grow * a.hidden + 8 * u) * 2);
+  }
+  const uint32_t lds_wave = (uint32_t)(wvu * kHCopies * 1024);
+  const int nk = a.hidden / kGBK;
+  auto issue = [&](int t) {                     // copies of stage t (t >= nk: stage 0 again)
+    const int te = t < nk ? t : 0;
+    const uint32_t lds = (uint32_t)(uintptr_t)(lds_ptr_t)ring[t % kHStages] + lds_wave;
+    const char* src = reinterpret_cast<const char*>(is_b ? a.w : a.x) + (int64_t)te * kGBK * 2;
+#pragma unroll
+    for (int i = 0; i < kHCopies; ++i) dma16_sbase(src, goff[i], lds + i * 1024);
+  };
+  const int rh = wv & 1, j = wv >> 1;
+  const int lpt = a.d / 32;                     // low 16-column tiles per head
+  int ct[4];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int L = 2 * j + e;
+    const int lo = (L / lpt) * (a.d / 16) + L % lpt;
+    ct[e] = lo;
+    ct[e + 2] = lo + lpt;
+  }
+  f32x4_t acc[8][4];                            // [row tile][column tile]
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[i][e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < kHStages - 1; ++t) issue(t);
+  for (int t = 0; t < nk; ++t) {
+    asm_wait_vmcnt<(kHStages - 2) * kHCopies>();   // stage t has landed (this thread's part)
+    lds_barrier();                                 // ... everyone's; slot (t - 1) % S is free
+    issue(t + kHStages - 1);
+    const char* st = ring[t % kHStages];
+    uint4 bf[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = ct[e] * 16 + c16;
+      bf[e] = *reinterpret_cast<const uint4*>(st + kHHalfBytes + r * 64 + ((g16 ^ ((r >> 1) & 3)) * 16));
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = rh * 128 + i * 16 + c16;
+      const uint4 af = *reinterpret_cast<const uint4*>(st + r * 64 + ((g16 ^ ((r >> 1) & 3)) * 16));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[i][e] = mma_step(bf16_t{}, af, bf[e], acc[i][e]);
+    }
+  }
+  asm_wait_vmcnt<0>();                          // no copy still writes into the ring
+  // epilogue: lane holds rows 4 g16 + k of each row tile, column c16 of each column tile
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int colg = col0 + ct[e] * 16 + c16;   // global low column
+    const int head = colg / a.d, pair = colg % a.d;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int r = row0 + rh * 128 + i * 16 + 4 * g16 + k;
+        if (r < a.n_rows) {
+          const double ang = (double)a.pos[r] * a.inv_freq[pair];
+          const double kk = rint(ang * 0.15915494309189535);
+          const double red = fma(-kk, 2.4492935982947064e-16, fma(-kk, 6.283185307179586, ang));
+          float sn, cs;
+          __sincosf((float)red, &sn, &cs);
+          const float lo = acc[i][e][k], hi = acc[i][e + 2][k];
+          uint16_t* orow = a.out + (int64_t)head * a.out_head_stride + (int64_t)r * a.d;
+          orow[pair] = to_bf16_rne(fmaf(lo, cs, -hi * sn));
+          orow[a.half + pair] = to_bf16_rne(fmaf(hi, cs, lo * sn));
+        }
+        // one row at a time: the scheduler would otherwise interleave the double-precision
+        // angle work of many rows and run out of registers beside the 128 accumulators
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  }
+}
+
 bool project_tiled(int n_rows, int hidden, int n_heads, int head_dim) {
   const int64_t ncols = (int64_t)n_heads * head_dim;
   return n_rows >= kGT && ncols % kGT == 0 && hidden % kGBK == 0 &&
@@ -492,20 +604,34 @@ hipError_t launch_project_rope(int n_rows, int hidden, const void* x, int n_head
     return hipGetLastError();
   }
   if (project_tiled(n_rows, hidden, n_heads, head_dim)) {
-    // whole 128-row blocks on the tiles; the rows past the last whole block (a partial
-    // block would cost as much as a full one, in a round of its own at the end of the
-    // launch) through the small-row kernel, as a row range of the same output
-    const int nrb = n_rows / kGT, ncb = (int)((int64_t)n_heads * head_dim / kGT);
-    const int rest = n_rows - nrb * kGT;
-    ProjArgs am = a;
-    am.n_rows = nrb * kGT;
-    hipLaunchKernelGGL(project_tile_kernel, dim3(xcd_grid(nrb * ncb)), dim3(256), 0, st, am, nrb, ncb);
-    if (rest == 0) return hipGetLastError();
-    ProjArgs ar = a;
-    ar.x = a.x + (int64_t)nrb * kGT * hidden;
-    ar.pos = a.pos + nrb * kGT;
-    ar.out = a.out + (int64_t)nrb * kGT * head_dim;
-    ar.n_rows = rest;
+    // Whole tiles only (a partial block would cost as much as a full one, in a round of its
+    // own at the end of a launch): 256-row blocks on the large tiles when the columns come
+    // in 256s, then whole 128-row blocks, then the rest through the small-row kernel, each
+    // launch on a row range of the same output.
+    const int64_t ncols = (int64_t)n_heads * head_dim;
+    auto range = [&](int r0, int n) {
+      ProjArgs ar = a;
+      ar.x = a.x + (int64_t)r0 * hidden;
+      ar.pos = a.pos + r0;
+      ar.out = a.out + (int64_t)r0 * head_dim;
+      ar.n_rows = n;
+      return ar;
+    };
+    int done = 0;
+    if (ncols % kHT == 0 && n_rows >= kHT) {
+      const int nrb = n_rows / kHT, ncb = (int)(ncols / kHT);
+      hipLaunchKernelGGL(project_tile256_kernel, dim3(xcd_grid(nrb * ncb)), dim3(64 * kHWaves), 0, st,
+                         range(0, nrb * kHT), nrb, ncb);
+      done = nrb * kHT;
+    }
+    if (n_rows - done >= kGT) {
+      const int nrb = (n_rows - done) / kGT, ncb = (int)(ncols / kGT);
+      hipLaunchKernelGGL(project_tile_kernel, dim3(xcd_grid(nrb * ncb)), dim3(256), 0, st,
+                         range(done, nrb * kGT), nrb, ncb);
+      done += nrb * kGT;
+    }
+    if (done == n_rows) return hipGetLastError();
+    const ProjArgs ar = range(done, n_rows - done);
     return hidden % 256 == 0 ? launch_proj_waves<8>(ar, st) : launch_proj_waves<4>(ar, st);
   }
   // eight wavefronts split the hidden dimension (each keeps 8 K steps of loads in flight),

@@ -1136,6 +1136,8 @@ PROJ_CASES = {
     "split_rows_64": (64, 4096, 4, 128, 1000, None),
     "d64_ragged_rows": (130, 1024, 4, 64, 0, None),
     "tiles_and_122_rows": (250, 1024, 4, 128, 5, None),
+    "tiles_256_128_and_16_rows": (400, 1024, 4, 128, 7, None),
+    "tiles_256_d64": (300, 512, 8, 64, 11, None),
     "one_row": (1, 128, 1, 64, 7, None),
     "h2o_all_rows_sampled": (8194, 4096, 32, 128, 0, 48),
 }
