@@ -57,27 +57,38 @@ __device__ __forceinline__ uint4 lds_frag(const char* lds, int r, int s, int g16
   return *reinterpret_cast<const uint4*>(lds + swz(r, s * 4 + g16));
 }
 
-// Global loads of a 64-row block (rows clamped to the sequence); 4 units per thread.  The
-// address is a wave-uniform base at row min(r0, N - 1) plus a 32-bit lane offset below 16
-// KB, which the compiler turns into scalar-base loads (one vector add, min, subtract and
-// shift per load instead of a 64-bit multiply-add chain).
+// Global loads of a 64-row block (rows clamped to the sequence); 4 units per thread, unit
+// u = tid % 16 of rows tid / 16 + 16 i.  The address is a wave-uniform base at row
+// rb = min(r0, N - 1) plus a 32-bit lane offset below 16 KB (scalar-base loads): the row
+// offset is clamped to lim = N - 1 - rb, so a load costs one min and one shift-add.
 __device__ __forceinline__ void block_load(const char* base, int r0, int N, int tid, uint4 (&st)[4]) {
   const int rb = min(r0, N - 1);
+  const int lim = N - 1 - rb;
   const char* b0 = base + (int64_t)rb * RowBytes;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int e = tid + 256 * i;
-    const int r = e >> 4, u = e & 15;
-    const uint32_t off = (uint32_t)((min(r0 + r, N - 1) - rb) * RowBytes + u * 16);
+    const uint32_t off = (uint32_t)(min((tid >> 4) + 16 * i, lim) * RowBytes + (tid & 15) * 16);
     st[i] = load16(b0 + off);
   }
 }
 
+// LDS stores of the block loaded above.  ONE_ADDR: the units of rows tid / 16 + 16 i sit
+// 16 rows (4 KB) apart under the swizzle (which depends on the row mod 16 only), so one
+// address serves the four stores through the instruction's offset field (fewer vector
+// instructions; in the row-LSE kernel, which has no registers to spare, the compiler then
+// spills, so it computes each address).
+template <bool ONE_ADDR>
 __device__ __forceinline__ void block_store(char* lds, int tid, const uint4 (&st)[4]) {
+  if constexpr (ONE_ADDR) {
+    char* p = lds + swz(tid >> 4, tid & 15);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int e = tid + 256 * i;
-    *reinterpret_cast<uint4*>(lds + swz(e >> 4, e & 15)) = st[i];
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(p + 16 * RowBytes * i) = st[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = tid + 256 * i;
+      *reinterpret_cast<uint4*>(lds + swz(e >> 4, e & 15)) = st[i];
+    }
   }
 }
 
@@ -163,7 +174,7 @@ __global__ __launch_bounds__(256, 3) void h2o_lse_kernel(H2oArgs a) {
     block_load(kb, 0, N, tid, st);
     for (int t = 0; t < ntile; ++t) {
       char* buf = lds[t & 1];
-      block_store(buf, tid, st);
+      block_store<false>(buf, tid, st);
       __syncthreads();
       if (t + 1 < ntile) block_load(kb, (t + 1) * KTL, N, tid, st);
       const int j0 = t * KTL;
@@ -247,7 +258,7 @@ __global__ __launch_bounds__(256) void h2o_colsum_kernel(H2oArgs a, float* part,
   if (tid < RB) lst = lh[min(rlo + tid, N - 1)];
   for (int it = 0; it < nblk; ++it) {
     const int cur = it & 1;
-    block_store(qlds[cur], tid, st);
+    block_store<true>(qlds[cur], tid, st);
     if (tid < RB) llds[cur][tid] = lst * kLog2e;
     __syncthreads();
     const int r0 = rlo + (it % per) * RB;
