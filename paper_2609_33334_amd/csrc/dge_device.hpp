@@ -120,14 +120,16 @@ __device__ __forceinline__ void rebase_lse_update(const float (&x)[R][NV], float
       for (int i = 0; i + w < NV; i += 2 * w) e[i] += e[i + w];
     return e[0];
   };
+  // one wave-wide test for all R sums: their maximum against the limit (the sums are
+  // never NaN: finite or masked (-inf) logits give exponentials in [0, inf])
   float ns[R];
-  bool out = false;
+  float big = 0.0f;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     ns[r] = s[r] + batch(r, m[r]);
-    out = out || !(ns[r] < kSumLimit);
+    big = fmaxf(big, ns[r]);
   }
-  if (__any(out)) {
+  if (__builtin_amdgcn_ballot_w64(!(big < kSumLimit)) != 0) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       if (!(ns[r] < kSumLimit)) {
