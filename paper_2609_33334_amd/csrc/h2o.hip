@@ -103,7 +103,9 @@ template <bool MASK>
 __device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N, int c16,
                                          int g16, const uint4 (&qf)[4][NS], float scale,
                                          float (&m)[4], float (&sm)[4]) {
-#pragma unroll 1
+  // two subtiles per loop iteration: their fragment reads take immediate LDS offsets (a
+  // full unroll runs out of registers at three wavefronts per SIMD)
+#pragma unroll 2
   for (int sub = 0; sub < KTL / 16; ++sub) {
     uint4 kf[NS];
 #pragma unroll
