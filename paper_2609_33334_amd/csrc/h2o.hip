@@ -8,9 +8,10 @@
 // lse (skipped when the caller supplies it): a workgroup owns a pair of 64-row blocks
 //   (one from each end of the sequence, so every workgroup does the same causal work)
 //   of one KV head; wavefront g is query head g of the group and keeps its 4 row tiles
-//   of Q in registers.  64-key tiles of K are staged once in XOR-swizzled LDS and read
-//   by all G wavefronts.  The product is taken transposed (A = keys, B = query rows) so
-//   a lane holds 4 keys of one row and keeps that row's (reference, sum) in registers.
+//   of Q in registers.  64-key tiles of K stream through a ring of XOR-swizzled LDS
+//   tiles (global->LDS copies, two in flight) and are read by all G wavefronts.  The
+//   product is taken transposed (A = keys, B = query rows) so a lane holds 4 keys of one
+//   row and keeps that row's (reference, sum) in registers.
 //
 // colsum: a workgroup owns a 128-key block and a 512-row segment of one KV head; each
 //   wavefront keeps two 16-key tiles of K in registers.  For every query head of the
@@ -57,7 +58,8 @@ __device__ __forceinline__ uint4 lds_frag(const char* lds, int r, int s, int g16
   return *reinterpret_cast<const uint4*>(lds + swz(r, s * 4 + g16));
 }
 
-// Global loads of a 64-row block (rows clamped to the sequence); 4 units per thread, unit
+// Global loads of a 64-row Q block of the colsum kernel (rows clamped to the sequence);
+// 4 units per thread, unit
 // u = tid % 16 of rows tid / 16 + 16 i.  The address is a wave-uniform base at row
 // rb = min(r0, N - 1) plus a 32-bit lane offset below 16 KB (scalar-base loads): the row
 // offset is clamped to lim = N - 1 - rb, so a load costs one min and one shift-add.
@@ -72,24 +74,13 @@ __device__ __forceinline__ void block_load(const char* base, int r0, int N, int 
   }
 }
 
-// LDS stores of the block loaded above.  ONE_ADDR: the units of rows tid / 16 + 16 i sit
-// 16 rows (4 KB) apart under the swizzle (which depends on the row mod 16 only), so one
-// address serves the four stores through the instruction's offset field (fewer vector
-// instructions; in the row-LSE kernel, which has no registers to spare, the compiler then
-// spills, so it computes each address).
-template <bool ONE_ADDR>
+// LDS stores of the block loaded above: the units of rows tid / 16 + 16 i sit 16 rows
+// (4 KB) apart under the swizzle (which depends on the row mod 16 only), so one address
+// serves the four stores through the instruction's offset field.
 __device__ __forceinline__ void block_store(char* lds, int tid, const uint4 (&st)[4]) {
-  if constexpr (ONE_ADDR) {
-    char* p = lds + swz(tid >> 4, tid & 15);
+  char* p = lds + swz(tid >> 4, tid & 15);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(p + 16 * RowBytes * i) = st[i];
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = tid + 256 * i;
-      *reinterpret_cast<uint4*>(lds + swz(e >> 4, e & 15)) = st[i];
-    }
-  }
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(p + 16 * RowBytes * i) = st[i];
 }
 
 // ------------------------------------------------------------------------------------
@@ -133,6 +124,25 @@ __device__ __forceinline__ void lse_tile(const char* buf, int j0, int r0, int N,
   }
 }
 
+// K tiles of the row-LSE kernel stream through a ring of kLseStages 16 KB LDS tiles filled
+// by global->LDS copies (kLseStages - 1 in flight while one is on the matrix cores; a copy
+// past the last tile re-reads tile 0, so every wait has a fixed count).  Copy i of thread
+// tid fills the 16 bytes at 1024 (4 wv + i) + 16 lane of a tile with the unit that belongs
+// there under the swizzle (unit u of row r at u ^ (r % 16)); rows past the sequence read
+// its last row (their logits are masked).
+constexpr int kLseStages = 3;
+constexpr int kLseCopies = KTL * RowBytes / (256 * 16);
+
+__device__ __forceinline__ void lse_tile_copy(const char* kb, int j0, int N, uint32_t lds_tile,
+                                              const uint32_t (&row)[kLseCopies],
+                                              const uint32_t (&col)[kLseCopies]) {
+  const uint32_t lim = (uint32_t)(N - 1 - j0);
+  const char* base = kb + (int64_t)j0 * RowBytes;
+#pragma unroll
+  for (int i = 0; i < kLseCopies; ++i)
+    dma16_sbase(base, min(row[i], lim) * RowBytes + col[i], lds_tile + i * 1024);
+}
+
 // Three workgroups per compute unit (168 registers): every block pair of the
 // Llama-3-8B-shaped layer (65 pairs x 8 KV heads) is resident in one round.
 __global__ __launch_bounds__(256, 3) void h2o_lse_kernel(H2oArgs a) {
@@ -152,41 +162,65 @@ __global__ __launch_bounds__(256, 3) void h2o_lse_kernel(H2oArgs a) {
   const int hq = h * a.G + (active ? wvu : 0);
   const char* kb = reinterpret_cast<const char*>(a.k + (int64_t)h * a.kv_head_stride + s0 * D);
   const char* qb = reinterpret_cast<const char*>(a.q + (int64_t)hq * a.total_rows * D + s0 * D);
-  __shared__ __attribute__((aligned(16))) char lds[2][KTL * RowBytes];
+  __shared__ __attribute__((aligned(16))) char ring[kLseStages][KTL * RowBytes];
+  uint32_t crow[kLseCopies], ccol[kLseCopies];
+#pragma unroll
+  for (int i = 0; i < kLseCopies; ++i) {
+    const int o = ((wv * kLseCopies + i) * 64 + lane) * 16;
+    const int r = o / RowBytes, pu = (o % RowBytes) / 16;
+    crow[i] = (uint32_t)r;
+    ccol[i] = (uint32_t)((pu ^ (r & 15)) * 16);
+  }
+  const uint32_t lds_wave = (uint32_t)(wvu * kLseCopies * 1024);
 
   for (int side = 0; side < 2; ++side) {
     const int rb = side == 0 ? pair : nrb - 1 - pair;
     if (side == 1 && rb == pair) break;     // odd count: the middle block once
     if (rb >= nrb || rb < 0) break;
     const int r0 = rb * RB;
-    // Q fragments of this wavefront's 4 row tiles (B operand: lane supplies row c16)
-    uint4 qf[4][NS];
+    const int last = min(r0 + RB, N);       // keys [0, last) can be seen by this block
+    const int ntile = (last + KTL - 1) / KTL;
+    auto issue = [&](int t) {               // copies of tile t (t >= ntile: tile 0 again)
+      lse_tile_copy(kb, t < ntile ? t * KTL : 0, N,
+                    (uint32_t)(uintptr_t)(lds_ptr_t)ring[t % kLseStages] + lds_wave, crow, ccol);
+    };
+    lds_barrier();                          // the previous side is done with the ring
+    // Q fragments of this wavefront's 4 row tiles (B operand: lane supplies row c16), from
+    // asm so that no compiler wait drains the copies; they land with the first tile
+    u32x4_t qa[4][NS];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
       const char* row = qb + (int64_t)min(r0 + rt * 16 + c16, N - 1) * RowBytes;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) qf[rt][s] = load16(row + (s * 4 + g16) * 16);
+      for (int s = 0; s < NS; ++s) qa[rt][s] = async_load16(row + (s * 4 + g16) * 16);
     }
+#pragma unroll
+    for (int t = 0; t < kLseStages - 1; ++t) issue(t);
+    asm_wait_vmcnt<(kLseStages - 2) * kLseCopies>();   // tile 0 (and the fragments) landed
+    uint4 qf[4][NS];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        reg_fence(qa[rt][s]);
+        qf[rt][s] = as_uint4(qa[rt][s]);
+      }
     float m[4], sm[4];                      // reference and sum (rebase_lse_update)
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) { m[rt] = kLazyRefInit; sm[rt] = 0.0f; }
-    const int last = min(r0 + RB, N);       // keys [0, last) can be seen by this block
-    const int ntile = (last + KTL - 1) / KTL;
-    uint4 st[4];
-    block_load(kb, 0, N, tid, st);
     for (int t = 0; t < ntile; ++t) {
-      char* buf = lds[t & 1];
-      block_store<false>(buf, tid, st);
-      __syncthreads();
-      if (t + 1 < ntile) block_load(kb, (t + 1) * KTL, N, tid, st);
+      if (t > 0) asm_wait_vmcnt<(kLseStages - 2) * kLseCopies>();   // tile t landed (own copies)
+      lds_barrier();                        // ... everyone's; slot (t - 1) % S is free
+      issue(t + kLseStages - 1);
+      const char* buf = ring[t % kLseStages];
       const int j0 = t * KTL;
       if (active) {
         // tiles that reach the block's diagonal (or the sequence end) run the masked body
         if (j0 + KTL > r0) lse_tile<true>(buf, j0, r0, N, c16, g16, qf, a.scale_log2, m, sm);
         else lse_tile<false>(buf, j0, r0, N, c16, g16, qf, a.scale_log2, m, sm);
       }
-      __syncthreads();
     }
+    asm_wait_vmcnt<0>();                    // no copy still writes into the ring
     if (active) {
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) {
@@ -262,7 +296,7 @@ __global__ __launch_bounds__(256, 4) void h2o_colsum_kernel(H2oArgs a, float* pa
   if (tid < RB) lst = lh[min(rlo + tid, N - 1)];
   for (int it = 0; it < nblk; ++it) {
     const int cur = it & 1;
-    block_store<true>(qlds[cur], tid, st);
+    block_store(qlds[cur], tid, st);
     if (tid < RB) llds[cur][tid] = lst * kLog2e;
     __syncthreads();
     const int r0 = rlo + (it % per) * RB;
