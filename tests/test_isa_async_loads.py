@@ -3,8 +3,8 @@
 The scoring kernels issue register loads from inline asm that the compiler does not
 track; build() compiles such sources to gfx950 assembly and refuses the library when a
 load's registers are touched before a covering wait on some path, or when a kernel of
-the file spills.  These tests run that check on score.hip and show that build() refuses
-a kernel forced to spill."""
+the file spills.  These tests run that check on every such source and show that build()
+refuses a kernel forced to spill."""
 import os
 import tempfile
 
@@ -42,12 +42,25 @@ def _write(tmp, attr):
     return src
 
 
-def test_score_asm_loads_waited_on_every_path():
-    src = os.path.join(build.CSRC, "score.hip")
+ASM_LOAD_SOURCES = ("score.hip", "h2o.hip", "attend.hip", "project.hip")
+
+
+@pytest.mark.parametrize("name", ASM_LOAD_SOURCES)
+def test_asm_loads_waited_on_every_path(name):
+    src = os.path.join(build.CSRC, name)
     with open(src) as fh:
         assert isa_check.uses_asm_loads(fh.read())
     problems = build.verify_source(src)
     assert problems == [], "\n".join(problems[:20])
+
+
+def test_every_asm_load_source_is_listed():
+    users = []
+    for src in build.sources():
+        with open(src) as fh:
+            if isa_check.uses_asm_loads(fh.read()):
+                users.append(os.path.basename(src))
+    assert sorted(users) == sorted(ASM_LOAD_SOURCES)
 
 
 def test_build_refuses_a_spilling_asm_load_kernel():
