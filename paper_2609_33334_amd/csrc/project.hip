@@ -521,6 +521,9 @@ __global__ __launch_bounds__(64 * kHWaves, 1) void project_tile256_kernel(ProjAr
           const double ang = (double)a.pos[r] * a.inv_freq[pair];
           const double kk = rint(ang * 0.15915494309189535);
           const double red = fma(-kk, 2.4492935982947064e-16, fma(-kk, 6.283185307179586, ang));
+          // the hardware sine and cosine on the reduced angle (error ~1e-6, far below the
+          // bf16 rounding of the result): with the library sincosf the 64 rotations of a
+          // lane are too large to unroll, and the accumulators then go to scratch memory
           float sn, cs;
           __sincosf((float)red, &sn, &cs);
           const float lo = acc[i][e][k], hi = acc[i][e + 2][k];
@@ -528,9 +531,6 @@ __global__ __launch_bounds__(64 * kHWaves, 1) void project_tile256_kernel(ProjAr
           orow[pair] = to_bf16_rne(fmaf(lo, cs, -hi * sn));
           orow[a.half + pair] = to_bf16_rne(fmaf(hi, cs, lo * sn));
         }
-        // one row at a time: the scheduler would otherwise interleave the double-precision
-        // angle work of many rows and run out of registers beside the 128 accumulators
-        __builtin_amdgcn_sched_barrier(0);
       }
   }
 }

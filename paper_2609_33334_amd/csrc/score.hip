@@ -36,8 +36,8 @@
 //   by r, so the 16 lanes that read one fragment column hit 16 different bank groups.
 //   Three tiles are always in flight (a 4-stage ring of 16 KB buffers; two with three
 //   workgroups per compute unit; dummy copies past the end of a chunk keep every wait
-//   count fixed) while one is on the matrix cores; the loop's barriers wait on LDS traffic only, so the copies are never
-//   drained early.
+//   count fixed) while one is on the matrix cores; the loop's barriers wait on LDS
+//   traffic only, so the copies are never drained early.
 // - Tile bodies are branch-free: all products of a tile (or of a group of subtiles)
 //   are issued before their results are used, so the exp2 work overlaps the matrix
 //   cores; a separate masked body runs only where a tile reaches past the first
