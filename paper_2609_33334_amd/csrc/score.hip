@@ -859,8 +859,16 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
   // tokens, 3% and 7% faster walking 64 tiles than 16).
   const int64_t tiles_total = (int64_t)g.n_kv_heads * ((total_rows(g) + KT - 1) / KT);
   const int64_t nmax = max_seq_rows(g);
-  int iters = (int)((tiles_total + 255) / 256);
-  iters = iters < 1 ? 1 : (iters > 64 ? 64 : iters);
+  // The chunk count follows from that walk length; the chunks are then made equal (the
+  // longest sequence's tiles spread evenly over its chunks instead of leaving a last
+  // chunk of a few keys).
+  const int64_t seq_tiles = nmax > 0 ? (nmax + KT - 1) / KT : 1;
+  auto balanced = [&](int walk) {
+    walk = walk < 1 ? 1 : (walk > 64 ? 64 : walk);
+    const int64_t chunks = (seq_tiles + walk - 1) / walk;
+    return (int)((seq_tiles + chunks - 1) / chunks);
+  };
+  int iters = balanced((int)((tiles_total + 255) / 256));
   p.tiles_per_wave = iters;
   p.chunk_keys = KT * iters;
   p.n_chunks = (int)((nmax + p.chunk_keys - 1) / p.chunk_keys);
@@ -868,8 +876,7 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
   // the colsum pass walks about one tile per 512 of the launch (twice the workgroups of
   // the stats pass on small launches: one 4096-token layer of 8 KV heads 0.6 us faster
   // with 2 tiles per colsum workgroup and 3 per stats workgroup than with 3 and 3)
-  int citers = (int)((tiles_total + 511) / 512);
-  citers = citers < 1 ? 1 : (citers > 64 ? 64 : citers);
+  const int citers = balanced((int)((tiles_total + 511) / 512));
   p.c_tiles = citers;
   p.c_chunk_keys = KT * citers;
   p.c_n_chunks = (int)((nmax + p.c_chunk_keys - 1) / p.c_chunk_keys);
