@@ -853,7 +853,7 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
     p.rt = 0;
   }
   // Every workgroup loads its query fragments once and streams several 64-key tiles:
-  // about one tile-walk per 256 tiles of the launch, at most 64 tiles (measured on
+  // about one tile-walk per 256 tiles of the launch, at most 64 or 128 tiles (measured on
   // MI355X: one 4096-token layer of 8 KV heads 0.5 us faster with 3 tiles per workgroup
   // than with 2; 32 layers scored in one launch, at 16K tokens or at batch 8 of 16K-32K
   // tokens, 3% and 7% faster walking 64 tiles than 16).
@@ -861,12 +861,21 @@ ScorePlan plan_score(const dge_geom_t& g, int rows_mode) {
   const int64_t nmax = max_seq_rows(g);
   // The chunk count follows from that walk length; the chunks are then made equal (the
   // longest sequence's tiles spread evenly over its chunks instead of leaving a last
-  // chunk of a few keys).
+  // chunk of a few keys).  Walks may reach 128 tiles while a pass keeps at least
+  // kLongWalkUnits workgroups (32 layers of a batch of 8 sequences of 16K-32K tokens:
+  // 1.3% faster than at most 64; 32 layers of one 16K sequence, 768 workgroups at 128:
+  // 1.5% slower, so it stays at 64).
+  constexpr int64_t kLongWalkUnits = 4096;
   const int64_t seq_tiles = nmax > 0 ? (nmax + KT - 1) / KT : 1;
   auto balanced = [&](int walk) {
-    walk = walk < 1 ? 1 : (walk > 64 ? 64 : walk);
-    const int64_t chunks = (seq_tiles + walk - 1) / walk;
-    return (int)((seq_tiles + chunks - 1) / chunks);
+    auto even = [&](int cap) {
+      const int w = walk < 1 ? 1 : (walk > cap ? cap : walk);
+      const int64_t chunks = (seq_tiles + w - 1) / w;
+      return (int)((seq_tiles + chunks - 1) / chunks);
+    };
+    const int w128 = even(128);
+    const int64_t units128 = (seq_tiles + w128 - 1) / w128 * g.n_kv_heads * g.batch;
+    return units128 >= kLongWalkUnits ? w128 : even(64);
   };
   int iters = balanced((int)((tiles_total + 255) / 256));
   p.tiles_per_wave = iters;
