@@ -138,7 +138,7 @@ dge_status_t dge_score_with_lse(const dge_geom_t *geom, int32_t rows, const void
  * fixed scratch array that the library holds in every GPU's memory until the process
  * ends.  No allocation of any kind is made by this call.
  *   Limit: the call needs dge_workspace_size(geom, DGE_OP_SCORE)-style scratch for its
- *   rows mode of at most DGE_NOALLOC_SCRATCH_BYTES (16 MiB: e.g. 32 layers x 8 KV heads x
+ *   rows mode of at most DGE_NOALLOC_SCRATCH_BYTES (16 MiB: e.g. 64 layers x 8 KV heads x
  *   8 sequences of up to 32K rows, 34 scoring rows, G = 4); larger geometries return
  *   DGE_ERR_WORKSPACE before anything is launched.
  *   Every call on one GPU shares that GPU's scratch, and calls keep no state in it between

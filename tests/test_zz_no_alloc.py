@@ -56,7 +56,8 @@ def test_score_noalloc_other_rows_modes_and_oversize():
         ref = dge.score(g, mode, qm, k)
         torch.cuda.synchronize()
         assert torch.equal(got.view(torch.int32), ref.view(torch.int32)), mode
-    big = dge.Geometry(2048, 512, 128, 32, 2, [32768] * 8, device=DEV)
+    # 128 Llama-3-8B layers x 8 sequences of 32K rows (64 such layers fit the scratch)
+    big = dge.Geometry(4096, 1024, 128, 32, 2, [32768] * 8, device=DEV)
     assert dge.workspace_size(big, dge.OP_SCORE) > _lib.NOALLOC_SCRATCH_BYTES
     raw = torch.empty(4, dtype=torch.float32, device=DEV)
     st = _lib.lib().dge_score_noalloc(ctypes.byref(big.c), dge.ROWS_WINDOW_DRAFT, q.data_ptr(), k.data_ptr(),
