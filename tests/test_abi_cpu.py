@@ -134,8 +134,9 @@ def test_score_noalloc_validation(L):
     assert call(_G(w=0, k=0)) == _lib.DGE_ERR_INVALID
     assert call(_G(), raw=None) == _lib.DGE_ERR_INVALID
     assert call(_G(), k=FAKE + 8) == _lib.DGE_ERR_INVALID
-    # 8 sequences of 32K rows over 512 KV heads, 136 query rows per head: ~18.9 MB of partials
-    big = _G(lens=(32768,) * 8, hq=2048, hkv=512, w=32, k=2)
+    # 8 sequences of 32K rows over 1024 KV heads (128 Llama-3-8B layers), 136 query rows
+    # per head: ~23.6 MB of partials
+    big = _G(lens=(32768,) * 8, hq=4096, hkv=1024, w=32, k=2)
     n = ctypes.c_size_t(0)
     assert L.dge_workspace_size(big.p, 0, ctypes.byref(n)) == 0
     assert n.value > _lib.NOALLOC_SCRATCH_BYTES
