@@ -597,6 +597,150 @@ __global__ __launch_bounds__(kThreads, (stats_waves<T, D, FT, RT>())) void score
   }
 }
 
+// Stats pass with one K stream per wavefront (bf16, d = 128, every row tile of the head
+// in each wavefront's registers: at most 9 tiles, i.e. 144 rows).  The workgroup's chunk
+// is split into four runs of 16-key subtiles, one per wavefront; each wavefront streams
+// its run through a private 5-stage ring of 4 KB subtiles (global->LDS copies, the same
+// swizzle as the 64-key tiles) with its own vmcnt waits and no workgroup barrier, and
+// keeps (reference, sum) of its lane's row of every tile.  The four runs' sums merge once
+// at the end, through LDS, into the same chunk partial the four-wavefront kernel writes.
+// A barrier per 64-key tile couples the four wavefronts of that kernel: with random bf16
+// operands the stats arithmetic then slows the K stream by a sixth (2.6-2.9 ms for 14 GB
+// against 2.3 ms for private rings, same arithmetic per byte, measured on MI355X).
+constexpr int kWaveStages = 5;          // 4 subtiles in flight per wavefront
+constexpr int kSubKeys = 16;
+// Only on walks of at least this many 64-key tiles: every wavefront loads all the row
+// tiles' queries (36 KB at 9 tiles), which short walks do not amortise (one 4096-token
+// layer, 3-tile walks: 21.5 -> 24.9 us).
+constexpr int kWaveStatsMinTiles = 32;
+
+template <int NQ>
+__global__ __launch_bounds__(kThreads, 2) void score_stats_wave_kernel(ScoreArgs a) {
+  using T = bf16_t;
+  constexpr int D = 128;
+  using KTl = KTile<T, D>;
+  constexpr int NS = RowChunks<T, D>::kSteps;
+  constexpr int S = kWaveStages;
+  constexpr int kSubBytes = kSubKeys * KTl::kRowBytes;
+  constexpr int kCopies = kSubBytes / (kWave * 16);          // 4 copy instructions per subtile
+  static_assert(NQ * kSubKeys * sizeof(float2) <= kSubBytes, "exchange exceeds a ring buffer");
+  prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
+                a.kv_head_stride, a.q_head_stride, a.M, a.n_rows, a.G, a.M_pad, a.offs);
+  const int units = a.n_chunks * a.n_kv_heads * a.batch;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int chunk = unit % a.n_chunks, h = (unit / a.n_chunks) % a.n_kv_heads,
+            b = unit / (a.n_chunks * a.n_kv_heads);
+  const int64_t s0 = a.offs[b];
+  const int N = (int)(a.offs[b + 1] - s0);
+  const int c0 = chunk * a.chunk_keys;
+  if (c0 >= N) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform for the copies
+  const int g16 = lane >> 4, c16 = lane & 15;
+  const int p0 = N - a.p0_from_end;
+  const int c1 = min(N, c0 + a.chunk_keys);
+  const int nsub = (c1 - c0 + kSubKeys - 1) / kSubKeys;
+  const int per = (nsub + 3) / 4;                        // subtiles per wavefront
+  const int w0 = c0 + wv * per * kSubKeys;               // first key of this wavefront's run
+  const int nw = max(0, min(per, nsub - wv * per));      // wave-uniform
+  const char* kb = reinterpret_cast<const char*>(a.k) +
+                   ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
+  float* part = a.partial + ((int64_t)(b * a.n_kv_heads + h) * a.n_chunks + chunk) * a.M_pad;
+  __shared__ __attribute__((aligned(16))) char ring[4][S][kSubBytes];
+  char (*buf)[kSubBytes] = ring[wv];
+
+  float mref[NQ], srow[NQ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) { mref[i] = kLazyRefInit; srow[i] = 0.0f; }
+  if (nw > 0) {
+    // lane's 16-byte unit of a subtile: row r, stored at the swizzled position of its
+    // linear index (as for the 64-key tiles); rows past the sequence read its last row
+    uint32_t row[kCopies], col[kCopies];
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i) {
+      const int e = i * kWave + lane, r = e / KTl::kUnits, u = e % KTl::kUnits;
+      row[i] = (uint32_t)r;
+      col[i] = (uint32_t)((u ^ (r % KTl::kUnits)) * 16);
+    }
+    auto issue = [&](int t) {                  // subtile t of the run; past its end a
+      const int js = t < nw ? w0 + t * kSubKeys : 0;   // dummy copy of the first subtile
+      const uint32_t lim = (uint32_t)(N - 1 - js);
+      const char* base = kb + (int64_t)js * KTl::kRowBytes;
+      const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_ptr_t)buf[t % S]);
+#pragma unroll
+      for (int i = 0; i < kCopies; ++i)
+        dma16_sbase(base, min(row[i], lim) * KTl::kRowBytes + col[i], lds + i * kWave * 16);
+    };
+    u32x4_t qf[NQ][NS];
+    load_q_frags<T, D, 0, NQ>(a, h, b, 0, wv, c16, g16, qf);   // slot i = row tile i
+#pragma unroll
+    for (int t = 0; t < S - 1; ++t) issue(t);
+    q_fence(qf);                               // queries and the first subtiles landed
+    for (int t = 0; t < nw; ++t) {
+      if (t > 0) asm_wait_vmcnt<(S - 2) * kCopies>();   // subtile t landed
+      wait_lgkmcnt0();                         // own reads of the buffer refilled next done
+      issue(t + S - 1);
+      const char* lds = buf[t % S];
+      const int j0 = w0 + t * kSubKeys;
+      uint4 kf[NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) kf[s] = ktile_frag<T, D>(lds, c16, s, g16);
+      f32x4_t acc[NQ];
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int i = 0; i < NQ; ++i) acc[i] = mma_step(T{}, kf[s], as_uint4(qf[i][s]), acc[i]);
+      float x[NQ][4];
+      if (j0 + kSubKeys - 1 > p0) {            // reaches past the first scoring position
+#pragma unroll
+        for (int i = 0; i < NQ; ++i) {
+          const int m = i * 16 + c16;
+          const bool live = m < a.M;
+          const int pos = p0 + (live ? m % a.n_rows : 0);
+#pragma unroll
+          for (int t2 = 0; t2 < 4; ++t2) x[i][t2] = stats_mask(acc[i][t2], j0 + 4 * g16 + t2, live, pos, N);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NQ; ++i)
+#pragma unroll
+          for (int t2 = 0; t2 < 4; ++t2) x[i][t2] = acc[i][t2];
+      }
+      rebase_lse_update<NQ, 4>(x, a.scale_log2, mref, srow);
+    }
+    asm_wait_vmcnt<0>();                       // no copy still writes into the ring
+  }
+  // the four lane groups of each row, then the four wavefronts' runs (each wavefront
+  // writes into its own first ring buffer, which no copy of any wavefront targets now)
+  float2* xw = reinterpret_cast<float2*>(&ring[wv][0][0]);
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const float m = mref[i];
+    float sm = srow[i];
+    const float mx = fmaxf(fmaxf(m, shfl_xor_f<16>(m)), fmaxf(shfl_xor_f<32>(m), shfl_xor_f<48>(m)));
+    sm *= rescale(m, mx);
+    sm += shfl_xor_f<16>(sm);
+    sm += shfl_xor_f<32>(sm);
+    if (g16 == 0) xw[i * 16 + c16] = make_float2(mx, sm);
+  }
+  lds_barrier();
+  if (tid < a.M) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) m = fmaxf(m, reinterpret_cast<const float2*>(&ring[w][0][0])[tid].x);
+    float sum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float2 v = reinterpret_cast<const float2*>(&ring[w][0][0])[tid];
+      sum += v.y * rescale(v.x, m);
+    }
+    part[tid] = m + __log2f(sum);
+  }
+}
+
 // Merging each query row's chunk partials (log2-sum-exps, -inf for a chunk whose keys
 // are all masked for the row) into log2 of its normaliser, in one of two layouts:
 // - score_reduce_rows_kernel, for at most kReduceBatch chunks (long chunks: the
@@ -756,7 +900,15 @@ template <typename T, int D, int FT, int RT>
 hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st) {
   const dim3 grid(xcd_grid(a.n_chunks * g.n_kv_heads * g.batch));
   if (a.lse_in == nullptr) {   // normalisers computed here: stats and reduce first
-    hipLaunchKernelGGL((score_stats_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
+    constexpr int NQW = 4 * FT + RT;         // row tiles of a single row group
+    if constexpr (std::is_same<T, bf16_t>::value && D == 128 && (NQW == 8 || NQW == 9)) {
+      if (a.groups == 1 && a.n_tiles == NQW && a.iters >= kWaveStatsMinTiles)
+        hipLaunchKernelGGL((score_stats_wave_kernel<NQW>), grid, dim3(kThreads), 0, st, a);
+      else
+        hipLaunchKernelGGL((score_stats_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((score_stats_kernel<T, D, FT, RT>), grid, dim3(kThreads), 0, st, a);
+    }
     if (a.n_chunks <= kReduceBatch)
       hipLaunchKernelGGL(score_reduce_rows_kernel, dim3((a.M_pad + 63) / 64, g.n_kv_heads, g.batch),
                          dim3(64), 0, st, a);

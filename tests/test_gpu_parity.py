@@ -255,6 +255,31 @@ def test_score_layer_major_long_walks():
         check_scores(raw[l * H:(l + 1) * H], want, f"layer copy {l}")
 
 
+@pytest.mark.parametrize("mode", [oracle.ROWS_WINDOW_DRAFT, oracle.ROWS_WINDOW])
+def test_score_long_walks_short_last_chunks(mode):
+    # eight stacked copies of a ragged three-sequence layer (64 KV heads): the launch walks
+    # 64 tiles per workgroup, which takes the stats pass with one K stream per wavefront
+    # (9 or 8 row tiles); two sequences end 20 and 70 keys into their last 4096-key chunk,
+    # whose 2 and 5 subtiles of 16 keys leave some wavefronts of the workgroup no keys
+    wl = di.small_variant("c3", [16382, 12306, 8260])
+    assert tuple(wl.cached_lens) == (16384, 12308, 8262)
+    _log(f"score parity: long walks, short last chunks, mode {mode}")
+    x = di.make_layer(wl, layer=3, with_v=False)
+    nl = 8
+    g = dge.Geometry(wl.n_q_heads * nl, wl.n_kv_heads * nl, wl.head_dim, wl.window, wl.k_draft,
+                     wl.cached_lens, device=DEV)
+    q, qb = mode_rows(x, wl, mode)
+    raw = dge.score(g, mode, to_dev(qb, "bf16").repeat(nl, 1, 1),
+                    to_dev(x.k_bits, "bf16").repeat(nl, 1, 1))
+    torch.cuda.synchronize()
+    raw = raw.cpu().numpy()
+    want = oracle.window_scores(q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                wl.k_draft, mode)
+    H = wl.n_kv_heads
+    for l in range(nl):
+        check_scores(raw[l * H:(l + 1) * H], want, f"layer copy {l}")
+
+
 @pytest.mark.parametrize("case", ["c2", "c2_ragged", "c1"])
 def test_score_lse_single_pass(case):
     wl = {"c2": di.WORKLOADS["c2"], "c2_ragged": SCORE_CASES["c2_ragged"], "c1": di.WORKLOADS["c1"]}[case]
