@@ -614,6 +614,48 @@ constexpr int kSubKeys = 16;
 // layer, 3-tile walks: 21.5 -> 24.9 us).
 constexpr int kWaveStatsMinTiles = 32;
 
+// One wavefront's run of 16-key subtiles (bf16, d = 128) through its private S-stage
+// ring: subtile t lands in buf[t % S]; past the run's end a dummy copy of the sequence's
+// first subtile keeps every wait count fixed.  Lane l copies 16-byte unit e = i*64 + l
+// (row e / 16) to its linear LDS position, fetching the unit that belongs there under the
+// XOR swizzle of the 64-key tiles; rows past the sequence read its last row.
+template <int S>
+struct WaveRun {
+  using KTl = KTile<bf16_t, 128>;
+  static constexpr int kSubBytes = kSubKeys * KTl::kRowBytes;
+  static constexpr int kCopies = kSubBytes / (kWave * 16);     // 4 instructions per subtile
+  const char* kb;
+  char (*buf)[kSubBytes];
+  int w0, nw, N;
+  uint32_t off[kCopies];         // the unit's byte offset within a subtile (row * 256 + column)
+  __device__ __forceinline__ WaveRun(const char* kb_, char (*buf_)[kSubBytes], int w0_, int nw_,
+                                     int N_, int lane)
+      : kb(kb_), buf(buf_), w0(w0_), nw(nw_), N(N_) {
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i) {
+      const int e = i * kWave + lane, r = e / KTl::kUnits, u = e % KTl::kUnits;
+      off[i] = (uint32_t)(r * KTl::kRowBytes + (u ^ (r % KTl::kUnits)) * 16);
+    }
+  }
+  __device__ __forceinline__ void issue(int t) const {
+    const int js = t < nw ? w0 + t * kSubKeys : 0;
+    const uint32_t lim = (uint32_t)(N - 1 - js);
+    const char* base = kb + (int64_t)js * KTl::kRowBytes;
+    const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_ptr_t)buf[t % S]);
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i) {
+      const uint32_t r = off[i] / KTl::kRowBytes;      // a shift
+      dma16_sbase(base, off[i] - (r - min(r, lim)) * KTl::kRowBytes, lds + i * kWave * 16);
+    }
+  }
+  // subtile t landed (S - 1 in flight), and this wavefront's reads of the buffer that
+  // the next copy refills are done
+  __device__ __forceinline__ void wait(int t) const {
+    if (t > 0) asm_wait_vmcnt<(S - 2) * kCopies>();
+    wait_lgkmcnt0();
+  }
+};
+
 template <int NQ>
 __global__ __launch_bounds__(kThreads, 2) void score_stats_wave_kernel(ScoreArgs a) {
   using T = bf16_t;
@@ -621,8 +663,7 @@ __global__ __launch_bounds__(kThreads, 2) void score_stats_wave_kernel(ScoreArgs
   using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int S = kWaveStages;
-  constexpr int kSubBytes = kSubKeys * KTl::kRowBytes;
-  constexpr int kCopies = kSubBytes / (kWave * 16);          // 4 copy instructions per subtile
+  constexpr int kSubBytes = WaveRun<S>::kSubBytes;
   static_assert(NQ * kSubKeys * sizeof(float2) <= kSubBytes, "exchange exceeds a ring buffer");
   prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
                 a.kv_head_stride, a.q_head_stride, a.M, a.n_rows, a.G, a.M_pad, a.offs);
@@ -654,33 +695,15 @@ __global__ __launch_bounds__(kThreads, 2) void score_stats_wave_kernel(ScoreArgs
 #pragma unroll
   for (int i = 0; i < NQ; ++i) { mref[i] = kLazyRefInit; srow[i] = 0.0f; }
   if (nw > 0) {
-    // lane's 16-byte unit of a subtile: row r, stored at the swizzled position of its
-    // linear index (as for the 64-key tiles); rows past the sequence read its last row
-    uint32_t row[kCopies], col[kCopies];
-#pragma unroll
-    for (int i = 0; i < kCopies; ++i) {
-      const int e = i * kWave + lane, r = e / KTl::kUnits, u = e % KTl::kUnits;
-      row[i] = (uint32_t)r;
-      col[i] = (uint32_t)((u ^ (r % KTl::kUnits)) * 16);
-    }
-    auto issue = [&](int t) {                  // subtile t of the run; past its end a
-      const int js = t < nw ? w0 + t * kSubKeys : 0;   // dummy copy of the first subtile
-      const uint32_t lim = (uint32_t)(N - 1 - js);
-      const char* base = kb + (int64_t)js * KTl::kRowBytes;
-      const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_ptr_t)buf[t % S]);
-#pragma unroll
-      for (int i = 0; i < kCopies; ++i)
-        dma16_sbase(base, min(row[i], lim) * KTl::kRowBytes + col[i], lds + i * kWave * 16);
-    };
+    const WaveRun<S> run(kb, buf, w0, nw, N, lane);
     u32x4_t qf[NQ][NS];
     load_q_frags<T, D, 0, NQ>(a, h, b, 0, wv, c16, g16, qf);   // slot i = row tile i
 #pragma unroll
-    for (int t = 0; t < S - 1; ++t) issue(t);
+    for (int t = 0; t < S - 1; ++t) run.issue(t);
     q_fence(qf);                               // queries and the first subtiles landed
     for (int t = 0; t < nw; ++t) {
-      if (t > 0) asm_wait_vmcnt<(S - 2) * kCopies>();   // subtile t landed
-      wait_lgkmcnt0();                         // own reads of the buffer refilled next done
-      issue(t + S - 1);
+      run.wait(t);
+      run.issue(t + S - 1);
       const char* lds = buf[t % S];
       const int j0 = w0 + t * kSubKeys;
       uint4 kf[NS];
@@ -896,6 +919,122 @@ __global__ __launch_bounds__(kThreads, W) void score_colsum_kernel(ScoreArgs a) 
   }
 }
 
+// Colsum pass with one K stream per wavefront, as the stats pass above (bf16, d = 128,
+// at most 9 row tiles, long walks): each wavefront streams its run of 16-key subtiles
+// through a private 4-stage ring, computes every row tile's products (A = query rows),
+// sums each key's column in-lane (4 rows of each tile) and over the four lane groups, and
+// writes the keys itself; no LDS reduction across wavefronts.  Row r's normaliser enters
+// as the products' initial accumulator, -c_r / s (s = log2(e) / sqrt(d)), so that
+// 2^(s acc) = 2^(s x - c_r) and the normalisers share the accumulator registers (next to
+// the query fragments at two wavefronts per SIMD there is no room for them); they are
+// staged once per workgroup in LDS and read as 16-byte broadcasts for every subtile.
+constexpr int kWaveColsumStages = 4;
+
+template <int NQ>
+__global__ __launch_bounds__(kThreads, 2) void score_colsum_wave_kernel(ScoreArgs a) {
+  using T = bf16_t;
+  constexpr int D = 128;
+  constexpr int NS = RowChunks<T, D>::kSteps;
+  constexpr int S = kWaveColsumStages;
+  constexpr int kSubBytes = WaveRun<S>::kSubBytes;
+  prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
+                a.kv_head_stride, a.q_head_stride, a.M, a.n_rows, a.G, a.M_pad, a.offs);
+  const int units = a.n_chunks * a.n_kv_heads * a.batch;
+  const int unit = xcd_unit(units);
+  if (unit >= units) return;
+  const int chunk = unit % a.n_chunks, h = (unit / a.n_chunks) % a.n_kv_heads,
+            b = unit / (a.n_chunks * a.n_kv_heads);
+  const int64_t s0 = a.offs[b];
+  const int N = (int)(a.offs[b + 1] - s0);
+  const int c0 = chunk * a.chunk_keys;
+  if (c0 >= N) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g16 = lane >> 4, c16 = lane & 15;
+  const int p0 = N - a.p0_from_end;
+  const int c1 = min(N, c0 + a.chunk_keys);
+  const int nsub = (c1 - c0 + kSubKeys - 1) / kSubKeys;
+  const int per = (nsub + 3) / 4;
+  const int w0 = c0 + wv * per * kSubKeys;
+  const int nw = max(0, min(per, nsub - wv * per));
+  const char* kb = reinterpret_cast<const char*>(a.k) +
+                   ((int64_t)h * a.kv_head_stride + s0 * D) * Elem<T>::kBytes;
+  float* out = a.raw + (int64_t)h * a.total_rows + s0;
+  __shared__ __attribute__((aligned(16))) char ring[4][S][kSubBytes];
+  __shared__ __attribute__((aligned(16))) float cinit[NQ * 16];
+  // -c_r / s per row from the natural-log LSE of the caller or the log2-domain merged
+  // partials; -inf for padding rows, whose terms are then exactly 0
+  if (tid < NQ * 16) {
+    float c = -INFINITY;
+    if (tid < a.M) {
+      float cr;
+      if (a.lse_in != nullptr) {
+        const int g = tid / a.n_rows, r = tid - g * a.n_rows;
+        cr = a.lse_in[(int64_t)(h * a.G + g) * (a.q_head_stride / D) + b * a.n_rows + r] * kLog2e;
+      } else {
+        cr = a.rowc[(int64_t)(b * a.n_kv_heads + h) * a.M_pad + tid];
+      }
+      c = -cr / a.scale_log2;
+    }
+    cinit[tid] = c;
+  }
+  lds_barrier();
+  if (nw == 0) return;                         // no barrier follows
+  const WaveRun<S> run(kb, ring[wv], w0, nw, N, lane);
+  u32x4_t qf[NQ][NS];
+  load_q_frags<T, D, 0, NQ>(a, h, b, 0, wv, c16, g16, qf);
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t) run.issue(t);
+  q_fence(qf);
+  for (int t = 0; t < nw; ++t) {
+    run.wait(t);
+    run.issue(t + S - 1);
+    const char* lds = ring[wv][t % S];
+    const int j0 = w0 + t * kSubKeys, j = j0 + c16;
+    uint4 kf[NS];
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) kf[s2] = ktile_frag<T, D>(lds, c16, s2, g16);
+    // lane (c16, g16) accumulates rows 16 i + 4 g16 + t2 of tile i for key j, starting
+    // from those rows' -c_r / s
+    f32x4_t acc[NQ];
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) {
+      const float4 c = *reinterpret_cast<const float4*>(&cinit[i * 16 + 4 * g16]);
+      acc[i] = f32x4_t{c.x, c.y, c.z, c.w};
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2)
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) acc[i] = mma_step(T{}, as_uint4(qf[i][s2]), kf[s2], acc[i]);
+    float colp = 0.0f;
+    if (j0 + kSubKeys - 1 > p0) {              // reaches past the first scoring position
+      int mb = 4 * g16;                        // row positions derived here, not hoisted
+      asm volatile("" : "+v"(mb));
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) {
+        float e[4];
+#pragma unroll
+        for (int t2 = 0; t2 < 4; ++t2) {
+          const int m = i * 16 + mb + t2;
+          const int r = m < a.M ? m % a.n_rows : 0;     // padding rows add 0 anyway
+          e[t2] = fast_exp2(acc[i][t2] * a.scale_log2);
+          e[t2] = (j < N && j <= p0 + r) ? e[t2] : 0.0f;
+        }
+        colp += (e[0] + e[1]) + (e[2] + e[3]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NQ; ++i)
+        colp += (fast_exp2(acc[i][0] * a.scale_log2) + fast_exp2(acc[i][1] * a.scale_log2)) +
+                (fast_exp2(acc[i][2] * a.scale_log2) + fast_exp2(acc[i][3] * a.scale_log2));
+    }
+    colp += shfl_xor_f<16>(colp);
+    colp += shfl_xor_f<32>(colp);
+    if (g16 == 0 && j < c1) out[j] = colp * a.inv_G;
+  }
+  asm_wait_vmcnt<0>();                         // no copy still writes into the ring
+}
+
 template <typename T, int D, int FT, int RT>
 hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st) {
   const dim3 grid(xcd_grid(a.n_chunks * g.n_kv_heads * g.batch));
@@ -924,6 +1063,13 @@ hipError_t launch_typed(const ScoreArgs& a, const dge_geom_t& g, hipStream_t st)
   const int cunits = ac.n_chunks * g.n_kv_heads * g.batch;
   const dim3 gridc(xcd_grid(cunits));
   constexpr int W2 = score_waves<T, D, FT, RT>(), W3 = colsum_max_waves<T, D, FT, RT>();
+  constexpr int NQC = 4 * FT + RT;
+  if constexpr (std::is_same<T, bf16_t>::value && D == 128 && (NQC == 8 || NQC == 9)) {
+    if (ac.groups == 1 && ac.n_tiles == NQC && ac.iters >= kWaveStatsMinTiles) {
+      hipLaunchKernelGGL((score_colsum_wave_kernel<NQC>), gridc, dim3(kThreads), 0, st, ac);
+      return hipGetLastError();
+    }
+  }
   if (W3 != W2 && cunits >= kColsumThreeWaveUnits)
     hipLaunchKernelGGL((score_colsum_kernel<T, D, FT, RT, W3>), gridc, dim3(kThreads), 0, st, ac);
   else

@@ -280,6 +280,30 @@ def test_score_long_walks_short_last_chunks(mode):
         check_scores(raw[l * H:(l + 1) * H], want, f"layer copy {l}")
 
 
+def test_score_lse_long_walks_short_last_chunks():
+    # the single pass with the rows' LSE supplied, on the stacked ragged layers above: 64-tile
+    # walks take the colsum pass with one K stream per wavefront, the normalisers entering
+    # as its products' initial accumulators
+    wl = di.small_variant("c3", [16382, 12306, 8260])
+    _log("score with supplied row LSE: long walks, short last chunks")
+    x = di.make_layer(wl, layer=3, with_v=False)
+    nl = 8
+    g = dge.Geometry(wl.n_q_heads * nl, wl.n_kv_heads * nl, wl.head_dim, wl.window, wl.k_draft,
+                     wl.cached_lens, device=DEV)
+    lse = oracle.scoring_row_lse(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                 wl.k_draft)
+    lse_d = torch.from_numpy(lse.astype(np.float32)).to(DEV).repeat(nl, 1).contiguous()
+    raw = dge.score_lse(g, dge.ROWS_WINDOW_DRAFT, to_dev(x.q_bits, "bf16").repeat(nl, 1, 1),
+                        to_dev(x.k_bits, "bf16").repeat(nl, 1, 1), lse_d)
+    torch.cuda.synchronize()
+    raw = raw.cpu().numpy()
+    want = oracle.window_scores(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                wl.k_draft)
+    H = wl.n_kv_heads
+    for l in range(nl):
+        check_scores(raw[l * H:(l + 1) * H], want, f"score_lse layer copy {l}")
+
+
 @pytest.mark.parametrize("case", ["c2", "c2_ragged", "c1"])
 def test_score_lse_single_pass(case):
     wl = {"c2": di.WORKLOADS["c2"], "c2_ragged": SCORE_CASES["c2_ragged"], "c1": di.WORKLOADS["c1"]}[case]
