@@ -48,6 +48,11 @@
 // - colsum uses A = query rows, B = keys: a lane holds 4 rows of ONE key, the sum
 //   over rows is in-lane, then across the 4 lane groups (permlane swaps) and the 4
 //   wavefronts (LDS, double-buffered, flushed after the next tile's barrier).
+// On long walks at Llama-3-8B geometry (bf16, d = 128, 8 or 9 row tiles) both passes
+// instead give each wavefront every row tile and its own run of 16-key subtiles through
+// a private ring, with no barrier in the loop (score_stats_wave_kernel,
+// score_colsum_wave_kernel): under the passes' arithmetic on random operands the
+// per-tile barrier of the shared ring slows the K stream.
 #include <type_traits>
 
 #include "dge_device.hpp"
