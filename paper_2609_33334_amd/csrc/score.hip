@@ -665,7 +665,6 @@ template <int NQ>
 __global__ __launch_bounds__(kThreads, 2) void score_stats_wave_kernel(ScoreArgs a) {
   using T = bf16_t;
   constexpr int D = 128;
-  using KTl = KTile<T, D>;
   constexpr int NS = RowChunks<T, D>::kSteps;
   constexpr int S = kWaveStages;
   constexpr int kSubBytes = WaveRun<S>::kSubBytes;
