@@ -605,14 +605,16 @@ __global__ __launch_bounds__(kThreads, (stats_waves<T, D, FT, RT>())) void score
 // Stats pass with one K stream per wavefront (bf16, d = 128, every row tile of the head
 // in each wavefront's registers: at most 9 tiles, i.e. 144 rows).  The workgroup's chunk
 // is split into four runs of 16-key subtiles, one per wavefront; each wavefront streams
-// its run through a private 5-stage ring of 4 KB subtiles (global->LDS copies, the same
+// its run through a private 4-stage ring of 4 KB subtiles (global->LDS copies, the same
 // swizzle as the 64-key tiles) with its own vmcnt waits and no workgroup barrier, and
 // keeps (reference, sum) of its lane's row of every tile.  The four runs' sums merge once
 // at the end, through LDS, into the same chunk partial the four-wavefront kernel writes.
 // A barrier per 64-key tile couples the four wavefronts of that kernel: with random bf16
 // operands the stats arithmetic then slows the K stream by a sixth (2.6-2.9 ms for 14 GB
 // against 2.3 ms for private rings, same arithmetic per byte, measured on MI355X).
-constexpr int kWaveStages = 5;          // 4 subtiles in flight per wavefront
+// Ring depth of both per-wavefront passes: 3 subtiles in flight per wavefront (measured
+// on the stats pass: 4 stages 1-2% faster than 5 or 3).
+constexpr int kWaveStages = 4;
 constexpr int kSubKeys = 16;
 // Only on walks of at least this many 64-key tiles: every wavefront loads all the row
 // tiles' queries (36 KB at 9 tiles), which short walks do not amortise (one 4096-token
@@ -932,14 +934,12 @@ __global__ __launch_bounds__(kThreads, W) void score_colsum_kernel(ScoreArgs a) 
 // 2^(s acc) = 2^(s x - c_r) and the normalisers share the accumulator registers (next to
 // the query fragments at two wavefronts per SIMD there is no room for them); they are
 // staged once per workgroup in LDS and read as 16-byte broadcasts for every subtile.
-constexpr int kWaveColsumStages = 4;
-
 template <int NQ>
 __global__ __launch_bounds__(kThreads, 2) void score_colsum_wave_kernel(ScoreArgs a) {
   using T = bf16_t;
   constexpr int D = 128;
   constexpr int NS = RowChunks<T, D>::kSteps;
-  constexpr int S = kWaveColsumStages;
+  constexpr int S = kWaveStages;
   constexpr int kSubBytes = WaveRun<S>::kSubBytes;
   prefetch_args(a.q, a.k, a.n_chunks, a.n_kv_heads, a.batch, a.chunk_keys, a.p0_from_end,
                 a.kv_head_stride, a.q_head_stride, a.M, a.n_rows, a.G, a.M_pad, a.offs);
