@@ -280,6 +280,30 @@ def test_score_long_walks_short_last_chunks(mode):
         check_scores(raw[l * H:(l + 1) * H], want, f"layer copy {l}")
 
 
+@pytest.mark.parametrize("case", ["g8_w16_k2", "g2_w64_k4"])
+def test_score_long_walks_other_group_sizes(case):
+    # the per-wavefront passes serve any 8 or 9 row tiles: 8 query heads per KV head with
+    # 18 scoring rows (144 rows, no padding row) and 2 heads with 68 rows (136 rows, 8
+    # padding rows), eight stacked layers so that the walks are long
+    kw = {"g8_w16_k2": dict(n_q_heads=64, window=16, k_draft=2),
+          "g2_w64_k4": dict(n_q_heads=16, window=64, k_draft=4)}[case]
+    wl = di.small_variant("c3", [16382, 8260], plant="none", **kw)
+    _log(f"score parity: long walks, {case}")
+    x = di.make_layer(wl, layer=1, with_v=False)
+    nl = 8
+    g = dge.Geometry(wl.n_q_heads * nl, wl.n_kv_heads * nl, wl.head_dim, wl.window, wl.k_draft,
+                     wl.cached_lens, device=DEV)
+    raw = dge.score(g, oracle.ROWS_WINDOW_DRAFT, to_dev(x.q_bits, "bf16").repeat(nl, 1, 1),
+                    to_dev(x.k_bits, "bf16").repeat(nl, 1, 1))
+    torch.cuda.synchronize()
+    raw = raw.cpu().numpy()
+    want = oracle.window_scores(x.q, x.k, wl.kv_offsets, wl.n_q_heads, wl.n_kv_heads, wl.window,
+                                wl.k_draft)
+    H = wl.n_kv_heads
+    for l in range(nl):
+        check_scores(raw[l * H:(l + 1) * H], want, f"{case} layer copy {l}")
+
+
 def test_score_lse_long_walks_short_last_chunks():
     # the single pass with the rows' LSE supplied, on the stacked ragged layers above: 64-tile
     # walks take the colsum pass with one K stream per wavefront, the normalisers entering
